@@ -1,0 +1,208 @@
+/*
+ * libpnn -- the training forward / backward pass of a parareal neural network (Lee, Lee & Park,
+ * "Parareal Neural Networks Emulating a Parallel-in-time Algorithm") on one AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The network f-bar (eq. (barf)) is h o [coarse correction] o {g^j o C^j}_{j=1..N}:
+ *
+ *   x_j = C^j(x),  y_j = g^j(x_j)                    (eq. (xjyj), Alg. para2)      pnn_pre_fwd,
+ *                                                                                  parareal_fine_fwd
+ *   r_j = y_j - x_{j+1} (j < N), r_N = 0             (eq. (rk))                    parareal_combine_fwd
+ *   rt_1 = r_1, rt_{j+1} = r_{j+1} + F^j(rt_j)       (eq. (tilderk))               coarse_fwd
+ *   ytilde = y_N + rt_N                              (eq. (tildey))                coarse_fwd (j = N-1)
+ *   logits = h(ytilde), loss, D_N = dL/dytilde       (Alg. para3, first line)      pnn_head_fwd_bwd
+ *   D_j = D_{j+1} . dF^j/drt_j, dL/deta_j            (Alg. para3, eq. (etak))      coarse_bwd
+ *   dL/dphi_j = D_j . dg^j/dphi_j, D_j . dg^j/dx_j   (Alg. para3, eq. (phij))      parareal_fine_bwd
+ *   dL/dx_j = D_j . dg^j/dx_j - D_{j-1}              (eq. (deltaj))                parareal_combine_bwd
+ *   dL/ddelta_j                                       (eq. (deltaj))                pnn_pre_bwd
+ *
+ * All N fine sub-networks g^j run in the same kernel launches (grouped convolutions over N
+ * independent weight sets).  The coarse network is sequential by definition (Sec. 3.1) and runs
+ * one block F^j per call.
+ *
+ * Conventions for every entry point
+ *   - Every tensor pointer is a DEVICE pointer owned by the caller.  Activations are NHWC and
+ *     dense ([batch][H][W][C]); convolution filters are [c_out][k][k][c_in].
+ *   - Storage type: PNN_F32 plans store everything in float; PNN_BF16 plans store activations,
+ *     activation gradients and filters as bfloat16 bit patterns (uint16_t) and keep BN
+ *     parameters, every parameter gradient, the head and the loss in float.  Arithmetic is fp32
+ *     (bf16 MFMA operands with fp32 accumulation).
+ *   - Entry points never allocate, free or synchronise.  All work is enqueued on the given
+ *     stream, in stream order.  Only pnn_plan_create allocates (host memory only).
+ *   - Workspaces: the caller allocates one "saved" buffer (activations kept from the forward for
+ *     the backward; pnn_workspace_size(PNN_WS_SAVED)) and one "scratch" buffer (temporaries;
+ *     PNN_WS_SCRATCH), both at least 256-byte aligned, and passes the same ones to every call of a
+ *     step.  Calls that share a scratch buffer must not overlap in time.
+ *   - Return value: PNN_OK (0) or a negative pnn_status; on error nothing has been enqueued,
+ *     except for PNN_ERR_HIP (a launch failed; earlier launches of the same call may have run).
+ *     No C++ exception crosses this interface.  Asynchronous kernel faults surface at the
+ *     caller's next synchronisation.
+ */
+#ifndef PNN_H
+#define PNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int pnn_status;
+enum {
+  PNN_OK = 0,
+  PNN_ERR_NULL = -1,        /* a required pointer is NULL */
+  PNN_ERR_SHAPE = -2,       /* inconsistent shapes / node list */
+  PNN_ERR_DTYPE = -3,       /* unknown storage type */
+  PNN_ERR_WORKSPACE = -4,   /* unknown workspace kind */
+  PNN_ERR_UNSUPPORTED = -5, /* a valid network this library does not run (e.g. channels not a multiple of 16) */
+  PNN_ERR_HIP = -6,         /* a HIP call failed */
+  PNN_ERR_INDEX = -7        /* sub-network / coarse block index out of range */
+};
+
+typedef enum { PNN_F32 = 0, PNN_BF16 = 1 } pnn_dtype;
+
+/* Node kinds of a segment (see pnn_segment_desc). */
+enum {
+  PNN_OP_CONV = 0,     /* dst = conv_{k,stride,pad}(A) [+ res];  A = ReLU(BN_bn(src)) if bn >= 0 else src */
+  PNN_OP_BNACT = 1,    /* dst = pool(ReLU(BN_bn(src))) [+ res];  pool = 2x2/2 max pool when pool == 2 */
+  PNN_OP_MAXPOOL3 = 2  /* dst = 3x3 / stride 2 / pad 1 max pool of src (preprocessing only) */
+};
+
+/* One node.  Slots are tensors of the segment: slot 0 is its input.  Convolution is
+ * cross-correlation with zero padding and no bias.  BN is batch normalisation in training mode
+ * (batch statistics over N, H, W; biased variance; eps = 1e-5) with per-channel gamma / beta. */
+typedef struct {
+  int op;
+  int src, dst;        /* slot indices */
+  int bn;              /* BN instance applied to src (with ReLU) before the op, or -1 */
+  int pool;            /* PNN_OP_BNACT: 0 or 2 */
+  int k, stride, pad;  /* PNN_OP_CONV: k in {1, 3} */
+  int cout;            /* PNN_OP_CONV: output channels */
+  int res;             /* slot added to the result, or -1 */
+} pnn_node_desc;
+
+/* A segment: C^j, g^j or F^j as a list of nodes in evaluation order.  bn_slot[b] is the slot
+ * that BN instance b normalises; all nodes naming b share its activation. */
+typedef struct {
+  int in_h, in_w, in_c;
+  int n_nodes;
+  const pnn_node_desc* nodes;
+  int n_bn;
+  const int* bn_slot;
+  int out_slot;
+} pnn_segment_desc;
+
+/* The whole network (eq. (barf)): N preprocessing operators, N sub-networks, N-1 coarse blocks
+ * and a head (global average pool + linear layer with bias, softmax cross-entropy). */
+typedef struct {
+  int dtype;                       /* pnn_dtype */
+  int batch;
+  int img_h, img_w, img_c;
+  int n_sub;                       /* N >= 1 */
+  int n_classes;
+  const pnn_segment_desc* pre;     /* [N]   C^j : image  -> X_{j-1} */
+  const pnn_segment_desc* fine;    /* [N]   g^j : X_{j-1} -> X_j    */
+  const pnn_segment_desc* coarse;  /* [N-1] F^j : X_j -> X_{j+1}    */
+} pnn_net_desc;
+
+typedef struct pnn_plan pnn_plan;
+
+/* Validate a network description and build a plan (shapes, parameter / workspace layouts, launch
+ * schedules).  The description is copied; the caller may free it afterwards.  Allocates host
+ * memory only.  Errors: PNN_ERR_NULL, PNN_ERR_DTYPE, PNN_ERR_SHAPE, PNN_ERR_UNSUPPORTED. */
+pnn_status pnn_plan_create(const pnn_net_desc* desc, pnn_plan** out);
+void pnn_plan_destroy(pnn_plan* plan);
+
+typedef enum { PNN_WS_SAVED = 0, PNN_WS_SCRATCH = 1 } pnn_ws_kind;
+pnn_status pnn_workspace_size(const pnn_plan* plan, int kind, size_t* bytes);
+
+/* Parameter layout of one segment (part 0 = C^j, 1 = g^j, 2 = F^j; index j is 0-based).
+ * A parameter buffer holds the conv filters of the segment's nodes in node order (storage type),
+ * then gamma[C], beta[C] of every BN instance (float).  A gradient buffer has the same order with
+ * everything in float.  offsets[i] (i < n_nodes) is the byte offset of node i's filter (or
+ * SIZE_MAX for nodes without one); offsets[n_nodes + 2b] / [n_nodes + 2b + 1] are the offsets of
+ * gamma / beta of BN b.  `offsets` needs n_nodes + 2 n_bn entries and may be NULL.  grad = 0:
+ * parameter buffer, grad = 1: gradient buffer.  *total receives the buffer size in bytes. */
+pnn_status pnn_param_layout(const pnn_plan* plan, int part, int j, int grad, size_t* offsets,
+                            size_t* total);
+
+/* Shape (H, W, C) of sub-network j's input x_j (which = 0) or output y_j (which = 1). */
+pnn_status pnn_tensor_shape(const pnn_plan* plan, int which, int j, int* h, int* w, int* c);
+
+/* ---- forward (Alg. para2) ----------------------------------------------------------------- */
+
+/* x_j = C^j(image) for j = 0..N-1 (eq. (xjyj)).  image: [B][img_h][img_w][img_c]; x[j]: X_{j-1}
+ * shaped.  delta[j]: parameter buffer of C^j (may be NULL when C^j has no parameters). */
+pnn_status pnn_pre_fwd(pnn_plan* plan, const void* image, void* const* x, const void* const* delta,
+                       void* saved, void* scratch, void* stream);
+
+/* y_j = g^j(x_j) for all j in one set of grouped launches (Alg. para2, parallel loop).  Stores
+ * the layer inputs and BN statistics needed by parareal_fine_bwd in `saved`. */
+pnn_status parareal_fine_fwd(pnn_plan* plan, const void* const* x, const void* const* phi,
+                             void* const* y, void* saved, void* scratch, void* stream);
+
+/* r_j = y_j - x_{j+1}, j = 0..N-2 (eq. (rk)), r[j] shaped like y_j.  rnorm2 (nullable, float[N-1])
+ * receives ||r_j||^2 (the interface mismatch the coarse network corrects, Sec. 3.1). */
+pnn_status parareal_combine_fwd(pnn_plan* plan, const void* const* y, const void* const* x,
+                                void* const* r, float* rnorm2, void* scratch, void* stream);
+
+/* One coarse block, j = 0..N-2 (eq. (tilderk)): rt_next = add + F^j(rt_j).  Pass add = r_{j+1}
+ * for j < N-2 and add = y_N for j = N-2; then rt_next = ytilde (eq. (tildey), r_N = 0).
+ * rt_j: X_j shaped (rt_0 = r_0), rt_next and add: X_{j+1} shaped.  rt_next must not alias
+ * rt_j. */
+pnn_status coarse_fwd(pnn_plan* plan, int j, const void* rt_j, const void* eta_j, const void* add,
+                      void* rt_next, void* saved, void* scratch, void* stream);
+
+/* Postprocessing h and the loss, forward and backward (Alg. para3, first line): logits =
+ * mean_{h,w}(ytilde) W^T + b (eps = [W (classes x C) | b (classes)] float), loss = mean softmax
+ * cross-entropy over the batch.  Writes logits[B][classes] (float, nullable), *loss (float,
+ * device), D_N = dL/dytilde (X_N shaped) and deps = [dW | db] (float). labels: int32[B]. */
+pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps,
+                            const int32_t* labels, float* logits, float* loss, void* D_N,
+                            float* deps, void* scratch, void* stream);
+
+/* ---- backward (Alg. para3) ---------------------------------------------------------------- */
+
+/* D_j = D_{j+1} . dF^j/drt_j and deta_j = D_{j+1} . dF^j/deta_j (eq. (etak)), j = N-2..0,
+ * called in that order.  D_next: X_{j+1} shaped, D_j: X_j shaped (must not alias D_next),
+ * deta_j: gradient buffer of F^j (overwritten). */
+pnn_status coarse_bwd(pnn_plan* plan, int j, const void* D_next, const void* rt_j,
+                      const void* eta_j, const void* saved, void* D_j, float* deta_j,
+                      void* scratch, void* stream);
+
+/* For all j at once (Alg. para3, parallel loop; dL/dy_j = D_j by eq. (ingredient1)):
+ * dphi[j] = D_j . dg^j/dphi_j (gradient buffer, overwritten) and dx[j] = D_j . dg^j/dx_j
+ * (X_{j-1} shaped).  dy[j] = D_j. */
+pnn_status parareal_fine_bwd(pnn_plan* plan, const void* const* dy, const void* const* x,
+                             const void* const* phi, const void* saved, void* const* dx,
+                             float* const* dphi, void* scratch, void* stream);
+
+/* dx[j] -= D_{j-1} in place for j = 1..N-1 (eq. (deltaj), the -D_{j-1} term; D_0 = 0). */
+pnn_status parareal_combine_bwd(pnn_plan* plan, void* const* dx, const void* const* D,
+                                void* stream);
+
+/* ddelta[j] = dL/ddelta_j from g_j = dL/dx_j (after parareal_combine_bwd), eq. (deltaj).  No
+ * gradient with respect to the image is formed.  ddelta[j] may be NULL for a C^j without
+ * parameters. */
+pnn_status pnn_pre_bwd(pnn_plan* plan, const void* image, const void* const* g,
+                       const void* const* delta, const void* saved, float* const* ddelta,
+                       void* scratch, void* stream);
+
+/* ---- misc ----------------------------------------------------------------------------------- */
+
+const char* pnn_status_string(pnn_status s);
+
+/* Per-kernel-family GPU time accounting with HIP events recorded on the call's stream around
+ * every launch of one family (0 = off).  Families: 1 = grouped conv forward / data-gradient
+ * kernel, 2 = weight-gradient kernel.  pnn_timing_read synchronises on the recorded events and
+ * returns the summed milliseconds, the launch count, and the summed multiply-add count
+ * (2 x MACs = FLOPs) and minimum HBM bytes of those launches; it resets the accumulators. */
+pnn_status pnn_timing_enable(pnn_plan* plan, int family);
+pnn_status pnn_timing_read(pnn_plan* plan, double* ms, long long* launches, double* flops,
+                           double* bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PNN_H */

@@ -1,0 +1,431 @@
+// Grouped implicit-GEMM convolution kernels for gfx950 (forward, data gradient, weight gradient).
+//
+// Convolution, its data gradient and its weight gradient are the three contractions of every
+// layer of the fine sub-networks g^j and coarse blocks F^j (Sec. 3, Alg. para2 / para3).  One
+// launch runs the same layer position of all N sub-networks: every group is an independent
+// problem with its own tensors and filters.
+//
+// Operands are NHWC rows gathered with 16-byte loads straight into MFMA lane fragments (bf16:
+// v_mfma_f32_16x16x32_bf16, fp32: v_mfma_f32_16x16x4f32); accumulation is fp32.  A workgroup of
+// four waves owns a 128-row x (16 wn)-column output tile; each wave 32 rows.
+#include "device_common.h"
+#include "pnn_internal.h"
+
+namespace pnn {
+
+// ------------------------------------------------------------------------------------------------
+// forward / data-gradient convolution
+// ------------------------------------------------------------------------------------------------
+
+template <typename T, int MODE, bool VEC>
+__device__ __forceinline__ void gather_a(const ConvProb& P, int n, int p, int q, bool rowok, int k0,
+                                         Frag<T>& a) {
+  constexpr int VE = St<T>::VE;
+  if constexpr (VEC) {
+    const int tap = k0 / P.Cg;
+    const int c0 = k0 - tap * P.Cg;
+    const int r = tap / P.k;
+    const int s = tap - r * P.k;
+    int ih, iw;
+    bool ok = rowok && k0 < P.K;
+    if constexpr (MODE == MODE_FWD) {
+      ih = p * P.stride + r - P.pad;
+      iw = q * P.stride + s - P.pad;
+    } else {
+      const int th = p + P.pad - r, tw = q + P.pad - s;
+      ok = ok && th >= 0 && tw >= 0 && (th % P.stride) == 0 && (tw % P.stride) == 0;
+      ih = th / P.stride;
+      iw = tw / P.stride;
+    }
+    ok = ok && (unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W;
+    if (!ok) {
+      a.zero();
+      return;
+    }
+    const long idx = (((long)n * P.H + ih) * P.W + iw) * P.Cg + c0;
+    if (MODE == MODE_FWD && P.pro != nullptr) {
+      Chunk<T> c;
+      load_chunk<T>(P.in, idx, c);
+#pragma unroll
+      for (int e = 0; e < VE; ++e)
+        c.v[e] = fmaxf(fmaf(c.v[e], P.pro[c0 + e], P.pro[P.Cg + c0 + e]), 0.0f);
+      a.from_chunk(c);
+    } else {
+      a.from_raw(*(const uint4*)((const T*)P.in + idx));
+    }
+  } else {
+    Chunk<T> c;
+#pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      const int kk = k0 + e;
+      float v = 0.0f;
+      if (rowok && kk < P.K) {
+        const int tap = kk / P.Cg;
+        const int ch = kk - tap * P.Cg;
+        const int r = tap / P.k;
+        const int s = tap - r * P.k;
+        int ih, iw;
+        bool ok = true;
+        if constexpr (MODE == MODE_FWD) {
+          ih = p * P.stride + r - P.pad;
+          iw = q * P.stride + s - P.pad;
+        } else {
+          const int th = p + P.pad - r, tw = q + P.pad - s;
+          ok = th >= 0 && tw >= 0 && (th % P.stride) == 0 && (tw % P.stride) == 0;
+          ih = th / P.stride;
+          iw = tw / P.stride;
+        }
+        ok = ok && (unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W;
+        if (ok) {
+          v = St<T>::ld(P.in, (((long)n * P.H + ih) * P.W + iw) * P.Cg + ch);
+          if (MODE == MODE_FWD && P.pro != nullptr) v = fmaxf(fmaf(v, P.pro[ch], P.pro[P.Cg + ch]), 0.0f);
+        }
+      }
+      c.v[e] = v;
+    }
+    a.from_chunk(c);
+  }
+}
+
+template <typename T, bool VEC>
+__device__ __forceinline__ void load_b(const ConvProb& P, int col, int k0, Frag<T>& b) {
+  constexpr int VE = St<T>::VE;
+  if constexpr (VEC) {
+    if (k0 < P.K)
+      b.from_raw(*(const uint4*)((const T*)P.wmat + (long)col * P.K + k0));
+    else
+      b.zero();
+  } else {
+    Chunk<T> c;
+#pragma unroll
+    for (int e = 0; e < VE; ++e)
+      c.v[e] = (k0 + e < P.K) ? St<T>::ld(P.wmat, (long)col * P.K + k0 + e) : 0.0f;
+    b.from_chunk(c);
+  }
+}
+
+template <typename T, int MODE, bool VEC>
+__global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
+  constexpr int VE = St<T>::VE;
+  constexpr int KS = 4 * VE;
+  __shared__ float red[4][64][2];
+
+  const int gi = find_group(L);
+  const ConvProb& P = L.p[gi];
+  const int local = blockIdx.x - P.tile_begin;
+  const int tm = local / P.tiles_n;
+  const int tn = local - tm * P.tiles_n;
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15;
+  const int grp = lane >> 4;
+  const int mw = tm * CONV_BM + wave * 32;
+  const int n0 = tn * 16 * P.wn;
+  const int PQ = P.P * P.Q;
+
+  int rn[2], rp[2], rq[2];
+  bool rv[2];
+#pragma unroll
+  for (int wm = 0; wm < 2; ++wm) {
+    const int m = mw + wm * 16 + r16;
+    rv[wm] = m < P.M;
+    const int mm = rv[wm] ? m : 0;
+    rn[wm] = mm / PQ;
+    const int rem = mm - rn[wm] * PQ;
+    rp[wm] = rem / P.Q;
+    rq[wm] = rem - rp[wm] * P.Q;
+  }
+
+  f32x4 acc[2][4];
+#pragma unroll
+  for (int wm = 0; wm < 2; ++wm)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[wm][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int kk = 0; kk < P.K; kk += KS) {
+    const int k0 = kk + VE * grp;
+    Frag<T> a[2];
+#pragma unroll
+    for (int wm = 0; wm < 2; ++wm) gather_a<T, MODE, VEC>(P, rn[wm], rp[wm], rq[wm], rv[wm], k0, a[wm]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (j < P.wn) {
+        Frag<T> b;
+        load_b<T, VEC>(P, n0 + j * 16 + r16, k0, b);
+#pragma unroll
+        for (int wm = 0; wm < 2; ++wm) mma(a[wm], b, acc[wm][j]);
+      }
+    }
+  }
+
+  // ---- epilogue ----
+  float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
+  const bool bnmask = MODE == MODE_BWD && (P.flags & EPI_BN_MASK);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (j >= P.wn) continue;
+    const int col = n0 + j * 16 + r16;
+    float mean = 0.f, invstd = 0.f, sc = 0.f, sh = 0.f;
+    if (bnmask) {
+      mean = P.bnst[col];
+      invstd = P.bnst[P.ncol + col];
+      sc = P.bnst[2 * P.ncol + col];
+      sh = P.bnst[3 * P.ncol + col];
+    }
+#pragma unroll
+    for (int wm = 0; wm < 2; ++wm) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = mw + wm * 16 + grp * 4 + i;
+        if (m >= P.M) continue;
+        const long idx = (long)m * P.ncol + col;
+        float v = acc[wm][j][i];
+        if constexpr (MODE == MODE_FWD) {
+          if (P.res) v += St<T>::ld(P.res, idx);
+          if (P.ext) v += St<T>::ld(P.ext, idx);
+          St<T>::st(P.out, idx, v);
+          const float vr = St<T>::rnd(v);
+          s1[j] += vr;
+          s2[j] += vr * vr;
+        } else {
+          if (P.flags & EPI_ACC_IN) v += P.acc_in[idx];
+          if (P.flags & EPI_STORE_F32) {
+            P.out32[idx] = v;
+          } else if (bnmask) {
+            const float z = St<T>::ld(P.zsrc, idx);
+            const float y = fmaf(z, sc, sh);
+            const float d = y > 0.f ? v : 0.f;
+            St<T>::st(P.out, idx, d);
+            const float dr = St<T>::rnd(d);
+            s1[j] += dr;
+            s2[j] += dr * ((z - mean) * invstd);
+          } else {
+            if (P.res) v += St<T>::ld(P.res, idx);
+            St<T>::st(P.out, idx, v);
+          }
+        }
+      }
+    }
+  }
+
+  const bool stats = (MODE == MODE_FWD) ? (P.flags & EPI_STATS) != 0 : bnmask;
+  if (stats) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (j >= P.wn) continue;
+      float a = s1[j], b = s2[j];
+      a += __shfl_xor(a, 16, 64);
+      b += __shfl_xor(b, 16, 64);
+      a += __shfl_xor(a, 32, 64);
+      b += __shfl_xor(b, 32, 64);
+      if (grp == 0) {
+        red[wave][j * 16 + r16][0] = a;
+        red[wave][j * 16 + r16][1] = b;
+      }
+    }
+    __syncthreads();
+    const int t = threadIdx.x;
+    if (t < 16 * P.wn) {
+      const float a = ((red[0][t][0] + red[1][t][0]) + red[2][t][0]) + red[3][t][0];
+      const float b = ((red[0][t][1] + red[1][t][1]) + red[2][t][1]) + red[3][t][1];
+      P.part[(long)tm * 2 * P.ncol + n0 + t] = a;
+      P.part[((long)tm * 2 + 1) * P.ncol + n0 + t] = b;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// weight gradient: dW[co][(r,s,c)] = sum_m g[m][co] * act(in)[pixel(m) + tap(r,s)][c]
+// The m-reduction is split over workgroups (fp32 partials, summed in a fixed order afterwards).
+// Both operands are staged through LDS transposed to m-contiguous rows.
+// ------------------------------------------------------------------------------------------------
+
+template <typename T, bool VEC>
+__global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
+  constexpr int VE = St<T>::VE;
+  constexpr int KS = 4 * VE;
+  constexpr int KC = WGRAD_KC;
+  constexpr int LD = KC + VE;  // padded LDS row (elements); 16-byte aligned rows
+  __shared__ T gT[64 * LD];
+  __shared__ T aT[256 * LD];
+
+  const int gi = find_group(L);
+  const WgradProb& P = L.p[gi];
+  const int local = blockIdx.x - P.tile_begin;
+  const int tk = local % P.tiles_k;
+  const int rest = local / P.tiles_k;
+  const int tco = rest % P.tiles_co;
+  const int split = rest / P.tiles_co;
+  const int TCO = 16 * P.wr;
+  const int TK = 256 / P.wr;
+  const int co0 = tco * TCO;
+  const int kk0 = tk * TK;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int sr = wave % P.wr;
+  const int cgp = wave / P.wr;
+  const int m_begin = split * P.mchunk;
+  const int m_end = min(P.M, m_begin + P.mchunk);
+  const int PQ = P.P * P.Q;
+
+  f32x4 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int mc = m_begin; mc < m_end; mc += KC) {
+    // output-gradient tile: KC rows (m) x TCO columns (co), stored [co][m]
+    const int gcpr = TCO / VE;
+    for (int idx = tid; idx < KC * gcpr; idx += 256) {
+      const int mr = idx / gcpr;
+      const int cc = (idx - mr * gcpr) * VE;
+      const int m = mc + mr;
+      T vals[VE];
+      if (m < m_end) {
+        const uint4 u = *(const uint4*)((const T*)P.g + (long)m * P.Co + co0 + cc);
+        __builtin_memcpy(vals, &u, 16);
+      } else {
+#pragma unroll
+        for (int e = 0; e < VE; ++e) vals[e] = T(0);
+      }
+#pragma unroll
+      for (int e = 0; e < VE; ++e) gT[(cc + e) * LD + mr] = vals[e];
+    }
+    // activation tile: KC rows (m) x TK columns (r,s,c), stored [column][m]
+    const int acpr = TK / VE;
+    for (int idx = tid; idx < KC * acpr; idx += 256) {
+      const int mr = idx / acpr;
+      const int kc = (idx - mr * acpr) * VE;
+      const int m = mc + mr;
+      const int kidx = kk0 + kc;
+      Chunk<T> c;
+#pragma unroll
+      for (int e = 0; e < VE; ++e) c.v[e] = 0.f;
+      if (m < m_end && kidx < P.K) {
+        const int n = m / PQ;
+        const int rem = m - n * PQ;
+        const int p = rem / P.Q;
+        const int q = rem - p * P.Q;
+        if constexpr (VEC) {
+          const int tap = kidx / P.Cg;
+          const int c0 = kidx - tap * P.Cg;
+          const int r = tap / P.k, s = tap - (tap / P.k) * P.k;
+          const int ih = p * P.stride + r - P.pad, iw = q * P.stride + s - P.pad;
+          if ((unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W) {
+            load_chunk<T>(P.in, (((long)n * P.H + ih) * P.W + iw) * P.Cg + c0, c);
+            if (P.pro != nullptr) {
+#pragma unroll
+              for (int e = 0; e < VE; ++e)
+                c.v[e] = fmaxf(fmaf(c.v[e], P.pro[c0 + e], P.pro[P.Cg + c0 + e]), 0.0f);
+            }
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < VE; ++e) {
+            const int kx = kidx + e;
+            if (kx >= P.K) continue;
+            const int tap = kx / P.Cg;
+            const int ch = kx - tap * P.Cg;
+            const int r = tap / P.k, s = tap - (tap / P.k) * P.k;
+            const int ih = p * P.stride + r - P.pad, iw = q * P.stride + s - P.pad;
+            if ((unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W) {
+              float v = St<T>::ld(P.in, (((long)n * P.H + ih) * P.W + iw) * P.Cg + ch);
+              if (P.pro != nullptr) v = fmaxf(fmaf(v, P.pro[ch], P.pro[P.Cg + ch]), 0.0f);
+              c.v[e] = v;
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        if constexpr (sizeof(T) == 4)
+          aT[(kc + e) * LD + mr] = c.v[e];
+        else
+          aT[(kc + e) * LD + mr] = f2bf(c.v[e]);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < KC; ks += KS) {
+      Frag<T> a;
+      a.from_raw(*(const uint4*)&gT[(sr * 16 + r16) * LD + ks + VE * grp]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        Frag<T> b;
+        b.from_raw(*(const uint4*)&aT[(cgp * 64 + j * 16 + r16) * LD + ks + VE * grp]);
+        mma(a, b, acc[j]);
+      }
+    }
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int kidx = kk0 + cgp * 64 + j * 16 + r16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int co = co0 + sr * 16 + grp * 4 + i;
+      if (co < P.Co && kidx < P.K) P.part[((long)split * P.Co + co) * P.K + kidx] = acc[j][i];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void reduce_kernel(const ReduceLaunch L) {
+  const int gi = find_group(L);
+  const ReduceProb& P = L.p[gi];
+  const long base = (long)(blockIdx.x - P.tile_begin) * ELT_TILE;
+  for (int t = threadIdx.x; t < ELT_TILE; t += 256) {
+    const long i = base + t;
+    if (i >= P.n) break;
+    float s = 0.f;
+    for (int sp = 0; sp < P.splits; ++sp) s += P.part[(long)sp * P.n + i];
+    P.dst[i] = s;
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// launchers
+// ------------------------------------------------------------------------------------------------
+
+template <typename T>
+static int launch_conv_t(const ConvLaunch& L, int tiles, int mode, bool vec, hipStream_t s) {
+  if (mode == MODE_FWD) {
+    if (vec)
+      hipLaunchKernelGGL((conv_kernel<T, MODE_FWD, true>), dim3(tiles), dim3(256), 0, s, L);
+    else
+      hipLaunchKernelGGL((conv_kernel<T, MODE_FWD, false>), dim3(tiles), dim3(256), 0, s, L);
+  } else {
+    if (vec)
+      hipLaunchKernelGGL((conv_kernel<T, MODE_BWD, true>), dim3(tiles), dim3(256), 0, s, L);
+    else
+      hipLaunchKernelGGL((conv_kernel<T, MODE_BWD, false>), dim3(tiles), dim3(256), 0, s, L);
+  }
+  return (int)hipGetLastError();
+}
+
+int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, bool vec, hipStream_t s) {
+  return dtype == 1 ? launch_conv_t<uint16_t>(L, tiles, mode, vec, s)
+                    : launch_conv_t<float>(L, tiles, mode, vec, s);
+}
+
+int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s) {
+  if (dtype == 1) {
+    if (vec)
+      hipLaunchKernelGGL((wgrad_kernel<uint16_t, true>), dim3(tiles), dim3(256), 0, s, L);
+    else
+      hipLaunchKernelGGL((wgrad_kernel<uint16_t, false>), dim3(tiles), dim3(256), 0, s, L);
+  } else {
+    if (vec)
+      hipLaunchKernelGGL((wgrad_kernel<float, true>), dim3(tiles), dim3(256), 0, s, L);
+    else
+      hipLaunchKernelGGL((wgrad_kernel<float, false>), dim3(tiles), dim3(256), 0, s, L);
+  }
+  return (int)hipGetLastError();
+}
+
+int launch_reduce(const ReduceLaunch& L, int tiles, hipStream_t s) {
+  hipLaunchKernelGGL(reduce_kernel, dim3(tiles), dim3(256), 0, s, L);
+  return (int)hipGetLastError();
+}
+
+}  // namespace pnn

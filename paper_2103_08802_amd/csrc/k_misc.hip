@@ -1,0 +1,404 @@
+// Normalisation, pooling, parareal-combine and head kernels for gfx950.
+//
+// BN (training mode, Sec. 4: the layers H_l of VGG-16 / ResNet-1001 are convolution, batch
+// normalisation and ReLU) is split around the convolutions: its statistics are reduced from
+// per-tile partial sums written by the producing kernel, and its affine map + ReLU is applied in
+// the consuming kernel's operand load.  All reductions run in a fixed order (deterministic).
+#include "device_common.h"
+#include "pnn_internal.h"
+
+namespace pnn {
+
+// ------------------------------------------------------------------------------------------------
+// BN statistics from tile partials: mean, biased variance -> invstd, and the affine map
+// scale = gamma * invstd, shift = beta - mean * scale.  One thread per channel; fp64 sums.
+// ------------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void bn_fin_fwd_kernel(const FinLaunch L) {
+  int gi = 0;
+  for (int i = 1; i < L.n; ++i)
+    if (L.f[i].tile_begin <= (int)blockIdx.x) gi = i;
+  const BnFinProb& P = L.f[gi];
+  const int c = (blockIdx.x - P.tile_begin) * 256 + threadIdx.x;
+  if (c >= P.C) return;
+  double s = 0.0, s2 = 0.0;
+  for (int t = 0; t < P.ntiles; ++t) {
+    s += (double)P.part[(long)t * 2 * P.C + c];
+    s2 += (double)P.part[((long)t * 2 + 1) * P.C + c];
+  }
+  const double mean = s / (double)P.count;
+  double var = s2 / (double)P.count - mean * mean;
+  if (var < 0.0) var = 0.0;
+  const float invstd = (float)(1.0 / sqrt(var + (double)PNN_BN_EPS));
+  const float scale = P.gamma[c] * invstd;
+  P.stats[c] = (float)mean;
+  P.stats[P.C + c] = invstd;
+  P.stats[2 * P.C + c] = scale;
+  P.stats[3 * P.C + c] = P.beta[c] - (float)mean * scale;
+}
+
+// dbeta = sum dbn, dgamma = sum dbn * xhat (eq. of the BN backward), and the apply coefficients.
+__global__ __launch_bounds__(256) void bn_fin_bwd_kernel(const FinLaunch L) {
+  int gi = 0;
+  for (int i = 1; i < L.n; ++i)
+    if (L.b[i].tile_begin <= (int)blockIdx.x) gi = i;
+  const BnBwdFinProb& P = L.b[gi];
+  const int c = (blockIdx.x - P.tile_begin) * 256 + threadIdx.x;
+  if (c >= P.C) return;
+  double s = 0.0, s2 = 0.0;
+  for (int t = 0; t < P.ntiles; ++t) {
+    s += (double)P.part[(long)t * 2 * P.C + c];
+    s2 += (double)P.part[((long)t * 2 + 1) * P.C + c];
+  }
+  P.dbeta[c] = (float)s;
+  P.dgamma[c] = (float)s2;
+  const float invstd = P.stats[P.C + c];
+  P.coef[c] = P.gamma[c] * invstd;
+  P.coef[P.C + c] = (float)(s / (double)P.count);
+  P.coef[2 * P.C + c] = (float)(s2 / (double)P.count);
+}
+
+// Column sums / sums of squares of a stored tensor [M][C], COLSTAT_ROWS rows per workgroup.
+template <typename T>
+__global__ __launch_bounds__(256) void colstat_kernel(const ColStatLaunch L) {
+  const int gi = find_group(L);
+  const ColStatProb& P = L.p[gi];
+  const int tile = blockIdx.x - P.tile_begin;
+  const long r0 = (long)tile * COLSTAT_ROWS;
+  const long r1 = min(P.M, r0 + COLSTAT_ROWS);
+  for (int c = threadIdx.x; c < P.C; c += 256) {
+    float s = 0.f, s2 = 0.f;
+    for (long r = r0; r < r1; ++r) {
+      const float v = St<T>::ld(P.x, r * P.C + c);
+      s += v;
+      s2 += v * v;
+    }
+    P.part[(long)tile * 2 * P.C + c] = s;
+    P.part[((long)tile * 2 + 1) * P.C + c] = s2;
+  }
+}
+
+// out = skip + c1 * (dbn - mb - xhat * mbx), xhat = (z - mean) * invstd
+template <typename T>
+__global__ __launch_bounds__(256) void bn_apply_kernel(const BnApplyLaunch L) {
+  const int gi = find_group(L);
+  const BnApplyProb& P = L.p[gi];
+  const long base = (long)(blockIdx.x - P.tile_begin) * ELT_TILE;
+  for (int t = threadIdx.x; t < ELT_TILE; t += 256) {
+    const long i = base + t;
+    if (i >= P.n) break;
+    const int c = (int)(i % P.C);
+    const float z = St<T>::ld(P.z, i);
+    const float xh = (z - P.stats[c]) * P.stats[P.C + c];
+    float v = P.coef[c] * (St<T>::ld(P.dbn, i) - P.coef[P.C + c] - xh * P.coef[2 * P.C + c]);
+    if (P.skip) v += St<T>::ld(P.skip, i);
+    St<T>::st(P.out, i, v);
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// bnact: out = pool(ReLU(BN(z))) [+ res] [+ ext]; backward routes the output gradient to the first
+// maximum of each 2x2 window, masks it by ReLU' and reduces dbn, dbn * xhat per channel.
+// One workgroup = BNACT_PIX output pixels x all channels; a thread owns channels.
+// ------------------------------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void bnact_fwd_kernel(const BnActLaunch L) {
+  const int gi = find_group(L);
+  const BnActProb& P = L.p[gi];
+  const int pool = P.pool ? 2 : 1;
+  const int Ho = P.H / pool, Wo = P.W / pool;
+  const long px0 = (long)(blockIdx.x - P.tile_begin) * BNACT_PIX;
+  for (int c = threadIdx.x; c < P.C; c += 256) {
+    const float sc = P.stats[2 * P.C + c], sh = P.stats[3 * P.C + c];
+    for (int k = 0; k < BNACT_PIX; ++k) {
+      const long px = px0 + k;
+      if (px >= P.n_out) break;
+      const int n = (int)(px / ((long)Ho * Wo));
+      const int rem = (int)(px - (long)n * Ho * Wo);
+      const int p = rem / Wo, q = rem - (rem / Wo) * Wo;
+      float m = -INFINITY;
+      for (int a = 0; a < pool; ++a)
+        for (int b = 0; b < pool; ++b) {
+          const long zi = (((long)n * P.H + p * pool + a) * P.W + q * pool + b) * P.C + c;
+          const float y = fmaxf(fmaf(St<T>::ld(P.z, zi), sc, sh), 0.0f);
+          m = fmaxf(m, y);
+        }
+      const long oi = px * P.C + c;
+      if (P.res) m += St<T>::ld(P.res, oi);
+      if (P.ext) m += St<T>::ld(P.ext, oi);
+      St<T>::st(P.out, oi, m);
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void bnact_bwd_kernel(const BnActLaunch L) {
+  const int gi = find_group(L);
+  const BnActProb& P = L.p[gi];
+  const int pool = P.pool ? 2 : 1;
+  const int Ho = P.H / pool, Wo = P.W / pool;
+  const int tile = blockIdx.x - P.tile_begin;
+  const long px0 = (long)tile * BNACT_PIX;
+  for (int c = threadIdx.x; c < P.C; c += 256) {
+    const float mean = P.stats[c], invstd = P.stats[P.C + c];
+    const float sc = P.stats[2 * P.C + c], sh = P.stats[3 * P.C + c];
+    float s1 = 0.f, s2 = 0.f;
+    for (int k = 0; k < BNACT_PIX; ++k) {
+      const long px = px0 + k;
+      if (px >= P.n_out) break;
+      const int n = (int)(px / ((long)Ho * Wo));
+      const int rem = (int)(px - (long)n * Ho * Wo);
+      const int p = rem / Wo, q = rem - (rem / Wo) * Wo;
+      // first maximum of the window (row-major), on the unrounded activation
+      int arg = 0;
+      float best = 0.f;
+      for (int w = 0; w < pool * pool; ++w) {
+        const long zi = (((long)n * P.H + p * pool + w / pool) * P.W + q * pool + w % pool) * P.C + c;
+        const float y = fmaxf(fmaf(St<T>::ld(P.z, zi), sc, sh), 0.0f);
+        if (w == 0 || y > best) {
+          best = y;
+          arg = w;
+        }
+      }
+      const float gv = St<T>::ld(P.g, px * P.C + c);
+      for (int w = 0; w < pool * pool; ++w) {
+        const long zi = (((long)n * P.H + p * pool + w / pool) * P.W + q * pool + w % pool) * P.C + c;
+        const float z = St<T>::ld(P.z, zi);
+        const float y = fmaf(z, sc, sh);
+        const float d = (w == arg && y > 0.f) ? gv : 0.f;
+        St<T>::st(P.out, zi, d);
+        const float dr = St<T>::rnd(d);
+        s1 += dr;
+        s2 += dr * ((z - mean) * invstd);
+      }
+    }
+    P.part[(long)tile * 2 * P.C + c] = s1;
+    P.part[((long)tile * 2 + 1) * P.C + c] = s2;
+  }
+}
+
+// 3x3 / stride 2 / pad 1 max pool (preprocessing operators C^j, Sec. 4.1.1 and 4.2.1)
+template <typename T>
+__global__ __launch_bounds__(256) void maxpool3_kernel(const MaxPool3Launch L) {
+  const int gi = find_group(L);
+  const MaxPool3Prob& P = L.p[gi];
+  const long n_out = (long)P.B * P.Ho * P.Wo * P.C;
+  const long base = (long)(blockIdx.x - P.tile_begin) * ELT_TILE;
+  for (int t = threadIdx.x; t < ELT_TILE; t += 256) {
+    const long i = base + t;
+    if (i >= n_out) break;
+    const int c = (int)(i % P.C);
+    const long px = i / P.C;
+    const int q = (int)(px % P.Wo);
+    const int p = (int)((px / P.Wo) % P.Ho);
+    const int n = (int)(px / ((long)P.Wo * P.Ho));
+    float m = -INFINITY;
+    for (int a = 0; a < 3; ++a) {
+      const int ih = 2 * p + a - 1;
+      if (ih < 0 || ih >= P.H) continue;
+      for (int b = 0; b < 3; ++b) {
+        const int iw = 2 * q + b - 1;
+        if (iw < 0 || iw >= P.W) continue;
+        m = fmaxf(m, St<T>::ld(P.x, (((long)n * P.H + ih) * P.W + iw) * P.C + c));
+      }
+    }
+    St<T>::st(P.y, i, m);
+  }
+}
+
+// wt[c][t][o] = w[o][t][c]  (filter layout of the data-gradient convolution)
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_kernel(const TransposeLaunch L) {
+  const int gi = find_group(L);
+  const TransposeProb& P = L.p[gi];
+  const long n = (long)P.O * P.T * P.C;
+  const long base = (long)(blockIdx.x - P.tile_begin) * ELT_TILE;
+  for (int t = threadIdx.x; t < ELT_TILE; t += 256) {
+    const long i = base + t;   // index into wt
+    if (i >= n) break;
+    const int o = (int)(i % P.O);
+    const long ct = i / P.O;
+    const int tp = (int)(ct % P.T);
+    const int c = (int)(ct / P.T);
+    ((T*)P.wt)[i] = ((const T*)P.w)[((long)o * P.T + tp) * P.C + c];
+  }
+}
+
+// out = a - b (rounded to storage); optional per-tile partial of sum(out^2)
+template <typename T>
+__global__ __launch_bounds__(256) void sub_kernel(const AxpyLaunch L) {
+  __shared__ float red[4];
+  const int gi = find_group(L);
+  const AxpyProb& P = L.p[gi];
+  const int tile = blockIdx.x - P.tile_begin;
+  const long base = (long)tile * ELT_TILE;
+  float sq = 0.f;
+  for (int t = threadIdx.x; t < ELT_TILE; t += 256) {
+    const long i = base + t;
+    if (i >= P.n) break;
+    const float v = St<T>::ld(P.a, i) - St<T>::ld(P.b, i);
+    St<T>::st(P.out, i, v);
+    const float vr = St<T>::rnd(v);
+    sq += vr * vr;
+  }
+  if (P.sq_part != nullptr) {
+    sq = wave_sum(sq);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sq;
+    __syncthreads();
+    if (threadIdx.x == 0) P.sq_part[tile] = ((red[0] + red[1]) + red[2]) + red[3];
+  }
+}
+
+__global__ void sumsq_kernel(const float* part, int n, float* out) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    double s = 0.0;
+    for (int i = 0; i < n; ++i) s += part[i];
+    *out = (float)s;
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// head h: logits = mean_{hw}(ytilde) W^T + b, softmax cross-entropy (mean over the batch), and
+// D_N = dL/dytilde.  Kernel 1: one workgroup per sample.  Kernel 2: dW, db, loss (fixed order).
+// scratch: pooled [B][C], dlogits [B][K], loss_n [B]
+// ------------------------------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void head_sample_kernel(const void* yt, const float* eps,
+                                                          const int32_t* labels, float* logits,
+                                                          void* D_N, float* scratch, int B, int HW,
+                                                          int C, int K) {
+  extern __shared__ float sh[];  // pooled [C], z [K], dpooled [C]
+  float* pooled = sh;
+  float* z = sh + C;
+  __shared__ float red[2];
+  const int n = blockIdx.x;
+  const float* W = eps;
+  const float* bias = eps + (long)K * C;
+  for (int c = threadIdx.x; c < C; c += 256) {
+    float s = 0.f;
+    for (int h = 0; h < HW; ++h) s += St<T>::ld(yt, ((long)n * HW + h) * C + c);
+    pooled[c] = s / (float)HW;
+    scratch[(long)n * C + c] = pooled[c];
+  }
+  __syncthreads();
+  for (int k = threadIdx.x; k < K; k += 256) {
+    float s = bias[k];
+    for (int c = 0; c < C; ++c) s += W[(long)k * C + c] * pooled[c];
+    z[k] = s;
+    if (logits) logits[(long)n * K + k] = s;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float mx = -INFINITY;
+    for (int k = 0; k < K; ++k) mx = fmaxf(mx, z[k]);
+    double se = 0.0;
+    for (int k = 0; k < K; ++k) se += exp((double)(z[k] - mx));
+    red[0] = mx + (float)log(se);
+  }
+  __syncthreads();
+  const float lse = red[0];
+  const int lab = labels[n];
+  float* dlog = scratch + (long)B * C;
+  for (int k = threadIdx.x; k < K; k += 256) {
+    const float pk = expf(z[k] - lse);
+    const float d = (pk - (k == lab ? 1.f : 0.f)) / (float)B;
+    dlog[(long)n * K + k] = d;
+  }
+  if (threadIdx.x == 0) scratch[(long)B * C + (long)B * K + n] = lse - z[lab];
+  __syncthreads();
+  for (int c = threadIdx.x; c < C; c += 256) {
+    float s = 0.f;
+    for (int k = 0; k < K; ++k) s += dlog[(long)n * K + k] * W[(long)k * C + c];
+    const float d = s / (float)HW;
+    for (int h = 0; h < HW; ++h) St<T>::st(D_N, ((long)n * HW + h) * C + c, d);
+  }
+}
+
+__global__ __launch_bounds__(256) void head_reduce_kernel(const float* scratch, float* deps,
+                                                          float* loss, int B, int C, int K) {
+  const float* pooled = scratch;
+  const float* dlog = scratch + (long)B * C;
+  const long nW = (long)K * C;
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i < nW) {
+    const int k = (int)(i / C), c = (int)(i % C);
+    float s = 0.f;
+    for (int n = 0; n < B; ++n) s += dlog[(long)n * K + k] * pooled[(long)n * C + c];
+    deps[i] = s;
+  } else if (i < nW + K) {
+    const int k = (int)(i - nW);
+    float s = 0.f;
+    for (int n = 0; n < B; ++n) s += dlog[(long)n * K + k];
+    deps[i] = s;
+  } else if (i == nW + K) {
+    const float* ln = scratch + (long)B * C + (long)B * K;
+    double s = 0.0;
+    for (int n = 0; n < B; ++n) s += ln[n];
+    *loss = (float)(s / (double)B);
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// launchers
+// ------------------------------------------------------------------------------------------------
+#define PNN_LAUNCH_T(kern, L, tiles, dtype, s)                                        \
+  do {                                                                               \
+    if ((dtype) == 1)                                                                \
+      hipLaunchKernelGGL(kern<uint16_t>, dim3(tiles), dim3(256), 0, s, L);           \
+    else                                                                             \
+      hipLaunchKernelGGL(kern<float>, dim3(tiles), dim3(256), 0, s, L);              \
+    return (int)hipGetLastError();                                                   \
+  } while (0)
+
+int launch_bn_fin_fwd(const FinLaunch& L, int tiles, hipStream_t s) {
+  hipLaunchKernelGGL(bn_fin_fwd_kernel, dim3(tiles), dim3(256), 0, s, L);
+  return (int)hipGetLastError();
+}
+int launch_bn_fin_bwd(const FinLaunch& L, int tiles, hipStream_t s) {
+  hipLaunchKernelGGL(bn_fin_bwd_kernel, dim3(tiles), dim3(256), 0, s, L);
+  return (int)hipGetLastError();
+}
+int launch_colstat(const ColStatLaunch& L, int tiles, int dtype, hipStream_t s) {
+  PNN_LAUNCH_T(colstat_kernel, L, tiles, dtype, s);
+}
+int launch_bn_apply(const BnApplyLaunch& L, int tiles, int dtype, hipStream_t s) {
+  PNN_LAUNCH_T(bn_apply_kernel, L, tiles, dtype, s);
+}
+int launch_bnact_fwd(const BnActLaunch& L, int tiles, int dtype, hipStream_t s) {
+  PNN_LAUNCH_T(bnact_fwd_kernel, L, tiles, dtype, s);
+}
+int launch_bnact_bwd(const BnActLaunch& L, int tiles, int dtype, hipStream_t s) {
+  PNN_LAUNCH_T(bnact_bwd_kernel, L, tiles, dtype, s);
+}
+int launch_maxpool3(const MaxPool3Launch& L, int tiles, int dtype, hipStream_t s) {
+  PNN_LAUNCH_T(maxpool3_kernel, L, tiles, dtype, s);
+}
+int launch_transpose(const TransposeLaunch& L, int tiles, int dtype, hipStream_t s) {
+  PNN_LAUNCH_T(transpose_kernel, L, tiles, dtype, s);
+}
+int launch_sub(const AxpyLaunch& L, int tiles, int dtype, hipStream_t s) {
+  PNN_LAUNCH_T(sub_kernel, L, tiles, dtype, s);
+}
+int launch_sumsq(const float* part, int n, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(sumsq_kernel, dim3(1), dim3(64), 0, s, part, n, out);
+  return (int)hipGetLastError();
+}
+
+int launch_head(const void* yt, const float* eps, const int32_t* labels, float* logits, float* loss,
+                void* D_N, float* deps, float* scratch, int B, int HW, int C, int K, int dtype,
+                hipStream_t s) {
+  const size_t shm = sizeof(float) * (size_t)(C + K);
+  if (dtype == 1)
+    hipLaunchKernelGGL(head_sample_kernel<uint16_t>, dim3(B), dim3(256), shm, s, yt, eps, labels,
+                       logits, D_N, scratch, B, HW, C, K);
+  else
+    hipLaunchKernelGGL(head_sample_kernel<float>, dim3(B), dim3(256), shm, s, yt, eps, labels,
+                       logits, D_N, scratch, B, HW, C, K);
+  int e = (int)hipGetLastError();
+  if (e) return e;
+  const long n = (long)K * C + K + 1;
+  hipLaunchKernelGGL(head_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                     scratch, deps, loss, B, C, K);
+  return (int)hipGetLastError();
+}
+
+}  // namespace pnn

@@ -1,0 +1,1223 @@
+// libpnn host side: plan construction (shape inference, validation, parameter / workspace
+// layouts, level schedules) and the C-ABI entry points that enqueue the grouped kernels.
+//
+// Schedules.  Every node of a segment gets a level: 1 + the largest level of its inputs (slot 0
+// has level 0).  A forward call walks the levels upwards and issues, per level, ONE grouped launch
+// per kernel kind holding the nodes of that level of every segment in the call (for
+// parareal_fine_fwd: all N sub-networks, Alg. para2's parallel loop).  A backward call walks the
+// levels downwards (Alg. para3).
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "pnn.h"
+#include "pnn_internal.h"
+
+using namespace pnn;
+
+namespace {
+
+constexpr size_t NONE = (size_t)-1;
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline long cdiv(long a, long b) { return (a + b - 1) / b; }
+
+struct NodeP {
+  int op, src, dst, bn, pool, k, stride, pad, cout, res;
+  int level = 0;
+  int cin = 0, H = 0, W = 0, Ho = 0, Wo = 0;
+  size_t w_off = NONE, gw_off = NONE, wt_off = NONE;
+  bool dgrad = false;      // data gradient needed in the backward
+  bool first_of_two = false;
+};
+
+struct SlotP {
+  int H = 0, W = 0, C = 0;
+  long elems = 0;
+  int producer = -1;
+  int level = 0;
+  int bn = -1;
+  int res_consumer = -1;
+  int direct_consumer = -1;
+  std::vector<int> bn_consumers;
+  size_t saved_off = NONE;
+  size_t g_off = NONE;
+};
+
+struct BnP {
+  int slot = 0, C = 0;
+  size_t p_off = 0, gp_off = 0;
+  size_t stats_off = 0;
+  size_t part_off = 0;
+  int fwd_tiles = 0, bwd_tiles = 0;
+  size_t dbn_off = NONE, coef_off = NONE, datmp_off = NONE;
+  bool bnact_consumer = false;
+};
+
+struct SegP {
+  int part = 0, index = 0;
+  int in_h = 0, in_w = 0, in_c = 0;
+  std::vector<NodeP> nodes;
+  std::vector<SlotP> slots;
+  std::vector<BnP> bns;
+  std::vector<bool> needs;
+  int out = 0;
+  int max_level = 0;
+  size_t param_bytes = 0, grad_bytes = 0;
+  size_t saved_base = 0, saved_bytes = 0;
+  size_t scr_base = 0, scr_bytes = 0;
+};
+
+struct WgradGeom {
+  int wr, tiles_co, tiles_k, splits, mchunk;
+};
+
+}  // namespace
+
+struct pnn_plan {
+  int dtype = 0, es = 4;
+  int B = 0, N = 0, classes = 0;
+  int img_h = 0, img_w = 0, img_c = 0;
+  std::vector<SegP> pre, fine, coarse;
+  size_t saved_bytes = 0, scratch_bytes = 0;
+  size_t wpart_off = 0, wpart_bytes = 0;
+  size_t head_off = 0, head_bytes = 0;
+  size_t sq_off = 0, sq_bytes = 0;
+  // timing of one kernel family
+  int timing_family = 0;
+  std::vector<hipEvent_t> ev;
+  size_t ev_used = 0;
+  double t_flops = 0.0, t_bytes = 0.0;
+  long long t_launches = 0;
+};
+
+namespace {
+
+// ------------------------------------------------------------------------------------------------
+// plan construction
+// ------------------------------------------------------------------------------------------------
+
+WgradGeom wgrad_geom(int Co, int K, long M) {
+  WgradGeom g;
+  g.wr = (Co % 64 == 0) ? 4 : (Co % 32 == 0) ? 2 : 1;
+  g.tiles_co = Co / (16 * g.wr);
+  g.tiles_k = (int)cdiv(K, 256 / g.wr);
+  const long base = (long)g.tiles_co * g.tiles_k;
+  long splits = std::max(1L, std::min(cdiv(M, 512), cdiv(256, base)));
+  long mchunk = cdiv(cdiv(M, splits), WGRAD_KC) * WGRAD_KC;
+  g.mchunk = (int)mchunk;
+  g.splits = (int)cdiv(M, mchunk);
+  return g;
+}
+
+int conv_wn(int ncol) { return (ncol % 64 == 0) ? 4 : (ncol % 32 == 0) ? 2 : 1; }
+
+pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, int es, SegP& S) {
+  S.part = part;
+  S.index = index;
+  S.in_h = d.in_h;
+  S.in_w = d.in_w;
+  S.in_c = d.in_c;
+  if (d.in_h <= 0 || d.in_w <= 0 || d.in_c <= 0 || d.n_nodes < 0 || d.n_bn < 0) return PNN_ERR_SHAPE;
+  if (d.n_nodes > 0 && d.nodes == nullptr) return PNN_ERR_NULL;
+  if (d.n_bn > 0 && d.bn_slot == nullptr) return PNN_ERR_NULL;
+  int n_slots = 1;
+  for (int i = 0; i < d.n_nodes; ++i) n_slots = std::max(n_slots, std::max(d.nodes[i].dst, d.nodes[i].src) + 1);
+  if (d.out_slot < 0 || d.out_slot >= n_slots) return PNN_ERR_SHAPE;
+  S.slots.assign(n_slots, SlotP());
+  S.slots[0].H = d.in_h;
+  S.slots[0].W = d.in_w;
+  S.slots[0].C = d.in_c;
+  std::vector<bool> made(n_slots, false);
+  made[0] = true;
+  S.bns.resize(d.n_bn);
+  for (int b = 0; b < d.n_bn; ++b) {
+    if (d.bn_slot[b] < 0 || d.bn_slot[b] >= n_slots) return PNN_ERR_SHAPE;
+    S.bns[b].slot = d.bn_slot[b];
+    if (S.slots[d.bn_slot[b]].bn != -1) return PNN_ERR_SHAPE;   // one BN per slot
+    S.slots[d.bn_slot[b]].bn = b;
+  }
+  for (int i = 0; i < d.n_nodes; ++i) {
+    const pnn_node_desc& x = d.nodes[i];
+    NodeP n;
+    n.op = x.op; n.src = x.src; n.dst = x.dst; n.bn = x.bn; n.pool = x.pool; n.k = x.k;
+    n.stride = x.stride; n.pad = x.pad; n.cout = x.cout; n.res = x.res;
+    if (n.src < 0 || n.src >= n_slots || !made[n.src]) return PNN_ERR_SHAPE;
+    if (n.dst <= 0 || n.dst >= n_slots || made[n.dst]) return PNN_ERR_SHAPE;
+    if (n.res >= n_slots || (n.res >= 0 && !made[n.res])) return PNN_ERR_SHAPE;
+    if (n.bn >= d.n_bn || (n.bn >= 0 && S.bns[n.bn].slot != n.src)) return PNN_ERR_SHAPE;
+    const SlotP& s = S.slots[n.src];
+    n.cin = s.C; n.H = s.H; n.W = s.W;
+    int oc = s.C;
+    if (n.op == PNN_OP_CONV) {
+      if (n.k != 1 && n.k != 3) return PNN_ERR_UNSUPPORTED;
+      if (n.stride < 1 || n.stride > 2 || n.pad < 0 || n.pad >= n.k || n.cout <= 0) return PNN_ERR_SHAPE;
+      if (n.cout % 16 != 0) return PNN_ERR_UNSUPPORTED;
+      n.Ho = (s.H + 2 * n.pad - n.k) / n.stride + 1;
+      n.Wo = (s.W + 2 * n.pad - n.k) / n.stride + 1;
+      oc = n.cout;
+    } else if (n.op == PNN_OP_BNACT) {
+      if (n.bn < 0 || (n.pool != 0 && n.pool != 2)) return PNN_ERR_SHAPE;
+      if (n.pool == 2 && (s.H % 2 || s.W % 2)) return PNN_ERR_UNSUPPORTED;
+      n.Ho = n.pool ? s.H / 2 : s.H;
+      n.Wo = n.pool ? s.W / 2 : s.W;
+    } else if (n.op == PNN_OP_MAXPOOL3) {
+      if (part != 0 || n.bn >= 0) return PNN_ERR_UNSUPPORTED;
+      n.Ho = (s.H + 2 - 3) / 2 + 1;
+      n.Wo = (s.W + 2 - 3) / 2 + 1;
+    } else {
+      return PNN_ERR_SHAPE;
+    }
+    if (n.Ho <= 0 || n.Wo <= 0) return PNN_ERR_SHAPE;
+    SlotP& o = S.slots[n.dst];
+    o.H = n.Ho; o.W = n.Wo; o.C = oc;
+    o.producer = i;
+    if (n.res >= 0) {
+      const SlotP& r = S.slots[n.res];
+      if (r.H != o.H || r.W != o.W || r.C != o.C) return PNN_ERR_SHAPE;
+    }
+    n.level = 1 + std::max(s.level, n.res >= 0 ? S.slots[n.res].level : 0);
+    o.level = n.level;
+    made[n.dst] = true;
+    S.max_level = std::max(S.max_level, n.level);
+    S.nodes.push_back(n);
+  }
+  if (!made[d.out_slot]) return PNN_ERR_SHAPE;
+  S.out = d.out_slot;
+  for (auto& sl : S.slots) sl.elems = (long)B * sl.H * sl.W * sl.C;
+  // consumers
+  for (int i = 0; i < (int)S.nodes.size(); ++i) {
+    NodeP& n = S.nodes[i];
+    SlotP& s = S.slots[n.src];
+    if (n.res >= 0) {
+      if (S.slots[n.res].res_consumer != -1) return PNN_ERR_UNSUPPORTED;
+      S.slots[n.res].res_consumer = i;
+    }
+    if (n.op == PNN_OP_MAXPOOL3) continue;
+    if (n.bn >= 0) {
+      s.bn_consumers.push_back(i);
+      if (n.op == PNN_OP_BNACT) S.bns[n.bn].bnact_consumer = true;
+    } else {
+      if (s.direct_consumer != -1) return PNN_ERR_UNSUPPORTED;
+      s.direct_consumer = i;
+    }
+  }
+  for (auto& b : S.bns)
+    if (b.slot != 0 && S.nodes[S.slots[b.slot].producer].op != PNN_OP_CONV) return PNN_ERR_UNSUPPORTED;
+  for (auto& sl : S.slots) {
+    if (!sl.bn_consumers.empty() && sl.direct_consumer != -1) return PNN_ERR_UNSUPPORTED;
+    if (sl.bn_consumers.size() > 2) return PNN_ERR_UNSUPPORTED;
+    if (sl.bn != -1 && S.bns[sl.bn].bnact_consumer && sl.bn_consumers.size() != 1) return PNN_ERR_UNSUPPORTED;
+  }
+  const SlotP& so = S.slots[S.out];
+  if (so.res_consumer != -1 || !so.bn_consumers.empty() || so.direct_consumer != -1) return PNN_ERR_UNSUPPORTED;
+  if (part != 0 && S.out != 0) {
+    const SlotP& s0 = S.slots[0];
+    if (s0.bn_consumers.empty() && s0.direct_consumer == -1) return PNN_ERR_UNSUPPORTED;
+  }
+  // backward roles.  needs[s]: some parameter lies upstream of slot s (or the segment's input
+  // gradient is wanted, for g^j and F^j), so dL/ds must be formed.
+  S.needs.assign(n_slots, false);
+  S.needs[0] = part != 0;
+  for (auto& n : S.nodes)
+    S.needs[n.dst] = S.needs[n.src] || (n.res >= 0 && S.needs[n.res]) || n.op == PNN_OP_CONV || n.bn >= 0;
+  for (int i = 0; i < (int)S.nodes.size(); ++i) {
+    NodeP& n = S.nodes[i];
+    if (n.op == PNN_OP_MAXPOOL3 && S.needs[n.src]) return PNN_ERR_UNSUPPORTED;
+    if (n.op != PNN_OP_CONV) continue;
+    n.dgrad = S.needs[n.src] || n.bn >= 0;
+    if (n.dgrad && n.cin % 16 != 0) return PNN_ERR_UNSUPPORTED;
+  }
+  for (auto& sl : S.slots) {
+    if (sl.bn_consumers.size() == 2) {
+      // the consumer reached first in the backward (higher level, then later node) stores fp32
+      int a = sl.bn_consumers[0], b = sl.bn_consumers[1];
+      const bool a_first = S.nodes[a].level > S.nodes[b].level ||
+                           (S.nodes[a].level == S.nodes[b].level && a > b);
+      S.nodes[a_first ? a : b].first_of_two = true;
+    }
+  }
+  // parameter / gradient layout
+  size_t po = 0, go = 0;
+  for (auto& n : S.nodes) {
+    if (n.op != PNN_OP_CONV) continue;
+    const size_t cnt = (size_t)n.cout * n.k * n.k * n.cin;
+    n.w_off = po;
+    po = align256(po + cnt * es);
+    n.gw_off = go;
+    go = align256(go + cnt * 4);
+  }
+  for (auto& b : S.bns) {
+    b.C = S.slots[b.slot].C;
+    b.p_off = po;
+    po = align256(po + (size_t)b.C * 8);
+    b.gp_off = go;
+    go = align256(go + (size_t)b.C * 8);
+  }
+  S.param_bytes = po;
+  S.grad_bytes = go;
+  // saved workspace (relative): intermediate slots and BN statistics
+  size_t so_ = 0;
+  for (int s = 1; s < (int)S.slots.size(); ++s) {
+    if (s == S.out) continue;
+    S.slots[s].saved_off = so_;
+    so_ = align256(so_ + (size_t)S.slots[s].elems * es);
+  }
+  for (auto& b : S.bns) {
+    b.stats_off = so_;
+    so_ = align256(so_ + (size_t)b.C * 16);
+  }
+  S.saved_bytes = so_;
+  // segment scratch (relative): BN partials / dbn / coefficients, slot gradients, filter transposes
+  size_t sc = 0;
+  for (auto& b : S.bns) {
+    const SlotP& sl = S.slots[b.slot];
+    const long M = (long)B * sl.H * sl.W;
+    b.fwd_tiles = (int)cdiv(M, COLSTAT_ROWS);
+    b.bwd_tiles = (int)cdiv(M, CONV_BM);
+    if (b.bnact_consumer) {
+      const NodeP& c = S.nodes[sl.bn_consumers[0]];
+      b.bwd_tiles = (int)cdiv((long)B * c.Ho * c.Wo, BNACT_PIX);
+    }
+    const int tiles = std::max(b.fwd_tiles, b.bwd_tiles);
+    b.part_off = sc;
+    sc = align256(sc + (size_t)tiles * 2 * b.C * 4);
+    b.coef_off = sc;
+    sc = align256(sc + (size_t)b.C * 12);
+    if (!sl.bn_consumers.empty()) {
+      b.dbn_off = sc;
+      sc = align256(sc + (size_t)sl.elems * es);
+    }
+    if (sl.bn_consumers.size() == 2) {
+      b.datmp_off = sc;
+      sc = align256(sc + (size_t)sl.elems * 4);
+    }
+  }
+  for (int s = 1; s < (int)S.slots.size(); ++s) {
+    if (s == S.out) continue;
+    SlotP& sl = S.slots[s];
+    const bool alias = sl.bn_consumers.empty() && sl.direct_consumer == -1;
+    if (alias || !S.needs[s]) continue;
+    sl.g_off = sc;
+    sc = align256(sc + (size_t)sl.elems * es);
+  }
+  for (auto& n : S.nodes) {
+    if (n.op != PNN_OP_CONV || !n.dgrad) continue;
+    n.wt_off = sc;
+    sc = align256(sc + (size_t)n.cout * n.k * n.k * n.cin * es);
+  }
+  S.scr_bytes = sc;
+  return PNN_OK;
+}
+
+// wgrad partial bytes needed by one level of a set of segments run together
+size_t wgrad_level_bytes(const std::vector<SegP>& segs, int B) {
+  int maxL = 0;
+  for (auto& s : segs) maxL = std::max(maxL, s.max_level);
+  size_t best = 0;
+  for (int L = 1; L <= maxL; ++L) {
+    size_t tot = 0;
+    for (auto& s : segs)
+      for (auto& n : s.nodes) {
+        if (n.level != L || n.op != PNN_OP_CONV) continue;
+        const long M = (long)B * n.Ho * n.Wo;
+        const int K = n.k * n.k * n.cin;
+        WgradGeom g = wgrad_geom(n.cout, K, M);
+        tot = align256(tot + (size_t)g.splits * n.cout * K * 4);
+      }
+    best = std::max(best, tot);
+  }
+  return best;
+}
+
+bool same_shape(const SegP& a, int slot_a, int h, int w, int c) {
+  const SlotP& s = a.slots[slot_a];
+  return s.H == h && s.W == w && s.C == c;
+}
+
+// ------------------------------------------------------------------------------------------------
+// call-time machinery
+// ------------------------------------------------------------------------------------------------
+
+struct Ptrs {
+  const void* in = nullptr;
+  void* out = nullptr;
+  const void* params = nullptr;
+  float* grads = nullptr;
+  const void* ext = nullptr;
+  const void* gout = nullptr;
+  void* gin = nullptr;
+};
+
+struct Ctx {
+  pnn_plan* plan;
+  char* saved;
+  char* scratch;
+  hipStream_t stream;
+};
+
+inline char* cp(const void* p) { return (char*)const_cast<void*>(p); }
+
+void* slot_ptr(const Ctx& c, const SegP& S, const Ptrs& p, int s) {
+  if (s == 0) return const_cast<void*>(p.in);
+  if (s == S.out) return p.out;
+  return c.saved + S.saved_base + S.slots[s].saved_off;
+}
+float* stats_ptr(const Ctx& c, const SegP& S, int b) {
+  return (float*)(c.saved + S.saved_base + S.bns[b].stats_off);
+}
+float* part_ptr(const Ctx& c, const SegP& S, int b) {
+  return (float*)(c.scratch + S.scr_base + S.bns[b].part_off);
+}
+void* grad_ptr(const Ctx& c, const SegP& S, const Ptrs& p, int s) {
+  if (s == S.out) return const_cast<void*>(p.gout);
+  if (s == 0) return p.gin;
+  const SlotP& sl = S.slots[s];
+  if (sl.g_off == NONE) return grad_ptr(c, S, p, S.nodes[sl.res_consumer].dst);  // residual-only slot
+  return c.scratch + S.scr_base + sl.g_off;
+}
+void* skip_ptr(const Ctx& c, const SegP& S, const Ptrs& p, int s) {
+  const SlotP& sl = S.slots[s];
+  if (sl.res_consumer < 0) return nullptr;
+  return grad_ptr(c, S, p, S.nodes[sl.res_consumer].dst);
+}
+
+struct Timer {
+  pnn_plan* plan;
+  int family;
+  bool on;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  Timer(pnn_plan* p, int fam, hipStream_t s) : plan(p), family(fam) {
+    on = p->timing_family == fam && p->ev_used + 2 <= p->ev.size();
+    if (on) {
+      e0 = p->ev[p->ev_used];
+      e1 = p->ev[p->ev_used + 1];
+      p->ev_used += 2;
+      hipEventRecord(e0, s);
+    }
+  }
+  void done(hipStream_t s, double flops, double bytes) {
+    if (!on) return;
+    hipEventRecord(e1, s);
+    plan->t_flops += flops;
+    plan->t_bytes += bytes;
+    plan->t_launches += 1;
+  }
+};
+
+// Chunk a problem list into grouped launches of at most PNN_MAXG problems.
+template <typename Launch, typename Prob, typename TilesOf, typename Fire>
+int grouped(std::vector<Prob>& probs, TilesOf tiles_of, Fire fire) {
+  size_t i = 0;
+  while (i < probs.size()) {
+    Launch L;
+    L.n = 0;
+    int tiles = 0;
+    size_t first = i;
+    while (i < probs.size() && L.n < PNN_MAXG) {
+      Prob pr = probs[i];
+      pr.tile_begin = tiles;
+      tiles += tiles_of(pr);
+      L.p[L.n++] = pr;
+      ++i;
+    }
+    if (tiles > 0) {
+      int e = fire(L, tiles, first);
+      if (e) return PNN_ERR_HIP;
+    }
+  }
+  return PNN_OK;
+}
+
+int fin_launch(std::vector<BnFinProb>& fw, std::vector<BnBwdFinProb>& bw, hipStream_t s) {
+  for (size_t i = 0; i < fw.size(); i += PNN_MAXG) {
+    FinLaunch L;
+    L.n = 0;
+    int tiles = 0;
+    for (size_t k = i; k < fw.size() && L.n < PNN_MAXG; ++k) {
+      L.f[L.n] = fw[k];
+      L.f[L.n].tile_begin = tiles;
+      tiles += (int)cdiv(fw[k].C, 256);
+      L.n++;
+    }
+    if (launch_bn_fin_fwd(L, tiles, s)) return PNN_ERR_HIP;
+  }
+  for (size_t i = 0; i < bw.size(); i += PNN_MAXG) {
+    FinLaunch L;
+    L.n = 0;
+    int tiles = 0;
+    for (size_t k = i; k < bw.size() && L.n < PNN_MAXG; ++k) {
+      L.b[L.n] = bw[k];
+      L.b[L.n].tile_begin = tiles;
+      tiles += (int)cdiv(bw[k].C, 256);
+      L.n++;
+    }
+    if (launch_bn_fin_bwd(L, tiles, s)) return PNN_ERR_HIP;
+  }
+  return PNN_OK;
+}
+
+double conv_flops(const ConvProb& p) { return 2.0 * p.M * (double)p.ncol * p.K; }
+double conv_bytes(const ConvProb& p, int es, int mode) {
+  double b = (double)p.B * p.H * p.W * p.Cg * es + (double)p.ncol * p.K * es;
+  const double mo = (double)p.M * p.ncol;
+  if (mode == MODE_FWD) {
+    b += mo * es * (1 + (p.res ? 1 : 0) + (p.ext ? 1 : 0));
+  } else if (p.flags & EPI_STORE_F32) {
+    b += mo * 4;
+  } else if (p.flags & EPI_BN_MASK) {
+    b += mo * es * 2 + ((p.flags & EPI_ACC_IN) ? mo * 4 : 0);
+  } else {
+    b += mo * es * (1 + (p.res ? 1 : 0));
+  }
+  return b;
+}
+
+int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode, bool vec) {
+  pnn_plan* plan = c.plan;
+  return grouped<ConvLaunch>(
+      probs, [](const ConvProb& p) { return p.tiles_m * p.tiles_n; },
+      [&](const ConvLaunch& L, int tiles, size_t) {
+        double fl = 0, by = 0;
+        for (int i = 0; i < L.n; ++i) {
+          fl += conv_flops(L.p[i]);
+          by += conv_bytes(L.p[i], plan->es, mode);
+        }
+        Timer t(plan, 1, c.stream);
+        int e = launch_conv(L, tiles, plan->dtype, mode, vec, c.stream);
+        t.done(c.stream, fl, by);
+        return e;
+      });
+}
+
+ConvProb conv_common(const pnn_plan* plan, const NodeP& n) {
+  ConvProb p;
+  std::memset(&p, 0, sizeof(p));
+  p.k = n.k;
+  p.stride = n.stride;
+  p.pad = n.pad;
+  return p;
+}
+
+void set_tiles(ConvProb& p) {
+  p.tiles_m = (int)cdiv(p.M, CONV_BM);
+  p.wn = conv_wn(p.ncol);
+  p.tiles_n = p.ncol / (16 * p.wn);
+}
+
+// ------------------------------------------------------------------------------------------------
+// forward of a set of segments
+// ------------------------------------------------------------------------------------------------
+int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
+  pnn_plan* plan = c.plan;
+  const int B = plan->B, es = plan->es;
+  // identity segments
+  for (size_t i = 0; i < segs.size(); ++i) {
+    const SegP& S = *segs[i];
+    if (S.nodes.empty() && ptrs[i].out != ptrs[i].in) {
+      if (hipMemcpyAsync(ptrs[i].out, ptrs[i].in, (size_t)S.slots[0].elems * es,
+                         hipMemcpyDeviceToDevice, c.stream) != hipSuccess)
+        return PNN_ERR_HIP;
+    }
+  }
+  // statistics of BN instances on segment inputs
+  {
+    std::vector<ColStatProb> cs;
+    std::vector<BnFinProb> fw;
+    std::vector<BnBwdFinProb> none;
+    for (size_t i = 0; i < segs.size(); ++i) {
+      const SegP& S = *segs[i];
+      const SlotP& s0 = S.slots[0];
+      if (s0.bn < 0) continue;
+      const BnP& b = S.bns[s0.bn];
+      ColStatProb p;
+      p.x = ptrs[i].in;
+      p.part = part_ptr(c, S, s0.bn);
+      p.M = (long)B * s0.H * s0.W;
+      p.C = s0.C;
+      cs.push_back(p);
+      BnFinProb f;
+      f.part = p.part;
+      f.gamma = (const float*)(cp(ptrs[i].params) + b.p_off);
+      f.beta = f.gamma + b.C;
+      f.stats = stats_ptr(c, S, s0.bn);
+      f.ntiles = b.fwd_tiles;
+      f.C = b.C;
+      f.count = p.M;
+      fw.push_back(f);
+    }
+    int e = grouped<ColStatLaunch>(
+        cs, [](const ColStatProb& p) { return (int)cdiv(p.M, COLSTAT_ROWS); },
+        [&](const ColStatLaunch& L, int tiles, size_t) { return launch_colstat(L, tiles, plan->dtype, c.stream); });
+    if (e) return e;
+    if (fin_launch(fw, none, c.stream)) return PNN_ERR_HIP;
+  }
+  int maxL = 0;
+  for (auto* s : segs) maxL = std::max(maxL, s->max_level);
+  for (int L = 1; L <= maxL; ++L) {
+    std::vector<ConvProb> cv_vec, cv_gen;
+    std::vector<BnActProb> ba;
+    std::vector<MaxPool3Prob> mp;
+    std::vector<BnFinProb> fw;
+    std::vector<BnBwdFinProb> none;
+    for (size_t i = 0; i < segs.size(); ++i) {
+      const SegP& S = *segs[i];
+      const Ptrs& P = ptrs[i];
+      for (const NodeP& n : S.nodes) {
+        if (n.level != L) continue;
+        const SlotP& so = S.slots[n.dst];
+        const void* ext = (n.dst == S.out) ? P.ext : nullptr;
+        if (n.op == PNN_OP_CONV) {
+          ConvProb p = conv_common(plan, n);
+          p.in = slot_ptr(c, S, P, n.src);
+          p.wmat = cp(P.params) + n.w_off;
+          p.out = slot_ptr(c, S, P, n.dst);
+          p.res = n.res >= 0 ? slot_ptr(c, S, P, n.res) : nullptr;
+          p.ext = ext;
+          p.pro = n.bn >= 0 ? stats_ptr(c, S, n.bn) + 2 * S.bns[n.bn].C : nullptr;
+          if (so.bn >= 0) {
+            p.part = part_ptr(c, S, so.bn);
+            p.flags = EPI_STATS;
+          }
+          p.B = B; p.H = n.H; p.W = n.W; p.Cg = n.cin;
+          p.P = n.Ho; p.Q = n.Wo; p.ncol = n.cout;
+          p.M = B * n.Ho * n.Wo;
+          p.K = n.k * n.k * n.cin;
+          set_tiles(p);
+          (n.cin % (16 / es) == 0 ? cv_vec : cv_gen).push_back(p);
+        } else if (n.op == PNN_OP_BNACT) {
+          BnActProb p;
+          std::memset(&p, 0, sizeof(p));
+          p.z = slot_ptr(c, S, P, n.src);
+          p.out = slot_ptr(c, S, P, n.dst);
+          p.res = n.res >= 0 ? slot_ptr(c, S, P, n.res) : nullptr;
+          p.ext = ext;
+          p.stats = stats_ptr(c, S, n.bn);
+          p.B = B; p.H = n.H; p.W = n.W; p.C = n.cin; p.pool = n.pool;
+          p.n_out = (long)B * n.Ho * n.Wo;
+          ba.push_back(p);
+        } else {
+          MaxPool3Prob p;
+          p.x = slot_ptr(c, S, P, n.src);
+          p.y = slot_ptr(c, S, P, n.dst);
+          p.B = B; p.H = n.H; p.W = n.W; p.C = n.cin; p.Ho = n.Ho; p.Wo = n.Wo;
+          mp.push_back(p);
+        }
+        if (so.bn >= 0) {
+          const BnP& b = S.bns[so.bn];
+          BnFinProb f;
+          f.part = part_ptr(c, S, so.bn);
+          f.gamma = (const float*)(cp(P.params) + b.p_off);
+          f.beta = f.gamma + b.C;
+          f.stats = stats_ptr(c, S, so.bn);
+          f.ntiles = (int)cdiv((long)B * so.H * so.W, CONV_BM);
+          f.C = b.C;
+          f.count = (long)B * so.H * so.W;
+          fw.push_back(f);
+        }
+      }
+    }
+    int e;
+    if ((e = fire_conv(c, cv_vec, MODE_FWD, true))) return e;
+    if ((e = fire_conv(c, cv_gen, MODE_FWD, false))) return e;
+    e = grouped<BnActLaunch>(
+        ba, [](const BnActProb& p) { return (int)cdiv(p.n_out, BNACT_PIX); },
+        [&](const BnActLaunch& Lx, int tiles, size_t) { return launch_bnact_fwd(Lx, tiles, plan->dtype, c.stream); });
+    if (e) return e;
+    e = grouped<MaxPool3Launch>(
+        mp, [](const MaxPool3Prob& p) { return (int)cdiv((long)p.B * p.Ho * p.Wo * p.C, ELT_TILE); },
+        [&](const MaxPool3Launch& Lx, int tiles, size_t) { return launch_maxpool3(Lx, tiles, plan->dtype, c.stream); });
+    if (e) return e;
+    if (fin_launch(fw, none, c.stream)) return PNN_ERR_HIP;
+  }
+  return PNN_OK;
+}
+
+// ------------------------------------------------------------------------------------------------
+// backward of a set of segments
+// ------------------------------------------------------------------------------------------------
+void bn_bwd_finalize(const Ctx& c, const SegP& S, const Ptrs& P, int s, std::vector<BnBwdFinProb>& fin,
+                     std::vector<BnApplyProb>& app) {
+  const SlotP& sl = S.slots[s];
+  if (sl.bn < 0 || sl.bn_consumers.empty()) return;
+  const BnP& b = S.bns[sl.bn];
+  BnBwdFinProb f;
+  f.part = part_ptr(c, S, sl.bn);
+  f.gamma = (const float*)(cp(P.params) + b.p_off);
+  f.stats = stats_ptr(c, S, sl.bn);
+  f.dgamma = (float*)(cp(P.grads) + b.gp_off);
+  f.dbeta = f.dgamma + b.C;
+  f.coef = (float*)(c.scratch + S.scr_base + b.coef_off);
+  f.ntiles = b.bwd_tiles;
+  f.C = b.C;
+  f.count = (long)c.plan->B * sl.H * sl.W;
+  fin.push_back(f);
+  if (!S.needs[s]) return;
+  BnApplyProb a;
+  a.dbn = c.scratch + S.scr_base + b.dbn_off;
+  a.z = slot_ptr(c, S, P, s);
+  a.skip = skip_ptr(c, S, P, s);
+  a.out = grad_ptr(c, S, P, s);
+  a.stats = f.stats;
+  a.coef = f.coef;
+  a.n = sl.elems;
+  a.C = sl.C;
+  app.push_back(a);
+}
+
+int fire_finalize(const Ctx& c, std::vector<BnBwdFinProb>& fin, std::vector<BnApplyProb>& app) {
+  std::vector<BnFinProb> none;
+  if (fin_launch(none, fin, c.stream)) return PNN_ERR_HIP;
+  return grouped<BnApplyLaunch>(
+      app, [](const BnApplyProb& p) { return (int)cdiv(p.n, ELT_TILE); },
+      [&](const BnApplyLaunch& L, int tiles, size_t) { return launch_bn_apply(L, tiles, c.plan->dtype, c.stream); });
+}
+
+int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
+  pnn_plan* plan = c.plan;
+  const int B = plan->B, es = plan->es;
+  // filters of the data-gradient convolutions, [c_in][k][k][c_out]
+  {
+    std::vector<TransposeProb> tp;
+    for (size_t i = 0; i < segs.size(); ++i) {
+      const SegP& S = *segs[i];
+      for (const NodeP& n : S.nodes) {
+        if (n.op != PNN_OP_CONV || !n.dgrad) continue;
+        TransposeProb p;
+        p.w = cp(ptrs[i].params) + n.w_off;
+        p.wt = c.scratch + S.scr_base + n.wt_off;
+        p.O = n.cout;
+        p.T = n.k * n.k;
+        p.C = n.cin;
+        tp.push_back(p);
+      }
+    }
+    int e = grouped<TransposeLaunch>(
+        tp, [](const TransposeProb& p) { return (int)cdiv((long)p.O * p.T * p.C, ELT_TILE); },
+        [&](const TransposeLaunch& L, int tiles, size_t) { return launch_transpose(L, tiles, plan->dtype, c.stream); });
+    if (e) return e;
+  }
+  int maxL = 0;
+  for (auto* s : segs) maxL = std::max(maxL, s->max_level);
+  char* wpart = c.scratch + plan->wpart_off;
+  for (int L = maxL; L >= 1; --L) {
+    // A: gradients of the slots produced at this level
+    {
+      std::vector<BnBwdFinProb> fin;
+      std::vector<BnApplyProb> app;
+      for (size_t i = 0; i < segs.size(); ++i) {
+        const SegP& S = *segs[i];
+        for (const NodeP& n : S.nodes)
+          if (n.level == L && n.dst != S.out) bn_bwd_finalize(c, S, ptrs[i], n.dst, fin, app);
+      }
+      int e = fire_finalize(c, fin, app);
+      if (e) return e;
+    }
+    // B + C: weight gradients
+    std::vector<WgradProb> wg_vec, wg_gen;
+    std::vector<ReduceProb> red;
+    size_t woff = 0;
+    for (size_t i = 0; i < segs.size(); ++i) {
+      const SegP& S = *segs[i];
+      const Ptrs& P = ptrs[i];
+      for (const NodeP& n : S.nodes) {
+        if (n.level != L || n.op != PNN_OP_CONV) continue;
+        WgradProb p;
+        std::memset(&p, 0, sizeof(p));
+        p.g = grad_ptr(c, S, P, n.dst);
+        p.in = slot_ptr(c, S, P, n.src);
+        p.pro = n.bn >= 0 ? stats_ptr(c, S, n.bn) + 2 * S.bns[n.bn].C : nullptr;
+        p.B = B; p.H = n.H; p.W = n.W; p.Cg = n.cin; p.P = n.Ho; p.Q = n.Wo; p.Co = n.cout;
+        p.k = n.k; p.stride = n.stride; p.pad = n.pad;
+        p.M = B * n.Ho * n.Wo;
+        p.K = n.k * n.k * n.cin;
+        WgradGeom g = wgrad_geom(p.Co, p.K, p.M);
+        p.wr = g.wr; p.tiles_co = g.tiles_co; p.tiles_k = g.tiles_k; p.splits = g.splits; p.mchunk = g.mchunk;
+        p.part = (float*)(wpart + woff);
+        woff = align256(woff + (size_t)g.splits * p.Co * p.K * 4);
+        (n.cin % (16 / es) == 0 ? wg_vec : wg_gen).push_back(p);
+        ReduceProb r;
+        r.part = p.part;
+        r.dst = (float*)(cp(P.grads) + n.gw_off);
+        r.n = (long)p.Co * p.K;
+        r.splits = g.splits;
+        red.push_back(r);
+      }
+    }
+    for (int v = 0; v < 2; ++v) {
+      auto& list = v == 0 ? wg_vec : wg_gen;
+      int e = grouped<WgradLaunch>(
+          list, [](const WgradProb& p) { return p.tiles_co * p.tiles_k * p.splits; },
+          [&](const WgradLaunch& Lx, int tiles, size_t) {
+            double fl = 0, by = 0;
+            for (int i = 0; i < Lx.n; ++i) {
+              const WgradProb& p = Lx.p[i];
+              fl += 2.0 * p.M * (double)p.Co * p.K;
+              by += (double)p.M * p.Co * es + (double)p.B * p.H * p.W * p.Cg * es + (double)p.Co * p.K * 4;
+            }
+            Timer t(plan, 2, c.stream);
+            int e2 = launch_wgrad(Lx, tiles, plan->dtype, v == 0, c.stream);
+            t.done(c.stream, fl, by);
+            return e2;
+          });
+      if (e) return e;
+    }
+    {
+      int e = grouped<ReduceLaunch>(
+          red, [](const ReduceProb& p) { return (int)cdiv(p.n, ELT_TILE); },
+          [&](const ReduceLaunch& Lx, int tiles, size_t) { return launch_reduce(Lx, tiles, c.stream); });
+      if (e) return e;
+    }
+    // D + E: data gradients (first of two BN consumers, then the rest) and bnact backward
+    for (int phase = 0; phase < 2; ++phase) {
+      std::vector<ConvProb> dg;
+      std::vector<BnActProb> ba;
+      for (size_t i = 0; i < segs.size(); ++i) {
+        const SegP& S = *segs[i];
+        const Ptrs& P = ptrs[i];
+        for (const NodeP& n : S.nodes) {
+          if (n.level != L) continue;
+          if (n.op == PNN_OP_BNACT && phase == 1) {
+            const BnP& b = S.bns[n.bn];
+            BnActProb p;
+            std::memset(&p, 0, sizeof(p));
+            p.z = slot_ptr(c, S, P, n.src);
+            p.out = c.scratch + S.scr_base + b.dbn_off;
+            p.g = grad_ptr(c, S, P, n.dst);
+            p.stats = stats_ptr(c, S, n.bn);
+            p.part = part_ptr(c, S, n.bn);
+            p.B = B; p.H = n.H; p.W = n.W; p.C = n.cin; p.pool = n.pool;
+            p.n_out = (long)B * n.Ho * n.Wo;
+            ba.push_back(p);
+            continue;
+          }
+          if (n.op != PNN_OP_CONV || !n.dgrad) continue;
+          if ((phase == 0) != n.first_of_two) continue;
+          ConvProb p = conv_common(plan, n);
+          p.in = grad_ptr(c, S, P, n.dst);
+          p.wmat = c.scratch + S.scr_base + n.wt_off;
+          p.B = B; p.H = n.Ho; p.W = n.Wo; p.Cg = n.cout;
+          p.P = n.H; p.Q = n.W; p.ncol = n.cin;
+          p.M = B * n.H * n.W;
+          p.K = n.k * n.k * n.cout;
+          if (n.bn >= 0) {
+            const BnP& b = S.bns[n.bn];
+            if (n.first_of_two) {
+              p.flags = EPI_STORE_F32;
+              p.out32 = (float*)(c.scratch + S.scr_base + b.datmp_off);
+            } else {
+              p.flags = EPI_BN_MASK;
+              p.out = c.scratch + S.scr_base + b.dbn_off;
+              p.zsrc = slot_ptr(c, S, P, n.src);
+              p.bnst = stats_ptr(c, S, n.bn);
+              p.part = part_ptr(c, S, n.bn);
+              if (b.datmp_off != NONE) {
+                p.flags |= EPI_ACC_IN;
+                p.acc_in = (const float*)(c.scratch + S.scr_base + b.datmp_off);
+              }
+            }
+          } else {
+            p.out = grad_ptr(c, S, P, n.src);
+            p.res = skip_ptr(c, S, P, n.src);
+          }
+          set_tiles(p);
+          dg.push_back(p);
+        }
+      }
+      int e = fire_conv(c, dg, MODE_BWD, true);
+      if (e) return e;
+      e = grouped<BnActLaunch>(
+          ba, [](const BnActProb& p) { return (int)cdiv(p.n_out, BNACT_PIX); },
+          [&](const BnActLaunch& Lx, int tiles, size_t) { return launch_bnact_bwd(Lx, tiles, plan->dtype, c.stream); });
+      if (e) return e;
+    }
+  }
+  // gradient of the segment inputs
+  {
+    std::vector<BnBwdFinProb> fin;
+    std::vector<BnApplyProb> app;
+    for (size_t i = 0; i < segs.size(); ++i) {
+      const SegP& S = *segs[i];
+      if (S.part == 0 || ptrs[i].gin == nullptr) continue;
+      bn_bwd_finalize(c, S, ptrs[i], 0, fin, app);
+    }
+    int e = fire_finalize(c, fin, app);
+    if (e) return e;
+  }
+  return PNN_OK;
+}
+
+bool ok_ctx(pnn_plan* plan, void* saved, void* scratch) {
+  return plan != nullptr && (plan->saved_bytes == 0 || saved != nullptr) &&
+         (plan->scratch_bytes == 0 || scratch != nullptr);
+}
+
+}  // namespace
+
+// ================================================================================================
+// C ABI
+// ================================================================================================
+
+extern "C" {
+
+const char* pnn_status_string(pnn_status s) {
+  switch (s) {
+    case PNN_OK: return "ok";
+    case PNN_ERR_NULL: return "a required pointer is NULL";
+    case PNN_ERR_SHAPE: return "inconsistent shapes or node list";
+    case PNN_ERR_DTYPE: return "unknown storage type";
+    case PNN_ERR_WORKSPACE: return "unknown workspace kind";
+    case PNN_ERR_UNSUPPORTED: return "network form not supported by this library";
+    case PNN_ERR_HIP: return "a HIP call failed";
+    case PNN_ERR_INDEX: return "index out of range";
+    default: return "unknown status";
+  }
+}
+
+pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
+  if (d == nullptr || out == nullptr) return PNN_ERR_NULL;
+  *out = nullptr;
+  if (d->dtype != PNN_F32 && d->dtype != PNN_BF16) return PNN_ERR_DTYPE;
+  if (d->n_sub < 1 || d->batch < 1 || d->n_classes < 1 || d->img_h < 1 || d->img_w < 1 || d->img_c < 1)
+    return PNN_ERR_SHAPE;
+  if (d->pre == nullptr || d->fine == nullptr || (d->n_sub > 1 && d->coarse == nullptr)) return PNN_ERR_NULL;
+  pnn_plan* p = new (std::nothrow) pnn_plan();
+  if (p == nullptr) return PNN_ERR_HIP;
+  p->dtype = d->dtype;
+  p->es = d->dtype == PNN_BF16 ? 2 : 4;
+  p->B = d->batch;
+  p->N = d->n_sub;
+  p->classes = d->n_classes;
+  p->img_h = d->img_h;
+  p->img_w = d->img_w;
+  p->img_c = d->img_c;
+  const int N = d->n_sub;
+  p->pre.resize(N);
+  p->fine.resize(N);
+  p->coarse.resize(N - 1);
+  pnn_status st = PNN_OK;
+  for (int j = 0; j < N && st == PNN_OK; ++j) st = build_segment(d->pre[j], 0, j, p->B, p->es, p->pre[j]);
+  for (int j = 0; j < N && st == PNN_OK; ++j) st = build_segment(d->fine[j], 1, j, p->B, p->es, p->fine[j]);
+  for (int j = 0; j < N - 1 && st == PNN_OK; ++j) st = build_segment(d->coarse[j], 2, j, p->B, p->es, p->coarse[j]);
+  // shapes along the network: C^j -> g^j, g^j -> F^j -> X_{j+1}, r_j = y_j - x_{j+1}
+  for (int j = 0; j < N && st == PNN_OK; ++j) {
+    const SegP &pr = p->pre[j], &fi = p->fine[j];
+    if (pr.in_h != d->img_h || pr.in_w != d->img_w || pr.in_c != d->img_c) st = PNN_ERR_SHAPE;
+    const SlotP& po = pr.slots[pr.out];
+    if (!same_shape(fi, 0, po.H, po.W, po.C)) st = PNN_ERR_SHAPE;
+    if (j + 1 < N) {
+      const SlotP& yo = fi.slots[fi.out];
+      const SegP& cr = p->coarse[j];
+      const SegP& f2 = p->fine[j + 1];
+      const SlotP& y2 = f2.slots[f2.out];
+      if (!same_shape(cr, 0, yo.H, yo.W, yo.C)) st = PNN_ERR_SHAPE;
+      if (!same_shape(cr, cr.out, y2.H, y2.W, y2.C)) st = PNN_ERR_SHAPE;
+      if (!same_shape(f2, 0, yo.H, yo.W, yo.C)) st = PNN_ERR_SHAPE;   // x_{j+1} in X_j
+      if (cr.nodes.empty()) st = PNN_ERR_UNSUPPORTED;
+    }
+  }
+  if (st != PNN_OK) {
+    delete p;
+    return st;
+  }
+  // workspace layout: saved = [pre | fine | coarse]; scratch = [shared | per segment]
+  size_t sv = 0;
+  for (auto* v : {&p->pre, &p->fine, &p->coarse})
+    for (auto& s : *v) {
+      s.saved_base = sv;
+      sv = align256(sv + s.saved_bytes);
+    }
+  p->saved_bytes = sv;
+  size_t wp = wgrad_level_bytes(p->fine, p->B);
+  wp = std::max(wp, wgrad_level_bytes(p->pre, p->B));
+  for (auto& s : p->coarse) wp = std::max(wp, wgrad_level_bytes(std::vector<SegP>{s}, p->B));
+  size_t sc = 0;
+  p->wpart_off = sc;
+  p->wpart_bytes = wp;
+  sc = align256(sc + wp);
+  const SlotP& yo = p->fine[N - 1].slots[p->fine[N - 1].out];
+  p->head_off = sc;
+  p->head_bytes = (size_t)p->B * (yo.C + p->classes + 1) * 4;
+  sc = align256(sc + p->head_bytes);
+  long sqt = 0;
+  for (int j = 0; j + 1 < N; ++j) sqt += cdiv(p->fine[j].slots[p->fine[j].out].elems, ELT_TILE);
+  p->sq_off = sc;
+  p->sq_bytes = (size_t)sqt * 4;
+  sc = align256(sc + p->sq_bytes);
+  for (auto* v : {&p->pre, &p->fine, &p->coarse})
+    for (auto& s : *v) {
+      s.scr_base = sc;
+      sc = align256(sc + s.scr_bytes);
+    }
+  p->scratch_bytes = sc;
+  *out = p;
+  return PNN_OK;
+}
+
+void pnn_plan_destroy(pnn_plan* plan) {
+  if (plan == nullptr) return;
+  for (auto e : plan->ev) hipEventDestroy(e);
+  delete plan;
+}
+
+pnn_status pnn_workspace_size(const pnn_plan* plan, int kind, size_t* bytes) {
+  if (plan == nullptr || bytes == nullptr) return PNN_ERR_NULL;
+  if (kind == PNN_WS_SAVED) *bytes = plan->saved_bytes;
+  else if (kind == PNN_WS_SCRATCH) *bytes = plan->scratch_bytes;
+  else return PNN_ERR_WORKSPACE;
+  return PNN_OK;
+}
+
+pnn_status pnn_param_layout(const pnn_plan* plan, int part, int j, int grad, size_t* offsets, size_t* total) {
+  if (plan == nullptr || total == nullptr) return PNN_ERR_NULL;
+  const std::vector<SegP>* v = part == 0 ? &plan->pre : part == 1 ? &plan->fine : part == 2 ? &plan->coarse : nullptr;
+  if (v == nullptr || j < 0 || j >= (int)v->size()) return PNN_ERR_INDEX;
+  const SegP& S = (*v)[j];
+  *total = grad ? S.grad_bytes : S.param_bytes;
+  if (offsets) {
+    const size_t nn = S.nodes.size();
+    for (size_t i = 0; i < nn; ++i) offsets[i] = grad ? S.nodes[i].gw_off : S.nodes[i].w_off;
+    for (size_t b = 0; b < S.bns.size(); ++b) {
+      const size_t o = grad ? S.bns[b].gp_off : S.bns[b].p_off;
+      offsets[nn + 2 * b] = o;
+      offsets[nn + 2 * b + 1] = o + (size_t)S.bns[b].C * 4;
+    }
+  }
+  return PNN_OK;
+}
+
+pnn_status pnn_tensor_shape(const pnn_plan* plan, int which, int j, int* h, int* w, int* c) {
+  if (plan == nullptr || h == nullptr || w == nullptr || c == nullptr) return PNN_ERR_NULL;
+  if (j < 0 || j >= plan->N || which < 0 || which > 1) return PNN_ERR_INDEX;
+  const SegP& S = plan->fine[j];
+  const SlotP& s = S.slots[which == 0 ? 0 : S.out];
+  *h = s.H;
+  *w = s.W;
+  *c = s.C;
+  return PNN_OK;
+}
+
+pnn_status pnn_pre_fwd(pnn_plan* plan, const void* image, void* const* x, const void* const* delta,
+                       void* saved, void* scratch, void* stream) {
+  if (!ok_ctx(plan, saved, scratch) || image == nullptr || x == nullptr) return PNN_ERR_NULL;
+  Ctx c{plan, (char*)saved, (char*)scratch, (hipStream_t)stream};
+  std::vector<const SegP*> segs;
+  std::vector<Ptrs> ptrs;
+  for (int j = 0; j < plan->N; ++j) {
+    const SegP& S = plan->pre[j];
+    if (x[j] == nullptr) return PNN_ERR_NULL;
+    if (S.param_bytes > 0 && (delta == nullptr || delta[j] == nullptr)) return PNN_ERR_NULL;
+    Ptrs p;
+    p.in = image;
+    p.out = x[j];
+    p.params = delta ? delta[j] : nullptr;
+    segs.push_back(&S);
+    ptrs.push_back(p);
+  }
+  return run_fwd(c, segs, ptrs);
+}
+
+pnn_status parareal_fine_fwd(pnn_plan* plan, const void* const* x, const void* const* phi, void* const* y,
+                             void* saved, void* scratch, void* stream) {
+  if (!ok_ctx(plan, saved, scratch) || x == nullptr || phi == nullptr || y == nullptr) return PNN_ERR_NULL;
+  Ctx c{plan, (char*)saved, (char*)scratch, (hipStream_t)stream};
+  std::vector<const SegP*> segs;
+  std::vector<Ptrs> ptrs;
+  for (int j = 0; j < plan->N; ++j) {
+    if (x[j] == nullptr || phi[j] == nullptr || y[j] == nullptr) return PNN_ERR_NULL;
+    Ptrs p;
+    p.in = x[j];
+    p.out = y[j];
+    p.params = phi[j];
+    segs.push_back(&plan->fine[j]);
+    ptrs.push_back(p);
+  }
+  return run_fwd(c, segs, ptrs);
+}
+
+pnn_status parareal_combine_fwd(pnn_plan* plan, const void* const* y, const void* const* x, void* const* r,
+                                float* rnorm2, void* scratch, void* stream) {
+  if (plan == nullptr) return PNN_ERR_NULL;
+  if (plan->N == 1) return PNN_OK;
+  if (y == nullptr || x == nullptr || r == nullptr) return PNN_ERR_NULL;
+  if (rnorm2 != nullptr && scratch == nullptr) return PNN_ERR_NULL;
+  hipStream_t s = (hipStream_t)stream;
+  std::vector<AxpyProb> pr;
+  float* sq = rnorm2 ? (float*)((char*)scratch + plan->sq_off) : nullptr;
+  long off = 0;
+  for (int j = 0; j + 1 < plan->N; ++j) {
+    if (y[j] == nullptr || x[j + 1] == nullptr || r[j] == nullptr) return PNN_ERR_NULL;
+    AxpyProb p;
+    p.a = y[j];
+    p.b = x[j + 1];
+    p.out = r[j];
+    p.n = plan->fine[j].slots[plan->fine[j].out].elems;
+    p.sq_part = sq ? sq + off : nullptr;
+    off += cdiv(p.n, ELT_TILE);
+    pr.push_back(p);
+  }
+  int e = grouped<AxpyLaunch>(
+      pr, [](const AxpyProb& p) { return (int)cdiv(p.n, ELT_TILE); },
+      [&](const AxpyLaunch& L, int tiles, size_t) { return launch_sub(L, tiles, plan->dtype, s); });
+  if (e) return e;
+  if (sq) {
+    off = 0;
+    for (int j = 0; j + 1 < plan->N; ++j) {
+      const int t = (int)cdiv(pr[j].n, ELT_TILE);
+      if (launch_sumsq(sq + off, t, rnorm2 + j, s)) return PNN_ERR_HIP;
+      off += t;
+    }
+  }
+  return PNN_OK;
+}
+
+pnn_status coarse_fwd(pnn_plan* plan, int j, const void* rt_j, const void* eta_j, const void* add,
+                      void* rt_next, void* saved, void* scratch, void* stream) {
+  if (!ok_ctx(plan, saved, scratch)) return PNN_ERR_NULL;
+  if (j < 0 || j >= plan->N - 1) return PNN_ERR_INDEX;
+  if (rt_j == nullptr || eta_j == nullptr || add == nullptr || rt_next == nullptr) return PNN_ERR_NULL;
+  if (rt_j == rt_next) return PNN_ERR_SHAPE;
+  Ctx c{plan, (char*)saved, (char*)scratch, (hipStream_t)stream};
+  Ptrs p;
+  p.in = rt_j;
+  p.out = rt_next;
+  p.params = eta_j;
+  p.ext = add;
+  return run_fwd(c, {&plan->coarse[j]}, {p});
+}
+
+pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps, const int32_t* labels,
+                            float* logits, float* loss, void* D_N, float* deps, void* scratch, void* stream) {
+  if (plan == nullptr || ytilde == nullptr || eps == nullptr || labels == nullptr || loss == nullptr ||
+      D_N == nullptr || deps == nullptr || scratch == nullptr)
+    return PNN_ERR_NULL;
+  const SegP& S = plan->fine[plan->N - 1];
+  const SlotP& yo = S.slots[S.out];
+  if (plan->classes > 4096 || yo.C > 8192) return PNN_ERR_UNSUPPORTED;
+  int e = launch_head(ytilde, eps, labels, logits, loss, D_N, deps,
+                      (float*)((char*)scratch + plan->head_off), plan->B, yo.H * yo.W, yo.C,
+                      plan->classes, plan->dtype, (hipStream_t)stream);
+  return e ? PNN_ERR_HIP : PNN_OK;
+}
+
+pnn_status coarse_bwd(pnn_plan* plan, int j, const void* D_next, const void* rt_j, const void* eta_j,
+                      const void* saved, void* D_j, float* deta_j, void* scratch, void* stream) {
+  if (!ok_ctx(plan, const_cast<void*>(saved), scratch)) return PNN_ERR_NULL;
+  if (j < 0 || j >= plan->N - 1) return PNN_ERR_INDEX;
+  if (D_next == nullptr || rt_j == nullptr || eta_j == nullptr || D_j == nullptr || deta_j == nullptr)
+    return PNN_ERR_NULL;
+  if (D_j == D_next) return PNN_ERR_SHAPE;
+  Ctx c{plan, (char*)const_cast<void*>(saved), (char*)scratch, (hipStream_t)stream};
+  Ptrs p;
+  p.in = rt_j;
+  p.params = eta_j;
+  p.grads = deta_j;
+  p.gout = D_next;
+  p.gin = D_j;
+  return run_bwd(c, {&plan->coarse[j]}, {p});
+}
+
+pnn_status parareal_fine_bwd(pnn_plan* plan, const void* const* dy, const void* const* x,
+                             const void* const* phi, const void* saved, void* const* dx, float* const* dphi,
+                             void* scratch, void* stream) {
+  if (!ok_ctx(plan, const_cast<void*>(saved), scratch)) return PNN_ERR_NULL;
+  if (dy == nullptr || x == nullptr || phi == nullptr || dx == nullptr || dphi == nullptr) return PNN_ERR_NULL;
+  Ctx c{plan, (char*)const_cast<void*>(saved), (char*)scratch, (hipStream_t)stream};
+  std::vector<const SegP*> segs;
+  std::vector<Ptrs> ptrs;
+  for (int j = 0; j < plan->N; ++j) {
+    if (dy[j] == nullptr || x[j] == nullptr || phi[j] == nullptr || dx[j] == nullptr || dphi[j] == nullptr)
+      return PNN_ERR_NULL;
+    Ptrs p;
+    p.in = x[j];
+    p.params = phi[j];
+    p.grads = dphi[j];
+    p.gout = dy[j];
+    p.gin = dx[j];
+    segs.push_back(&plan->fine[j]);
+    ptrs.push_back(p);
+  }
+  return run_bwd(c, segs, ptrs);
+}
+
+pnn_status parareal_combine_bwd(pnn_plan* plan, void* const* dx, const void* const* D, void* stream) {
+  if (plan == nullptr) return PNN_ERR_NULL;
+  if (plan->N == 1) return PNN_OK;
+  if (dx == nullptr || D == nullptr) return PNN_ERR_NULL;
+  std::vector<AxpyProb> pr;
+  for (int j = 1; j < plan->N; ++j) {
+    if (dx[j] == nullptr || D[j - 1] == nullptr) return PNN_ERR_NULL;
+    AxpyProb p;
+    p.a = dx[j];
+    p.b = D[j - 1];
+    p.out = dx[j];
+    p.sq_part = nullptr;
+    p.n = plan->fine[j].slots[0].elems;
+    pr.push_back(p);
+  }
+  hipStream_t s = (hipStream_t)stream;
+  return grouped<AxpyLaunch>(
+      pr, [](const AxpyProb& p) { return (int)cdiv(p.n, ELT_TILE); },
+      [&](const AxpyLaunch& L, int tiles, size_t) { return launch_sub(L, tiles, plan->dtype, s); });
+}
+
+pnn_status pnn_pre_bwd(pnn_plan* plan, const void* image, const void* const* g, const void* const* delta,
+                       const void* saved, float* const* ddelta, void* scratch, void* stream) {
+  if (!ok_ctx(plan, const_cast<void*>(saved), scratch) || image == nullptr || g == nullptr) return PNN_ERR_NULL;
+  Ctx c{plan, (char*)const_cast<void*>(saved), (char*)scratch, (hipStream_t)stream};
+  std::vector<const SegP*> segs;
+  std::vector<Ptrs> ptrs;
+  for (int j = 0; j < plan->N; ++j) {
+    const SegP& S = plan->pre[j];
+    if (S.grad_bytes == 0 || ddelta == nullptr || ddelta[j] == nullptr) continue;
+    if (g[j] == nullptr || delta == nullptr || delta[j] == nullptr) return PNN_ERR_NULL;
+    Ptrs p;
+    p.in = image;
+    p.params = delta[j];
+    p.grads = ddelta[j];
+    p.gout = g[j];
+    p.gin = nullptr;
+    segs.push_back(&S);
+    ptrs.push_back(p);
+  }
+  if (segs.empty()) return PNN_OK;
+  return run_bwd(c, segs, ptrs);
+}
+
+pnn_status pnn_timing_enable(pnn_plan* plan, int family) {
+  if (plan == nullptr) return PNN_ERR_NULL;
+  if (family < 0 || family > 2) return PNN_ERR_INDEX;
+  plan->timing_family = family;
+  if (family != 0 && plan->ev.empty()) {
+    plan->ev.resize(16384);
+    for (auto& e : plan->ev)
+      if (hipEventCreate(&e) != hipSuccess) return PNN_ERR_HIP;
+  }
+  plan->ev_used = 0;
+  plan->t_flops = plan->t_bytes = 0.0;
+  plan->t_launches = 0;
+  return PNN_OK;
+}
+
+pnn_status pnn_timing_read(pnn_plan* plan, double* ms, long long* launches, double* flops, double* bytes) {
+  if (plan == nullptr || ms == nullptr) return PNN_ERR_NULL;
+  double tot = 0.0;
+  for (size_t i = 0; i + 1 < plan->ev_used; i += 2) {
+    if (hipEventSynchronize(plan->ev[i + 1]) != hipSuccess) return PNN_ERR_HIP;
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, plan->ev[i], plan->ev[i + 1]) != hipSuccess) return PNN_ERR_HIP;
+    tot += t;
+  }
+  *ms = tot;
+  if (launches) *launches = plan->t_launches;
+  if (flops) *flops = plan->t_flops;
+  if (bytes) *bytes = plan->t_bytes;
+  plan->ev_used = 0;
+  plan->t_flops = plan->t_bytes = 0.0;
+  plan->t_launches = 0;
+  return PNN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,225 @@
+// Internal declarations of libpnn: grouped-launch problem descriptors shared by the host plan
+// code and the gfx950 kernels, plus the launchers.
+//
+// A grouped launch carries up to PNN_MAXG independent problems by value in its kernel
+// arguments (the N fine sub-networks of one depth level are the groups of one launch).  Every
+// problem owns a contiguous range [tile_begin, tile_begin + tiles) of the launch's workgroups.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#define PNN_MAXG 20
+#define PNN_BN_EPS 1e-5f
+
+namespace pnn {
+
+enum { MODE_FWD = 0, MODE_BWD = 1 };
+
+// conv epilogue flags
+enum {
+  EPI_STATS = 1,      // FWD: per-column sum / sum of squares of the stored output -> part
+  EPI_BN_MASK = 2,    // BWD: dbn = v * [ReLU(BN(z)) > 0] stored, sums of dbn and dbn * xhat -> part
+  EPI_STORE_F32 = 4,  // BWD: v stored as float to out32 (first of two consumers of one BN)
+  EPI_ACC_IN = 8,     // BWD: v += acc_in before the epilogue
+};
+
+// Implicit-GEMM convolution problem.  FWD: out[m][n] = sum_k A[m][k] wmat[n][k] with
+// A[m][(r,s,c)] = act(in)[pixel(m) + tap(r,s)][c].  BWD (data gradient): the same with the
+// transposed-convolution gather: A = output gradient, wmat = filter transposed to [c_in][r][s][c_out].
+struct ConvProb {
+  const void* in;       // gathered tensor [B][H][W][Cg] (storage type)
+  const void* wmat;     // [ncol][K], K contiguous (storage type)
+  void* out;            // [M][ncol] storage type
+  const void* res;      // addend [M][ncol] (nullable); BWD: the skip gradient
+  const void* ext;      // second addend [M][ncol] (nullable)
+  const float* pro;     // FWD prologue scale[Cg], shift[Cg]: A = ReLU(x * scale + shift) (nullable)
+  float* part;          // per-tile column partial sums [tiles_m][2][ncol]
+  const void* zsrc;     // BWD + EPI_BN_MASK: BN input z [M][ncol]
+  const float* bnst;    // BWD + EPI_BN_MASK: mean, invstd, scale, shift [4][ncol]
+  const float* acc_in;  // EPI_ACC_IN: [M][ncol] float
+  float* out32;         // EPI_STORE_F32: [M][ncol] float
+  int B, H, W, Cg;      // gathered tensor
+  int P, Q;             // output pixel grid (M = B * P * Q)
+  int ncol;
+  int k, stride, pad;   // forward convolution geometry (BWD gathers through its transpose)
+  int M, K;
+  int tiles_m, tiles_n, wn;
+  int flags;
+  int tile_begin;
+};
+struct ConvLaunch {
+  int n;
+  ConvProb p[PNN_MAXG];
+};
+
+// Weight gradient: part[split][co][kk] = sum over the split's rows m of g[m][co] * A[m][kk].
+struct WgradProb {
+  const void* g;        // [M][Co]
+  const void* in;       // [B][H][W][Cg]
+  const float* pro;     // prologue scale / shift (nullable)
+  float* part;          // [splits][Co][K] float
+  int B, H, W, Cg, P, Q, Co, k, stride, pad, M, K;
+  int wr;               // tile = (16 wr) output channels x (256 / wr) filter columns
+  int tiles_co, tiles_k, splits, mchunk;
+  int tile_begin;
+};
+struct WgradLaunch {
+  int n;
+  WgradProb p[PNN_MAXG];
+};
+
+// Sum of split partials: dst[i] = sum_s part[s * n + i] (float).
+struct ReduceProb {
+  const float* part;
+  float* dst;
+  long n;
+  int splits;
+  int tile_begin;
+};
+struct ReduceLaunch {
+  int n;
+  ReduceProb p[PNN_MAXG];
+};
+
+// Forward BN statistics: per-channel batch mean / variance from tile partials.
+struct BnFinProb {
+  const float* part;    // [ntiles][2][C]
+  const float* gamma;
+  const float* beta;
+  float* stats;         // mean, invstd, scale, shift [4][C]
+  int ntiles, C;
+  long count;
+  int tile_begin;
+};
+// Backward BN reductions: dbeta = sum dbn, dgamma = sum dbn * xhat; coefficients of the apply.
+struct BnBwdFinProb {
+  const float* part;    // [ntiles][2][C]
+  const float* gamma;
+  const float* stats;
+  float* dgamma;
+  float* dbeta;
+  float* coef;          // c1 = gamma * invstd, mb = dbeta / M, mbx = dgamma / M  [3][C]
+  int ntiles, C;
+  long count;
+  int tile_begin;
+};
+struct FinLaunch {
+  int n;
+  union {
+    BnFinProb f[PNN_MAXG];
+    BnBwdFinProb b[PNN_MAXG];
+  };
+};
+
+// Column statistics of a stored tensor [M][C] (BN of a segment input).
+struct ColStatProb {
+  const void* x;
+  float* part;          // [tiles][2][C]
+  long M;
+  int C;
+  int tile_begin;
+};
+struct ColStatLaunch {
+  int n;
+  ColStatProb p[PNN_MAXG];
+};
+
+// out = skip + c1 * (dbn - mb - xhat * mbx), xhat = (z - mean) * invstd  (BN backward apply).
+struct BnApplyProb {
+  const void* dbn;
+  const void* z;
+  const void* skip;     // nullable
+  void* out;
+  const float* stats;
+  const float* coef;
+  long n;
+  int C;
+  int tile_begin;
+};
+struct BnApplyLaunch {
+  int n;
+  BnApplyProb p[PNN_MAXG];
+};
+
+// bnact: out = pool(ReLU(z * scale + shift)) [+ res] [+ ext]  (pool 0 or 2x2/2)
+// bnact backward: dbn[z] = [y > 0] * (routed g), with per-tile sums of dbn and dbn * xhat.
+struct BnActProb {
+  const void* z;
+  void* out;            // FWD: pooled output; BWD: dbn (z shaped)
+  const void* res;      // FWD addend (nullable)
+  const void* ext;      // FWD addend (nullable)
+  const void* g;        // BWD: gradient of the output
+  const float* stats;
+  float* part;          // BWD: [tiles][2][C]
+  int B, H, W, C, pool;
+  long n_out;           // output pixels (B * Ho * Wo)
+  int tile_begin;
+};
+struct BnActLaunch {
+  int n;
+  BnActProb p[PNN_MAXG];
+};
+
+// Elementwise / small kernels.
+struct MaxPool3Prob {
+  const void* x;
+  void* y;
+  int B, H, W, C, Ho, Wo;
+  int tile_begin;
+};
+struct MaxPool3Launch {
+  int n;
+  MaxPool3Prob p[PNN_MAXG];
+};
+
+struct TransposeProb {   // wt[c][r][s][o] = w[o][r][s][c]
+  const void* w;
+  void* wt;
+  int O, T, C;           // T = k * k taps
+  int tile_begin;
+};
+struct TransposeLaunch {
+  int n;
+  TransposeProb p[PNN_MAXG];
+};
+
+struct AxpyProb {        // out = a - b (rounded to storage); partial sum of squares (nullable)
+  const void* a;
+  const void* b;
+  void* out;
+  float* sq_part;        // [tiles]
+  long n;
+  int tile_begin;
+};
+struct AxpyLaunch {
+  int n;
+  AxpyProb p[PNN_MAXG];
+};
+
+int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, bool vec, hipStream_t s);
+int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s);
+int launch_reduce(const ReduceLaunch& L, int tiles, hipStream_t s);
+int launch_bn_fin_fwd(const FinLaunch& L, int tiles, hipStream_t s);
+int launch_bn_fin_bwd(const FinLaunch& L, int tiles, hipStream_t s);
+int launch_colstat(const ColStatLaunch& L, int tiles, int dtype, hipStream_t s);
+int launch_bn_apply(const BnApplyLaunch& L, int tiles, int dtype, hipStream_t s);
+int launch_bnact_fwd(const BnActLaunch& L, int tiles, int dtype, hipStream_t s);
+int launch_bnact_bwd(const BnActLaunch& L, int tiles, int dtype, hipStream_t s);
+int launch_maxpool3(const MaxPool3Launch& L, int tiles, int dtype, hipStream_t s);
+int launch_transpose(const TransposeLaunch& L, int tiles, int dtype, hipStream_t s);
+int launch_sub(const AxpyLaunch& L, int tiles, int dtype, hipStream_t s);
+int launch_sumsq(const float* part, int n, float* out, hipStream_t s);
+int launch_head(const void* yt, const float* eps, const int32_t* labels, float* logits,
+                float* loss, void* D_N, float* deps, float* scratch, int B, int HW, int C,
+                int K, int dtype, hipStream_t s);
+
+// tile sizes shared by host and device code
+constexpr int CONV_BM = 128;       // rows of M per conv workgroup
+constexpr int ELT_TILE = 2048;     // elements per workgroup of elementwise kernels
+constexpr int COLSTAT_ROWS = 128;  // rows per column-statistics workgroup
+constexpr int BNACT_PIX = 32;      // output pixels per bnact workgroup
+constexpr int WGRAD_KC = 32;       // rows of m per wgrad LDS stage
+
+}  // namespace pnn

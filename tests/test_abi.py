@@ -1,0 +1,85 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports every entry point that
+include/pnn.h declares, builds plans for the five workloads, lays out parameters consistently with
+the network descriptions, and rejects bad input with the documented status codes."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import pnn_synth as S
+from oracle.net import param_count
+
+B = pytest.importorskip("paper_2103_08802_amd.binding")
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "pnn.h")
+
+
+def _lib_or_skip():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.skip("libpnn.so not built")
+    return B.lib()
+
+
+def test_header_declarations_are_exported():
+    L = _lib_or_skip()
+    text = open(HEADER).read()
+    declared = set(re.findall(r"^\s*(?:pnn_status|void|const char\*)\s+(\w+)\s*\(", text, re.M))
+    assert declared == set(B.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+@pytest.mark.parametrize("idx", range(5))
+def test_plans_and_layouts(idx):
+    _lib_or_skip()
+    net = S.config(idx, 2)
+    p = B.Plan(net)
+    assert p.workspace_size(B.PNN_WS_SAVED) >= 0
+    assert p.workspace_size(B.PNN_WS_SCRATCH) > 0
+    pc = param_count(net)
+    es = 2 if net.dtype == "bf16" else 4
+    for part, segs, counts in ((0, net.pre, pc["pre"]), (1, net.fine, pc["fine"]), (2, net.coarse, pc["coarse"])):
+        for j, seg in enumerate(segs):
+            offs, tot = p.param_layout(part, j, 0)
+            goffs, gtot = p.param_layout(part, j, 1)
+            n_conv = sum(1 for n in seg.nodes if n.op == "conv")
+            bn_params = sum(2 * S.segment_shapes(seg)[s][2] for s in seg.bns)
+            conv_params = counts[j] - bn_params
+            assert tot >= conv_params * es + bn_params * 4
+            assert gtot >= (conv_params + bn_params) * 4
+            assert all(o % 256 == 0 for o, n in zip(offs, seg.nodes) if n.op == "conv")
+            assert len([o for o, n in zip(offs, seg.nodes) if n.op == "conv"]) == n_conv
+    for j in range(net.n_sub):
+        sh = S.segment_shapes(net.fine[j])
+        assert p.tensor_shape(0, j) == sh[0]
+        assert p.tensor_shape(1, j) == sh[net.fine[j].out]
+    p.close()
+
+
+def test_error_codes():
+    L = _lib_or_skip()
+    h = ctypes.c_void_p()
+    assert L.pnn_plan_create(None, ctypes.byref(h)) == -1                      # PNN_ERR_NULL
+    net = S.config(0)
+    d = B._DescHolder(net)
+    d.desc.dtype = 7
+    assert L.pnn_plan_create(ctypes.byref(d.desc), ctypes.byref(h)) == -3      # PNN_ERR_DTYPE
+    d = B._DescHolder(net)
+    d.desc.fine[1].in_c = 8                                                    # X_1 mismatch
+    assert L.pnn_plan_create(ctypes.byref(d.desc), ctypes.byref(h)) == -2      # PNN_ERR_SHAPE
+    net2 = S.config(0)
+    net2.fine[0].nodes[0].cout = 24                                            # not a multiple of 16
+    d = B._DescHolder(net2)
+    assert L.pnn_plan_create(ctypes.byref(d.desc), ctypes.byref(h)) in (-2, -5)
+    net3 = S.config(0)
+    net3.fine[0].nodes[1].src = 5                                              # slot not produced yet
+    d = B._DescHolder(net3)
+    assert L.pnn_plan_create(ctypes.byref(d.desc), ctypes.byref(h)) == -2
+    p = B.Plan(S.config(0))
+    v = ctypes.c_size_t()
+    assert L.pnn_workspace_size(p.handle, 9, ctypes.byref(v)) == -4            # PNN_ERR_WORKSPACE
+    assert L.pnn_param_layout(p.handle, 1, 5, 0, None, ctypes.byref(v)) == -7  # PNN_ERR_INDEX
+    assert L.coarse_fwd(p.handle, 3, 1, 1, 1, 2, 1, 1, None) == -7
+    assert L.parareal_fine_fwd(p.handle, None, None, None, 1, 1, None) == -1
+    assert B.pnn_status_string(-5) == "network form not supported by this library"
+    p.close()
