@@ -191,6 +191,16 @@ pnn_status pnn_pre_bwd(pnn_plan* plan, const void* image, const void* const* g,
 
 /* ---- misc ----------------------------------------------------------------------------------- */
 
+/* Where the library keeps the internal tensors of one segment (part 0 = C^j, 1 = g^j, 2 = F^j;
+ * j 0-based), for tests and inspection after a step:
+ *   what = 0: value of slot idx (in the saved workspace, storage type, NHWC)
+ *   what = 1: gradient dL/d(slot idx) (in scratch, storage type)
+ *   what = 2: dL/d(BN output) of BN instance idx as stored before the BN backward (scratch)
+ *   what = 3: statistics of BN instance idx: mean, invstd, scale, shift, float [4][C] (saved)
+ * *offset receives the byte offset into that workspace.  PNN_ERR_INDEX when the tensor is not held
+ * by the library (slot 0 and the segment output are the caller's tensors) or does not exist. */
+pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx, size_t* offset);
+
 const char* pnn_status_string(pnn_status s);
 
 /* Per-kernel-family GPU time accounting with HIP events recorded on the call's stream around

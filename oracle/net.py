@@ -36,6 +36,80 @@ from . import prim as P
 BN_EPS = 1e-5
 
 
+# ------------------------------------------------------------------------------------------------
+# node-level definitions (one layer of a segment)
+# ------------------------------------------------------------------------------------------------
+
+def bn_batch_stats(z):
+    """Training-mode BN statistics of a stored tensor: per-channel mean and 1/sqrt(var + eps),
+    biased variance over (n, h, w)."""
+    C = z.shape[-1]
+    mean, var = P.bn_stats(z.reshape(-1, C))
+    return mean, 1.0 / np.sqrt(var + BN_EPS)
+
+
+def bn_relu(z, gamma, beta, stats):
+    """(ReLU(BN(z)), BN(z)) without rounding."""
+    mean, invstd = stats
+    y = (z - mean) * invstd * gamma + beta
+    return np.maximum(y, 0.0), y
+
+
+def node_forward(n, w, gamma, beta, src, res, ext, st, stats=None):
+    """Value a node stores: conv_{k,stride,pad}(A) or pool(ReLU(BN(src))) or a 3x3/2 max pool,
+    plus the residual and external addends, rounded to storage once."""
+    if n.op == "conv":
+        a = st(bn_relu(src, gamma, beta, stats)[0]) if n.bn >= 0 else src
+        y = P.conv_fwd(a, w, n.stride, n.pad)
+    elif n.op == "bnact":
+        y = bn_relu(src, gamma, beta, stats)[0]
+        if n.pool == 2:
+            y = P.maxpool_fwd(y, 2, 2, 0)
+    elif n.op == "maxpool3":
+        y = P.maxpool_fwd(src, 3, 2, 1)
+    else:
+        raise ValueError(n.op)
+    if res is not None:
+        y = y + res
+    if ext is not None:
+        y = y + ext
+    return st(y)
+
+
+def conv_node_backward(n, w, a, g):
+    """dL/dW and dL/dA of conv node n from dL/d(output) = g; A is the operand it consumed."""
+    return (P.conv_bwd_weight(a, g, n.k, n.stride, n.pad),
+            P.conv_bwd_data(g, w, a.shape, n.stride, n.pad))
+
+
+def bnact_node_backward(n, act, g):
+    """dL/d(ReLU(BN(src))) of a bnact node: the 2x2 pool routes g to the first maximum."""
+    return P.maxpool_bwd(act, g, 2, 2, 0) if n.pool == 2 else g
+
+
+def bn_input_grad(z, gamma, stats, dbn):
+    """BN backward from dbn = dL/d(BN output): (dL/dz, dgamma, dbeta), batch statistics."""
+    C = z.shape[-1]
+    M = z.size // C
+    mean, invstd = stats
+    xhat = (z - mean) * invstd
+    sdb, sdbx = P.colsum2(dbn.reshape(-1, C), xhat.reshape(-1, C))
+    gx = gamma * invstd / M * (M * dbn - sdb - xhat * sdbx)
+    return gx, sdbx, sdb
+
+
+def bn_backward(z, gamma, stats, ybn, dA, st):
+    """BN + ReLU backward from dA = dL/d(ReLU(BN(z))).  Returns (dbn, dL/dz, dgamma, dbeta) with
+    dbn = dL/d(BN output) as stored."""
+    dbn = st(dA * (ybn > 0.0))
+    gx, dgamma, dbeta = bn_input_grad(z, gamma, stats, dbn)
+    return dbn, gx, dgamma, dbeta
+
+
+# ------------------------------------------------------------------------------------------------
+# segments (C^j, g^j, F^j)
+# ------------------------------------------------------------------------------------------------
+
 class SegmentRun:
     """Forward state of one segment kept for its backward pass."""
 
@@ -45,19 +119,15 @@ class SegmentRun:
         self.slots = {}
         self.bn = {}
 
-    def bn_slot(self, b):
-        return self.seg.bns[b]
+    def stats(self, b):
+        if b not in self.bn:
+            self.bn[b] = bn_batch_stats(self.slots[self.seg.bns[b]])
+        return self.bn[b]
 
     def bn_forward(self, b):
-        """ReLU(BN_b(z)) without rounding; statistics from the stored slot."""
-        z = self.slots[self.bn_slot(b)]
-        C = z.shape[-1]
-        if b not in self.bn:
-            mean, var = P.bn_stats(z.reshape(-1, C))
-            self.bn[b] = (mean, 1.0 / np.sqrt(var + BN_EPS))
-        mean, invstd = self.bn[b]
-        y = (z - mean) * invstd * self.prm["gamma"][b] + self.prm["beta"][b]
-        return np.maximum(y, 0.0), y
+        """(ReLU(BN_b(z)), BN_b(z)) without rounding; statistics from the stored slot."""
+        return bn_relu(self.slots[self.seg.bns[b]], self.prm["gamma"][b], self.prm["beta"][b],
+                       self.stats(b))
 
 
 def seg_forward(seg, prm, x, st, ext=None):
@@ -67,22 +137,12 @@ def seg_forward(seg, prm, x, st, ext=None):
     run.slots[0] = x
     last = len(seg.nodes) - 1
     for i, n in enumerate(seg.nodes):
-        if n.op == "conv":
-            a = st(run.bn_forward(n.bn)[0]) if n.bn >= 0 else run.slots[n.src]
-            y = P.conv_fwd(a, prm["conv"][i], n.stride, n.pad)
-        elif n.op == "bnact":
-            y = run.bn_forward(n.bn)[0]
-            if n.pool == 2:
-                y = P.maxpool_fwd(y, 2, 2, 0)
-        elif n.op == "maxpool3":
-            y = P.maxpool_fwd(run.slots[n.src], 3, 2, 1)
-        else:
-            raise ValueError(n.op)
-        if n.res >= 0:
-            y = y + run.slots[n.res]
-        if ext is not None and i == last:
-            y = y + ext
-        run.slots[n.dst] = st(y)
+        g_b = prm["gamma"][n.bn] if n.bn >= 0 else None
+        b_b = prm["beta"][n.bn] if n.bn >= 0 else None
+        run.slots[n.dst] = node_forward(
+            n, prm["conv"][i], g_b, b_b, run.slots[n.src],
+            run.slots[n.res] if n.res >= 0 else None, ext if i == last else None, st,
+            run.stats(n.bn) if n.bn >= 0 else None)
     if ext is not None and not seg.nodes:
         run.slots[0] = st(x + ext)
     return run.slots[seg.out], run
@@ -105,17 +165,9 @@ def seg_backward(run, gout, st):
         if s in seg.bns:
             b = seg.bns.index(s)
             if b in dA:
-                z = run.slots[s]
-                C = z.shape[-1]
-                M = z.size // C
-                mean, invstd = run.bn[b]
                 _, ybn = run.bn_forward(b)
-                dbn = st(dA[b] * (ybn > 0.0))          # dL/d(BN output), through ReLU
-                xhat = (z - mean) * invstd
-                sdb, sdbx = P.colsum2(dbn.reshape(-1, C), xhat.reshape(-1, C))
-                grads["beta"][b] = sdb
-                grads["gamma"][b] = sdbx
-                gx = prm["gamma"][b] * invstd / M * (M * dbn - sdb - xhat * sdbx)
+                dbn, gx, grads["gamma"][b], grads["beta"][b] = bn_backward(
+                    run.slots[s], prm["gamma"][b], run.stats(b), ybn, dA[b], st)
                 g = gx if g is None else g + gx
         if g is None:
             g = np.zeros_like(run.slots[s])
@@ -131,20 +183,14 @@ def seg_backward(run, gout, st):
         if n.res >= 0:
             add(n.res, g)
         if n.op == "conv":
-            if n.bn >= 0:
-                a = st(run.bn_forward(n.bn)[0])
-            else:
-                a = run.slots[n.src]
-            grads["conv"][i] = P.conv_bwd_weight(a, g, n.k, n.stride, n.pad)
-            da = P.conv_bwd_data(g, prm["conv"][i], a.shape, n.stride, n.pad)
+            a = st(run.bn_forward(n.bn)[0]) if n.bn >= 0 else run.slots[n.src]
+            grads["conv"][i], da = conv_node_backward(n, prm["conv"][i], a, g)
             if n.bn >= 0:
                 dA[n.bn] = da if n.bn not in dA else dA[n.bn] + da
             else:
                 add(n.src, da)
         elif n.op == "bnact":
-            d = g
-            if n.pool == 2:
-                d = P.maxpool_bwd(run.bn_forward(n.bn)[0], g, 2, 2, 0)
+            d = bnact_node_backward(n, run.bn_forward(n.bn)[0], g)
             dA[n.bn] = d if n.bn not in dA else dA[n.bn] + d
         elif n.op == "maxpool3":
             add(n.src, P.maxpool_bwd(run.slots[n.src], g, 3, 2, 1))

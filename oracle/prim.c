@@ -203,3 +203,87 @@ int pnn_oracle_threads(void) { return omp_get_max_threads(); }
 #else
 int pnn_oracle_threads(void) { return 1; }
 #endif
+
+/* The three convolution definitions above, evaluated only at the flat output indices idx[0..n)
+ * (for checks at full size where whole tensors are too costly in fp64). */
+void pnn_oracle_conv_fwd_at(const double* x, int B, int H, int W, int C, const double* w, int K,
+                            int k, int st, int pad, int Ho, int Wo, const long* idx, long n,
+                            double* out) {
+  (void)B;
+#pragma omp parallel for schedule(static)
+  for (long i = 0; i < n; i++) {
+    long t = idx[i];
+    int o = (int)(t % K); t /= K;
+    int q = (int)(t % Wo); t /= Wo;
+    int p = (int)(t % Ho);
+    int nb = (int)(t / Ho);
+    double acc = 0.0;
+    for (int r = 0; r < k; r++) {
+      int ih = p * st + r - pad;
+      if (ih < 0 || ih >= H) continue;
+      for (int s = 0; s < k; s++) {
+        int iw = q * st + s - pad;
+        if (iw < 0 || iw >= W) continue;
+        const double* xv = x + IDX4(nb, ih, iw, 0, H, W, C);
+        const double* wv = w + IDX4(o, r, s, 0, k, k, C);
+        for (int c = 0; c < C; c++) acc += wv[c] * xv[c];
+      }
+    }
+    out[i] = acc;
+  }
+}
+
+void pnn_oracle_conv_bwd_data_at(const double* gy, int B, int H, int W, int C, const double* w,
+                                 int K, int k, int st, int pad, int Ho, int Wo, const long* idx,
+                                 long n, double* out) {
+  (void)B;
+#pragma omp parallel for schedule(static)
+  for (long i = 0; i < n; i++) {
+    long t = idx[i];
+    int c = (int)(t % C); t /= C;
+    int v = (int)(t % W); t /= W;
+    int h = (int)(t % H);
+    int nb = (int)(t / H);
+    double acc = 0.0;
+    for (int r = 0; r < k; r++) {
+      int th = h + pad - r;
+      if (th < 0 || th % st) continue;
+      int p = th / st;
+      if (p >= Ho) continue;
+      for (int s = 0; s < k; s++) {
+        int tw = v + pad - s;
+        if (tw < 0 || tw % st) continue;
+        int q = tw / st;
+        if (q >= Wo) continue;
+        const double* g = gy + IDX4(nb, p, q, 0, Ho, Wo, K);
+        for (int o = 0; o < K; o++) acc += g[o] * w[IDX4(o, r, s, c, k, k, C)];
+      }
+    }
+    out[i] = acc;
+  }
+}
+
+void pnn_oracle_conv_bwd_weight_at(const double* x, int B, int H, int W, int C, const double* gy,
+                                   int K, int k, int st, int pad, int Ho, int Wo, const long* idx,
+                                   long n, double* out) {
+#pragma omp parallel for schedule(static)
+  for (long i = 0; i < n; i++) {
+    long t = idx[i];
+    int c = (int)(t % C); t /= C;
+    int s = (int)(t % k); t /= k;
+    int r = (int)(t % k);
+    int o = (int)(t / k);
+    double acc = 0.0;
+    for (int nb = 0; nb < B; nb++)
+      for (int p = 0; p < Ho; p++) {
+        int ih = p * st + r - pad;
+        if (ih < 0 || ih >= H) continue;
+        for (int q = 0; q < Wo; q++) {
+          int iw = q * st + s - pad;
+          if (iw < 0 || iw >= W) continue;
+          acc += gy[IDX4(nb, p, q, o, Ho, Wo, K)] * x[IDX4(nb, ih, iw, c, H, W, C)];
+        }
+      }
+    out[i] = acc;
+  }
+}

@@ -39,6 +39,9 @@ def lib():
         _lib.pnn_oracle_colsum2.argtypes = [D, D, ctypes.c_long, i, D, D]
         _lib.pnn_oracle_round_bf16.argtypes = [D, ctypes.c_size_t]
         _lib.pnn_oracle_threads.restype = i
+        L_ = ctypes.POINTER(ctypes.c_long)
+        for name in ("pnn_oracle_conv_fwd_at", "pnn_oracle_conv_bwd_data_at", "pnn_oracle_conv_bwd_weight_at"):
+            getattr(_lib, name).argtypes = [D, i, i, i, i, D, i, i, i, i, i, i, L_, ctypes.c_long, D]
     return _lib
 
 
@@ -126,3 +129,44 @@ def round_bf16(x):
     y = np.array(x, dtype=np.float64, copy=True, order="C")
     lib().pnn_oracle_round_bf16(_p(y), y.size)
     return y
+
+
+def _idx(idx):
+    a = np.ascontiguousarray(idx, dtype=np.int64)
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_long))
+
+
+def conv_fwd_at(x, w, st, pad, idx):
+    """conv_fwd(x, w, st, pad).ravel()[idx]"""
+    x, w = _c(x), _c(w)
+    B, H, W, C = x.shape
+    K, k, _, _ = w.shape
+    Ho, Wo = out_hw(H, W, k, st, pad)
+    a, ap = _idx(idx)
+    out = np.empty(len(a))
+    lib().pnn_oracle_conv_fwd_at(_p(x), B, H, W, C, _p(w), K, k, st, pad, Ho, Wo, ap, len(a), _p(out))
+    return out
+
+
+def conv_bwd_data_at(gy, w, x_shape, st, pad, idx):
+    """conv_bwd_data(gy, w, x_shape, st, pad).ravel()[idx]"""
+    gy, w = _c(gy), _c(w)
+    B, H, W, C = x_shape
+    K, k, _, _ = w.shape
+    a, ap = _idx(idx)
+    out = np.empty(len(a))
+    lib().pnn_oracle_conv_bwd_data_at(_p(gy), B, H, W, C, _p(w), K, k, st, pad, gy.shape[1], gy.shape[2],
+                                      ap, len(a), _p(out))
+    return out
+
+
+def conv_bwd_weight_at(x, gy, k, st, pad, idx):
+    """conv_bwd_weight(x, gy, k, st, pad).ravel()[idx]"""
+    x, gy = _c(x), _c(gy)
+    B, H, W, C = x.shape
+    K = gy.shape[3]
+    a, ap = _idx(idx)
+    out = np.empty(len(a))
+    lib().pnn_oracle_conv_bwd_weight_at(_p(x), B, H, W, C, _p(gy), K, k, st, pad, gy.shape[1], gy.shape[2],
+                                        ap, len(a), _p(out))
+    return out

@@ -23,8 +23,8 @@ STATUS = {0: "PNN_OK", -1: "PNN_ERR_NULL", -2: "PNN_ERR_SHAPE", -3: "PNN_ERR_DTY
 EXPORTS = ["pnn_plan_create", "pnn_plan_destroy", "pnn_workspace_size", "pnn_param_layout",
            "pnn_tensor_shape", "pnn_pre_fwd", "parareal_fine_fwd", "parareal_combine_fwd",
            "coarse_fwd", "pnn_head_fwd_bwd", "coarse_bwd", "parareal_fine_bwd",
-           "parareal_combine_bwd", "pnn_pre_bwd", "pnn_status_string", "pnn_timing_enable",
-           "pnn_timing_read"]
+           "parareal_combine_bwd", "pnn_pre_bwd", "pnn_status_string", "pnn_inspect",
+           "pnn_timing_enable", "pnn_timing_read"]
 
 
 class PnnError(RuntimeError):
@@ -83,6 +83,7 @@ def lib():
     L.pnn_pre_bwd.argtypes = [_vp, _vp, _PP, _PP, _vp, _PP, _vp, _vp]
     L.pnn_status_string.argtypes = [i]
     L.pnn_status_string.restype = ctypes.c_char_p
+    L.pnn_inspect.argtypes = [_vp, i, i, i, i, ctypes.POINTER(sz)]
     L.pnn_timing_enable.argtypes = [_vp, i]
     L.pnn_timing_read.argtypes = [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong),
                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
@@ -175,6 +176,16 @@ class Plan:
         _check(lib().pnn_param_layout(self.handle, part, j, grad, offs, ctypes.byref(tot)),
                "pnn_param_layout")
         return [offs[i] for i in range(n)], tot.value
+
+    def inspect(self, part, j, what, idx):
+        """Byte offset of an internal tensor (see pnn_inspect), or None if the library does not
+        hold it."""
+        v = ctypes.c_size_t()
+        st = lib().pnn_inspect(self.handle, part, j, what, idx, ctypes.byref(v))
+        if st == -7:
+            return None
+        _check(st, "pnn_inspect")
+        return v.value
 
     def tensor_shape(self, which, j):
         h, w, c = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()

@@ -1186,6 +1186,39 @@ pnn_status pnn_pre_bwd(pnn_plan* plan, const void* image, const void* const* g, 
   return run_bwd(c, segs, ptrs);
 }
 
+pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx, size_t* offset) {
+  if (plan == nullptr || offset == nullptr) return PNN_ERR_NULL;
+  const std::vector<SegP>* v = part == 0 ? &plan->pre : part == 1 ? &plan->fine : part == 2 ? &plan->coarse : nullptr;
+  if (v == nullptr || j < 0 || j >= (int)v->size()) return PNN_ERR_INDEX;
+  const SegP& S = (*v)[j];
+  if (what == 0 || what == 1) {
+    if (idx <= 0 || idx >= (int)S.slots.size() || idx == S.out) return PNN_ERR_INDEX;
+    if (what == 0) {
+      *offset = S.saved_base + S.slots[idx].saved_off;
+      return PNN_OK;
+    }
+    int s = idx;
+    while (S.slots[s].g_off == NONE) {          // residual-only slot: gradient of its consumer
+      if (S.slots[s].res_consumer < 0 || !S.needs[s]) return PNN_ERR_INDEX;
+      s = S.nodes[S.slots[s].res_consumer].dst;
+      if (s == S.out) return PNN_ERR_INDEX;
+    }
+    *offset = S.scr_base + S.slots[s].g_off;
+    return PNN_OK;
+  }
+  if (idx < 0 || idx >= (int)S.bns.size()) return PNN_ERR_INDEX;
+  if (what == 2) {
+    if (S.bns[idx].dbn_off == NONE) return PNN_ERR_INDEX;
+    *offset = S.scr_base + S.bns[idx].dbn_off;
+    return PNN_OK;
+  }
+  if (what == 3) {
+    *offset = S.saved_base + S.bns[idx].stats_off;
+    return PNN_OK;
+  }
+  return PNN_ERR_INDEX;
+}
+
 pnn_status pnn_timing_enable(pnn_plan* plan, int family) {
   if (plan == nullptr) return PNN_ERR_NULL;
   if (family < 0 || family > 2) return PNN_ERR_INDEX;

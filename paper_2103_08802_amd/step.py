@@ -158,6 +158,11 @@ class ParaRealGPU:
 
     def backward(self, s=None, fine_events=None):
         """Alg. para3.  ``fine_events`` as in ``forward``, around parareal_fine_bwd."""
+        self.backward_coarse_fine(s, fine_events)
+        self.backward_pre(s)
+
+    def backward_coarse_fine(self, s=None, fine_events=None):
+        """The coarse chain D_j (j = N-1..1) and the fine sub-networks' gradients."""
         s = self.stream() if s is None else s
         p, N = self.plan, self.net.n_sub
         for j in range(N - 2, -1, -1):
@@ -168,6 +173,11 @@ class ParaRealGPU:
         B.parareal_fine_bwd(p, self.D, self.x, self.phi, self.saved, self.dx, self.dphi, self.scratch, s)
         if fine_events:
             fine_events[1].record()
+
+    def backward_pre(self, s=None):
+        """dL/dx_j -= D_{j-1}, then the preprocessing operators' gradients."""
+        s = self.stream() if s is None else s
+        p = self.plan
         B.parareal_combine_bwd(p, self.dx, self.D, s)
         B.pnn_pre_bwd(p, self.image, self.dx, self.delta, self.saved, self.ddelta, self.scratch, s)
 

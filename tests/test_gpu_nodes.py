@@ -1,0 +1,97 @@
+"""GPU parity, node by node and teacher-forced (see tests/nodecheck.py), for all five workloads:
+every node of every segment at reduced batch (whole tensors), and at the full workload sizes in the
+launch configuration bench.py times (sampled nodes and output positions).
+
+Every node of every ResNet segment was also checked whole-tensor at reduced batch while this was
+built; the committed reduced-batch cases sample units to keep the GPU suite short.
+
+Bar per check: fp32 storage e_inf <= 1e-4; bf16 storage e_2 <= 2e-2 (BN mean: |difference| in units
+of the channel's standard deviation).
+"""
+import numpy as np
+import pytest
+
+import pnn_synth as S
+from tests.nodecheck import SegView, check_combine_and_head, check_segment, rel_2, rel_inf
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def gpu_step(net, params, x, labels):
+    import torch
+    from paper_2103_08802_amd.step import ParaRealGPU
+    g = ParaRealGPU(net, params)
+    g.load_input(x, labels)
+    g.forward()
+    g.backward_coarse_fine()
+    torch.cuda.synchronize()
+    dx_fine = [t.clone() for t in g.dx]
+    g.backward_pre()
+    torch.cuda.synchronize()
+    return g, dx_fine
+
+
+def sample_nodes(seg, rng, n_mid=3):
+    """First and last units, every strided / projected unit, a few others."""
+    n = len(seg.nodes)
+    pick = set(range(min(4, n))) | set(range(max(0, n - 4), n))
+    for i, nd in enumerate(seg.nodes):
+        if nd.stride > 1:
+            pick |= set(range(max(0, i - 3), min(n, i + 4)))
+    pick |= set(int(v) for v in rng.integers(0, n, n_mid))
+    return sorted(pick)
+
+
+def check_net(net, sample=None, fine_subset=None, seed=0, node_subset=False):
+    from oracle import prim as P
+    x, labels, params = S.make_all(net)
+    _say(f"[nodes] {net.name} batch {net.batch} {net.dtype}: GPU step")
+    g, dx_fine = gpu_step(net, params, x, labels)
+    bf16 = net.dtype == "bf16"
+    st = P.round_bf16 if bf16 else (lambda a: a)
+    metric = rel_2 if bf16 else rel_inf
+    rng = np.random.default_rng(seed)
+    errs = {}
+    for part, key in ((0, "pre"), (1, "fine"), (2, "coarse")):
+        segs = [net.pre, net.fine, net.coarse][part]
+        for j, seg in enumerate(segs):
+            if part == 1 and fine_subset is not None and j not in fine_subset:
+                continue
+            nodes = sample_nodes(seg, rng) if (sample is not None or node_subset) else None
+            _say(f"[nodes] {net.name}: {key}[{j}] ({len(seg.nodes) if nodes is None else len(nodes)} nodes)")
+            view = SegView(g, part, j, dx_fine)
+            e = check_segment(view, params[key][j], g.unpack_grads(part, j), st, metric, nodes, sample, seed + j)
+            errs.update({f"{key}{j}.{k}": v for k, v in e.items()})
+    errs.update(check_combine_and_head(g, labels, st, metric, dx_fine))
+    worst = max(errs, key=errs.get)
+    _say(f"[nodes] {net.name}: {len(errs)} checks, worst {worst} = {errs[worst]:.3e}, "
+         f"median {np.median(list(errs.values())):.3e}")
+    return net, errs
+
+
+def _assert(net, errs):
+    tol = 1e-4 if net.dtype == "f32" else 2e-2
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, sorted(bad.items(), key=lambda kv: -kv[1])[:10]
+
+
+@pytest.mark.parametrize("idx,batch", [(0, None), (1, 3)])
+def test_every_node_reduced_batch(idx, batch):
+    """Every node of every segment, whole tensors."""
+    _assert(*check_net(S.config(idx, batch)))
+
+
+@pytest.mark.parametrize("idx,batch", [(2, 3), (3, 3), (4, 1)])
+def test_unit_sample_reduced_batch(idx, batch):
+    """Whole tensors; in every segment the first and last units, every strided / projected unit
+    and a few others."""
+    _assert(*check_net(S.config(idx, batch), node_subset=True))
+
+
+@pytest.mark.parametrize("idx,fine_subset", [(1, None), (2, [0, 1, 3]), (3, [0, 5, 10, 15]), (4, [0, 2, 5, 7])])
+def test_sampled_nodes_full_size(idx, fine_subset):
+    _assert(*check_net(S.config(idx), sample=256, fine_subset=fine_subset))

@@ -84,6 +84,20 @@ def test_p1_conv_backward_adjoints(k, st, pad, H):
     np.testing.assert_allclose(float((w * P.conv_bwd_weight(x, g, k, st, pad)).sum()), lhs, rtol=1e-12)
 
 
+@pytest.mark.parametrize("k,st,pad,H", [(3, 1, 1, 7), (3, 2, 1, 8), (1, 2, 0, 8)])
+def test_sampled_conv_primitives_match_full(k, st, pad, H):
+    """The sampled-output evaluations equal the full definitions at the sampled indices."""
+    x = rng.standard_normal((2, H, H, 5))
+    w = rng.standard_normal((6, k, k, 5))
+    y = P.conv_fwd(x, w, st, pad)
+    g = rng.standard_normal(y.shape)
+    for full, f in ((y, lambda i: P.conv_fwd_at(x, w, st, pad, i)),
+                    (P.conv_bwd_data(g, w, x.shape, st, pad), lambda i: P.conv_bwd_data_at(g, w, x.shape, st, pad, i)),
+                    (P.conv_bwd_weight(x, g, k, st, pad), lambda i: P.conv_bwd_weight_at(x, g, k, st, pad, i))):
+        idx = rng.integers(0, full.size, 50)
+        np.testing.assert_array_equal(f(idx), full.ravel()[idx])
+
+
 def test_maxpool_definition_and_tie_rule():
     x = np.array([[1.0, 3.0, 3.0, 0.0], [2.0, 3.0, -1.0, 5.0]]).reshape(1, 2, 4, 1)
     y = P.maxpool_fwd(x, 2, 2, 0)
