@@ -228,8 +228,8 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
     if (t < 16 * P.wn) {
       const float a = ((red[0][t][0] + red[1][t][0]) + red[2][t][0]) + red[3][t][0];
       const float b = ((red[0][t][1] + red[1][t][1]) + red[2][t][1]) + red[3][t][1];
-      P.part[(long)tm * 2 * P.ncol + n0 + t] = a;
-      P.part[((long)tm * 2 + 1) * P.ncol + n0 + t] = b;
+      float2* pp = (float2*)P.part + (long)tm * P.ncol + n0 + t;
+      *pp = make_float2(a, b);
     }
   }
 }
@@ -370,19 +370,6 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
   }
 }
 
-__global__ __launch_bounds__(256) void reduce_kernel(const ReduceLaunch L) {
-  const int gi = find_group(L);
-  const ReduceProb& P = L.p[gi];
-  const long base = (long)(blockIdx.x - P.tile_begin) * ELT_TILE;
-  for (int t = threadIdx.x; t < ELT_TILE; t += 256) {
-    const long i = base + t;
-    if (i >= P.n) break;
-    float s = 0.f;
-    for (int sp = 0; sp < P.splits; ++sp) s += P.part[(long)sp * P.n + i];
-    P.dst[i] = s;
-  }
-}
-
 // ------------------------------------------------------------------------------------------------
 // launchers
 // ------------------------------------------------------------------------------------------------
@@ -423,9 +410,5 @@ int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream
   return (int)hipGetLastError();
 }
 
-int launch_reduce(const ReduceLaunch& L, int tiles, hipStream_t s) {
-  hipLaunchKernelGGL(reduce_kernel, dim3(tiles), dim3(256), 0, s, L);
-  return (int)hipGetLastError();
-}
 
 }  // namespace pnn

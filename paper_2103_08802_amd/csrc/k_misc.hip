@@ -10,51 +10,71 @@
 namespace pnn {
 
 // ------------------------------------------------------------------------------------------------
-// BN statistics from tile partials: mean, biased variance -> invstd, and the affine map
-// scale = gamma * invstd, shift = beta - mean * scale.  One thread per channel; fp64 sums.
+// Column reduction of tile partials (split-K weight gradients, BN statistics, BN backward sums),
+// fused with the BN finalisation.  A workgroup owns RED_COLS columns; its 8 row lanes sum
+// interleaved rows in fp64 and are combined in a fixed order (deterministic).
 // ------------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void bn_fin_fwd_kernel(const FinLaunch L) {
-  int gi = 0;
-  for (int i = 1; i < L.n; ++i)
-    if (L.f[i].tile_begin <= (int)blockIdx.x) gi = i;
-  const BnFinProb& P = L.f[gi];
-  const int c = (blockIdx.x - P.tile_begin) * 256 + threadIdx.x;
-  if (c >= P.C) return;
-  double s = 0.0, s2 = 0.0;
-  for (int t = 0; t < P.ntiles; ++t) {
-    s += (double)P.part[(long)t * 2 * P.C + c];
-    s2 += (double)P.part[((long)t * 2 + 1) * P.C + c];
+__global__ __launch_bounds__(256) void colred_kernel(const ColRedLaunch L) {
+  __shared__ double red[8][RED_COLS];
+  __shared__ double sum[RED_COLS];
+  const int gi = find_group(L);
+  const ColRedProb& P = L.p[gi];
+  const int c0 = (blockIdx.x - P.tile_begin) * RED_COLS;
+  const int cl = threadIdx.x % RED_COLS;
+  const int rl = threadIdx.x / RED_COLS;
+  const int col = c0 + cl;
+  double acc = 0.0;
+  if (col < P.ncols) {
+    const float* p = P.part + col;
+    int r = rl;
+    double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+    for (; r + 24 < P.rows; r += 32) {
+      a0 += (double)p[(long)r * P.ncols];
+      a1 += (double)p[(long)(r + 8) * P.ncols];
+      a2 += (double)p[(long)(r + 16) * P.ncols];
+      a3 += (double)p[(long)(r + 24) * P.ncols];
+    }
+    for (; r < P.rows; r += 8) a0 += (double)p[(long)r * P.ncols];
+    acc = (a0 + a1) + (a2 + a3);
   }
-  const double mean = s / (double)P.count;
-  double var = s2 / (double)P.count - mean * mean;
-  if (var < 0.0) var = 0.0;
-  const float invstd = (float)(1.0 / sqrt(var + (double)PNN_BN_EPS));
-  const float scale = P.gamma[c] * invstd;
-  P.stats[c] = (float)mean;
-  P.stats[P.C + c] = invstd;
-  P.stats[2 * P.C + c] = scale;
-  P.stats[3 * P.C + c] = P.beta[c] - (float)mean * scale;
-}
-
-// dbeta = sum dbn, dgamma = sum dbn * xhat (eq. of the BN backward), and the apply coefficients.
-__global__ __launch_bounds__(256) void bn_fin_bwd_kernel(const FinLaunch L) {
-  int gi = 0;
-  for (int i = 1; i < L.n; ++i)
-    if (L.b[i].tile_begin <= (int)blockIdx.x) gi = i;
-  const BnBwdFinProb& P = L.b[gi];
-  const int c = (blockIdx.x - P.tile_begin) * 256 + threadIdx.x;
-  if (c >= P.C) return;
-  double s = 0.0, s2 = 0.0;
-  for (int t = 0; t < P.ntiles; ++t) {
-    s += (double)P.part[(long)t * 2 * P.C + c];
-    s2 += (double)P.part[((long)t * 2 + 1) * P.C + c];
+  red[rl][cl] = acc;
+  __syncthreads();
+  double tot = 0.0;
+  if (rl == 0) {
+    tot = red[0][cl];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) tot += red[k][cl];
+    sum[cl] = tot;
   }
-  P.dbeta[c] = (float)s;
-  P.dgamma[c] = (float)s2;
-  const float invstd = P.stats[P.C + c];
-  P.coef[c] = P.gamma[c] * invstd;
-  P.coef[P.C + c] = (float)(s / (double)P.count);
-  P.coef[2 * P.C + c] = (float)(s2 / (double)P.count);
+  __syncthreads();
+  if (rl != 0 || col >= P.ncols) return;
+  if (P.mode == RED_SUM) {
+    P.dst[col] = (float)tot;
+    return;
+  }
+  // BN modes: column 2c holds the first sum of channel c, column 2c+1 the second
+  if (cl & 1) return;
+  const int C = P.ncols / 2;
+  const int c = col / 2;
+  const double s1 = sum[cl], s2 = sum[cl + 1];
+  const double M = (double)P.count;
+  if (P.mode == RED_BN_FWD) {
+    const double mean = s1 / M;
+    double var = s2 / M - mean * mean;
+    if (var < 0.0) var = 0.0;
+    const float invstd = (float)(1.0 / sqrt(var + (double)PNN_BN_EPS));
+    const float scale = P.gamma[c] * invstd;
+    P.stats[c] = (float)mean;
+    P.stats[C + c] = invstd;
+    P.stats[2 * C + c] = scale;
+    P.stats[3 * C + c] = P.beta[c] - (float)mean * scale;
+  } else {
+    P.dbeta[c] = (float)s1;
+    P.dgamma[c] = (float)s2;
+    P.coef[c] = P.gamma[c] * P.stats[C + c];
+    P.coef[C + c] = (float)(s1 / M);
+    P.coef[2 * C + c] = (float)(s2 / M);
+  }
 }
 
 // Column sums / sums of squares of a stored tensor [M][C], COLSTAT_ROWS rows per workgroup.
@@ -72,8 +92,7 @@ __global__ __launch_bounds__(256) void colstat_kernel(const ColStatLaunch L) {
       s += v;
       s2 += v * v;
     }
-    P.part[(long)tile * 2 * P.C + c] = s;
-    P.part[((long)tile * 2 + 1) * P.C + c] = s2;
+    ((float2*)P.part)[(long)tile * P.C + c] = make_float2(s, s2);
   }
 }
 
@@ -171,8 +190,7 @@ __global__ __launch_bounds__(256) void bnact_bwd_kernel(const BnActLaunch L) {
         s2 += dr * ((z - mean) * invstd);
       }
     }
-    P.part[(long)tile * 2 * P.C + c] = s1;
-    P.part[((long)tile * 2 + 1) * P.C + c] = s2;
+    ((float2*)P.part)[(long)tile * P.C + c] = make_float2(s1, s2);
   }
 }
 
@@ -349,12 +367,8 @@ __global__ __launch_bounds__(256) void head_reduce_kernel(const float* scratch, 
     return (int)hipGetLastError();                                                   \
   } while (0)
 
-int launch_bn_fin_fwd(const FinLaunch& L, int tiles, hipStream_t s) {
-  hipLaunchKernelGGL(bn_fin_fwd_kernel, dim3(tiles), dim3(256), 0, s, L);
-  return (int)hipGetLastError();
-}
-int launch_bn_fin_bwd(const FinLaunch& L, int tiles, hipStream_t s) {
-  hipLaunchKernelGGL(bn_fin_bwd_kernel, dim3(tiles), dim3(256), 0, s, L);
+int launch_colred(const ColRedLaunch& L, int tiles, hipStream_t s) {
+  hipLaunchKernelGGL(colred_kernel, dim3(tiles), dim3(256), 0, s, L);
   return (int)hipGetLastError();
 }
 int launch_colstat(const ColStatLaunch& L, int tiles, int dtype, hipStream_t s) {

@@ -431,32 +431,24 @@ int grouped(std::vector<Prob>& probs, TilesOf tiles_of, Fire fire) {
   return PNN_OK;
 }
 
-int fin_launch(std::vector<BnFinProb>& fw, std::vector<BnBwdFinProb>& bw, hipStream_t s) {
-  for (size_t i = 0; i < fw.size(); i += PNN_MAXG) {
-    FinLaunch L;
-    L.n = 0;
-    int tiles = 0;
-    for (size_t k = i; k < fw.size() && L.n < PNN_MAXG; ++k) {
-      L.f[L.n] = fw[k];
-      L.f[L.n].tile_begin = tiles;
-      tiles += (int)cdiv(fw[k].C, 256);
-      L.n++;
-    }
-    if (launch_bn_fin_fwd(L, tiles, s)) return PNN_ERR_HIP;
-  }
-  for (size_t i = 0; i < bw.size(); i += PNN_MAXG) {
-    FinLaunch L;
-    L.n = 0;
-    int tiles = 0;
-    for (size_t k = i; k < bw.size() && L.n < PNN_MAXG; ++k) {
-      L.b[L.n] = bw[k];
-      L.b[L.n].tile_begin = tiles;
-      tiles += (int)cdiv(bw[k].C, 256);
-      L.n++;
-    }
-    if (launch_bn_fin_bwd(L, tiles, s)) return PNN_ERR_HIP;
-  }
-  return PNN_OK;
+int fire_colred(std::vector<ColRedProb>& probs, hipStream_t s) {
+  return grouped<ColRedLaunch>(
+      probs, [](const ColRedProb& p) { return (int)cdiv(p.ncols, RED_COLS); },
+      [&](const ColRedLaunch& L, int tiles, size_t) { return launch_colred(L, tiles, s); });
+}
+
+ColRedProb bn_fwd_red(const float* part, int rows, const float* gamma, float* stats, int C, long count) {
+  ColRedProb r;
+  std::memset(&r, 0, sizeof(r));
+  r.part = part;
+  r.rows = rows;
+  r.ncols = 2 * C;
+  r.mode = RED_BN_FWD;
+  r.gamma = gamma;
+  r.beta = gamma + C;
+  r.stats = stats;
+  r.count = count;
+  return r;
 }
 
 double conv_flops(const ConvProb& p) { return 2.0 * p.M * (double)p.ncol * p.K; }
@@ -525,8 +517,7 @@ int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
   // statistics of BN instances on segment inputs
   {
     std::vector<ColStatProb> cs;
-    std::vector<BnFinProb> fw;
-    std::vector<BnBwdFinProb> none;
+    std::vector<ColRedProb> fw;
     for (size_t i = 0; i < segs.size(); ++i) {
       const SegP& S = *segs[i];
       const SlotP& s0 = S.slots[0];
@@ -538,21 +529,14 @@ int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
       p.M = (long)B * s0.H * s0.W;
       p.C = s0.C;
       cs.push_back(p);
-      BnFinProb f;
-      f.part = p.part;
-      f.gamma = (const float*)(cp(ptrs[i].params) + b.p_off);
-      f.beta = f.gamma + b.C;
-      f.stats = stats_ptr(c, S, s0.bn);
-      f.ntiles = b.fwd_tiles;
-      f.C = b.C;
-      f.count = p.M;
-      fw.push_back(f);
+      fw.push_back(bn_fwd_red(p.part, b.fwd_tiles, (const float*)(cp(ptrs[i].params) + b.p_off),
+                              stats_ptr(c, S, s0.bn), b.C, p.M));
     }
     int e = grouped<ColStatLaunch>(
         cs, [](const ColStatProb& p) { return (int)cdiv(p.M, COLSTAT_ROWS); },
         [&](const ColStatLaunch& L, int tiles, size_t) { return launch_colstat(L, tiles, plan->dtype, c.stream); });
     if (e) return e;
-    if (fin_launch(fw, none, c.stream)) return PNN_ERR_HIP;
+    if (fire_colred(fw, c.stream)) return PNN_ERR_HIP;
   }
   int maxL = 0;
   for (auto* s : segs) maxL = std::max(maxL, s->max_level);
@@ -560,8 +544,7 @@ int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
     std::vector<ConvProb> cv_vec, cv_gen;
     std::vector<BnActProb> ba;
     std::vector<MaxPool3Prob> mp;
-    std::vector<BnFinProb> fw;
-    std::vector<BnBwdFinProb> none;
+    std::vector<ColRedProb> fw;
     for (size_t i = 0; i < segs.size(); ++i) {
       const SegP& S = *segs[i];
       const Ptrs& P = ptrs[i];
@@ -607,15 +590,9 @@ int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
         }
         if (so.bn >= 0) {
           const BnP& b = S.bns[so.bn];
-          BnFinProb f;
-          f.part = part_ptr(c, S, so.bn);
-          f.gamma = (const float*)(cp(P.params) + b.p_off);
-          f.beta = f.gamma + b.C;
-          f.stats = stats_ptr(c, S, so.bn);
-          f.ntiles = (int)cdiv((long)B * so.H * so.W, CONV_BM);
-          f.C = b.C;
-          f.count = (long)B * so.H * so.W;
-          fw.push_back(f);
+          const long cnt = (long)B * so.H * so.W;
+          fw.push_back(bn_fwd_red(part_ptr(c, S, so.bn), (int)cdiv(cnt, CONV_BM),
+                                  (const float*)(cp(P.params) + b.p_off), stats_ptr(c, S, so.bn), b.C, cnt));
         }
       }
     }
@@ -630,7 +607,7 @@ int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
         mp, [](const MaxPool3Prob& p) { return (int)cdiv((long)p.B * p.Ho * p.Wo * p.C, ELT_TILE); },
         [&](const MaxPool3Launch& Lx, int tiles, size_t) { return launch_maxpool3(Lx, tiles, plan->dtype, c.stream); });
     if (e) return e;
-    if (fin_launch(fw, none, c.stream)) return PNN_ERR_HIP;
+    if (fire_colred(fw, c.stream)) return PNN_ERR_HIP;
   }
   return PNN_OK;
 }
@@ -638,20 +615,22 @@ int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
 // ------------------------------------------------------------------------------------------------
 // backward of a set of segments
 // ------------------------------------------------------------------------------------------------
-void bn_bwd_finalize(const Ctx& c, const SegP& S, const Ptrs& P, int s, std::vector<BnBwdFinProb>& fin,
+void bn_bwd_finalize(const Ctx& c, const SegP& S, const Ptrs& P, int s, std::vector<ColRedProb>& fin,
                      std::vector<BnApplyProb>& app) {
   const SlotP& sl = S.slots[s];
   if (sl.bn < 0 || sl.bn_consumers.empty()) return;
   const BnP& b = S.bns[sl.bn];
-  BnBwdFinProb f;
+  ColRedProb f;
+  std::memset(&f, 0, sizeof(f));
   f.part = part_ptr(c, S, sl.bn);
+  f.rows = b.bwd_tiles;
+  f.ncols = 2 * b.C;
+  f.mode = RED_BN_BWD;
   f.gamma = (const float*)(cp(P.params) + b.p_off);
   f.stats = stats_ptr(c, S, sl.bn);
   f.dgamma = (float*)(cp(P.grads) + b.gp_off);
   f.dbeta = f.dgamma + b.C;
   f.coef = (float*)(c.scratch + S.scr_base + b.coef_off);
-  f.ntiles = b.bwd_tiles;
-  f.C = b.C;
   f.count = (long)c.plan->B * sl.H * sl.W;
   fin.push_back(f);
   if (!S.needs[s]) return;
@@ -667,9 +646,8 @@ void bn_bwd_finalize(const Ctx& c, const SegP& S, const Ptrs& P, int s, std::vec
   app.push_back(a);
 }
 
-int fire_finalize(const Ctx& c, std::vector<BnBwdFinProb>& fin, std::vector<BnApplyProb>& app) {
-  std::vector<BnFinProb> none;
-  if (fin_launch(none, fin, c.stream)) return PNN_ERR_HIP;
+int fire_finalize(const Ctx& c, std::vector<ColRedProb>& fin, std::vector<BnApplyProb>& app) {
+  if (fire_colred(fin, c.stream)) return PNN_ERR_HIP;
   return grouped<BnApplyLaunch>(
       app, [](const BnApplyProb& p) { return (int)cdiv(p.n, ELT_TILE); },
       [&](const BnApplyLaunch& L, int tiles, size_t) { return launch_bn_apply(L, tiles, c.plan->dtype, c.stream); });
@@ -705,7 +683,7 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
   for (int L = maxL; L >= 1; --L) {
     // A: gradients of the slots produced at this level
     {
-      std::vector<BnBwdFinProb> fin;
+      std::vector<ColRedProb> fin;
       std::vector<BnApplyProb> app;
       for (size_t i = 0; i < segs.size(); ++i) {
         const SegP& S = *segs[i];
@@ -717,7 +695,7 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
     }
     // B + C: weight gradients
     std::vector<WgradProb> wg_vec, wg_gen;
-    std::vector<ReduceProb> red;
+    std::vector<ColRedProb> red;
     size_t woff = 0;
     for (size_t i = 0; i < segs.size(); ++i) {
       const SegP& S = *segs[i];
@@ -738,11 +716,13 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
         p.part = (float*)(wpart + woff);
         woff = align256(woff + (size_t)g.splits * p.Co * p.K * 4);
         (n.cin % (16 / es) == 0 ? wg_vec : wg_gen).push_back(p);
-        ReduceProb r;
+        ColRedProb r;
+        std::memset(&r, 0, sizeof(r));
         r.part = p.part;
         r.dst = (float*)(cp(P.grads) + n.gw_off);
-        r.n = (long)p.Co * p.K;
-        r.splits = g.splits;
+        r.rows = g.splits;
+        r.ncols = p.Co * p.K;
+        r.mode = RED_SUM;
         red.push_back(r);
       }
     }
@@ -764,12 +744,7 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
           });
       if (e) return e;
     }
-    {
-      int e = grouped<ReduceLaunch>(
-          red, [](const ReduceProb& p) { return (int)cdiv(p.n, ELT_TILE); },
-          [&](const ReduceLaunch& Lx, int tiles, size_t) { return launch_reduce(Lx, tiles, c.stream); });
-      if (e) return e;
-    }
+    if (fire_colred(red, c.stream)) return PNN_ERR_HIP;
     // D + E: data gradients (first of two BN consumers, then the rest) and bnact backward
     for (int phase = 0; phase < 2; ++phase) {
       std::vector<ConvProb> dg;
@@ -836,7 +811,7 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
   }
   // gradient of the segment inputs
   {
-    std::vector<BnBwdFinProb> fin;
+    std::vector<ColRedProb> fin;
     std::vector<BnApplyProb> app;
     for (size_t i = 0; i < segs.size(); ++i) {
       const SegP& S = *segs[i];

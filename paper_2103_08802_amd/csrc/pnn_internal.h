@@ -35,7 +35,7 @@ struct ConvProb {
   const void* res;      // addend [M][ncol] (nullable); BWD: the skip gradient
   const void* ext;      // second addend [M][ncol] (nullable)
   const float* pro;     // FWD prologue scale[Cg], shift[Cg]: A = ReLU(x * scale + shift) (nullable)
-  float* part;          // per-tile column partial sums [tiles_m][2][ncol]
+  float* part;          // per-tile column partial sums [tiles_m][ncol][2]
   const void* zsrc;     // BWD + EPI_BN_MASK: BN input z [M][ncol]
   const float* bnst;    // BWD + EPI_BN_MASK: mean, invstd, scale, shift [4][ncol]
   const float* acc_in;  // EPI_ACC_IN: [M][ncol] float
@@ -70,53 +70,36 @@ struct WgradLaunch {
   WgradProb p[PNN_MAXG];
 };
 
-// Sum of split partials: dst[i] = sum_s part[s * n + i] (float).
-struct ReduceProb {
+// Column reduction of tile partials part[rows][ncols] in a fixed order (fp64 sums), fused with what
+// the sums are for:
+//   RED_SUM     dst[c] = sum_r part[r][c]                               (split-K weight gradients)
+//   RED_BN_FWD  ncols = 2C, part[r][c][2] = (sum z, sum z^2) -> mean, invstd, scale, shift [4][C]
+//   RED_BN_BWD  ncols = 2C, part[r][c][2] = (sum dbn, sum dbn*xhat) -> dbeta, dgamma and the
+//               apply coefficients c1 = gamma * invstd, mb = dbeta / M, mbx = dgamma / M  [3][C]
+enum { RED_SUM = 0, RED_BN_FWD = 1, RED_BN_BWD = 2 };
+struct ColRedProb {
   const float* part;
-  float* dst;
-  long n;
-  int splits;
-  int tile_begin;
-};
-struct ReduceLaunch {
-  int n;
-  ReduceProb p[PNN_MAXG];
-};
-
-// Forward BN statistics: per-channel batch mean / variance from tile partials.
-struct BnFinProb {
-  const float* part;    // [ntiles][2][C]
-  const float* gamma;
-  const float* beta;
-  float* stats;         // mean, invstd, scale, shift [4][C]
-  int ntiles, C;
-  long count;
-  int tile_begin;
-};
-// Backward BN reductions: dbeta = sum dbn, dgamma = sum dbn * xhat; coefficients of the apply.
-struct BnBwdFinProb {
-  const float* part;    // [ntiles][2][C]
-  const float* gamma;
-  const float* stats;
-  float* dgamma;
+  float* dst;            // RED_SUM
+  const float* gamma;    // BN modes
+  const float* beta;     // RED_BN_FWD
+  float* stats;          // RED_BN_FWD: written; RED_BN_BWD: read (invstd)
+  float* dgamma;         // RED_BN_BWD
   float* dbeta;
-  float* coef;          // c1 = gamma * invstd, mb = dbeta / M, mbx = dgamma / M  [3][C]
-  int ntiles, C;
-  long count;
+  float* coef;
+  long count;            // BN: number of rows M of the normalised tensor
+  int rows, ncols, mode;
   int tile_begin;
 };
-struct FinLaunch {
+struct ColRedLaunch {
   int n;
-  union {
-    BnFinProb f[PNN_MAXG];
-    BnBwdFinProb b[PNN_MAXG];
-  };
+  ColRedProb p[PNN_MAXG];
 };
+constexpr int RED_COLS = 32;       // columns per column-reduce workgroup (8 row lanes x 32)
 
 // Column statistics of a stored tensor [M][C] (BN of a segment input).
 struct ColStatProb {
   const void* x;
-  float* part;          // [tiles][2][C]
+  float* part;          // [tiles][C][2]
   long M;
   int C;
   int tile_begin;
@@ -152,7 +135,7 @@ struct BnActProb {
   const void* ext;      // FWD addend (nullable)
   const void* g;        // BWD: gradient of the output
   const float* stats;
-  float* part;          // BWD: [tiles][2][C]
+  float* part;          // BWD: [tiles][C][2]
   int B, H, W, C, pool;
   long n_out;           // output pixels (B * Ho * Wo)
   int tile_begin;
@@ -200,9 +183,7 @@ struct AxpyLaunch {
 
 int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, bool vec, hipStream_t s);
 int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s);
-int launch_reduce(const ReduceLaunch& L, int tiles, hipStream_t s);
-int launch_bn_fin_fwd(const FinLaunch& L, int tiles, hipStream_t s);
-int launch_bn_fin_bwd(const FinLaunch& L, int tiles, hipStream_t s);
+int launch_colred(const ColRedLaunch& L, int tiles, hipStream_t s);
 int launch_colstat(const ColStatLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_bn_apply(const BnApplyLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_bnact_fwd(const BnActLaunch& L, int tiles, int dtype, hipStream_t s);
