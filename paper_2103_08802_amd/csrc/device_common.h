@@ -56,6 +56,20 @@ __device__ __forceinline__ void load_chunk(const void* base, long idx, Chunk<T>&
   }
 }
 
+template <typename T>
+__device__ __forceinline__ void store_chunk(void* base, long idx, const float* v) {
+  if constexpr (sizeof(T) == 4) {
+    *(float4*)((float*)base + idx) = make_float4(v[0], v[1], v[2], v[3]);
+  } else {
+    uint4 u;
+    u.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+    u.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+    u.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
+    u.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+    *(uint4*)((uint16_t*)base + idx) = u;
+  }
+}
+
 // MFMA fragment: the lane's 16 bytes of an A or B operand.
 template <typename T> struct Frag;
 template <> struct Frag<uint16_t> {

@@ -15,13 +15,40 @@ namespace pnn {
 
 // ------------------------------------------------------------------------------------------------
 // forward / data-gradient convolution
+//
+// GK = gather kind: GK_POINT  1x1 / stride 1 / pad 0 (row m of A is row m of the input),
+//                   GK_VEC    any geometry, channels a multiple of the 16-byte chunk,
+//                   GK_SCALAR any geometry, element-wise gather (e.g. 3-channel images).
+// The BN prologue's (scale, shift) and the data-gradient epilogue's BN statistics are staged in LDS
+// once per workgroup.  The epilogue stages the fp32 tile through LDS so that every thread owns
+// 16-byte column chunks: residual / mask-source loads and output stores are 16-byte vectors, and
+// each thread's BN partial sums cover fixed columns (combined in a fixed order).
 // ------------------------------------------------------------------------------------------------
+enum { GK_POINT = 0, GK_VEC = 1, GK_SCALAR = 2 };
+constexpr int CONV_PRO_MAXC = 512;
+constexpr int ACC_LD = 64 + 4;
 
-template <typename T, int MODE, bool VEC>
-__device__ __forceinline__ void gather_a(const ConvProb& P, int n, int p, int q, bool rowok, int k0,
-                                         Frag<T>& a) {
+template <typename T, int MODE, int GK>
+__device__ __forceinline__ void gather_a(const ConvProb& P, const float2* pro, int m, int n, int p, int q,
+                                         bool rowok, int k0, Frag<T>& a) {
   constexpr int VE = St<T>::VE;
-  if constexpr (VEC) {
+  const bool prologue = MODE == MODE_FWD && P.pro != nullptr;
+  if constexpr (GK == GK_POINT) {
+    if (!(rowok && k0 < P.K)) {
+      a.zero();
+      return;
+    }
+    const long idx = (long)m * P.Cg + k0;
+    if (prologue) {
+      Chunk<T> c;
+      load_chunk<T>(P.in, idx, c);
+#pragma unroll
+      for (int e = 0; e < VE; ++e) c.v[e] = fmaxf(fmaf(c.v[e], pro[k0 + e].x, pro[k0 + e].y), 0.0f);
+      a.from_chunk(c);
+    } else {
+      a.from_raw(*(const uint4*)((const T*)P.in + idx));
+    }
+  } else if constexpr (GK == GK_VEC) {
     const int tap = k0 / P.Cg;
     const int c0 = k0 - tap * P.Cg;
     const int r = tap / P.k;
@@ -43,12 +70,11 @@ __device__ __forceinline__ void gather_a(const ConvProb& P, int n, int p, int q,
       return;
     }
     const long idx = (((long)n * P.H + ih) * P.W + iw) * P.Cg + c0;
-    if (MODE == MODE_FWD && P.pro != nullptr) {
+    if (prologue) {
       Chunk<T> c;
       load_chunk<T>(P.in, idx, c);
 #pragma unroll
-      for (int e = 0; e < VE; ++e)
-        c.v[e] = fmaxf(fmaf(c.v[e], P.pro[c0 + e], P.pro[P.Cg + c0 + e]), 0.0f);
+      for (int e = 0; e < VE; ++e) c.v[e] = fmaxf(fmaf(c.v[e], pro[c0 + e].x, pro[c0 + e].y), 0.0f);
       a.from_chunk(c);
     } else {
       a.from_raw(*(const uint4*)((const T*)P.in + idx));
@@ -78,7 +104,7 @@ __device__ __forceinline__ void gather_a(const ConvProb& P, int n, int p, int q,
         ok = ok && (unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W;
         if (ok) {
           v = St<T>::ld(P.in, (((long)n * P.H + ih) * P.W + iw) * P.Cg + ch);
-          if (MODE == MODE_FWD && P.pro != nullptr) v = fmaxf(fmaf(v, P.pro[ch], P.pro[P.Cg + ch]), 0.0f);
+          if (prologue) v = fmaxf(fmaf(v, pro[ch].x, pro[ch].y), 0.0f);
         }
       }
       c.v[e] = v;
@@ -104,36 +130,53 @@ __device__ __forceinline__ void load_b(const ConvProb& P, int col, int k0, Frag<
   }
 }
 
-template <typename T, int MODE, bool VEC>
+template <typename T, int MODE, int GK>
 __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   constexpr int VE = St<T>::VE;
   constexpr int KS = 4 * VE;
-  __shared__ float red[4][64][2];
+  __shared__ float2 pro_s[CONV_PRO_MAXC];
+  __shared__ float4 bn_s[64];
+  __shared__ float acc_s[CONV_BM * ACC_LD];
 
   const int gi = find_group(L);
   const ConvProb& P = L.p[gi];
   const int local = blockIdx.x - P.tile_begin;
   const int tm = local / P.tiles_n;
   const int tn = local - tm * P.tiles_n;
-  const int wave = threadIdx.x >> 6;
-  const int lane = threadIdx.x & 63;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int lane = tid & 63;
   const int r16 = lane & 15;
   const int grp = lane >> 4;
   const int mw = tm * CONV_BM + wave * 32;
   const int n0 = tn * 16 * P.wn;
   const int PQ = P.P * P.Q;
+  const bool bnmask = MODE == MODE_BWD && (P.flags & EPI_BN_MASK);
 
-  int rn[2], rp[2], rq[2];
+  if (MODE == MODE_FWD && P.pro != nullptr)
+    for (int c = tid; c < P.Cg; c += 256) pro_s[c] = make_float2(P.pro[c], P.pro[P.Cg + c]);
+  if (bnmask && tid < 16 * P.wn) {
+    const int col = n0 + tid;
+    bn_s[tid] = make_float4(P.bnst[col], P.bnst[P.ncol + col], P.bnst[2 * P.ncol + col], P.bnst[3 * P.ncol + col]);
+  }
+  __syncthreads();
+
+  int rm[2], rn[2], rp[2], rq[2];
   bool rv[2];
 #pragma unroll
   for (int wm = 0; wm < 2; ++wm) {
     const int m = mw + wm * 16 + r16;
     rv[wm] = m < P.M;
     const int mm = rv[wm] ? m : 0;
-    rn[wm] = mm / PQ;
-    const int rem = mm - rn[wm] * PQ;
-    rp[wm] = rem / P.Q;
-    rq[wm] = rem - rp[wm] * P.Q;
+    rm[wm] = mm;
+    if constexpr (GK != GK_POINT) {
+      rn[wm] = mm / PQ;
+      const int rem = mm - rn[wm] * PQ;
+      rp[wm] = rem / P.Q;
+      rq[wm] = rem - rp[wm] * P.Q;
+    } else {
+      rn[wm] = rp[wm] = rq[wm] = 0;
+    }
   }
 
   f32x4 acc[2][4];
@@ -146,89 +189,123 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
     const int k0 = kk + VE * grp;
     Frag<T> a[2];
 #pragma unroll
-    for (int wm = 0; wm < 2; ++wm) gather_a<T, MODE, VEC>(P, rn[wm], rp[wm], rq[wm], rv[wm], k0, a[wm]);
+    for (int wm = 0; wm < 2; ++wm) gather_a<T, MODE, GK>(P, pro_s, rm[wm], rn[wm], rp[wm], rq[wm], rv[wm], k0, a[wm]);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       if (j < P.wn) {
         Frag<T> b;
-        load_b<T, VEC>(P, n0 + j * 16 + r16, k0, b);
+        load_b<T, GK != GK_SCALAR>(P, n0 + j * 16 + r16, k0, b);
 #pragma unroll
         for (int wm = 0; wm < 2; ++wm) mma(a[wm], b, acc[wm][j]);
       }
     }
   }
 
-  // ---- epilogue ----
-  float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
-  const bool bnmask = MODE == MODE_BWD && (P.flags & EPI_BN_MASK);
+  // ---- epilogue: stage the fp32 tile in LDS ----
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (j >= P.wn) continue;
-    const int col = n0 + j * 16 + r16;
-    float mean = 0.f, invstd = 0.f, sc = 0.f, sh = 0.f;
-    if (bnmask) {
-      mean = P.bnst[col];
-      invstd = P.bnst[P.ncol + col];
-      sc = P.bnst[2 * P.ncol + col];
-      sh = P.bnst[3 * P.ncol + col];
+  for (int wm = 0; wm < 2; ++wm)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (j >= P.wn) continue;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        acc_s[(wave * 32 + wm * 16 + grp * 4 + i) * ACC_LD + j * 16 + r16] = acc[wm][j][i];
     }
+  __syncthreads();
+
+  const int BNc = 16 * P.wn;
+  const int ncc = BNc / VE;           // column chunks per row
+  const int rpp = 256 / ncc;          // rows per pass
+  const int cc = tid % ncc;
+  const int c0 = cc * VE;
+  float s1[VE], s2[VE];
 #pragma unroll
-    for (int wm = 0; wm < 2; ++wm) {
+  for (int e = 0; e < VE; ++e) s1[e] = s2[e] = 0.f;
+  for (int r = tid / ncc; r < CONV_BM; r += rpp) {
+    const int m = tm * CONV_BM + r;
+    if (m >= P.M) break;
+    const long idx = (long)m * P.ncol + n0 + c0;
+    float v[VE];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int m = mw + wm * 16 + grp * 4 + i;
-        if (m >= P.M) continue;
-        const long idx = (long)m * P.ncol + col;
-        float v = acc[wm][j][i];
-        if constexpr (MODE == MODE_FWD) {
-          if (P.res) v += St<T>::ld(P.res, idx);
-          if (P.ext) v += St<T>::ld(P.ext, idx);
-          St<T>::st(P.out, idx, v);
-          const float vr = St<T>::rnd(v);
-          s1[j] += vr;
-          s2[j] += vr * vr;
-        } else {
-          if (P.flags & EPI_ACC_IN) v += P.acc_in[idx];
-          if (P.flags & EPI_STORE_F32) {
-            P.out32[idx] = v;
-          } else if (bnmask) {
-            const float z = St<T>::ld(P.zsrc, idx);
-            const float y = fmaf(z, sc, sh);
-            const float d = y > 0.f ? v : 0.f;
-            St<T>::st(P.out, idx, d);
-            const float dr = St<T>::rnd(d);
-            s1[j] += dr;
-            s2[j] += dr * ((z - mean) * invstd);
-          } else {
-            if (P.res) v += St<T>::ld(P.res, idx);
-            St<T>::st(P.out, idx, v);
-          }
+    for (int e = 0; e < VE; ++e) v[e] = acc_s[r * ACC_LD + c0 + e];
+    if constexpr (MODE == MODE_FWD) {
+      if (P.res) {
+        Chunk<T> x;
+        load_chunk<T>(P.res, idx, x);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) v[e] += x.v[e];
+      }
+      if (P.ext) {
+        Chunk<T> x;
+        load_chunk<T>(P.ext, idx, x);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) v[e] += x.v[e];
+      }
+      store_chunk<T>(P.out, idx, v);
+#pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        const float vr = St<T>::rnd(v[e]);
+        s1[e] += vr;
+        s2[e] += vr * vr;
+      }
+    } else {
+      if (P.flags & EPI_ACC_IN) {
+#pragma unroll
+        for (int e = 0; e < VE; e += 4) {
+          const float4 x = *(const float4*)(P.acc_in + idx + e);
+          v[e] += x.x; v[e + 1] += x.y; v[e + 2] += x.z; v[e + 3] += x.w;
         }
+      }
+      if (P.flags & EPI_STORE_F32) {
+#pragma unroll
+        for (int e = 0; e < VE; e += 4) *(float4*)(P.out32 + idx + e) = make_float4(v[e], v[e + 1], v[e + 2], v[e + 3]);
+      } else if (bnmask) {
+        Chunk<T> z;
+        load_chunk<T>(P.zsrc, idx, z);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          const float4 b = bn_s[c0 + e];
+          v[e] = fmaf(z.v[e], b.z, b.w) > 0.f ? v[e] : 0.f;
+        }
+        store_chunk<T>(P.out, idx, v);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          const float4 b = bn_s[c0 + e];
+          const float dr = St<T>::rnd(v[e]);
+          s1[e] += dr;
+          s2[e] += dr * ((z.v[e] - b.x) * b.y);
+        }
+      } else {
+        if (P.res) {
+          Chunk<T> x;
+          load_chunk<T>(P.res, idx, x);
+#pragma unroll
+          for (int e = 0; e < VE; ++e) v[e] += x.v[e];
+        }
+        store_chunk<T>(P.out, idx, v);
       }
     }
   }
 
   const bool stats = (MODE == MODE_FWD) ? (P.flags & EPI_STATS) != 0 : bnmask;
   if (stats) {
+    __syncthreads();                   // acc_s reused: [rpp][BNc] sums, then sums of products
+    float* red1 = acc_s;
+    float* red2 = acc_s + 256 * VE;
+    const int rr = tid / ncc;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (j >= P.wn) continue;
-      float a = s1[j], b = s2[j];
-      a += __shfl_xor(a, 16, 64);
-      b += __shfl_xor(b, 16, 64);
-      a += __shfl_xor(a, 32, 64);
-      b += __shfl_xor(b, 32, 64);
-      if (grp == 0) {
-        red[wave][j * 16 + r16][0] = a;
-        red[wave][j * 16 + r16][1] = b;
-      }
+    for (int e = 0; e < VE; ++e) {
+      red1[rr * BNc + c0 + e] = s1[e];
+      red2[rr * BNc + c0 + e] = s2[e];
     }
     __syncthreads();
-    const int t = threadIdx.x;
-    if (t < 16 * P.wn) {
-      const float a = ((red[0][t][0] + red[1][t][0]) + red[2][t][0]) + red[3][t][0];
-      const float b = ((red[0][t][1] + red[1][t][1]) + red[2][t][1]) + red[3][t][1];
-      float2* pp = (float2*)P.part + (long)tm * P.ncol + n0 + t;
+    if (tid < BNc) {
+      float a = 0.f, b = 0.f;
+      for (int k = 0; k < rpp; ++k) {
+        a += red1[k * BNc + tid];
+        b += red2[k * BNc + tid];
+      }
+      float2* pp = (float2*)P.part + (long)tm * P.ncol + n0 + tid;
       *pp = make_float2(a, b);
     }
   }
@@ -374,25 +451,25 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
 // launchers
 // ------------------------------------------------------------------------------------------------
 
-template <typename T>
-static int launch_conv_t(const ConvLaunch& L, int tiles, int mode, bool vec, hipStream_t s) {
-  if (mode == MODE_FWD) {
-    if (vec)
-      hipLaunchKernelGGL((conv_kernel<T, MODE_FWD, true>), dim3(tiles), dim3(256), 0, s, L);
-    else
-      hipLaunchKernelGGL((conv_kernel<T, MODE_FWD, false>), dim3(tiles), dim3(256), 0, s, L);
-  } else {
-    if (vec)
-      hipLaunchKernelGGL((conv_kernel<T, MODE_BWD, true>), dim3(tiles), dim3(256), 0, s, L);
-    else
-      hipLaunchKernelGGL((conv_kernel<T, MODE_BWD, false>), dim3(tiles), dim3(256), 0, s, L);
-  }
-  return (int)hipGetLastError();
+template <typename T, int MODE>
+static void launch_conv_m(const ConvLaunch& L, int tiles, int gk, hipStream_t s) {
+  if (gk == GK_POINT)
+    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_POINT>), dim3(tiles), dim3(256), 0, s, L);
+  else if (gk == GK_VEC)
+    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_VEC>), dim3(tiles), dim3(256), 0, s, L);
+  else
+    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_SCALAR>), dim3(tiles), dim3(256), 0, s, L);
 }
 
-int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, bool vec, hipStream_t s) {
-  return dtype == 1 ? launch_conv_t<uint16_t>(L, tiles, mode, vec, s)
-                    : launch_conv_t<float>(L, tiles, mode, vec, s);
+int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, hipStream_t s) {
+  if (dtype == 1) {
+    if (mode == MODE_FWD) launch_conv_m<uint16_t, MODE_FWD>(L, tiles, gk, s);
+    else launch_conv_m<uint16_t, MODE_BWD>(L, tiles, gk, s);
+  } else {
+    if (mode == MODE_FWD) launch_conv_m<float, MODE_FWD>(L, tiles, gk, s);
+    else launch_conv_m<float, MODE_BWD>(L, tiles, gk, s);
+  }
+  return (int)hipGetLastError();
 }
 
 int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s) {

@@ -69,11 +69,16 @@ __global__ __launch_bounds__(256) void colred_kernel(const ColRedLaunch L) {
     P.stats[2 * C + c] = scale;
     P.stats[3 * C + c] = P.beta[c] - (float)mean * scale;
   } else {
+    // dL/dz = c1 (dbn - mb - xhat mbx), xhat = (z - mean) invstd, c1 = gamma invstd, mb = sum dbn / M,
+    // mbx = sum dbn xhat / M; written as A dbn + B z + K per channel
     P.dbeta[c] = (float)s1;
     P.dgamma[c] = (float)s2;
-    P.coef[c] = P.gamma[c] * P.stats[C + c];
-    P.coef[C + c] = (float)(s1 / M);
-    P.coef[2 * C + c] = (float)(s2 / M);
+    const double invstd = (double)P.stats[C + c], mean = (double)P.stats[c];
+    const double c1 = (double)P.gamma[c] * invstd;
+    const double mb = s1 / M, mbx = s2 / M;
+    P.coef[c] = (float)c1;
+    P.coef[C + c] = (float)(-c1 * mbx * invstd);
+    P.coef[2 * C + c] = (float)(c1 * (mbx * invstd * mean - mb));
   }
 }
 
@@ -96,21 +101,32 @@ __global__ __launch_bounds__(256) void colstat_kernel(const ColStatLaunch L) {
   }
 }
 
-// out = skip + c1 * (dbn - mb - xhat * mbx), xhat = (z - mean) * invstd
+// out = A dbn + B z + K [+ skip] per channel (the BN backward, coefficients from the column
+// reduce); 16-byte chunks, C a multiple of the chunk.
 template <typename T>
 __global__ __launch_bounds__(256) void bn_apply_kernel(const BnApplyLaunch L) {
+  constexpr int VE = St<T>::VE;
   const int gi = find_group(L);
   const BnApplyProb& P = L.p[gi];
   const long base = (long)(blockIdx.x - P.tile_begin) * ELT_TILE;
-  for (int t = threadIdx.x; t < ELT_TILE; t += 256) {
+  for (int t = threadIdx.x * VE; t < ELT_TILE; t += 256 * VE) {
     const long i = base + t;
     if (i >= P.n) break;
-    const int c = (int)(i % P.C);
-    const float z = St<T>::ld(P.z, i);
-    const float xh = (z - P.stats[c]) * P.stats[P.C + c];
-    float v = P.coef[c] * (St<T>::ld(P.dbn, i) - P.coef[P.C + c] - xh * P.coef[2 * P.C + c]);
-    if (P.skip) v += St<T>::ld(P.skip, i);
-    St<T>::st(P.out, i, v);
+    const int c0 = (int)(i % P.C);
+    Chunk<T> d, z;
+    load_chunk<T>(P.dbn, i, d);
+    load_chunk<T>(P.z, i, z);
+    float v[VE];
+#pragma unroll
+    for (int e = 0; e < VE; ++e)
+      v[e] = fmaf(P.coef[c0 + e], d.v[e], fmaf(P.coef[P.C + c0 + e], z.v[e], P.coef[2 * P.C + c0 + e]));
+    if (P.skip) {
+      Chunk<T> k;
+      load_chunk<T>(P.skip, i, k);
+#pragma unroll
+      for (int e = 0; e < VE; ++e) v[e] += k.v[e];
+    }
+    store_chunk<T>(P.out, i, v);
   }
 }
 

@@ -204,8 +204,10 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
       s.direct_consumer = i;
     }
   }
-  for (auto& b : S.bns)
+  for (auto& b : S.bns) {
     if (b.slot != 0 && S.nodes[S.slots[b.slot].producer].op != PNN_OP_CONV) return PNN_ERR_UNSUPPORTED;
+    if (S.slots[b.slot].C % 16 != 0 || S.slots[b.slot].C > 512) return PNN_ERR_UNSUPPORTED;
+  }
   for (auto& sl : S.slots) {
     if (!sl.bn_consumers.empty() && sl.direct_consumer != -1) return PNN_ERR_UNSUPPORTED;
     if (sl.bn_consumers.size() > 2) return PNN_ERR_UNSUPPORTED;
@@ -467,7 +469,7 @@ double conv_bytes(const ConvProb& p, int es, int mode) {
   return b;
 }
 
-int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode, bool vec) {
+int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk) {
   pnn_plan* plan = c.plan;
   return grouped<ConvLaunch>(
       probs, [](const ConvProb& p) { return p.tiles_m * p.tiles_n; },
@@ -478,10 +480,27 @@ int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode, bool vec) {
           by += conv_bytes(L.p[i], plan->es, mode);
         }
         Timer t(plan, 1, c.stream);
-        int e = launch_conv(L, tiles, plan->dtype, mode, vec, c.stream);
+        int e = launch_conv(L, tiles, plan->dtype, mode, gk, c.stream);
         t.done(c.stream, fl, by);
         return e;
       });
+}
+
+// Gather kind of a convolution problem: 0 pointwise, 1 vector gather, 2 element-wise gather.
+int gather_kind(const ConvProb& p, int es) {
+  if (p.Cg % (16 / es) != 0) return 2;
+  if (p.k == 1 && p.stride == 1 && p.pad == 0) return 0;
+  return 1;
+}
+
+int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode) {
+  std::vector<ConvProb> by[3];
+  for (auto& p : probs) by[gather_kind(p, c.plan->es)].push_back(p);
+  for (int gk = 0; gk < 3; ++gk) {
+    int e = fire_conv_gk(c, by[gk], mode, gk);
+    if (e) return e;
+  }
+  return PNN_OK;
 }
 
 ConvProb conv_common(const pnn_plan* plan, const NodeP& n) {
@@ -597,8 +616,8 @@ int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
       }
     }
     int e;
-    if ((e = fire_conv(c, cv_vec, MODE_FWD, true))) return e;
-    if ((e = fire_conv(c, cv_gen, MODE_FWD, false))) return e;
+    if ((e = fire_conv(c, cv_vec, MODE_FWD))) return e;
+    if ((e = fire_conv(c, cv_gen, MODE_FWD))) return e;
     e = grouped<BnActLaunch>(
         ba, [](const BnActProb& p) { return (int)cdiv(p.n_out, BNACT_PIX); },
         [&](const BnActLaunch& Lx, int tiles, size_t) { return launch_bnact_fwd(Lx, tiles, plan->dtype, c.stream); });
@@ -801,7 +820,7 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
           dg.push_back(p);
         }
       }
-      int e = fire_conv(c, dg, MODE_BWD, true);
+      int e = fire_conv(c, dg, MODE_BWD);
       if (e) return e;
       e = grouped<BnActLaunch>(
           ba, [](const BnActProb& p) { return (int)cdiv(p.n_out, BNACT_PIX); },

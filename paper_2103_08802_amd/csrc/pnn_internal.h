@@ -181,7 +181,8 @@ struct AxpyLaunch {
   AxpyProb p[PNN_MAXG];
 };
 
-int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, bool vec, hipStream_t s);
+// gk: 0 = pointwise (1x1, stride 1, pad 0), 1 = vector gather, 2 = element-wise gather
+int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, hipStream_t s);
 int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s);
 int launch_colred(const ColRedLaunch& L, int tiles, hipStream_t s);
 int launch_colstat(const ColStatLaunch& L, int tiles, int dtype, hipStream_t s);
