@@ -313,18 +313,103 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
 
 // ------------------------------------------------------------------------------------------------
 // weight gradient: dW[co][(r,s,c)] = sum_m g[m][co] * act(in)[pixel(m) + tap(r,s)][c]
-// The m-reduction is split over workgroups (fp32 partials, summed in a fixed order afterwards).
-// Both operands are staged through LDS transposed to m-contiguous rows.
+//
+// A workgroup owns a (16 wr) x 64 tile of dW and a range of m (split-K; fp32 partials are summed
+// in a fixed order by the column reduce).  Both operands are staged m-major through LDS with
+// 16-byte global loads; the MFMA fragments (8 consecutive m per lane) are read column-wise from
+// rows padded to 8 bytes past a 16-byte multiple, which keeps the four m-groups of a wave on
+// disjoint banks.  wr waves cover the tile's rows; the other 4 / wr wave groups split each LDS
+// stage's m-steps and are summed in LDS at the end.  Global loads of the next stage are issued
+// before the current stage is consumed.
 // ------------------------------------------------------------------------------------------------
+constexpr int WG_KC = 128;                 // m rows per LDS stage
+constexpr int WG_TK = 64;                  // dW columns per workgroup tile
+
+template <typename T>
+struct WgCfg {
+  static constexpr int VE = St<T>::VE;
+  static constexpr int PADE = 8 / sizeof(T);         // 8-byte row padding
+  static constexpr int RSA = WG_TK + PADE;            // activation tile row stride (elements)
+  static constexpr int AC = WG_KC * WG_TK / VE / 256; // activation chunks per thread per stage
+  static constexpr int GC = WG_KC * 64 / VE / 256;    // max output-gradient chunks per thread
+};
+
+template <typename T>
+__device__ __forceinline__ void lds_store8(T* p, uint4 u) {
+  // 16 bytes as two 8-byte stores (rows are 8-byte aligned)
+  *(uint2*)p = make_uint2(u.x, u.y);
+  *(uint2*)(p + 8 / sizeof(T)) = make_uint2(u.z, u.w);
+}
+
+template <typename T, bool VEC>
+__device__ __forceinline__ uint4 wg_gather(const WgradProb& P, const float2* pro, int m, int kidx,
+                                           int col) {
+  constexpr int VE = St<T>::VE;
+  const int PQ = P.P * P.Q;
+  uint4 zero = make_uint4(0, 0, 0, 0);
+  if (m >= P.M || kidx >= P.K) return zero;
+  const int n = m / PQ;
+  const int rem = m - n * PQ;
+  const int p = rem / P.Q;
+  const int q = rem - p * P.Q;
+  if constexpr (VEC) {
+    const int tap = kidx / P.Cg;
+    const int c0 = kidx - tap * P.Cg;
+    const int r = tap / P.k, s = tap - (tap / P.k) * P.k;
+    const int ih = p * P.stride + r - P.pad, iw = q * P.stride + s - P.pad;
+    if ((unsigned)ih >= (unsigned)P.H || (unsigned)iw >= (unsigned)P.W) return zero;
+    const long idx = (((long)n * P.H + ih) * P.W + iw) * P.Cg + c0;
+    if (P.pro == nullptr) return *(const uint4*)((const T*)P.in + idx);
+    Chunk<T> c;
+    load_chunk<T>(P.in, idx, c);
+    float v[VE];
+#pragma unroll
+    for (int e = 0; e < VE; ++e) v[e] = fmaxf(fmaf(c.v[e], pro[col + e].x, pro[col + e].y), 0.0f);
+    uint4 u;
+    store_chunk<T>(&u, 0, v);
+    return u;
+  } else {
+    float v[VE];
+#pragma unroll
+    for (int e = 0; e < VE; ++e) {
+      v[e] = 0.f;
+      const int kx = kidx + e;
+      if (kx >= P.K) continue;
+      const int tap = kx / P.Cg;
+      const int ch = kx - tap * P.Cg;
+      const int r = tap / P.k, s = tap - (tap / P.k) * P.k;
+      const int ih = p * P.stride + r - P.pad, iw = q * P.stride + s - P.pad;
+      if ((unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W) {
+        float x = St<T>::ld(P.in, (((long)n * P.H + ih) * P.W + iw) * P.Cg + ch);
+        if (P.pro != nullptr) x = fmaxf(fmaf(x, pro[col + e].x, pro[col + e].y), 0.0f);
+        v[e] = x;
+      }
+    }
+    uint4 u;
+    store_chunk<T>(&u, 0, v);
+    return u;
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void lds_frag(const T* base, int row0, int rs, int col, Frag<T>& f) {
+  constexpr int VE = St<T>::VE;
+  T tmp[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) tmp[e] = base[(row0 + e) * rs + col];
+  uint4 u;
+  __builtin_memcpy(&u, tmp, 16);
+  f.from_raw(u);
+}
 
 template <typename T, bool VEC>
 __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
-  constexpr int VE = St<T>::VE;
+  using C = WgCfg<T>;
+  constexpr int VE = C::VE;
   constexpr int KS = 4 * VE;
-  constexpr int KC = WGRAD_KC;
-  constexpr int LD = KC + VE;  // padded LDS row (elements); 16-byte aligned rows
-  __shared__ T gT[64 * LD];
-  __shared__ T aT[256 * LD];
+  __shared__ T lg[WG_KC * (64 + C::PADE)];
+  __shared__ T la[WG_KC * C::RSA];
+  __shared__ float2 pro_s[WG_TK];
 
   const int gi = find_group(L);
   const WgradProb& P = L.p[gi];
@@ -334,111 +419,110 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
   const int tco = rest % P.tiles_co;
   const int split = rest / P.tiles_co;
   const int TCO = 16 * P.wr;
-  const int TK = 256 / P.wr;
+  const int RSG = TCO + C::PADE;
   const int co0 = tco * TCO;
-  const int kk0 = tk * TK;
+  const int kk0 = tk * WG_TK;
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
   const int r16 = lane & 15, grp = lane >> 4;
-  const int sr = wave % P.wr;
-  const int cgp = wave / P.wr;
+  const int sr = wave % P.wr;          // row sub-tile of this wave
+  const int ms = 4 / P.wr;             // m-split factor
+  const int msi = wave / P.wr;
   const int m_begin = split * P.mchunk;
   const int m_end = min(P.M, m_begin + P.mchunk);
-  const int PQ = P.P * P.Q;
+
+  if (P.pro != nullptr && tid < WG_TK) {
+    const int kidx = kk0 + tid;
+    const int c = kidx < P.K ? kidx % P.Cg : 0;
+    pro_s[tid] = make_float2(P.pro[c], P.pro[P.Cg + c]);
+  }
+  __syncthreads();
+
+  const int gcpr = TCO / VE;           // output-gradient chunks per row
+  const int gchunks = WG_KC * gcpr;
+  constexpr int acpr = WG_TK / VE;     // activation chunks per row
+  uint4 ga[C::GC], aa[C::AC];
+
+  auto load_stage = [&](int mc) {
+#pragma unroll
+    for (int i = 0; i < C::GC; ++i) {
+      const int idx = tid + i * 256;
+      ga[i] = make_uint4(0, 0, 0, 0);
+      if (idx < gchunks) {
+        const int row = idx / gcpr, cc = (idx - row * gcpr) * VE;
+        const int m = mc + row;
+        if (m < m_end) ga[i] = *(const uint4*)((const T*)P.g + (long)m * P.Co + co0 + cc);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < C::AC; ++i) {
+      const int idx = tid + i * 256;
+      const int row = idx / acpr, cc = (idx - row * acpr) * VE;
+      const int m = mc + row;
+      aa[i] = m < m_end ? wg_gather<T, VEC>(P, pro_s, m, kk0 + cc, cc) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_stage = [&]() {
+#pragma unroll
+    for (int i = 0; i < C::GC; ++i) {
+      const int idx = tid + i * 256;
+      if (idx < gchunks) {
+        const int row = idx / gcpr, cc = (idx - row * gcpr) * VE;
+        lds_store8<T>(lg + row * RSG + cc, ga[i]);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < C::AC; ++i) {
+      const int idx = tid + i * 256;
+      const int row = idx / acpr, cc = (idx - row * acpr) * VE;
+      lds_store8<T>(la + row * C::RSA + cc, aa[i]);
+    }
+  };
 
   f32x4 acc[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int mc = m_begin; mc < m_end; mc += KC) {
-    // output-gradient tile: KC rows (m) x TCO columns (co), stored [co][m]
-    const int gcpr = TCO / VE;
-    for (int idx = tid; idx < KC * gcpr; idx += 256) {
-      const int mr = idx / gcpr;
-      const int cc = (idx - mr * gcpr) * VE;
-      const int m = mc + mr;
-      T vals[VE];
-      if (m < m_end) {
-        const uint4 u = *(const uint4*)((const T*)P.g + (long)m * P.Co + co0 + cc);
-        __builtin_memcpy(vals, &u, 16);
-      } else {
-#pragma unroll
-        for (int e = 0; e < VE; ++e) vals[e] = T(0);
-      }
-#pragma unroll
-      for (int e = 0; e < VE; ++e) gT[(cc + e) * LD + mr] = vals[e];
-    }
-    // activation tile: KC rows (m) x TK columns (r,s,c), stored [column][m]
-    const int acpr = TK / VE;
-    for (int idx = tid; idx < KC * acpr; idx += 256) {
-      const int mr = idx / acpr;
-      const int kc = (idx - mr * acpr) * VE;
-      const int m = mc + mr;
-      const int kidx = kk0 + kc;
-      Chunk<T> c;
-#pragma unroll
-      for (int e = 0; e < VE; ++e) c.v[e] = 0.f;
-      if (m < m_end && kidx < P.K) {
-        const int n = m / PQ;
-        const int rem = m - n * PQ;
-        const int p = rem / P.Q;
-        const int q = rem - p * P.Q;
-        if constexpr (VEC) {
-          const int tap = kidx / P.Cg;
-          const int c0 = kidx - tap * P.Cg;
-          const int r = tap / P.k, s = tap - (tap / P.k) * P.k;
-          const int ih = p * P.stride + r - P.pad, iw = q * P.stride + s - P.pad;
-          if ((unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W) {
-            load_chunk<T>(P.in, (((long)n * P.H + ih) * P.W + iw) * P.Cg + c0, c);
-            if (P.pro != nullptr) {
-#pragma unroll
-              for (int e = 0; e < VE; ++e)
-                c.v[e] = fmaxf(fmaf(c.v[e], P.pro[c0 + e], P.pro[P.Cg + c0 + e]), 0.0f);
-            }
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < VE; ++e) {
-            const int kx = kidx + e;
-            if (kx >= P.K) continue;
-            const int tap = kx / P.Cg;
-            const int ch = kx - tap * P.Cg;
-            const int r = tap / P.k, s = tap - (tap / P.k) * P.k;
-            const int ih = p * P.stride + r - P.pad, iw = q * P.stride + s - P.pad;
-            if ((unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W) {
-              float v = St<T>::ld(P.in, (((long)n * P.H + ih) * P.W + iw) * P.Cg + ch);
-              if (P.pro != nullptr) v = fmaxf(fmaf(v, P.pro[ch], P.pro[P.Cg + ch]), 0.0f);
-              c.v[e] = v;
-            }
-          }
-        }
-      }
-#pragma unroll
-      for (int e = 0; e < VE; ++e) {
-        if constexpr (sizeof(T) == 4)
-          aT[(kc + e) * LD + mr] = c.v[e];
-        else
-          aT[(kc + e) * LD + mr] = f2bf(c.v[e]);
-      }
-    }
+  if (m_begin < m_end) load_stage(m_begin);
+  for (int mc = m_begin; mc < m_end; mc += WG_KC) {
+    store_stage();
     __syncthreads();
-#pragma unroll
-    for (int ks = 0; ks < KC; ks += KS) {
+    if (mc + WG_KC < m_end) load_stage(mc + WG_KC);
+    for (int st = msi; st < WG_KC / KS; st += ms) {
+      const int row0 = st * KS + VE * grp;
       Frag<T> a;
-      a.from_raw(*(const uint4*)&gT[(sr * 16 + r16) * LD + ks + VE * grp]);
+      lds_frag<T>(lg, row0, RSG, sr * 16 + r16, a);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         Frag<T> b;
-        b.from_raw(*(const uint4*)&aT[(cgp * 64 + j * 16 + r16) * LD + ks + VE * grp]);
+        lds_frag<T>(la, row0, C::RSA, j * 16 + r16, b);
         mma(a, b, acc[j]);
       }
     }
     __syncthreads();
   }
 
+  // combine the m-split wave groups (fixed order) and write the partial tile
+  float* red = (float*)la;             // ms x wr x 16 x 64 floats <= 16 KB
+  if (ms > 1) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        red[((msi * P.wr + sr) * 16 + grp * 4 + i) * 64 + j * 16 + r16] = acc[j][i];
+    __syncthreads();
+    if (msi == 0) {
+      for (int k = 1; k < ms; ++k)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[j][i] += red[((k * P.wr + sr) * 16 + grp * 4 + i) * 64 + j * 16 + r16];
+    }
+  }
+  if (msi != 0) return;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int kidx = kk0 + cgp * 64 + j * 16 + r16;
+    const int kidx = kk0 + j * 16 + r16;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int co = co0 + sr * 16 + grp * 4 + i;

@@ -99,14 +99,15 @@ namespace {
 // plan construction
 // ------------------------------------------------------------------------------------------------
 
+// Weight-gradient tiling: (16 wr) x 64 dW tiles, split-K over m in multiples of 128 rows.
 WgradGeom wgrad_geom(int Co, int K, long M) {
   WgradGeom g;
   g.wr = (Co % 64 == 0) ? 4 : (Co % 32 == 0) ? 2 : 1;
   g.tiles_co = Co / (16 * g.wr);
-  g.tiles_k = (int)cdiv(K, 256 / g.wr);
+  g.tiles_k = (int)cdiv(K, 64);
   const long base = (long)g.tiles_co * g.tiles_k;
   long splits = std::max(1L, std::min(cdiv(M, 512), cdiv(256, base)));
-  long mchunk = cdiv(cdiv(M, splits), WGRAD_KC) * WGRAD_KC;
+  long mchunk = cdiv(cdiv(M, splits), 128) * 128;
   g.mchunk = (int)mchunk;
   g.splits = (int)cdiv(M, mchunk);
   return g;

@@ -61,7 +61,7 @@ struct WgradProb {
   const float* pro;     // prologue scale / shift (nullable)
   float* part;          // [splits][Co][K] float
   int B, H, W, Cg, P, Q, Co, k, stride, pad, M, K;
-  int wr;               // tile = (16 wr) output channels x (256 / wr) filter columns
+  int wr;               // tile = (16 wr) output channels x 64 filter columns
   int tiles_co, tiles_k, splits, mchunk;
   int tile_begin;
 };
@@ -202,6 +202,6 @@ constexpr int CONV_BM = 128;       // rows of M per conv workgroup
 constexpr int ELT_TILE = 2048;     // elements per workgroup of elementwise kernels
 constexpr int COLSTAT_ROWS = 128;  // rows per column-statistics workgroup
 constexpr int BNACT_PIX = 32;      // output pixels per bnact workgroup
-constexpr int WGRAD_KC = 32;       // rows of m per wgrad LDS stage
+
 
 }  // namespace pnn
