@@ -124,6 +124,15 @@ __device__ __forceinline__ int find_group(const Launch& L) {
   return g;
 }
 
+// x / d and x % d for a divisor given with log2(d) (>= 0) or as a plain value (lg < 0)
+__device__ __forceinline__ int div_l2(int x, int d, int lg) { return lg >= 0 ? (x >> lg) : x / d; }
+
+// (r, s) of tap t of a k x k filter, k in {1, 3}
+__device__ __forceinline__ void tap_rs(int t, int k, int& r, int& s) {
+  r = (k == 3) ? ((t * 11) >> 5) : 0;
+  s = t - r * k;
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);

@@ -26,7 +26,6 @@ namespace pnn {
 // ------------------------------------------------------------------------------------------------
 enum { GK_POINT = 0, GK_VEC = 1, GK_SCALAR = 2 };
 constexpr int CONV_PRO_MAXC = 512;
-constexpr int ACC_LD = 64 + 4;
 
 template <typename T, int MODE, int GK>
 __device__ __forceinline__ void gather_a(const ConvProb& P, const float2* pro, int m, int n, int p, int q,
@@ -49,10 +48,10 @@ __device__ __forceinline__ void gather_a(const ConvProb& P, const float2* pro, i
       a.from_raw(*(const uint4*)((const T*)P.in + idx));
     }
   } else if constexpr (GK == GK_VEC) {
-    const int tap = k0 / P.Cg;
+    const int tap = div_l2(k0, P.Cg, P.cg_log2);
     const int c0 = k0 - tap * P.Cg;
-    const int r = tap / P.k;
-    const int s = tap - r * P.k;
+    int r, s;
+    tap_rs(tap, P.k, r, s);
     int ih, iw;
     bool ok = rowok && k0 < P.K;
     if constexpr (MODE == MODE_FWD) {
@@ -60,9 +59,14 @@ __device__ __forceinline__ void gather_a(const ConvProb& P, const float2* pro, i
       iw = q * P.stride + s - P.pad;
     } else {
       const int th = p + P.pad - r, tw = q + P.pad - s;
-      ok = ok && th >= 0 && tw >= 0 && (th % P.stride) == 0 && (tw % P.stride) == 0;
-      ih = th / P.stride;
-      iw = tw / P.stride;
+      if (P.stride == 1) {
+        ih = th;
+        iw = tw;
+      } else {   // stride 2
+        ok = ok && th >= 0 && tw >= 0 && ((th | tw) & 1) == 0;
+        ih = th >> 1;
+        iw = tw >> 1;
+      }
     }
     ok = ok && (unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W;
     if (!ok) {
@@ -130,13 +134,19 @@ __device__ __forceinline__ void load_b(const ConvProb& P, int col, int k0, Frag<
   }
 }
 
-template <typename T, int MODE, int GK>
+// WM row sub-tiles of 16 per wave, WN = 8 / WM column sub-tiles: a workgroup owns a
+// (64 WM) x (16 WN) tile, so narrow problems (16 columns) get 512-row tiles and keep eight
+// operand fragments in flight per wave.
+template <typename T, int MODE, int GK, int WM>
 __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   constexpr int VE = St<T>::VE;
   constexpr int KS = 4 * VE;
+  constexpr int WN = 8 / WM;
+  constexpr int BM = 64 * WM;
+  constexpr int LDA = 16 * WN + 4;
   __shared__ float2 pro_s[CONV_PRO_MAXC];
   __shared__ float4 bn_s[64];
-  __shared__ float acc_s[CONV_BM * ACC_LD];
+  __shared__ float acc_s[BM * LDA];
 
   const int gi = find_group(L);
   const ConvProb& P = L.p[gi];
@@ -148,86 +158,82 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   const int lane = tid & 63;
   const int r16 = lane & 15;
   const int grp = lane >> 4;
-  const int mw = tm * CONV_BM + wave * 32;
+  const int mw = tm * BM + wave * 16 * WM;
   const int n0 = tn * 16 * P.wn;
   const int PQ = P.P * P.Q;
   const bool bnmask = MODE == MODE_BWD && (P.flags & EPI_BN_MASK);
 
   if (MODE == MODE_FWD && P.pro != nullptr)
     for (int c = tid; c < P.Cg; c += 256) pro_s[c] = make_float2(P.pro[c], P.pro[P.Cg + c]);
-  if (bnmask && tid < 16 * P.wn) {
+  if (bnmask && tid < 16 * WN) {
     const int col = n0 + tid;
     bn_s[tid] = make_float4(P.bnst[col], P.bnst[P.ncol + col], P.bnst[2 * P.ncol + col], P.bnst[3 * P.ncol + col]);
   }
   __syncthreads();
 
-  int rm[2], rn[2], rp[2], rq[2];
-  bool rv[2];
+  int rm[WM], rn[WM], rp[WM], rq[WM];
+  bool rv[WM];
 #pragma unroll
-  for (int wm = 0; wm < 2; ++wm) {
+  for (int wm = 0; wm < WM; ++wm) {
     const int m = mw + wm * 16 + r16;
     rv[wm] = m < P.M;
     const int mm = rv[wm] ? m : 0;
     rm[wm] = mm;
     if constexpr (GK != GK_POINT) {
-      rn[wm] = mm / PQ;
+      rn[wm] = div_l2(mm, PQ, P.pq_log2);
       const int rem = mm - rn[wm] * PQ;
-      rp[wm] = rem / P.Q;
+      rp[wm] = div_l2(rem, P.Q, P.q_log2);
       rq[wm] = rem - rp[wm] * P.Q;
     } else {
       rn[wm] = rp[wm] = rq[wm] = 0;
     }
   }
 
-  f32x4 acc[2][4];
+  f32x4 acc[WM][WN];
 #pragma unroll
-  for (int wm = 0; wm < 2; ++wm)
+  for (int wm = 0; wm < WM; ++wm)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[wm][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < WN; ++j) acc[wm][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   for (int kk = 0; kk < P.K; kk += KS) {
     const int k0 = kk + VE * grp;
-    Frag<T> a[2];
+    Frag<T> a[WM];
 #pragma unroll
-    for (int wm = 0; wm < 2; ++wm) gather_a<T, MODE, GK>(P, pro_s, rm[wm], rn[wm], rp[wm], rq[wm], rv[wm], k0, a[wm]);
+    for (int wm = 0; wm < WM; ++wm) gather_a<T, MODE, GK>(P, pro_s, rm[wm], rn[wm], rp[wm], rq[wm], rv[wm], k0, a[wm]);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (j < P.wn) {
-        Frag<T> b;
-        load_b<T, GK != GK_SCALAR>(P, n0 + j * 16 + r16, k0, b);
+    for (int j = 0; j < WN; ++j) {
+      Frag<T> b;
+      load_b<T, GK != GK_SCALAR>(P, n0 + j * 16 + r16, k0, b);
 #pragma unroll
-        for (int wm = 0; wm < 2; ++wm) mma(a[wm], b, acc[wm][j]);
-      }
+      for (int wm = 0; wm < WM; ++wm) mma(a[wm], b, acc[wm][j]);
     }
   }
 
   // ---- epilogue: stage the fp32 tile in LDS ----
 #pragma unroll
-  for (int wm = 0; wm < 2; ++wm)
+  for (int wm = 0; wm < WM; ++wm)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (j >= P.wn) continue;
+    for (int j = 0; j < WN; ++j)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        acc_s[(wave * 32 + wm * 16 + grp * 4 + i) * ACC_LD + j * 16 + r16] = acc[wm][j][i];
-    }
+        acc_s[(wave * 16 * WM + wm * 16 + grp * 4 + i) * LDA + j * 16 + r16] = acc[wm][j][i];
   __syncthreads();
 
-  const int BNc = 16 * P.wn;
-  const int ncc = BNc / VE;           // column chunks per row
-  const int rpp = 256 / ncc;          // rows per pass
+  constexpr int BNc = 16 * WN;
+  constexpr int ncc = BNc / VE;       // column chunks per row
+  constexpr int rpp = 256 / ncc;      // rows per pass
   const int cc = tid % ncc;
   const int c0 = cc * VE;
   float s1[VE], s2[VE];
 #pragma unroll
   for (int e = 0; e < VE; ++e) s1[e] = s2[e] = 0.f;
-  for (int r = tid / ncc; r < CONV_BM; r += rpp) {
-    const int m = tm * CONV_BM + r;
+  for (int r = tid / ncc; r < BM; r += rpp) {
+    const int m = tm * BM + r;
     if (m >= P.M) break;
     const long idx = (long)m * P.ncol + n0 + c0;
     float v[VE];
 #pragma unroll
-    for (int e = 0; e < VE; ++e) v[e] = acc_s[r * ACC_LD + c0 + e];
+    for (int e = 0; e < VE; ++e) v[e] = acc_s[r * LDA + c0 + e];
     if constexpr (MODE == MODE_FWD) {
       if (P.res) {
         Chunk<T> x;
@@ -341,24 +347,35 @@ __device__ __forceinline__ void lds_store8(T* p, uint4 u) {
   *(uint2*)(p + 8 / sizeof(T)) = make_uint2(u.z, u.w);
 }
 
+// Column of the activation tile a thread gathers: filter column kidx = (tap, c0), fixed per thread.
+struct WgCol {
+  int kidx, c0, r, s;
+};
+
+__device__ __forceinline__ WgCol wg_col(const WgradProb& P, int kidx) {
+  WgCol c;
+  c.kidx = kidx;
+  const int tap = div_l2(kidx, P.Cg, P.cg_log2);
+  c.c0 = kidx - tap * P.Cg;
+  tap_rs(tap, P.k, c.r, c.s);
+  return c;
+}
+
 template <typename T, bool VEC>
-__device__ __forceinline__ uint4 wg_gather(const WgradProb& P, const float2* pro, int m, int kidx,
+__device__ __forceinline__ uint4 wg_gather(const WgradProb& P, const float2* pro, int m, const WgCol& cl,
                                            int col) {
   constexpr int VE = St<T>::VE;
   const int PQ = P.P * P.Q;
   uint4 zero = make_uint4(0, 0, 0, 0);
-  if (m >= P.M || kidx >= P.K) return zero;
-  const int n = m / PQ;
+  if (m >= P.M || cl.kidx >= P.K) return zero;
+  const int n = div_l2(m, PQ, P.pq_log2);
   const int rem = m - n * PQ;
-  const int p = rem / P.Q;
+  const int p = div_l2(rem, P.Q, P.q_log2);
   const int q = rem - p * P.Q;
   if constexpr (VEC) {
-    const int tap = kidx / P.Cg;
-    const int c0 = kidx - tap * P.Cg;
-    const int r = tap / P.k, s = tap - (tap / P.k) * P.k;
-    const int ih = p * P.stride + r - P.pad, iw = q * P.stride + s - P.pad;
+    const int ih = p * P.stride + cl.r - P.pad, iw = q * P.stride + cl.s - P.pad;
     if ((unsigned)ih >= (unsigned)P.H || (unsigned)iw >= (unsigned)P.W) return zero;
-    const long idx = (((long)n * P.H + ih) * P.W + iw) * P.Cg + c0;
+    const long idx = (((long)n * P.H + ih) * P.W + iw) * P.Cg + cl.c0;
     if (P.pro == nullptr) return *(const uint4*)((const T*)P.in + idx);
     Chunk<T> c;
     load_chunk<T>(P.in, idx, c);
@@ -373,11 +390,12 @@ __device__ __forceinline__ uint4 wg_gather(const WgradProb& P, const float2* pro
 #pragma unroll
     for (int e = 0; e < VE; ++e) {
       v[e] = 0.f;
-      const int kx = kidx + e;
+      const int kx = cl.kidx + e;
       if (kx >= P.K) continue;
       const int tap = kx / P.Cg;
       const int ch = kx - tap * P.Cg;
-      const int r = tap / P.k, s = tap - (tap / P.k) * P.k;
+      int r, s;
+      tap_rs(tap, P.k, r, s);
       const int ih = p * P.stride + r - P.pad, iw = q * P.stride + s - P.pad;
       if ((unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W) {
         float x = St<T>::ld(P.in, (((long)n * P.H + ih) * P.W + iw) * P.Cg + ch);
@@ -391,15 +409,35 @@ __device__ __forceinline__ uint4 wg_gather(const WgradProb& P, const float2* pro
   }
 }
 
+// MFMA fragment of 8 (bf16) / 4 (fp32) consecutive m rows at one column of an m-major LDS tile:
+// lane (r16, grp) takes rows row0 .. row0 + VE - 1 (row0 includes VE * grp) of column cbase + r16.
+// bf16 uses the gfx950 LDS transpose read: within a 16-lane group, lane i receives element i % 4 of
+// the 8-byte words supplied by lanes 4e + i / 4 (e = 0..3), so lane j supplies the address of row
+// (row0 + j / 4) at column cbase + 4 (j % 4), and a second read covers rows row0 + 4 .. row0 + 7.
+typedef short v4s16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s16 lds_v4s16;
+
 template <typename T>
-__device__ __forceinline__ void lds_frag(const T* base, int row0, int rs, int col, Frag<T>& f) {
-  constexpr int VE = St<T>::VE;
-  T tmp[VE];
+__device__ __forceinline__ void lds_frag(const T* base, int row0, int rs, int cbase, int r16, Frag<T>& f) {
+  if constexpr (sizeof(T) == 2) {
+    const T* p0 = base + (row0 + (r16 >> 2)) * rs + cbase + 4 * (r16 & 3);
+    const v4s16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s16*)p0);
+    const v4s16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s16*)(p0 + 4 * rs));
+    uint4 u;
+    u.x = (uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16);
+    u.y = (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16);
+    u.z = (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16);
+    u.w = (uint32_t)(uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16);
+    f.from_raw(u);
+  } else {
+    constexpr int VE = St<T>::VE;
+    T tmp[VE];
 #pragma unroll
-  for (int e = 0; e < VE; ++e) tmp[e] = base[(row0 + e) * rs + col];
-  uint4 u;
-  __builtin_memcpy(&u, tmp, 16);
-  f.from_raw(u);
+    for (int e = 0; e < VE; ++e) tmp[e] = base[(row0 + e) * rs + cbase + r16];
+    uint4 u;
+    __builtin_memcpy(&u, tmp, 16);
+    f.from_raw(u);
+  }
 }
 
 template <typename T, bool VEC>
@@ -441,6 +479,9 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
   const int gcpr = TCO / VE;           // output-gradient chunks per row
   const int gchunks = WG_KC * gcpr;
   constexpr int acpr = WG_TK / VE;     // activation chunks per row
+  static_assert(256 % acpr == 0, "a thread keeps one activation column");
+  const int acol = (tid % acpr) * VE;
+  const WgCol wcol = wg_col(P, kk0 + acol);
   uint4 ga[C::GC], aa[C::AC];
 
   auto load_stage = [&](int mc) {
@@ -456,10 +497,9 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
     }
 #pragma unroll
     for (int i = 0; i < C::AC; ++i) {
-      const int idx = tid + i * 256;
-      const int row = idx / acpr, cc = (idx - row * acpr) * VE;
+      const int row = (tid + i * 256) / acpr;    // the thread's column acol is the same for every i
       const int m = mc + row;
-      aa[i] = m < m_end ? wg_gather<T, VEC>(P, pro_s, m, kk0 + cc, cc) : make_uint4(0, 0, 0, 0);
+      aa[i] = m < m_end ? wg_gather<T, VEC>(P, pro_s, m, wcol, acol) : make_uint4(0, 0, 0, 0);
     }
   };
   auto store_stage = [&]() {
@@ -491,11 +531,11 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
     for (int st = msi; st < WG_KC / KS; st += ms) {
       const int row0 = st * KS + VE * grp;
       Frag<T> a;
-      lds_frag<T>(lg, row0, RSG, sr * 16 + r16, a);
+      lds_frag<T>(lg, row0, RSG, sr * 16, r16, a);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         Frag<T> b;
-        lds_frag<T>(la, row0, C::RSA, j * 16 + r16, b);
+        lds_frag<T>(la, row0, C::RSA, j * 16, r16, b);
         mma(a, b, acc[j]);
       }
     }
@@ -535,23 +575,30 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
 // launchers
 // ------------------------------------------------------------------------------------------------
 
-template <typename T, int MODE>
-static void launch_conv_m(const ConvLaunch& L, int tiles, int gk, hipStream_t s) {
+template <typename T, int MODE, int WM>
+static void launch_conv_w(const ConvLaunch& L, int tiles, int gk, hipStream_t s) {
   if (gk == GK_POINT)
-    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_POINT>), dim3(tiles), dim3(256), 0, s, L);
+    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_POINT, WM>), dim3(tiles), dim3(256), 0, s, L);
   else if (gk == GK_VEC)
-    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_VEC>), dim3(tiles), dim3(256), 0, s, L);
+    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_VEC, WM>), dim3(tiles), dim3(256), 0, s, L);
   else
-    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_SCALAR>), dim3(tiles), dim3(256), 0, s, L);
+    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_SCALAR, WM>), dim3(tiles), dim3(256), 0, s, L);
 }
 
-int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, hipStream_t s) {
+template <typename T, int MODE>
+static void launch_conv_m(const ConvLaunch& L, int tiles, int gk, int wn, hipStream_t s) {
+  if (wn == 1) launch_conv_w<T, MODE, 8>(L, tiles, gk, s);
+  else if (wn == 2) launch_conv_w<T, MODE, 4>(L, tiles, gk, s);
+  else launch_conv_w<T, MODE, 2>(L, tiles, gk, s);
+}
+
+int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, hipStream_t s) {
   if (dtype == 1) {
-    if (mode == MODE_FWD) launch_conv_m<uint16_t, MODE_FWD>(L, tiles, gk, s);
-    else launch_conv_m<uint16_t, MODE_BWD>(L, tiles, gk, s);
+    if (mode == MODE_FWD) launch_conv_m<uint16_t, MODE_FWD>(L, tiles, gk, wn, s);
+    else launch_conv_m<uint16_t, MODE_BWD>(L, tiles, gk, wn, s);
   } else {
-    if (mode == MODE_FWD) launch_conv_m<float, MODE_FWD>(L, tiles, gk, s);
-    else launch_conv_m<float, MODE_BWD>(L, tiles, gk, s);
+    if (mode == MODE_FWD) launch_conv_m<float, MODE_FWD>(L, tiles, gk, wn, s);
+    else launch_conv_m<float, MODE_BWD>(L, tiles, gk, wn, s);
   }
   return (int)hipGetLastError();
 }

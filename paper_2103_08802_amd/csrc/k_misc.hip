@@ -11,11 +11,11 @@ namespace pnn {
 
 // ------------------------------------------------------------------------------------------------
 // Column reduction of tile partials (split-K weight gradients, BN statistics, BN backward sums),
-// fused with the BN finalisation.  A workgroup owns RED_COLS columns; its 8 row lanes sum
+// fused with the BN finalisation.  A workgroup owns RED_COLS columns; its RED_LANES row lanes sum
 // interleaved rows in fp64 and are combined in a fixed order (deterministic).
 // ------------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void colred_kernel(const ColRedLaunch L) {
-  __shared__ double red[8][RED_COLS];
+__global__ __launch_bounds__(1024) void colred_kernel(const ColRedLaunch L) {
+  __shared__ double red[RED_LANES][RED_COLS];
   __shared__ double sum[RED_COLS];
   const int gi = find_group(L);
   const ColRedProb& P = L.p[gi];
@@ -28,13 +28,14 @@ __global__ __launch_bounds__(256) void colred_kernel(const ColRedLaunch L) {
     const float* p = P.part + col;
     int r = rl;
     double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
-    for (; r + 24 < P.rows; r += 32) {
+    constexpr int S = RED_LANES;
+    for (; r + 3 * S < P.rows; r += 4 * S) {
       a0 += (double)p[(long)r * P.ncols];
-      a1 += (double)p[(long)(r + 8) * P.ncols];
-      a2 += (double)p[(long)(r + 16) * P.ncols];
-      a3 += (double)p[(long)(r + 24) * P.ncols];
+      a1 += (double)p[(long)(r + S) * P.ncols];
+      a2 += (double)p[(long)(r + 2 * S) * P.ncols];
+      a3 += (double)p[(long)(r + 3 * S) * P.ncols];
     }
-    for (; r < P.rows; r += 8) a0 += (double)p[(long)r * P.ncols];
+    for (; r < P.rows; r += S) a0 += (double)p[(long)r * P.ncols];
     acc = (a0 + a1) + (a2 + a3);
   }
   red[rl][cl] = acc;
@@ -43,7 +44,7 @@ __global__ __launch_bounds__(256) void colred_kernel(const ColRedLaunch L) {
   if (rl == 0) {
     tot = red[0][cl];
 #pragma unroll
-    for (int k = 1; k < 8; ++k) tot += red[k][cl];
+    for (int k = 1; k < RED_LANES; ++k) tot += red[k][cl];
     sum[cl] = tot;
   }
   __syncthreads();
@@ -384,7 +385,7 @@ __global__ __launch_bounds__(256) void head_reduce_kernel(const float* scratch, 
   } while (0)
 
 int launch_colred(const ColRedLaunch& L, int tiles, hipStream_t s) {
-  hipLaunchKernelGGL(colred_kernel, dim3(tiles), dim3(256), 0, s, L);
+  hipLaunchKernelGGL(colred_kernel, dim3(tiles), dim3(RED_COLS * RED_LANES), 0, s, L);
   return (int)hipGetLastError();
 }
 int launch_colstat(const ColStatLaunch& L, int tiles, int dtype, hipStream_t s) {

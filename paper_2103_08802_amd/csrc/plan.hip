@@ -113,7 +113,6 @@ WgradGeom wgrad_geom(int Co, int K, long M) {
   return g;
 }
 
-int conv_wn(int ncol) { return (ncol % 64 == 0) ? 4 : (ncol % 32 == 0) ? 2 : 1; }
 
 pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, int es, SegP& S) {
   S.part = part;
@@ -278,8 +277,9 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
   for (auto& b : S.bns) {
     const SlotP& sl = S.slots[b.slot];
     const long M = (long)B * sl.H * sl.W;
-    b.fwd_tiles = (int)cdiv(M, COLSTAT_ROWS);
-    b.bwd_tiles = (int)cdiv(M, CONV_BM);
+    b.C = sl.C;
+    b.fwd_tiles = (int)cdiv(M, b.slot == 0 ? COLSTAT_ROWS : conv_bm(b.C));
+    b.bwd_tiles = (int)cdiv(M, conv_bm(b.C));
     if (b.bnact_consumer) {
       const NodeP& c = S.nodes[sl.bn_consumers[0]];
       b.bwd_tiles = (int)cdiv((long)B * c.Ho * c.Wo, BNACT_PIX);
@@ -470,7 +470,7 @@ double conv_bytes(const ConvProb& p, int es, int mode) {
   return b;
 }
 
-int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk) {
+int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk, int wn) {
   pnn_plan* plan = c.plan;
   return grouped<ConvLaunch>(
       probs, [](const ConvProb& p) { return p.tiles_m * p.tiles_n; },
@@ -481,7 +481,7 @@ int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk) {
           by += conv_bytes(L.p[i], plan->es, mode);
         }
         Timer t(plan, 1, c.stream);
-        int e = launch_conv(L, tiles, plan->dtype, mode, gk, c.stream);
+        int e = launch_conv(L, tiles, plan->dtype, mode, gk, wn, c.stream);
         t.done(c.stream, fl, by);
         return e;
       });
@@ -495,12 +495,13 @@ int gather_kind(const ConvProb& p, int es) {
 }
 
 int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode) {
-  std::vector<ConvProb> by[3];
-  for (auto& p : probs) by[gather_kind(p, c.plan->es)].push_back(p);
-  for (int gk = 0; gk < 3; ++gk) {
-    int e = fire_conv_gk(c, by[gk], mode, gk);
-    if (e) return e;
-  }
+  std::vector<ConvProb> by[3][3];
+  for (auto& p : probs) by[gather_kind(p, c.plan->es)][p.wn == 1 ? 0 : p.wn == 2 ? 1 : 2].push_back(p);
+  for (int gk = 0; gk < 3; ++gk)
+    for (int w = 0; w < 3; ++w) {
+      int e = fire_conv_gk(c, by[gk][w], mode, gk, 1 << w);
+      if (e) return e;
+    }
   return PNN_OK;
 }
 
@@ -513,8 +514,18 @@ ConvProb conv_common(const pnn_plan* plan, const NodeP& n) {
   return p;
 }
 
+int log2_or(int v) {
+  if (v <= 0 || (v & (v - 1))) return -1;
+  int l = 0;
+  while ((1 << l) < v) ++l;
+  return l;
+}
+
 void set_tiles(ConvProb& p) {
-  p.tiles_m = (int)cdiv(p.M, CONV_BM);
+  p.cg_log2 = log2_or(p.Cg);
+  p.q_log2 = log2_or(p.Q);
+  p.pq_log2 = log2_or(p.P * p.Q);
+  p.tiles_m = (int)cdiv(p.M, conv_bm(p.ncol));
   p.wn = conv_wn(p.ncol);
   p.tiles_n = p.ncol / (16 * p.wn);
 }
@@ -611,7 +622,7 @@ int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
         if (so.bn >= 0) {
           const BnP& b = S.bns[so.bn];
           const long cnt = (long)B * so.H * so.W;
-          fw.push_back(bn_fwd_red(part_ptr(c, S, so.bn), (int)cdiv(cnt, CONV_BM),
+          fw.push_back(bn_fwd_red(part_ptr(c, S, so.bn), S.bns[so.bn].fwd_tiles,
                                   (const float*)(cp(P.params) + b.p_off), stats_ptr(c, S, so.bn), b.C, cnt));
         }
       }
@@ -699,9 +710,13 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
   }
   int maxL = 0;
   for (auto* s : segs) maxL = std::max(maxL, s->max_level);
+  // split-K weight-gradient sums of level L are reduced in the same launch as the BN backward
+  // finalisation of level L - 1 (independent of it); level L - 1's weight gradient reuses the
+  // partial region only after that launch (stream order)
   char* wpart = c.scratch + plan->wpart_off;
+  std::vector<ColRedProb> pending;
   for (int L = maxL; L >= 1; --L) {
-    // A: gradients of the slots produced at this level
+    // A: gradients of the slots produced at this level (+ the previous level's split-K sums)
     {
       std::vector<ColRedProb> fin;
       std::vector<BnApplyProb> app;
@@ -710,6 +725,8 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
         for (const NodeP& n : S.nodes)
           if (n.level == L && n.dst != S.out) bn_bwd_finalize(c, S, ptrs[i], n.dst, fin, app);
       }
+      fin.insert(fin.end(), pending.begin(), pending.end());
+      pending.clear();
       int e = fire_finalize(c, fin, app);
       if (e) return e;
     }
@@ -733,6 +750,9 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
         p.K = n.k * n.k * n.cin;
         WgradGeom g = wgrad_geom(p.Co, p.K, p.M);
         p.wr = g.wr; p.tiles_co = g.tiles_co; p.tiles_k = g.tiles_k; p.splits = g.splits; p.mchunk = g.mchunk;
+        p.cg_log2 = log2_or(p.Cg);
+        p.q_log2 = log2_or(p.Q);
+        p.pq_log2 = log2_or(p.P * p.Q);
         p.part = (float*)(wpart + woff);
         woff = align256(woff + (size_t)g.splits * p.Co * p.K * 4);
         (n.cin % (16 / es) == 0 ? wg_vec : wg_gen).push_back(p);
@@ -764,7 +784,7 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
           });
       if (e) return e;
     }
-    if (fire_colred(red, c.stream)) return PNN_ERR_HIP;
+    pending = std::move(red);
     // D + E: data gradients (first of two BN consumers, then the rest) and bnact backward
     for (int phase = 0; phase < 2; ++phase) {
       std::vector<ConvProb> dg;
@@ -829,9 +849,9 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
       if (e) return e;
     }
   }
-  // gradient of the segment inputs
+  // gradient of the segment inputs (+ the last level's split-K sums)
   {
-    std::vector<ColRedProb> fin;
+    std::vector<ColRedProb> fin = std::move(pending);
     std::vector<BnApplyProb> app;
     for (size_t i = 0; i < segs.size(); ++i) {
       const SegP& S = *segs[i];

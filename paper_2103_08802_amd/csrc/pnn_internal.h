@@ -47,6 +47,8 @@ struct ConvProb {
   int M, K;
   int tiles_m, tiles_n, wn;
   int flags;
+  int cg_log2;          // log2(Cg) when Cg is a power of two, else -1
+  int q_log2, pq_log2;  // log2(Q), log2(P*Q) when powers of two, else -1
   int tile_begin;
 };
 struct ConvLaunch {
@@ -63,6 +65,7 @@ struct WgradProb {
   int B, H, W, Cg, P, Q, Co, k, stride, pad, M, K;
   int wr;               // tile = (16 wr) output channels x 64 filter columns
   int tiles_co, tiles_k, splits, mchunk;
+  int cg_log2, q_log2, pq_log2;   // as in ConvProb
   int tile_begin;
 };
 struct WgradLaunch {
@@ -94,7 +97,8 @@ struct ColRedLaunch {
   int n;
   ColRedProb p[PNN_MAXG];
 };
-constexpr int RED_COLS = 32;       // columns per column-reduce workgroup (8 row lanes x 32)
+constexpr int RED_COLS = 32;       // columns per column-reduce workgroup
+constexpr int RED_LANES = 32;      // row lanes per column (1024 threads)
 
 // Column statistics of a stored tensor [M][C] (BN of a segment input).
 struct ColStatProb {
@@ -181,8 +185,9 @@ struct AxpyLaunch {
   AxpyProb p[PNN_MAXG];
 };
 
-// gk: 0 = pointwise (1x1, stride 1, pad 0), 1 = vector gather, 2 = element-wise gather
-int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, hipStream_t s);
+// gk: 0 = pointwise (1x1, stride 1, pad 0), 1 = vector gather, 2 = element-wise gather;
+// wn: 16-column sub-tiles per wave (1, 2, 4) shared by every problem of the launch
+int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, hipStream_t s);
 int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s);
 int launch_colred(const ColRedLaunch& L, int tiles, hipStream_t s);
 int launch_colstat(const ColStatLaunch& L, int tiles, int dtype, hipStream_t s);
@@ -198,7 +203,9 @@ int launch_head(const void* yt, const float* eps, const int32_t* labels, float* 
                 int K, int dtype, hipStream_t s);
 
 // tile sizes shared by host and device code
-constexpr int CONV_BM = 128;       // rows of M per conv workgroup
+// rows of M per conv workgroup for a problem with ncol output columns: 64 x (8 / wn)
+inline int conv_wn(int ncol) { return (ncol % 64 == 0) ? 4 : (ncol % 32 == 0) ? 2 : 1; }
+inline int conv_bm(int ncol) { return 64 * (8 / conv_wn(ncol)); }
 constexpr int ELT_TILE = 2048;     // elements per workgroup of elementwise kernels
 constexpr int COLSTAT_ROWS = 128;  // rows per column-statistics workgroup
 constexpr int BNACT_PIX = 32;      // output pixels per bnact workgroup
