@@ -58,6 +58,102 @@ def cpu_baseline(idx, batch=24):
                       f"{dt:.1f} s, fine conv FLOPs / whole-step time"}
 
 
+# sources a kernel family's code and launch shapes come from; a stored traffic figure is void
+# once any of them changes
+KERNEL_SOURCES = {
+    "conv_kernel": ["k_conv.hip", "device_common.h", "pnn_internal.h", "plan.hip"],
+    "wgrad_kernel": ["k_conv.hip", "device_common.h", "pnn_internal.h", "plan.hip"],
+}
+COPY_BYTES = 256 << 20          # the --copy-calibration copy
+
+
+def _sources_sha(kernel):
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2103_08802_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def stored_traffic(kernel):
+    """HBM bytes per launch of ``kernel`` measured with rocprofv3 PMC counters (FETCH_SIZE and
+    WRITE_SIZE passes, each scaled by the same counter's reading for a plain copy of known size),
+    kept in profiles/ with a hash of the kernel's sources; None once those sources have changed."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}.json")
+    if not os.path.exists(path) or kernel not in KERNEL_SOURCES:
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("sources_sha256") != _sources_sha(kernel):
+        return None
+    return rec["bytes_per_launch"]
+
+
+def _short(name):
+    return name.split("(")[0].replace("void ", "").split("<")[0].replace("pnn::", "")
+
+
+def summarize_pmc(fetch_csv, write_csv, kernel, cmd):
+    """Reduce two rocprofv3 --pmc counter CSVs (FETCH_SIZE, WRITE_SIZE; KiB per dispatch) of a
+    ``--copy-calibration`` run to HBM bytes per launch of ``kernel`` and store the result."""
+    import csv
+
+    def load(p):
+        per, copy = {}, None
+        for r in csv.DictReader(open(p)):
+            v = float(r["Counter_Value"]) * 1024.0
+            n = _short(r["Kernel_Name"])
+            if n == "__amd_rocclr_copyBuffer":
+                copy = max(copy or 0.0, v)        # the largest copy is the calibration copy
+            per.setdefault(n, []).append(v)
+        return per, copy
+
+    fe, fcopy = load(fetch_csv)
+    wr, wcopy = load(write_csv)
+    ffac, wfac = COPY_BYTES / fcopy, COPY_BYTES / wcopy
+    fb = sum(fe[kernel]) / len(fe[kernel]) * ffac
+    wb = sum(wr[kernel]) / len(wr[kernel]) * wfac
+    rec = {"kernel": kernel, "bytes_per_launch": round(fb + wb), "fetch_bytes_per_launch": round(fb),
+           "write_bytes_per_launch": round(wb), "dispatches": len(fe[kernel]),
+           "fetch_scale": round(ffac, 4), "write_scale": round(wfac, 4),
+           "calibration": f"one {COPY_BYTES >> 20} MiB device-to-device copy reads and writes "
+                          f"{COPY_BYTES} bytes; FETCH_SIZE read {fcopy:.0f}, WRITE_SIZE {wcopy:.0f}",
+           "command": cmd, "sources": KERNEL_SOURCES[kernel], "sources_sha256": _sources_sha(kernel)}
+    out = os.path.join(ROOT, "profiles", f"traffic_{kernel}.json")
+    with open(out, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(json.dumps(rec))
+
+
+def summarize_trace(stats_csv, trace_csv, out_md, title, cmd):
+    """Markdown summary of a rocprofv3 --kernel-trace --stats run: the per-instantiation statistics
+    and, per kernel family, the average duration over all its dispatches."""
+    import csv
+    rows = list(csv.DictReader(open(stats_csv)))
+    fam = {}
+    for r in csv.DictReader(open(trace_csv)):
+        n = _short(r["Kernel_Name"])
+        d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        t = fam.setdefault(n, [0, 0.0])
+        t[0] += 1
+        t[1] += d
+    with open(out_md, "w") as f:
+        f.write(f"# {title}\n\nCommand (from the repository root, on one MI355X):\n\n```\n{cmd}\n```\n\n")
+        f.write("Per kernel family, all dispatches of the run (warm-up, timed and instrumented steps):\n\n")
+        f.write("| family | dispatches | avg us | total ms |\n|---|---:|---:|---:|\n")
+        for n, (c, t) in sorted(fam.items(), key=lambda kv: -kv[1][1]):
+            f.write(f"| `{n}` | {c} | {t / c:.2f} | {t / 1e3:.1f} |\n")
+        f.write("\nPer instantiation (rocprofv3 --stats):\n\n")
+        f.write("| kernel | calls | avg us | min us | max us | total % |\n|---|---:|---:|---:|---:|---:|\n")
+        for r in rows[:24]:
+            name = r["Name"].split("(")[0].replace("void ", "")
+            f.write(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                    f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                    f"{float(r['Percentage']):.2f} |\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -67,7 +163,20 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 256 MiB device copy first (reference for HBM byte counters)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no GPU work: store HBM bytes per launch of --kernel from two PMC runs")
+    ap.add_argument("--summarize-trace", nargs=3, metavar=("STATS_CSV", "TRACE_CSV", "OUT_MD"),
+                    help="no GPU work: write a markdown summary of a kernel-trace run")
+    ap.add_argument("--kernel", default="conv_kernel")
+    ap.add_argument("--title", default="")
+    ap.add_argument("--cmd", default="", help="command that produced the CSVs (recorded)")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, args.kernel, args.cmd)
+        return
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace, args.title, args.cmd)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs the whole parareal network on ONE GPU (all N "
                           "fine sub-networks as grouped launches); --gpus must be 1"}))
@@ -127,7 +236,8 @@ def main():
     d = fam[dom]
     achieved = d["bytes"] / (d["ms"] * 1e-3) / 1e9
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": stored_traffic(dom),
+            "algorithmic_bytes_per_launch": round(d["bytes"] / max(d["launches"], 1)),
             "kernel": dom, "avg_launch_us": round(d["ms"] * 1e3 / max(d["launches"], 1), 2),
             "mfma_tflops": round(d["flops"] / (d["ms"] * 1e-3) / 1e12, 2)}
 

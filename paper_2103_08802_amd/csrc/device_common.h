@@ -39,8 +39,7 @@ struct Chunk {
 };
 
 template <typename T>
-__device__ __forceinline__ void load_chunk(const void* base, long idx, Chunk<T>& c) {
-  uint4 u = *(const uint4*)((const T*)base + idx);
+__device__ __forceinline__ void unpack_chunk(uint4 u, Chunk<T>& c) {
   if constexpr (sizeof(T) == 4) {
     c.v[0] = __uint_as_float(u.x);
     c.v[1] = __uint_as_float(u.y);
@@ -54,6 +53,11 @@ __device__ __forceinline__ void load_chunk(const void* base, long idx, Chunk<T>&
       c.v[2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
     }
   }
+}
+
+template <typename T>
+__device__ __forceinline__ void load_chunk(const void* base, long idx, Chunk<T>& c) {
+  unpack_chunk<T>(*(const uint4*)((const T*)base + idx), c);
 }
 
 template <typename T>

@@ -195,6 +195,25 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
 #pragma unroll
     for (int j = 0; j < WN; ++j) acc[wm][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // The epilogue's streamed operand (residual / skip gradient, or the BN input of the ReLU mask) is
+  // fetched before the K loop so that it overlaps the operand gathers.  Each thread owns fixed
+  // 16-byte column chunks of rows tid / ncc + k * rpp.
+  constexpr int BNc = 16 * WN;
+  constexpr int ncc = BNc / VE;       // column chunks per row
+  constexpr int rpp = 256 / ncc;      // rows per pass
+  constexpr int NCH = BM / rpp;       // chunks per thread
+  const int cc = tid % ncc;
+  const int c0 = cc * VE;
+  const void* pf = (MODE == MODE_FWD) ? P.res
+                   : ((P.flags & EPI_STORE_F32) ? nullptr : (bnmask ? P.zsrc : P.res));
+  uint4 pre[NCH];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const int m = tm * BM + tid / ncc + k * rpp;
+    pre[k] = (pf != nullptr && m < P.M) ? *(const uint4*)((const T*)pf + (long)m * P.ncol + n0 + c0)
+                                        : make_uint4(0, 0, 0, 0);
+  }
+
   for (int kk = 0; kk < P.K; kk += KS) {
     const int k0 = kk + VE * grp;
     Frag<T> a[WM];
@@ -219,27 +238,24 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
         acc_s[(wave * 16 * WM + wm * 16 + grp * 4 + i) * LDA + j * 16 + r16] = acc[wm][j][i];
   __syncthreads();
 
-  constexpr int BNc = 16 * WN;
-  constexpr int ncc = BNc / VE;       // column chunks per row
-  constexpr int rpp = 256 / ncc;      // rows per pass
-  const int cc = tid % ncc;
-  const int c0 = cc * VE;
   float s1[VE], s2[VE];
 #pragma unroll
   for (int e = 0; e < VE; ++e) s1[e] = s2[e] = 0.f;
-  for (int r = tid / ncc; r < BM; r += rpp) {
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const int r = tid / ncc + k * rpp;
     const int m = tm * BM + r;
     if (m >= P.M) break;
+    Chunk<T> pfc;
+    unpack_chunk<T>(pre[k], pfc);
     const long idx = (long)m * P.ncol + n0 + c0;
     float v[VE];
 #pragma unroll
     for (int e = 0; e < VE; ++e) v[e] = acc_s[r * LDA + c0 + e];
     if constexpr (MODE == MODE_FWD) {
       if (P.res) {
-        Chunk<T> x;
-        load_chunk<T>(P.res, idx, x);
 #pragma unroll
-        for (int e = 0; e < VE; ++e) v[e] += x.v[e];
+        for (int e = 0; e < VE; ++e) v[e] += pfc.v[e];
       }
       if (P.ext) {
         Chunk<T> x;
@@ -266,8 +282,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
 #pragma unroll
         for (int e = 0; e < VE; e += 4) *(float4*)(P.out32 + idx + e) = make_float4(v[e], v[e + 1], v[e + 2], v[e + 3]);
       } else if (bnmask) {
-        Chunk<T> z;
-        load_chunk<T>(P.zsrc, idx, z);
+        const Chunk<T>& z = pfc;
 #pragma unroll
         for (int e = 0; e < VE; ++e) {
           const float4 b = bn_s[c0 + e];
@@ -283,10 +298,8 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
         }
       } else {
         if (P.res) {
-          Chunk<T> x;
-          load_chunk<T>(P.res, idx, x);
 #pragma unroll
-          for (int e = 0; e < VE; ++e) v[e] += x.v[e];
+          for (int e = 0; e < VE; ++e) v[e] += pfc.v[e];
         }
         store_chunk<T>(P.out, idx, v);
       }
