@@ -131,6 +131,15 @@ __device__ __forceinline__ int find_group(const Launch& L) {
 // x / d and x % d for a divisor given with log2(d) (>= 0) or as a plain value (lg < 0)
 __device__ __forceinline__ int div_l2(int x, int d, int lg) { return lg >= 0 ? (x >> lg) : x / d; }
 
+// q = x / d, r = x % d for 0 <= x < 2^22 and 0 < d < 2^22, with rd = 1.0f / d: the float quotient
+// is within one of the true one and the remainder check corrects it.
+__device__ __forceinline__ void divmod_small(int x, int d, float rd, int& q, int& r) {
+  q = (int)((float)x * rd);
+  r = x - q * d;
+  if (r < 0) { --q; r += d; }
+  else if (r >= d) { ++q; r -= d; }
+}
+
 // (r, s) of tap t of a k x k filter, k in {1, 3}
 __device__ __forceinline__ void tap_rs(int t, int k, int& r, int& s) {
   r = (k == 3) ? ((t * 11) >> 5) : 0;

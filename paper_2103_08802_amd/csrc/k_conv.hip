@@ -18,13 +18,17 @@ namespace pnn {
 //
 // GK = gather kind: GK_POINT  1x1 / stride 1 / pad 0 (row m of A is row m of the input),
 //                   GK_VEC    any geometry, channels a multiple of the 16-byte chunk,
-//                   GK_SCALAR any geometry, element-wise gather (e.g. 3-channel images).
+//                   GK_SCALAR any geometry, element-wise gather (e.g. 3-channel images),
+//                   GK_HALO   3x3 / stride 1 / pad 1 (forward, and its data gradient, which is the
+//                             same stencil with the taps mirrored): the tile's input rows plus a
+//                             one-pixel halo are staged in LDS once, the filter column of each wave
+//                             is held in registers, and every K step reads A from LDS.
 // The BN prologue's (scale, shift) and the data-gradient epilogue's BN statistics are staged in LDS
 // once per workgroup.  The epilogue stages the fp32 tile through LDS so that every thread owns
 // 16-byte column chunks: residual / mask-source loads and output stores are 16-byte vectors, and
 // each thread's BN partial sums cover fixed columns (combined in a fixed order).
 // ------------------------------------------------------------------------------------------------
-enum { GK_POINT = 0, GK_VEC = 1, GK_SCALAR = 2 };
+enum { GK_POINT = 0, GK_VEC = 1, GK_SCALAR = 2, GK_HALO = 3 };
 constexpr int CONV_PRO_MAXC = 512;
 
 template <typename T, int MODE, int GK>
@@ -134,6 +138,123 @@ __device__ __forceinline__ void load_b(const ConvProb& P, int col, int k0, Frag<
   }
 }
 
+
+// GK_HALO main loop.  The tile's BM output rows are whole image rows (BM a multiple of Q): either
+// R = BM / Q rows of one image or BM / PQ whole images.  LDS holds those rows plus a one-pixel halo
+// of the (activated, for the forward prologue) input, pixel rows padded by 16 bytes so that the 16
+// consecutive pixels of an MFMA fragment fall on distinct banks; padding pixels are zeros.  Wave w
+// owns column sub-tile w % WN and 8 row sub-tiles; its filter fragments for all K steps (at most
+// CONV_HALO_NKB) are loaded into registers before the LDS fill completes.  Steps past K read a
+// valid A position; the filter fragment there is zero.
+template <typename T, int MODE, int WM>
+__device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, T* halo, int tm, int n0,
+                                          f32x4 (&acc)[WM][8 / WM]) {
+  constexpr int VE = St<T>::VE;
+  constexpr int KS = 4 * VE;
+  constexpr int WN = 8 / WM;
+  constexpr int BM = 64 * WM;
+  constexpr int PADE = 16 / sizeof(T);
+  constexpr int NKB = CONV_HALO_NKB;
+  constexpr int NL = 8;                      // halo chunks in flight per thread
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int PQ = P.P * P.Q;
+  const int QH = P.Q + 2;
+  const int PS = P.Cg + PADE;
+  const bool multi = BM > PQ;
+  const int R = multi ? P.P : BM / P.Q;
+  const int RH = R + 2;
+  const int nimg = multi ? BM / PQ : 1;
+  const int m0 = tm * BM;
+  const int n_first = div_l2(m0, PQ, P.pq_log2);
+  const int p0 = multi ? 0 : div_l2(m0 - n_first * PQ, P.Q, P.q_log2);
+  const int cpp = P.Cg / VE;
+  const int img_px = RH * QH;
+  const int total = nimg * img_px * cpp;
+  const int ct = wave % WN, rg = wave / WN;
+  const int nsteps = (P.K + KS - 1) / KS;
+
+  Frag<T> bq[NKB];
+#pragma unroll
+  for (int s = 0; s < NKB; ++s) {
+    if (s < nsteps) load_b<T, true>(P, n0 + ct * 16 + r16, s * KS + VE * grp, bq[s]);
+    else bq[s].zero();
+  }
+
+  const float r_cpp = 1.0f / cpp, r_img = 1.0f / img_px, r_qh = 1.0f / QH;
+  for (int base = 0; base < total; base += 256 * NL) {
+    uint4 v[NL];
+    int off[NL], cv[NL];
+    bool ok[NL];
+#pragma unroll
+    for (int u = 0; u < NL; ++u) {
+      const int idx = base + u * 256 + tid;
+      int pix, ch, i, rem, y, x;
+      divmod_small(idx, cpp, r_cpp, pix, ch);
+      if (nimg > 1) divmod_small(pix, img_px, r_img, i, rem);
+      else { i = 0; rem = pix; }
+      divmod_small(rem, QH, r_qh, y, x);
+      const int n = n_first + i, ih = p0 - 1 + y, iw = x - 1;
+      ok[u] = idx < total && n < P.B && (unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W;
+      off[u] = idx < total ? pix * PS + ch * VE : -1;
+      cv[u] = ch * VE;
+      const long g = ok[u] ? (((long)n * P.H + ih) * P.W + iw) * P.Cg + ch * VE : 0;
+      v[u] = *(const uint4*)((const T*)P.in + g);
+    }
+#pragma unroll
+    for (int u = 0; u < NL; ++u) {
+      if (off[u] < 0) continue;
+      uint4 w = make_uint4(0, 0, 0, 0);
+      if (ok[u]) {
+        if (MODE == MODE_FWD && P.pro != nullptr) {
+          Chunk<T> c;
+          unpack_chunk<T>(v[u], c);
+          float f[VE];
+#pragma unroll
+          for (int e = 0; e < VE; ++e) f[e] = fmaxf(fmaf(c.v[e], pro[cv[u] + e].x, pro[cv[u] + e].y), 0.0f);
+          store_chunk<T>(&w, 0, f);
+        } else {
+          w = v[u];
+        }
+      }
+      *(uint4*)(halo + off[u]) = w;
+    }
+  }
+
+  int rb[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    const int lm = (rg * 8 + t) * 16 + r16;
+    const int i = multi ? div_l2(lm, PQ, P.pq_log2) : 0;
+    const int rem = lm - i * R * P.Q;
+    const int pl = div_l2(rem, P.Q, P.q_log2);
+    const int ql = rem - pl * P.Q;
+    rb[t] = (i * RH + pl) * QH + ql;
+  }
+  __syncthreads();
+
+#pragma unroll
+  for (int s = 0; s < NKB; ++s) {
+    if (s < nsteps) {
+      int k0 = s * KS + VE * grp;
+      if (k0 >= P.K) k0 = 0;
+      const int tap = div_l2(k0, P.Cg, P.cg_log2);
+      const int c0 = k0 - tap * P.Cg;
+      int r, q;
+      tap_rs(tap, 3, r, q);
+      const int toff = (MODE == MODE_FWD) ? (r * QH + q) : ((2 - r) * QH + (2 - q));
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        Frag<T> a;
+        a.from_raw(*(const uint4*)(halo + (rb[t] + toff) * PS + c0));
+        mma(a, bq[s], acc[t / WN][t % WN]);
+      }
+    }
+  }
+  __syncthreads();                            // the halo region is reused by the epilogue
+}
+
 // WM row sub-tiles of 16 per wave, WN = 8 / WM column sub-tiles: a workgroup owns a
 // (64 WM) x (16 WN) tile, so narrow problems (16 columns) get 512-row tiles and keep eight
 // operand fragments in flight per wave.
@@ -144,9 +265,10 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   constexpr int WN = 8 / WM;
   constexpr int BM = 64 * WM;
   constexpr int LDA = 16 * WN + 4;
+  constexpr int ACC_WORDS = (GK == GK_HALO && CONV_HALO_BYTES / 4 > BM * LDA) ? CONV_HALO_BYTES / 4 : BM * LDA;
   __shared__ float2 pro_s[CONV_PRO_MAXC];
   __shared__ float4 bn_s[64];
-  __shared__ float acc_s[BM * LDA];
+  __shared__ __attribute__((aligned(16))) float acc_s[ACC_WORDS];
 
   const int gi = find_group(L);
   const ConvProb& P = L.p[gi];
@@ -174,7 +296,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   int rm[WM], rn[WM], rp[WM], rq[WM];
   bool rv[WM];
 #pragma unroll
-  for (int wm = 0; wm < WM; ++wm) {
+  for (int wm = 0; wm < WM && GK != GK_HALO; ++wm) {
     const int m = mw + wm * 16 + r16;
     rv[wm] = m < P.M;
     const int mm = rv[wm] ? m : 0;
@@ -214,7 +336,8 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
                                         : make_uint4(0, 0, 0, 0);
   }
 
-  for (int kk = 0; kk < P.K; kk += KS) {
+  if constexpr (GK == GK_HALO) conv_halo<T, MODE, WM>(P, pro_s, (T*)acc_s, tm, n0, acc);
+  for (int kk = 0; kk < P.K && GK != GK_HALO; kk += KS) {
     const int k0 = kk + VE * grp;
     Frag<T> a[WM];
 #pragma unroll
@@ -232,10 +355,13 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
 #pragma unroll
   for (int wm = 0; wm < WM; ++wm)
 #pragma unroll
-    for (int j = 0; j < WN; ++j)
+    for (int j = 0; j < WN; ++j) {
+      // row / column sub-tile of acc[wm][j]: waves split rows, or (GK_HALO) columns first
+      const int rt = (GK == GK_HALO) ? (wave / WN) * 8 + wm * WN + j : wave * WM + wm;
+      const int ct = (GK == GK_HALO) ? wave % WN : j;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        acc_s[(wave * 16 * WM + wm * 16 + grp * 4 + i) * LDA + j * 16 + r16] = acc[wm][j][i];
+      for (int i = 0; i < 4; ++i) acc_s[(rt * 16 + grp * 4 + i) * LDA + ct * 16 + r16] = acc[wm][j][i];
+    }
   __syncthreads();
 
   float s1[VE], s2[VE];
@@ -374,12 +500,17 @@ __device__ __forceinline__ WgCol wg_col(const WgradProb& P, int kidx) {
   return c;
 }
 
+// One 16-byte activation chunk of row m at the thread's filter column.  VEC: the raw stored values
+// (pending = true when the BN prologue still has to be applied, once the load has landed, so that a
+// stage's loads stay in flight across the previous stage's MMAs); padding chunks are zeros of the
+// activated tensor (pending = false).  Element-wise gather: final values.
 template <typename T, bool VEC>
 __device__ __forceinline__ uint4 wg_gather(const WgradProb& P, const float2* pro, int m, const WgCol& cl,
-                                           int col) {
+                                           int col, bool& pending) {
   constexpr int VE = St<T>::VE;
   const int PQ = P.P * P.Q;
   uint4 zero = make_uint4(0, 0, 0, 0);
+  pending = false;
   if (m >= P.M || cl.kidx >= P.K) return zero;
   const int n = div_l2(m, PQ, P.pq_log2);
   const int rem = m - n * PQ;
@@ -389,15 +520,8 @@ __device__ __forceinline__ uint4 wg_gather(const WgradProb& P, const float2* pro
     const int ih = p * P.stride + cl.r - P.pad, iw = q * P.stride + cl.s - P.pad;
     if ((unsigned)ih >= (unsigned)P.H || (unsigned)iw >= (unsigned)P.W) return zero;
     const long idx = (((long)n * P.H + ih) * P.W + iw) * P.Cg + cl.c0;
-    if (P.pro == nullptr) return *(const uint4*)((const T*)P.in + idx);
-    Chunk<T> c;
-    load_chunk<T>(P.in, idx, c);
-    float v[VE];
-#pragma unroll
-    for (int e = 0; e < VE; ++e) v[e] = fmaxf(fmaf(c.v[e], pro[col + e].x, pro[col + e].y), 0.0f);
-    uint4 u;
-    store_chunk<T>(&u, 0, v);
-    return u;
+    pending = P.pro != nullptr;
+    return *(const uint4*)((const T*)P.in + idx);
   } else {
     float v[VE];
 #pragma unroll
@@ -496,6 +620,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
   const int acol = (tid % acpr) * VE;
   const WgCol wcol = wg_col(P, kk0 + acol);
   uint4 ga[C::GC], aa[C::AC];
+  uint32_t apend = 0;                  // bit i: aa[i] still needs the BN prologue
 
   auto load_stage = [&](int mc) {
 #pragma unroll
@@ -508,11 +633,14 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
         if (m < m_end) ga[i] = *(const uint4*)((const T*)P.g + (long)m * P.Co + co0 + cc);
       }
     }
+    apend = 0;
 #pragma unroll
     for (int i = 0; i < C::AC; ++i) {
       const int row = (tid + i * 256) / acpr;    // the thread's column acol is the same for every i
       const int m = mc + row;
-      aa[i] = m < m_end ? wg_gather<T, VEC>(P, pro_s, m, wcol, acol) : make_uint4(0, 0, 0, 0);
+      bool pend = false;
+      aa[i] = m < m_end ? wg_gather<T, VEC>(P, pro_s, m, wcol, acol, pend) : make_uint4(0, 0, 0, 0);
+      apend |= (pend ? 1u : 0u) << i;
     }
   };
   auto store_stage = [&]() {
@@ -528,7 +656,16 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
     for (int i = 0; i < C::AC; ++i) {
       const int idx = tid + i * 256;
       const int row = idx / acpr, cc = (idx - row * acpr) * VE;
-      lds_store8<T>(la + row * C::RSA + cc, aa[i]);
+      uint4 u = aa[i];
+      if ((apend >> i) & 1u) {
+        Chunk<T> c;
+        unpack_chunk<T>(u, c);
+        float v[VE];
+#pragma unroll
+        for (int e = 0; e < VE; ++e) v[e] = fmaxf(fmaf(c.v[e], pro_s[acol + e].x, pro_s[acol + e].y), 0.0f);
+        store_chunk<T>(&u, 0, v);
+      }
+      lds_store8<T>(la + row * C::RSA + cc, u);
     }
   };
 
@@ -594,6 +731,8 @@ static void launch_conv_w(const ConvLaunch& L, int tiles, int gk, hipStream_t s)
     hipLaunchKernelGGL((conv_kernel<T, MODE, GK_POINT, WM>), dim3(tiles), dim3(256), 0, s, L);
   else if (gk == GK_VEC)
     hipLaunchKernelGGL((conv_kernel<T, MODE, GK_VEC, WM>), dim3(tiles), dim3(256), 0, s, L);
+  else if (gk == GK_HALO)
+    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_HALO, WM>), dim3(tiles), dim3(256), 0, s, L);
   else
     hipLaunchKernelGGL((conv_kernel<T, MODE, GK_SCALAR, WM>), dim3(tiles), dim3(256), 0, s, L);
 }

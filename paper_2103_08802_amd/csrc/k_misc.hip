@@ -15,10 +15,52 @@ namespace pnn {
 // interleaved rows in fp64 and are combined in a fixed order (deterministic).
 // ------------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void colred_kernel(const ColRedLaunch L) {
-  __shared__ double red[RED_LANES][RED_COLS];
+  __shared__ double red[2 * RED_LANES][RED_COLS];   // RED_SUM uses all of it, BN modes the first half
   __shared__ double sum[RED_COLS];
   const int gi = find_group(L);
   const ColRedProb& P = L.p[gi];
+  if (P.mode == RED_SUM) {
+    // 2^rl_log2 row lanes x (1024 >> rl_log2) column pairs; lane l sums rows l, l + RL, ... in
+    // order, then lane 0 adds the lanes' sums in lane order
+    const int RL = 1 << P.rl_log2;
+    const int CP = 1024 >> P.rl_log2;
+    const int rl = threadIdx.x >> (10 - P.rl_log2);
+    const int cp = threadIdx.x & (CP - 1);
+    const int col = (blockIdx.x - P.tile_begin) * 2 * CP + 2 * cp;
+    double a0 = 0.0, a1 = 0.0;
+    if (col < P.ncols) {
+      const float* p = P.part + col;
+      int r = rl;
+      for (; r + 3 * RL < P.rows; r += 4 * RL) {
+        float2 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = *(const float2*)(p + (long)(r + u * RL) * P.ncols);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          a0 += (double)v[u].x;
+          a1 += (double)v[u].y;
+        }
+      }
+      for (; r < P.rows; r += RL) {
+        const float2 v = *(const float2*)(p + (long)r * P.ncols);
+        a0 += (double)v.x;
+        a1 += (double)v.y;
+      }
+    }
+    double* red2 = &red[0][0];
+    red2[2 * threadIdx.x] = a0;
+    red2[2 * threadIdx.x + 1] = a1;
+    __syncthreads();
+    if (rl == 0 && col < P.ncols) {
+      for (int k = 1; k < RL; ++k) {
+        a0 += red2[2 * (k * CP + cp)];
+        a1 += red2[2 * (k * CP + cp) + 1];
+      }
+      P.dst[col] = (float)a0;
+      P.dst[col + 1] = (float)a1;
+    }
+    return;
+  }
   const int c0 = (blockIdx.x - P.tile_begin) * RED_COLS;
   const int cl = threadIdx.x % RED_COLS;
   const int rl = threadIdx.x / RED_COLS;
@@ -49,10 +91,6 @@ __global__ __launch_bounds__(1024) void colred_kernel(const ColRedLaunch L) {
   }
   __syncthreads();
   if (rl != 0 || col >= P.ncols) return;
-  if (P.mode == RED_SUM) {
-    P.dst[col] = (float)tot;
-    return;
-  }
   // BN modes: column 2c holds the first sum of channel c, column 2c+1 the second
   if (cl & 1) return;
   const int C = P.ncols / 2;

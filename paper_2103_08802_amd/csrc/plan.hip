@@ -436,7 +436,7 @@ int grouped(std::vector<Prob>& probs, TilesOf tiles_of, Fire fire) {
 
 int fire_colred(std::vector<ColRedProb>& probs, hipStream_t s) {
   return grouped<ColRedLaunch>(
-      probs, [](const ColRedProb& p) { return (int)cdiv(p.ncols, RED_COLS); },
+      probs, [](const ColRedProb& p) { return colred_tiles(p.ncols, p.mode, p.rl_log2); },
       [&](const ColRedLaunch& L, int tiles, size_t) { return launch_colred(L, tiles, s); });
 }
 
@@ -487,17 +487,33 @@ int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk, i
       });
 }
 
-// Gather kind of a convolution problem: 0 pointwise, 1 vector gather, 2 element-wise gather.
+// A 3x3 / stride 1 / pad 1 problem whose row tiles are whole image rows, whose input rows plus
+// halo fit CONV_HALO_BYTES of LDS and whose filter columns fit CONV_HALO_NKB K steps of registers.
+bool halo_ok(const ConvProb& p, int es) {
+  if (p.k != 3 || p.stride != 1 || p.pad != 1 || p.H != p.P || p.W != p.Q) return false;
+  const int ve = 16 / es;
+  if (p.K > 4 * ve * CONV_HALO_NKB) return false;
+  const int bm = 64 * (8 / p.wn);
+  const int pq = p.P * p.Q;
+  if (bm % p.Q != 0 || (pq % bm != 0 && bm % pq != 0)) return false;
+  const long nimg = bm > pq ? bm / pq : 1;
+  const long rows = bm > pq ? p.P : bm / p.Q;
+  return nimg * (rows + 2) * (p.Q + 2) * (long)(p.Cg + ve) * es <= CONV_HALO_BYTES;
+}
+
+// Gather kind of a convolution problem: 0 pointwise, 1 vector gather, 2 element-wise gather,
+// 3 halo tile.
 int gather_kind(const ConvProb& p, int es) {
   if (p.Cg % (16 / es) != 0) return 2;
   if (p.k == 1 && p.stride == 1 && p.pad == 0) return 0;
+  if (halo_ok(p, es)) return 3;
   return 1;
 }
 
 int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode) {
-  std::vector<ConvProb> by[3][3];
+  std::vector<ConvProb> by[4][3];
   for (auto& p : probs) by[gather_kind(p, c.plan->es)][p.wn == 1 ? 0 : p.wn == 2 ? 1 : 2].push_back(p);
-  for (int gk = 0; gk < 3; ++gk)
+  for (int gk = 0; gk < 4; ++gk)
     for (int w = 0; w < 3; ++w) {
       int e = fire_conv_gk(c, by[gk][w], mode, gk, 1 << w);
       if (e) return e;
@@ -763,6 +779,7 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
         r.rows = g.splits;
         r.ncols = p.Co * p.K;
         r.mode = RED_SUM;
+        r.rl_log2 = red_sum_rl_log2(r.rows);
         red.push_back(r);
       }
     }

@@ -75,7 +75,8 @@ struct WgradLaunch {
 
 // Column reduction of tile partials part[rows][ncols] in a fixed order (fp64 sums), fused with what
 // the sums are for:
-//   RED_SUM     dst[c] = sum_r part[r][c]                               (split-K weight gradients)
+//   RED_SUM     dst[c] = sum_r part[r][c]                               (split-K weight gradients;
+//               ncols even, two columns per thread, rows split over 2^rl_log2 lanes)
 //   RED_BN_FWD  ncols = 2C, part[r][c][2] = (sum z, sum z^2) -> mean, invstd, scale, shift [4][C]
 //   RED_BN_BWD  ncols = 2C, part[r][c][2] = (sum dbn, sum dbn*xhat) -> dbeta, dgamma and the
 //               apply coefficients c1 = gamma * invstd, mb = dbeta / M, mbx = dgamma / M  [3][C]
@@ -91,6 +92,7 @@ struct ColRedProb {
   float* coef;
   long count;            // BN: number of rows M of the normalised tensor
   int rows, ncols, mode;
+  int rl_log2;           // RED_SUM: log2 of the row lanes per column pair (0..5)
   int tile_begin;
 };
 struct ColRedLaunch {
@@ -99,6 +101,16 @@ struct ColRedLaunch {
 };
 constexpr int RED_COLS = 32;       // columns per column-reduce workgroup
 constexpr int RED_LANES = 32;      // row lanes per column (1024 threads)
+// RED_SUM row lanes: about eight rows per lane, at most 32 lanes
+inline int red_sum_rl_log2(int rows) {
+  int l = 0;
+  while (l < 5 && (8 << l) < rows) ++l;
+  return l;
+}
+inline int colred_tiles(int ncols, int mode, int rl_log2) {
+  const int cols = mode == RED_SUM ? (2048 >> rl_log2) : RED_COLS;
+  return (ncols + cols - 1) / cols;
+}
 
 // Column statistics of a stored tensor [M][C] (BN of a segment input).
 struct ColStatProb {
@@ -185,7 +197,8 @@ struct AxpyLaunch {
   AxpyProb p[PNN_MAXG];
 };
 
-// gk: 0 = pointwise (1x1, stride 1, pad 0), 1 = vector gather, 2 = element-wise gather;
+// gk: 0 = pointwise (1x1, stride 1, pad 0), 1 = vector gather, 2 = element-wise gather,
+//     3 = 3x3 / stride 1 / pad 1 through an LDS halo tile;
 // wn: 16-column sub-tiles per wave (1, 2, 4) shared by every problem of the launch
 int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, hipStream_t s);
 int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s);
@@ -209,6 +222,8 @@ inline int conv_bm(int ncol) { return 64 * (8 / conv_wn(ncol)); }
 constexpr int ELT_TILE = 2048;     // elements per workgroup of elementwise kernels
 constexpr int COLSTAT_ROWS = 128;  // rows per column-statistics workgroup
 constexpr int BNACT_PIX = 32;      // output pixels per bnact workgroup
+constexpr int CONV_HALO_BYTES = 40960;  // LDS of a 3x3 halo tile (input rows + halo, padded pixels)
+constexpr int CONV_HALO_NKB = 18;       // K steps whose filter fragments a wave keeps in registers
 
 
 }  // namespace pnn
