@@ -141,8 +141,9 @@ __device__ __forceinline__ void load_b(const ConvProb& P, int col, int k0, Frag<
 
 // GK_HALO main loop.  The tile's BM output rows are whole image rows (BM a multiple of Q): either
 // R = BM / Q rows of one image or BM / PQ whole images.  LDS holds those rows plus a one-pixel halo
-// of the (activated, for the forward prologue) input, pixel rows padded by 16 bytes so that the 16
-// consecutive pixels of an MFMA fragment fall on distinct banks; padding pixels are zeros.  Wave w
+// of the (activated, for the forward prologue) input; padding pixels are zeros.  A pixel's Cg
+// channels are followed by 0, 1 or 2 unused 16-byte chunks (conv_halo_pad) so that each half-wave's
+// A reads (16 pixels x an aligned chunk pair) fall on distinct LDS banks.  Wave w
 // owns column sub-tile w % WN and 8 row sub-tiles; its filter fragments for all K steps (at most
 // CONV_HALO_NKB) are loaded into registers before the LDS fill completes.  Steps past K read a
 // valid A position; the filter fragment there is zero.
@@ -153,7 +154,6 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
   constexpr int KS = 4 * VE;
   constexpr int WN = 8 / WM;
   constexpr int BM = 64 * WM;
-  constexpr int PADE = 16 / sizeof(T);
   constexpr int NKB = CONV_HALO_NKB;
   constexpr int NL = 8;                      // halo chunks in flight per thread
   const int tid = threadIdx.x;
@@ -161,7 +161,7 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
   const int r16 = lane & 15, grp = lane >> 4;
   const int PQ = P.P * P.Q;
   const int QH = P.Q + 2;
-  const int PS = P.Cg + PADE;
+  const int PS = P.Cg + conv_halo_pad(P.Cg / VE, P.Q) * VE;
   const bool multi = BM > PQ;
   const int R = multi ? P.P : BM / P.Q;
   const int RH = R + 2;
@@ -267,7 +267,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   constexpr int LDA = 16 * WN + 4;
   constexpr int ACC_WORDS = (GK == GK_HALO && CONV_HALO_BYTES / 4 > BM * LDA) ? CONV_HALO_BYTES / 4 : BM * LDA;
   __shared__ float2 pro_s[CONV_PRO_MAXC];
-  __shared__ float4 bn_s[64];
+  __shared__ __attribute__((aligned(16))) float bn_s[4][64];   // mean, invstd, scale, shift
   __shared__ __attribute__((aligned(16))) float acc_s[ACC_WORDS];
 
   const int gi = find_group(L);
@@ -289,7 +289,8 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
     for (int c = tid; c < P.Cg; c += 256) pro_s[c] = make_float2(P.pro[c], P.pro[P.Cg + c]);
   if (bnmask && tid < 16 * WN) {
     const int col = n0 + tid;
-    bn_s[tid] = make_float4(P.bnst[col], P.bnst[P.ncol + col], P.bnst[2 * P.ncol + col], P.bnst[3 * P.ncol + col]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) bn_s[k][tid] = P.bnst[k * P.ncol + col];
   }
   __syncthreads();
 
@@ -409,18 +410,22 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
         for (int e = 0; e < VE; e += 4) *(float4*)(P.out32 + idx + e) = make_float4(v[e], v[e + 1], v[e + 2], v[e + 3]);
       } else if (bnmask) {
         const Chunk<T>& z = pfc;
+        float mu[VE], is[VE], sc[VE], sh[VE];
 #pragma unroll
-        for (int e = 0; e < VE; ++e) {
-          const float4 b = bn_s[c0 + e];
-          v[e] = fmaf(z.v[e], b.z, b.w) > 0.f ? v[e] : 0.f;
+        for (int e = 0; e < VE; e += 4) {
+          *(float4*)&mu[e] = *(const float4*)&bn_s[0][c0 + e];
+          *(float4*)&is[e] = *(const float4*)&bn_s[1][c0 + e];
+          *(float4*)&sc[e] = *(const float4*)&bn_s[2][c0 + e];
+          *(float4*)&sh[e] = *(const float4*)&bn_s[3][c0 + e];
         }
+#pragma unroll
+        for (int e = 0; e < VE; ++e) v[e] = fmaf(z.v[e], sc[e], sh[e]) > 0.f ? v[e] : 0.f;
         store_chunk<T>(P.out, idx, v);
 #pragma unroll
         for (int e = 0; e < VE; ++e) {
-          const float4 b = bn_s[c0 + e];
           const float dr = St<T>::rnd(v[e]);
           s1[e] += dr;
-          s2[e] += dr * ((z.v[e] - b.x) * b.y);
+          s2[e] += dr * ((z.v[e] - mu[e]) * is[e]);
         }
       } else {
         if (P.res) {
@@ -437,18 +442,23 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
     __syncthreads();                   // acc_s reused: [rpp][BNc] sums, then sums of products
     float* red1 = acc_s;
     float* red2 = acc_s + 256 * VE;
+    // row rr of the [rpp][BNc] sums keeps its 16-byte slots XOR-swizzled by bit (3 - log2 WN) of
+    // rr, so that each half-wave's 16-byte writes fall on distinct banks
+    constexpr int SWB = WN == 4 ? 1 : (WN == 2 ? 2 : 3);
     const int rr = tid / ncc;
 #pragma unroll
-    for (int e = 0; e < VE; ++e) {
-      red1[rr * BNc + c0 + e] = s1[e];
-      red2[rr * BNc + c0 + e] = s2[e];
+    for (int e = 0; e < VE; e += 4) {
+      const int slot = ((c0 + e) >> 2) ^ ((rr >> SWB) & 1);
+      *(float4*)&red1[rr * BNc + slot * 4] = make_float4(s1[e], s1[e + 1], s1[e + 2], s1[e + 3]);
+      *(float4*)&red2[rr * BNc + slot * 4] = make_float4(s2[e], s2[e + 1], s2[e + 2], s2[e + 3]);
     }
     __syncthreads();
     if (tid < BNc) {
       float a = 0.f, b = 0.f;
       for (int k = 0; k < rpp; ++k) {
-        a += red1[k * BNc + tid];
-        b += red2[k * BNc + tid];
+        const int w = k * BNc + ((((tid >> 2) ^ ((k >> SWB) & 1))) << 2) + (tid & 3);
+        a += red1[w];
+        b += red2[w];
       }
       float2* pp = (float2*)P.part + (long)tm * P.ncol + n0 + tid;
       *pp = make_float2(a, b);

@@ -498,7 +498,8 @@ bool halo_ok(const ConvProb& p, int es) {
   if (bm % p.Q != 0 || (pq % bm != 0 && bm % pq != 0)) return false;
   const long nimg = bm > pq ? bm / pq : 1;
   const long rows = bm > pq ? p.P : bm / p.Q;
-  return nimg * (rows + 2) * (p.Q + 2) * (long)(p.Cg + ve) * es <= CONV_HALO_BYTES;
+  const long ps = p.Cg + (long)conv_halo_pad(p.Cg / ve, p.Q) * ve;
+  return nimg * (rows + 2) * (p.Q + 2) * ps * es <= CONV_HALO_BYTES;
 }
 
 // Gather kind of a convolution problem: 0 pointwise, 1 vector gather, 2 element-wise gather,

@@ -224,6 +224,8 @@ constexpr int COLSTAT_ROWS = 128;  // rows per column-statistics workgroup
 constexpr int BNACT_PIX = 32;      // output pixels per bnact workgroup
 constexpr int CONV_HALO_BYTES = 40960;  // LDS of a 3x3 halo tile (input rows + halo, padded pixels)
 constexpr int CONV_HALO_NKB = 18;       // K steps whose filter fragments a wave keeps in registers
+// unused 16-byte chunks after the cpp channel chunks of a halo pixel (output width Q)
+__host__ __device__ inline int conv_halo_pad(int cpp, int Q) { return cpp >= 4 ? (Q >= 16 ? 2 : 1) : 0; }
 
 
 }  // namespace pnn
