@@ -267,7 +267,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   constexpr int LDA = 16 * WN + 4;
   constexpr int ACC_WORDS = (GK == GK_HALO && CONV_HALO_BYTES / 4 > BM * LDA) ? CONV_HALO_BYTES / 4 : BM * LDA;
   __shared__ float2 pro_s[CONV_PRO_MAXC];
-  __shared__ __attribute__((aligned(16))) float bn_s[4][64];   // mean, invstd, scale, shift
+  __shared__ __attribute__((aligned(16))) float bn_s[7][64];   // mean, invstd, scale, shift; A, B, K
   __shared__ __attribute__((aligned(16))) float acc_s[ACC_WORDS];
 
   const int gi = find_group(L);
@@ -283,16 +283,8 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   const int mw = tm * BM + wave * 16 * WM;
   const int n0 = tn * 16 * P.wn;
   const int PQ = P.P * P.Q;
-  const bool bnmask = MODE == MODE_BWD && (P.flags & EPI_BN_MASK);
-
-  if (MODE == MODE_FWD && P.pro != nullptr)
-    for (int c = tid; c < P.Cg; c += 256) pro_s[c] = make_float2(P.pro[c], P.pro[P.Cg + c]);
-  if (bnmask && tid < 16 * WN) {
-    const int col = n0 + tid;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) bn_s[k][tid] = P.bnst[k * P.ncol + col];
-  }
-  __syncthreads();
+  const bool bnmask = MODE == MODE_BWD && (P.flags & (EPI_BN_MASK | EPI_BN_APPLY));
+  const bool bnapply = MODE == MODE_BWD && (P.flags & EPI_BN_APPLY);
 
   int rm[WM], rn[WM], rp[WM], rq[WM];
   bool rv[WM];
@@ -318,9 +310,11 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
 #pragma unroll
     for (int j = 0; j < WN; ++j) acc[wm][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // The epilogue's streamed operand (residual / skip gradient, or the BN input of the ReLU mask) is
-  // fetched before the K loop so that it overlaps the operand gathers.  Each thread owns fixed
-  // 16-byte column chunks of rows tid / ncc + k * rpp.
+  // Every global load that does not depend on LDS is issued before the LDS staging barrier: the
+  // epilogue's streamed operands (residual / skip gradient or the BN input of the ReLU mask, and a
+  // second addend: the coarse addend, or the skip gradient of the BN apply) and, for pointwise
+  // problems, the first K step's operands.  Each thread owns fixed 16-byte column chunks of rows
+  // tid / ncc + k * rpp in the epilogue.
   constexpr int BNc = 16 * WN;
   constexpr int ncc = BNc / VE;       // column chunks per row
   constexpr int rpp = 256 / ncc;      // rows per pass
@@ -329,16 +323,67 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   const int c0 = cc * VE;
   const void* pf = (MODE == MODE_FWD) ? P.res
                    : ((P.flags & EPI_STORE_F32) ? nullptr : (bnmask ? P.zsrc : P.res));
-  uint4 pre[NCH];
+  const void* pf2 = (MODE == MODE_FWD) ? P.ext : (bnapply ? P.res : nullptr);
+  uint4 pre[NCH], pre2[NCH];
 #pragma unroll
   for (int k = 0; k < NCH; ++k) {
     const int m = tm * BM + tid / ncc + k * rpp;
-    pre[k] = (pf != nullptr && m < P.M) ? *(const uint4*)((const T*)pf + (long)m * P.ncol + n0 + c0)
-                                        : make_uint4(0, 0, 0, 0);
+    const long o = (long)m * P.ncol + n0 + c0;
+    pre[k] = (pf != nullptr && m < P.M) ? *(const uint4*)((const T*)pf + o) : make_uint4(0, 0, 0, 0);
+    pre2[k] = (pf2 != nullptr && m < P.M) ? *(const uint4*)((const T*)pf2 + o) : make_uint4(0, 0, 0, 0);
+  }
+  uint4 a0raw[WM];
+  Frag<T> b0[WN];
+  if constexpr (GK == GK_POINT) {
+    const int k0 = VE * grp;
+#pragma unroll
+    for (int wm = 0; wm < WM; ++wm)
+      a0raw[wm] = (rv[wm] && k0 < P.K) ? *(const uint4*)((const T*)P.in + (long)rm[wm] * P.Cg + k0)
+                                       : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int j = 0; j < WN; ++j) load_b<T, true>(P, n0 + j * 16 + r16, k0, b0[j]);
+  }
+
+  if (MODE == MODE_FWD && P.pro != nullptr)
+    for (int c = tid; c < P.Cg; c += 256) pro_s[c] = make_float2(P.pro[c], P.pro[P.Cg + c]);
+  if (bnmask && tid < 16 * WN) {
+    const int col = n0 + tid;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) bn_s[k][tid] = P.bnst[k * P.ncol + col];
+    if (bnapply) {
+#pragma unroll
+      for (int k = 0; k < 3; ++k) bn_s[4 + k][tid] = P.coef[k * P.ncol + col];
+    }
+  }
+  __syncthreads();
+
+  int kstart = 0;
+  if constexpr (GK == GK_POINT) {
+    // first K step from the early loads; the BN prologue (scale, shift from LDS) applies now.
+    // Rows past M and columns past K are zeros of the activated operand.
+    const int k0 = VE * grp;
+    Frag<T> a[WM];
+#pragma unroll
+    for (int wm = 0; wm < WM; ++wm) {
+      if (MODE == MODE_FWD && P.pro != nullptr && rv[wm] && k0 < P.K) {
+        Chunk<T> c;
+        unpack_chunk<T>(a0raw[wm], c);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) c.v[e] = fmaxf(fmaf(c.v[e], pro_s[k0 + e].x, pro_s[k0 + e].y), 0.0f);
+        a[wm].from_chunk(c);
+      } else {
+        a[wm].from_raw(a0raw[wm]);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < WN; ++j)
+#pragma unroll
+      for (int wm = 0; wm < WM; ++wm) mma(a[wm], b0[j], acc[wm][j]);
+    kstart = KS;
   }
 
   if constexpr (GK == GK_HALO) conv_halo<T, MODE, WM>(P, pro_s, (T*)acc_s, tm, n0, acc);
-  for (int kk = 0; kk < P.K && GK != GK_HALO; kk += KS) {
+  for (int kk = kstart; kk < P.K && GK != GK_HALO; kk += KS) {
     const int k0 = kk + VE * grp;
     Frag<T> a[WM];
 #pragma unroll
@@ -386,7 +431,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
       }
       if (P.ext) {
         Chunk<T> x;
-        load_chunk<T>(P.ext, idx, x);
+        unpack_chunk<T>(pre2[k], x);
 #pragma unroll
         for (int e = 0; e < VE; ++e) v[e] += x.v[e];
       }
@@ -420,12 +465,32 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
         }
 #pragma unroll
         for (int e = 0; e < VE; ++e) v[e] = fmaf(z.v[e], sc[e], sh[e]) > 0.f ? v[e] : 0.f;
-        store_chunk<T>(P.out, idx, v);
+        if (bnapply) {
+          // the BN backward apply of the stored-dbn path, on dbn rounded as it would be stored
+          float ca[VE], cb[VE], ck[VE];
 #pragma unroll
-        for (int e = 0; e < VE; ++e) {
-          const float dr = St<T>::rnd(v[e]);
-          s1[e] += dr;
-          s2[e] += dr * ((z.v[e] - mu[e]) * is[e]);
+          for (int e = 0; e < VE; e += 4) {
+            *(float4*)&ca[e] = *(const float4*)&bn_s[4][c0 + e];
+            *(float4*)&cb[e] = *(const float4*)&bn_s[5][c0 + e];
+            *(float4*)&ck[e] = *(const float4*)&bn_s[6][c0 + e];
+          }
+#pragma unroll
+          for (int e = 0; e < VE; ++e) v[e] = fmaf(ca[e], St<T>::rnd(v[e]), fmaf(cb[e], z.v[e], ck[e]));
+          if (P.res) {
+            Chunk<T> x;
+            unpack_chunk<T>(pre2[k], x);
+#pragma unroll
+            for (int e = 0; e < VE; ++e) v[e] += x.v[e];
+          }
+          store_chunk<T>(P.out, idx, v);
+        } else {
+          if (!(P.flags & EPI_NO_STORE)) store_chunk<T>(P.out, idx, v);
+#pragma unroll
+          for (int e = 0; e < VE; ++e) {
+            const float dr = St<T>::rnd(v[e]);
+            s1[e] += dr;
+            s2[e] += dr * ((z.v[e] - mu[e]) * is[e]);
+          }
         }
       } else {
         if (P.res) {
@@ -437,7 +502,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
     }
   }
 
-  const bool stats = (MODE == MODE_FWD) ? (P.flags & EPI_STATS) != 0 : bnmask;
+  const bool stats = (MODE == MODE_FWD) ? (P.flags & EPI_STATS) != 0 : (bnmask && !bnapply);
   if (stats) {
     __syncthreads();                   // acc_s reused: [rpp][BNc] sums, then sums of products
     float* red1 = acc_s;

@@ -54,6 +54,7 @@ struct BnP {
   int fwd_tiles = 0, bwd_tiles = 0;
   size_t dbn_off = NONE, coef_off = NONE, datmp_off = NONE;
   bool bnact_consumer = false;
+  bool defer_apply = false;  // dbn not stored: the apply pass recomputes it (see build_segment)
 };
 
 struct SegP {
@@ -241,6 +242,18 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
       S.nodes[a_first ? a : b].first_of_two = true;
     }
   }
+  // BN backward without a stored dbn.  When the BN's only consumer is a pointwise convolution whose
+  // output gradient has fewer than twice the BN's channels, its data-gradient pass only reduces the
+  // BN sums, and a second pass of the same convolution forms dbn again and applies the BN backward:
+  // re-reading the narrow output gradient costs fewer bytes than writing and re-reading dbn.
+  for (auto& b : S.bns) {
+    const SlotP& sl = S.slots[b.slot];
+    if (sl.bn_consumers.size() != 1 || !S.needs[b.slot]) continue;
+    const NodeP& n = S.nodes[sl.bn_consumers[0]];
+    if (n.op != PNN_OP_CONV || !n.dgrad || n.k != 1 || n.stride != 1 || n.pad != 0) continue;
+    if (n.cout % (16 / es) != 0 || n.cout >= 2 * n.cin) continue;
+    b.defer_apply = true;
+  }
   // parameter / gradient layout
   size_t po = 0, go = 0;
   for (auto& n : S.nodes) {
@@ -289,7 +302,7 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
     sc = align256(sc + (size_t)tiles * 2 * b.C * 4);
     b.coef_off = sc;
     sc = align256(sc + (size_t)b.C * 12);
-    if (!sl.bn_consumers.empty()) {
+    if (!sl.bn_consumers.empty() && !b.defer_apply) {
       b.dbn_off = sc;
       sc = align256(sc + (size_t)sl.elems * es);
     }
@@ -462,8 +475,10 @@ double conv_bytes(const ConvProb& p, int es, int mode) {
     b += mo * es * (1 + (p.res ? 1 : 0) + (p.ext ? 1 : 0));
   } else if (p.flags & EPI_STORE_F32) {
     b += mo * 4;
+  } else if (p.flags & EPI_BN_APPLY) {
+    b += mo * es * (2 + (p.res ? 1 : 0));
   } else if (p.flags & EPI_BN_MASK) {
-    b += mo * es * 2 + ((p.flags & EPI_ACC_IN) ? mo * 4 : 0);
+    b += mo * es * ((p.flags & EPI_NO_STORE) ? 1 : 2) + ((p.flags & EPI_ACC_IN) ? mo * 4 : 0);
   } else {
     b += mo * es * (1 + (p.res ? 1 : 0));
   }
@@ -663,8 +678,20 @@ int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
 // ------------------------------------------------------------------------------------------------
 // backward of a set of segments
 // ------------------------------------------------------------------------------------------------
+// data gradient of conv node n: gathers dL/d(n.dst) through the transposed filter; epilogue unset
+ConvProb dgrad_base(const Ctx& c, const SegP& S, const Ptrs& P, const NodeP& n) {
+  ConvProb p = conv_common(c.plan, n);
+  p.in = grad_ptr(c, S, P, n.dst);
+  p.wmat = c.scratch + S.scr_base + n.wt_off;
+  p.B = c.plan->B; p.H = n.Ho; p.W = n.Wo; p.Cg = n.cout;
+  p.P = n.H; p.Q = n.W; p.ncol = n.cin;
+  p.M = c.plan->B * n.H * n.W;
+  p.K = n.k * n.k * n.cout;
+  return p;
+}
+
 void bn_bwd_finalize(const Ctx& c, const SegP& S, const Ptrs& P, int s, std::vector<ColRedProb>& fin,
-                     std::vector<BnApplyProb>& app) {
+                     std::vector<BnApplyProb>& app, std::vector<ConvProb>& rec) {
   const SlotP& sl = S.slots[s];
   if (sl.bn < 0 || sl.bn_consumers.empty()) return;
   const BnP& b = S.bns[sl.bn];
@@ -682,6 +709,18 @@ void bn_bwd_finalize(const Ctx& c, const SegP& S, const Ptrs& P, int s, std::vec
   f.count = (long)c.plan->B * sl.H * sl.W;
   fin.push_back(f);
   if (!S.needs[s]) return;
+  if (b.defer_apply) {
+    ConvProb p = dgrad_base(c, S, P, S.nodes[sl.bn_consumers[0]]);
+    p.flags = EPI_BN_APPLY;
+    p.zsrc = slot_ptr(c, S, P, s);
+    p.bnst = f.stats;
+    p.coef = f.coef;
+    p.out = grad_ptr(c, S, P, s);
+    p.res = skip_ptr(c, S, P, s);
+    set_tiles(p);
+    rec.push_back(p);
+    return;
+  }
   BnApplyProb a;
   a.dbn = c.scratch + S.scr_base + b.dbn_off;
   a.z = slot_ptr(c, S, P, s);
@@ -694,11 +733,14 @@ void bn_bwd_finalize(const Ctx& c, const SegP& S, const Ptrs& P, int s, std::vec
   app.push_back(a);
 }
 
-int fire_finalize(const Ctx& c, std::vector<ColRedProb>& fin, std::vector<BnApplyProb>& app) {
+int fire_finalize(const Ctx& c, std::vector<ColRedProb>& fin, std::vector<BnApplyProb>& app,
+                  std::vector<ConvProb>& rec) {
   if (fire_colred(fin, c.stream)) return PNN_ERR_HIP;
-  return grouped<BnApplyLaunch>(
+  int e = grouped<BnApplyLaunch>(
       app, [](const BnApplyProb& p) { return (int)cdiv(p.n, ELT_TILE); },
       [&](const BnApplyLaunch& L, int tiles, size_t) { return launch_bn_apply(L, tiles, c.plan->dtype, c.stream); });
+  if (e) return e;
+  return fire_conv(c, rec, MODE_BWD);
 }
 
 int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
@@ -737,14 +779,15 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
     {
       std::vector<ColRedProb> fin;
       std::vector<BnApplyProb> app;
+      std::vector<ConvProb> rec;
       for (size_t i = 0; i < segs.size(); ++i) {
         const SegP& S = *segs[i];
         for (const NodeP& n : S.nodes)
-          if (n.level == L && n.dst != S.out) bn_bwd_finalize(c, S, ptrs[i], n.dst, fin, app);
+          if (n.level == L && n.dst != S.out) bn_bwd_finalize(c, S, ptrs[i], n.dst, fin, app, rec);
       }
       fin.insert(fin.end(), pending.begin(), pending.end());
       pending.clear();
-      int e = fire_finalize(c, fin, app);
+      int e = fire_finalize(c, fin, app, rec);
       if (e) return e;
     }
     // B + C: weight gradients
@@ -828,21 +871,15 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
           }
           if (n.op != PNN_OP_CONV || !n.dgrad) continue;
           if ((phase == 0) != n.first_of_two) continue;
-          ConvProb p = conv_common(plan, n);
-          p.in = grad_ptr(c, S, P, n.dst);
-          p.wmat = c.scratch + S.scr_base + n.wt_off;
-          p.B = B; p.H = n.Ho; p.W = n.Wo; p.Cg = n.cout;
-          p.P = n.H; p.Q = n.W; p.ncol = n.cin;
-          p.M = B * n.H * n.W;
-          p.K = n.k * n.k * n.cout;
+          ConvProb p = dgrad_base(c, S, P, n);
           if (n.bn >= 0) {
             const BnP& b = S.bns[n.bn];
             if (n.first_of_two) {
               p.flags = EPI_STORE_F32;
               p.out32 = (float*)(c.scratch + S.scr_base + b.datmp_off);
             } else {
-              p.flags = EPI_BN_MASK;
-              p.out = c.scratch + S.scr_base + b.dbn_off;
+              p.flags = EPI_BN_MASK | (b.defer_apply ? EPI_NO_STORE : 0);
+              p.out = b.defer_apply ? nullptr : c.scratch + S.scr_base + b.dbn_off;
               p.zsrc = slot_ptr(c, S, P, n.src);
               p.bnst = stats_ptr(c, S, n.bn);
               p.part = part_ptr(c, S, n.bn);
@@ -871,12 +908,13 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
   {
     std::vector<ColRedProb> fin = std::move(pending);
     std::vector<BnApplyProb> app;
+    std::vector<ConvProb> rec;
     for (size_t i = 0; i < segs.size(); ++i) {
       const SegP& S = *segs[i];
       if (S.part == 0 || ptrs[i].gin == nullptr) continue;
-      bn_bwd_finalize(c, S, ptrs[i], 0, fin, app);
+      bn_bwd_finalize(c, S, ptrs[i], 0, fin, app, rec);
     }
-    int e = fire_finalize(c, fin, app);
+    int e = fire_finalize(c, fin, app, rec);
     if (e) return e;
   }
   return PNN_OK;

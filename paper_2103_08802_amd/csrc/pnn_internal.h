@@ -23,6 +23,9 @@ enum {
   EPI_BN_MASK = 2,    // BWD: dbn = v * [ReLU(BN(z)) > 0] stored, sums of dbn and dbn * xhat -> part
   EPI_STORE_F32 = 4,  // BWD: v stored as float to out32 (first of two consumers of one BN)
   EPI_ACC_IN = 8,     // BWD: v += acc_in before the epilogue
+  EPI_NO_STORE = 16,  // BWD + EPI_BN_MASK: BN sums only, dbn is not stored
+  EPI_BN_APPLY = 32,  // BWD: dbn = rnd(v * mask) as for EPI_BN_MASK, then the BN backward apply
+                      // out = A dbn + B z + K [+ res] (coefficients coef [3][ncol]); no sums
 };
 
 // Implicit-GEMM convolution problem.  FWD: out[m][n] = sum_k A[m][k] wmat[n][k] with
@@ -39,6 +42,7 @@ struct ConvProb {
   const void* zsrc;     // BWD + EPI_BN_MASK: BN input z [M][ncol]
   const float* bnst;    // BWD + EPI_BN_MASK: mean, invstd, scale, shift [4][ncol]
   const float* acc_in;  // EPI_ACC_IN: [M][ncol] float
+  const float* coef;    // EPI_BN_APPLY: A, B, K [3][ncol]
   float* out32;         // EPI_STORE_F32: [M][ncol] float
   int B, H, W, Cg;      // gathered tensor
   int P, Q;             // output pixel grid (M = B * P * Q)
