@@ -518,12 +518,31 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
       *(float4*)&red2[rr * BNc + slot * 4] = make_float4(s2[e], s2[e + 1], s2[e + 2], s2[e + 3]);
     }
     __syncthreads();
-    if (tid < BNc) {
+    // column tid % BNc, row group tid / BNc: sums over the group's rows in order, then over the
+    // groups in order
+    constexpr int NQ = 256 / BNc;
+    constexpr int RPQ = rpp / NQ;
+    static_assert(NQ * RPQ == rpp && 2 * 256 * VE + 512 <= ACC_WORDS, "stats reduce layout");
+    float* red3 = acc_s + 2 * 256 * VE;
+    {
+      const int col = tid % BNc, q = tid / BNc;
       float a = 0.f, b = 0.f;
-      for (int k = 0; k < rpp; ++k) {
-        const int w = k * BNc + ((((tid >> 2) ^ ((k >> SWB) & 1))) << 2) + (tid & 3);
+#pragma unroll
+      for (int k = q * RPQ; k < (q + 1) * RPQ; ++k) {
+        const int w = k * BNc + ((((col >> 2) ^ ((k >> SWB) & 1))) << 2) + (col & 3);
         a += red1[w];
         b += red2[w];
+      }
+      red3[q * BNc + col] = a;
+      red3[256 + q * BNc + col] = b;
+    }
+    __syncthreads();
+    if (tid < BNc) {
+      float a = 0.f, b = 0.f;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        a += red3[q * BNc + tid];
+        b += red3[256 + q * BNc + tid];
       }
       float2* pp = (float2*)P.part + (long)tm * P.ncol + n0 + tid;
       *pp = make_float2(a, b);
