@@ -144,16 +144,16 @@ __device__ __forceinline__ void load_b(const ConvProb& P, int col, int k0, Frag<
 // of the (activated, for the forward prologue) input; padding pixels are zeros.  A pixel's Cg
 // channels are followed by 0, 1 or 2 unused 16-byte chunks (conv_halo_pad) so that each half-wave's
 // A reads (16 pixels x an aligned chunk pair) fall on distinct LDS banks.  Wave w
-// owns column sub-tile w % WN and 8 row sub-tiles; its filter fragments for all K steps (at most
+// owns column sub-tile w % WN and WM * WN row sub-tiles; its filter fragments for all K steps (at most
 // CONV_HALO_NKB) are loaded into registers before the LDS fill completes.  Steps past K read a
 // valid A position; the filter fragment there is zero.
-template <typename T, int MODE, int WM>
+template <typename T, int MODE, int WM, int WN>
 __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, T* halo, int tm, int n0,
-                                          f32x4 (&acc)[WM][8 / WM]) {
+                                          f32x4 (&acc)[WM][WN]) {
   constexpr int VE = St<T>::VE;
   constexpr int KS = 4 * VE;
-  constexpr int WN = 8 / WM;
   constexpr int BM = 64 * WM;
+  constexpr int NT = WM * WN;                 // row sub-tiles per wave
   constexpr int NKB = CONV_HALO_NKB;
   constexpr int NL = 8;                      // halo chunks in flight per thread
   const int tid = threadIdx.x;
@@ -224,8 +224,8 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
 
   int rb[8];
 #pragma unroll
-  for (int t = 0; t < 8; ++t) {
-    const int lm = (rg * 8 + t) * 16 + r16;
+  for (int t = 0; t < NT; ++t) {
+    const int lm = (rg * NT + t) * 16 + r16;
     const int i = multi ? div_l2(lm, PQ, P.pq_log2) : 0;
     const int rem = lm - i * R * P.Q;
     const int pl = div_l2(rem, P.Q, P.q_log2);
@@ -245,7 +245,7 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
       tap_rs(tap, 3, r, q);
       const int toff = (MODE == MODE_FWD) ? (r * QH + q) : ((2 - r) * QH + (2 - q));
 #pragma unroll
-      for (int t = 0; t < 8; ++t) {
+      for (int t = 0; t < NT; ++t) {
         Frag<T> a;
         a.from_raw(*(const uint4*)(halo + (rb[t] + toff) * PS + c0));
         mma(a, bq[s], acc[t / WN][t % WN]);
@@ -255,17 +255,17 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
   __syncthreads();                            // the halo region is reused by the epilogue
 }
 
-// WM row sub-tiles of 16 per wave, WN = 8 / WM column sub-tiles: a workgroup owns a
-// (64 WM) x (16 WN) tile, so narrow problems (16 columns) get 512-row tiles and keep eight
-// operand fragments in flight per wave.
-template <typename T, int MODE, int GK, int WM>
+// WM row sub-tiles of 16 per wave, WN column sub-tiles: a workgroup owns a (64 WM) x (16 WN) tile
+// (WM * WN = CONV_SUBTILES, so narrow problems get taller tiles).
+template <typename T, int MODE, int GK, int WM, int WN>
 __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   constexpr int VE = St<T>::VE;
   constexpr int KS = 4 * VE;
-  constexpr int WN = 8 / WM;
   constexpr int BM = 64 * WM;
   constexpr int LDA = 16 * WN + 4;
-  constexpr int ACC_WORDS = (GK == GK_HALO && CONV_HALO_BYTES / 4 > BM * LDA) ? CONV_HALO_BYTES / 4 : BM * LDA;
+  constexpr int STAT_WORDS = 2 * 256 * VE + 512;   // BN sums reduce (epilogue)
+  constexpr int ACC_WORDS0 = BM * LDA > STAT_WORDS ? BM * LDA : STAT_WORDS;
+  constexpr int ACC_WORDS = (GK == GK_HALO && CONV_HALO_BYTES / 4 > ACC_WORDS0) ? CONV_HALO_BYTES / 4 : ACC_WORDS0;
   __shared__ float2 pro_s[CONV_PRO_MAXC];
   __shared__ __attribute__((aligned(16))) float bn_s[7][64];   // mean, invstd, scale, shift; A, B, K
   __shared__ __attribute__((aligned(16))) float acc_s[ACC_WORDS];
@@ -319,6 +319,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   constexpr int ncc = BNc / VE;       // column chunks per row
   constexpr int rpp = 256 / ncc;      // rows per pass
   constexpr int NCH = BM / rpp;       // chunks per thread
+  static_assert(NCH >= 1 && BM % rpp == 0, "epilogue chunk layout");
   const int cc = tid % ncc;
   const int c0 = cc * VE;
   const void* pf = (MODE == MODE_FWD) ? P.res
@@ -382,7 +383,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
     kstart = KS;
   }
 
-  if constexpr (GK == GK_HALO) conv_halo<T, MODE, WM>(P, pro_s, (T*)acc_s, tm, n0, acc);
+  if constexpr (GK == GK_HALO) conv_halo<T, MODE, WM, WN>(P, pro_s, (T*)acc_s, tm, n0, acc);
   for (int kk = kstart; kk < P.K && GK != GK_HALO; kk += KS) {
     const int k0 = kk + VE * grp;
     Frag<T> a[WM];
@@ -403,7 +404,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
 #pragma unroll
     for (int j = 0; j < WN; ++j) {
       // row / column sub-tile of acc[wm][j]: waves split rows, or (GK_HALO) columns first
-      const int rt = (GK == GK_HALO) ? (wave / WN) * 8 + wm * WN + j : wave * WM + wm;
+      const int rt = (GK == GK_HALO) ? (wave / WN) * (WM * WN) + wm * WN + j : wave * WM + wm;
       const int ct = (GK == GK_HALO) ? wave % WN : j;
 #pragma unroll
       for (int i = 0; i < 4; ++i) acc_s[(rt * 16 + grp * 4 + i) * LDA + ct * 16 + r16] = acc[wm][j][i];
@@ -522,7 +523,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
     // groups in order
     constexpr int NQ = 256 / BNc;
     constexpr int RPQ = rpp / NQ;
-    static_assert(NQ * RPQ == rpp && 2 * 256 * VE + 512 <= ACC_WORDS, "stats reduce layout");
+    static_assert(NQ * RPQ == rpp && STAT_WORDS <= ACC_WORDS, "stats reduce layout");
     float* red3 = acc_s + 2 * 256 * VE;
     {
       const int col = tid % BNc, q = tid / BNc;
@@ -819,23 +820,24 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
 // launchers
 // ------------------------------------------------------------------------------------------------
 
-template <typename T, int MODE, int WM>
+template <typename T, int MODE, int WN>
 static void launch_conv_w(const ConvLaunch& L, int tiles, int gk, hipStream_t s) {
+  constexpr int WM = CONV_SUBTILES / WN;
   if (gk == GK_POINT)
-    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_POINT, WM>), dim3(tiles), dim3(256), 0, s, L);
+    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_POINT, WM, WN>), dim3(tiles), dim3(256), 0, s, L);
   else if (gk == GK_VEC)
-    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_VEC, WM>), dim3(tiles), dim3(256), 0, s, L);
+    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_VEC, WM, WN>), dim3(tiles), dim3(256), 0, s, L);
   else if (gk == GK_HALO)
-    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_HALO, WM>), dim3(tiles), dim3(256), 0, s, L);
+    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_HALO, WM, WN>), dim3(tiles), dim3(256), 0, s, L);
   else
-    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_SCALAR, WM>), dim3(tiles), dim3(256), 0, s, L);
+    hipLaunchKernelGGL((conv_kernel<T, MODE, GK_SCALAR, WM, WN>), dim3(tiles), dim3(256), 0, s, L);
 }
 
 template <typename T, int MODE>
 static void launch_conv_m(const ConvLaunch& L, int tiles, int gk, int wn, hipStream_t s) {
-  if (wn == 1) launch_conv_w<T, MODE, 8>(L, tiles, gk, s);
-  else if (wn == 2) launch_conv_w<T, MODE, 4>(L, tiles, gk, s);
-  else launch_conv_w<T, MODE, 2>(L, tiles, gk, s);
+  if (wn == 1) launch_conv_w<T, MODE, 1>(L, tiles, gk, s);
+  else if (wn == 2) launch_conv_w<T, MODE, 2>(L, tiles, gk, s);
+  else launch_conv_w<T, MODE, 4>(L, tiles, gk, s);
 }
 
 int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, hipStream_t s) {

@@ -508,7 +508,7 @@ bool halo_ok(const ConvProb& p, int es) {
   if (p.k != 3 || p.stride != 1 || p.pad != 1 || p.H != p.P || p.W != p.Q) return false;
   const int ve = 16 / es;
   if (p.K > 4 * ve * CONV_HALO_NKB) return false;
-  const int bm = 64 * (8 / p.wn);
+  const int bm = 64 * (CONV_SUBTILES / p.wn);
   const int pq = p.P * p.Q;
   if (bm % p.Q != 0 || (pq % bm != 0 && bm % pq != 0)) return false;
   const long nimg = bm > pq ? bm / pq : 1;

@@ -220,9 +220,11 @@ int launch_head(const void* yt, const float* eps, const int32_t* labels, float* 
                 int K, int dtype, hipStream_t s);
 
 // tile sizes shared by host and device code
-// rows of M per conv workgroup for a problem with ncol output columns: 64 x (8 / wn)
+// conv workgroup tile: 16 x 16 sub-tiles per wave (row sub-tiles x column sub-tiles); a problem with
+// ncol output columns takes wn = 4, 2 or 1 column sub-tiles and 64 x (CONV_SUBTILES / wn) rows of M
+constexpr int CONV_SUBTILES = 8;
 inline int conv_wn(int ncol) { return (ncol % 64 == 0) ? 4 : (ncol % 32 == 0) ? 2 : 1; }
-inline int conv_bm(int ncol) { return 64 * (8 / conv_wn(ncol)); }
+inline int conv_bm(int ncol) { return 64 * (CONV_SUBTILES / conv_wn(ncol)); }
 constexpr int ELT_TILE = 2048;     // elements per workgroup of elementwise kernels
 constexpr int COLSTAT_ROWS = 128;  // rows per column-statistics workgroup
 constexpr int BNACT_PIX = 32;      // output pixels per bnact workgroup
