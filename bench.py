@@ -40,13 +40,13 @@ def fine_flops(net):
     return 3 * sum(conv_flops(s, net.batch) for s in net.fine)
 
 
-def cpu_baseline(idx, batch=24):
+def cpu_baseline(idx, batch=24, coarse="config"):
     """The fp64 oracle, as it stands, on a bounded sample of the same workload: one full step of the
     same network at a reduced batch.  Reported in the metric's unit (fine conv TFLOP/s)."""
     import pnn_synth as S
     from oracle import prim
     from oracle.net import ParaRealOracle
-    net = S.config(idx, batch)
+    net = S.config(idx, batch, coarse=coarse)
     x, labels, params = S.make_all(net)
     o = ParaRealOracle(net, params)
     t0 = time.perf_counter()
@@ -160,6 +160,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, help="workload index 0..4")
+    ap.add_argument("--coarse", default="config", choices=("config", "paper"),
+                    help="coarse blocks F^j: the workload's (one unit) or the paper's own networks")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 256 MiB device copy first (reference for HBM byte counters)")
@@ -195,7 +197,7 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    net = S.config(args.config)
+    net = S.config(args.config, coarse=args.coarse)
     x, labels, params = S.make_all(net)
     g = ParaRealGPU(net, params)
     g.load_input(x, labels)
@@ -243,7 +245,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args.config)
+        cpu = cpu_baseline(args.config, coarse=args.coarse)
 
     out = {
         "metric": "fine-subnet conv TFLOP/s (fwd+bwd, % bf16 MFMA peak) + images/s per step",

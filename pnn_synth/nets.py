@@ -338,21 +338,26 @@ def tiny_parareal(name="tiny-basic-n2", batch=4, hw=32, ch=16, n_sub=2, classes=
 # the five workloads
 # ----------------------------------------------------------------------------------------------
 
-def config(idx: int, batch: Optional[int] = None) -> Net:
-    """Workload ``idx`` (0..4); ``batch`` overrides the batch size (smaller parity cases)."""
+def config(idx: int, batch: Optional[int] = None, coarse: str = "config") -> Net:
+    """Workload ``idx`` (0..4); ``batch`` overrides the batch size (smaller parity cases);
+    ``coarse="paper"`` replaces the coarse blocks F^j of the VGG / ResNet workloads by the paper's
+    own coarse networks (ResNet: ceil(12/N) two-3x3 residual units per F^j, Sec. 4.2.1; VGG: two
+    3x3 convolutions and a max pool, Sec. 4.1.1)."""
+    sfx = "" if coarse == "config" else "-papercoarse"
     if idx == 0:
         return tiny_parareal(batch=batch or 4)
     if idx == 1:
-        return vgg_parareal("vgg16-parareal-n4", batch or 128, 32, 10, "bf16", (2001, 2002, 2003))
+        return vgg_parareal("vgg16-parareal-n4" + sfx, batch or 128, 32, 10, "bf16", (2001, 2002, 2003),
+                            coarse=coarse)
     if idx == 2:
-        return resnet_parareal("resnet1001-parareal-n4", batch or 64, 32, 4, 100, "bf16",
-                               (3001, 3002, 3003))
+        return resnet_parareal("resnet1001-parareal-n4" + sfx, batch or 64, 32, 4, 100, "bf16",
+                               (3001, 3002, 3003), coarse=coarse)
     if idx == 3:
-        return resnet_parareal("resnet1001-parareal-n16", batch or 128, 32, 16, 100, "bf16",
-                               (4001, 4002, 4003))
+        return resnet_parareal("resnet1001-parareal-n16" + sfx, batch or 128, 32, 16, 100, "bf16",
+                               (4001, 4002, 4003), coarse=coarse)
     if idx == 4:
-        return resnet_parareal("resnet1001-parareal-n8-64px", batch or 128, 64, 8, 200, "bf16",
-                               (5001, 5002, 5003))
+        return resnet_parareal("resnet1001-parareal-n8-64px" + sfx, batch or 128, 64, 8, 200, "bf16",
+                               (5001, 5002, 5003), coarse=coarse)
     raise ValueError(idx)
 
 

@@ -29,10 +29,11 @@ def test_header_declarations_are_exported():
         assert hasattr(L, name), name
 
 
-@pytest.mark.parametrize("idx", range(5))
-def test_plans_and_layouts(idx):
+@pytest.mark.parametrize("idx,coarse", [(i, "config") for i in range(5)] +
+                         [(i, "paper") for i in range(1, 5)])
+def test_plans_and_layouts(idx, coarse):
     _lib_or_skip()
-    net = S.config(idx, 2)
+    net = S.config(idx, 2, coarse=coarse)
     p = B.Plan(net)
     assert p.workspace_size(B.PNN_WS_SAVED) >= 0
     assert p.workspace_size(B.PNN_WS_SCRATCH) > 0

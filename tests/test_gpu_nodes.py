@@ -95,3 +95,12 @@ def test_unit_sample_reduced_batch(idx, batch):
 @pytest.mark.parametrize("idx,fine_subset", [(1, None), (2, [0, 1, 3]), (3, [0, 5, 10, 15]), (4, [0, 2, 5, 7])])
 def test_sampled_nodes_full_size(idx, fine_subset):
     _assert(*check_net(S.config(idx), sample=256, fine_subset=fine_subset))
+
+
+@pytest.mark.parametrize("idx,batch,sample,fine_subset",
+                         [(1, 3, None, None), (3, 3, None, [0, 15]), (3, None, 256, [0])])
+def test_paper_coarse_nodes(idx, batch, sample, fine_subset):
+    """The paper's coarse networks (Sec. 4.1.1, 4.2.1) in place of the workloads' coarse blocks:
+    every coarse node, at reduced batch (whole tensors) and, for the ResNet N = 16 workload, at the
+    full batch (sampled outputs)."""
+    _assert(*check_net(S.config(idx, batch, coarse="paper"), sample=sample, fine_subset=fine_subset))

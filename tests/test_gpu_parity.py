@@ -93,9 +93,9 @@ def _assert_tol(err, tol):
     assert not bad, sorted(bad.items(), key=lambda kv: -kv[1])[:10]
 
 
-def mini_resnet(n_sub, ups, batch, dtype="f32", hw=16):
+def mini_resnet(n_sub, ups, batch, dtype="f32", hw=16, coarse="config"):
     return resnet_parareal(f"mini-resnet-u{ups}-n{n_sub}", batch, hw, n_sub, 10, dtype, (7, 8, 9),
-                           units_per_stage=ups, widths=(64, 128, 256), stem=16)
+                           units_per_stage=ups, widths=(64, 128, 256), stem=16, coarse=coarse)
 
 
 def test_tiny_workload_fp32():
@@ -108,6 +108,21 @@ def test_resnet_forms_fp32(n_sub, ups, batch):
     """Bottleneck ResNets with strided projected units, N not a multiple of 3 (sub-networks
     straddle stages), ragged tiles: every tensor to 1e-4."""
     _assert_tol(run_net(mini_resnet(n_sub, ups, batch)), 1e-4)
+
+
+@pytest.mark.parametrize("n_sub,ups,batch", [(2, 2, 3), (3, 2, 2), (4, 4, 2)])
+def test_resnet_paper_coarse_fp32(n_sub, ups, batch):
+    """The paper's own coarse network (ceil(12/N) two-3x3 residual units per F^j, the first strided
+    with a projection at stage changes, Sec. 4.2.1): every tensor to 1e-4."""
+    _assert_tol(run_net(mini_resnet(n_sub, ups, batch, coarse="paper")), 1e-4)
+
+
+def test_vgg_paper_coarse_fp32():
+    """The VGG-16 workload with the paper's coarse blocks (two 3x3 convolutions and a max pool,
+    Sec. 4.1.1) in fp32 at batch 3: every tensor to 1e-4."""
+    net = S.config(1, 3, coarse="paper")
+    net.dtype = "f32"
+    _assert_tol(run_net(net), 1e-4)
 
 
 def test_vgg_workload_structure_fp32():
