@@ -243,6 +243,17 @@ def main():
             "kernel": dom, "avg_launch_us": round(d["ms"] * 1e3 / max(d["launches"], 1), 2),
             "mfma_tflops": round(d["flops"] / (d["ms"] * 1e-3) / 1e12, 2)}
 
+    # the parameter update (SGD, Nesterov momentum; not part of the step the metric times)
+    g.sgd_init()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g.sgd_step(0.01, 0.9, 1e-4, True)
+    e0.record()
+    for _ in range(args.steps):
+        g.sgd_step(0.01, 0.9, 1e-4, True)
+    e1.record()
+    torch.cuda.synchronize()
+    sgd_ms = e0.elapsed_time(e1) / args.steps
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args.config, coarse=args.coarse)
@@ -268,6 +279,7 @@ def main():
         "pct_bf16_mfma_peak": round(100.0 * tflops / peak, 3),
         "fine_ms_per_step": round(fine_ms, 3),
         "fine_gflop_per_step": round(ff / 1e9, 1),
+        "sgd_ms_per_step": round(sgd_ms, 3),
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -189,6 +189,25 @@ pnn_status pnn_pre_bwd(pnn_plan* plan, const void* image, const void* const* g,
                        const void* const* delta, const void* saved, float* const* ddelta,
                        void* scratch, void* stream);
 
+/* ---- parameter update ---------------------------------------------------------------------- */
+
+/* One step of stochastic gradient descent with momentum (Nesterov's form when nesterov != 0) and
+ * weight decay, the optimiser of the paper's training runs (Sec. 4: SGD, momentum 0.9, weight decay
+ * 5e-4 / 1e-4), for every parameter of one part of the network:
+ *     d = g + weight_decay * w;   v = mu * v + d;   w = w - lr * (nesterov ? d + mu * v : v)
+ * evaluated in fp32 per element; weight decay applies to every parameter.
+ *   part 0 / 1 / 2: the segments C^j / g^j / F^j (N, N, N - 1 of them).  params[j]: the segment's
+ *                   parameter buffer (filters in the storage type, written back rounded to
+ *                   nearest even for PNN_BF16; BN gamma / beta in float); grads[j]: its gradient
+ *                   buffer (float, pnn_param_layout(.., 1, ..)); momentum[j]: float buffer laid out
+ *                   like the gradient buffer, updated in place (zero before the first step).
+ *   part 3:         the head: params[0] = eps, grads[0] = deps, momentum[0]; K * C + K floats.
+ * Buffers may not alias one another.  PNN_ERR_INDEX for another part; PNN_ERR_NULL for a missing
+ * buffer of a segment that has parameters. */
+pnn_status pnn_sgd_step(pnn_plan* plan, int part, void* const* params, const float* const* grads,
+                        float* const* momentum, float lr, float mu, float weight_decay, int nesterov,
+                        void* stream);
+
 /* ---- misc ----------------------------------------------------------------------------------- */
 
 /* Where the library keeps the internal tensors of one segment (part 0 = C^j, 1 = g^j, 2 = F^j;

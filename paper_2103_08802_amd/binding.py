@@ -24,7 +24,7 @@ EXPORTS = ["pnn_plan_create", "pnn_plan_destroy", "pnn_workspace_size", "pnn_par
            "pnn_tensor_shape", "pnn_pre_fwd", "parareal_fine_fwd", "parareal_combine_fwd",
            "coarse_fwd", "pnn_head_fwd_bwd", "coarse_bwd", "parareal_fine_bwd",
            "parareal_combine_bwd", "pnn_pre_bwd", "pnn_status_string", "pnn_inspect",
-           "pnn_timing_enable", "pnn_timing_read"]
+           "pnn_timing_enable", "pnn_timing_read", "pnn_sgd_step"]
 
 
 class PnnError(RuntimeError):
@@ -87,6 +87,8 @@ def lib():
     L.pnn_timing_enable.argtypes = [_vp, i]
     L.pnn_timing_read.argtypes = [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong),
                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    f = ctypes.c_float
+    L.pnn_sgd_step.argtypes = [_vp, i, _PP, _PP, _PP, f, f, f, i, _vp]
     for name in EXPORTS:
         getattr(L, name)          # every declared entry point must be exported
     _lib = L
@@ -251,6 +253,14 @@ def parareal_combine_bwd(plan, dx, D, stream):
     a1, k1 = _arr(dx)
     a2, k2 = _arr(D)
     _check(lib().parareal_combine_bwd(plan.handle, a1, a2, stream), "parareal_combine_bwd")
+
+
+def pnn_sgd_step(plan, part, params, grads, momentum, lr, mu, weight_decay, nesterov, stream):
+    a1, k1 = _arr(params)
+    a2, k2 = _arr(grads)
+    a3, k3 = _arr(momentum)
+    _check(lib().pnn_sgd_step(plan.handle, part, a1, a2, a3, lr, mu, weight_decay, int(bool(nesterov)),
+                              stream), "pnn_sgd_step")
 
 
 def pnn_pre_bwd(plan, image, g, delta, saved, ddelta, scratch, stream):

@@ -170,6 +170,73 @@ __global__ __launch_bounds__(256) void bn_apply_kernel(const BnApplyLaunch L) {
 }
 
 // ------------------------------------------------------------------------------------------------
+// SGD with momentum (Nesterov optional) and weight decay over a list of parameter tensors; every
+// thread updates 8 consecutive elements of one tensor (16-byte / 32-byte vector accesses).
+// ------------------------------------------------------------------------------------------------
+__device__ __forceinline__ void sgd_elem(float& w, float g, float& v, float lr, float mu, float wd, bool nest) {
+  const float d = fmaf(wd, w, g);
+  v = fmaf(mu, v, d);
+  const float u = nest ? fmaf(mu, v, d) : v;
+  w = fmaf(-lr, u, w);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void sgd_kernel(const SgdLaunch L) {
+  const int t = blockIdx.x;
+  int lo = 0, hi = L.nt - 1;
+  while (lo < hi) {                    // last entry with chunk0 <= t
+    const int mid = (lo + hi + 1) >> 1;
+    if ((int)L.e[mid].chunk0 <= t) lo = mid;
+    else hi = mid - 1;
+  }
+  const SgdEnt& E = L.e[lo];
+  const long i0 = (long)(t - (int)E.chunk0) * SGD_CHUNK + threadIdx.x * 8;
+  if (i0 >= (long)E.count) return;
+  char* pb = (char*)L.p[E.seg] + E.p_off;
+  const float* gb = (const float*)((const char*)L.g[E.seg] + E.g_off) + i0;
+  float* vb = (float*)((char*)L.v[E.seg] + E.g_off) + i0;
+  const bool nest = L.nesterov != 0;
+  const int n = (int)min((long)8, (long)E.count - i0);
+  float w[8], g[8], v[8];
+  if (n == 8) {
+    const float4 g0 = *(const float4*)gb, g1 = *(const float4*)(gb + 4);
+    const float4 v0 = *(const float4*)vb, v1 = *(const float4*)(vb + 4);
+    g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w; g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
+    v[0] = v0.x; v[1] = v0.y; v[2] = v0.z; v[3] = v0.w; v[4] = v1.x; v[5] = v1.y; v[6] = v1.z; v[7] = v1.w;
+    if (E.f32 || sizeof(T) == 4) {
+      const float* wp = (const float*)pb + i0;
+      const float4 w0 = *(const float4*)wp, w1 = *(const float4*)(wp + 4);
+      w[0] = w0.x; w[1] = w0.y; w[2] = w0.z; w[3] = w0.w; w[4] = w1.x; w[5] = w1.y; w[6] = w1.z; w[7] = w1.w;
+    } else {
+      Chunk<uint16_t> c;
+      load_chunk<uint16_t>(pb, i0, c);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w[e] = c.v[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sgd_elem(w[e], g[e], v[e], L.lr, L.mu, L.wd, nest);
+    *(float4*)vb = make_float4(v[0], v[1], v[2], v[3]);
+    *(float4*)(vb + 4) = make_float4(v[4], v[5], v[6], v[7]);
+    if (E.f32 || sizeof(T) == 4) {
+      float* wp = (float*)pb + i0;
+      *(float4*)wp = make_float4(w[0], w[1], w[2], w[3]);
+      *(float4*)(wp + 4) = make_float4(w[4], w[5], w[6], w[7]);
+    } else {
+      store_chunk<uint16_t>(pb, i0, w);
+    }
+    return;
+  }
+  for (int e = 0; e < n; ++e) {        // tail of the tensor
+    float we = (E.f32 || sizeof(T) == 4) ? ((const float*)pb)[i0 + e] : St<uint16_t>::ld(pb, i0 + e);
+    float ve = vb[e];
+    sgd_elem(we, gb[e], ve, L.lr, L.mu, L.wd, nest);
+    vb[e] = ve;
+    if (E.f32 || sizeof(T) == 4) ((float*)pb)[i0 + e] = we;
+    else St<uint16_t>::st(pb, i0 + e, we);
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
 // bnact: out = pool(ReLU(BN(z))) [+ res] [+ ext]; backward routes the output gradient to the first
 // maximum of each 2x2 window, masks it by ReLU' and reduces dbn, dbn * xhat per channel.
 // One workgroup = BNACT_PIX output pixels x all channels; a thread owns channels.
@@ -425,6 +492,9 @@ __global__ __launch_bounds__(256) void head_reduce_kernel(const float* scratch, 
 int launch_colred(const ColRedLaunch& L, int tiles, hipStream_t s) {
   hipLaunchKernelGGL(colred_kernel, dim3(tiles), dim3(RED_COLS * RED_LANES), 0, s, L);
   return (int)hipGetLastError();
+}
+int launch_sgd(const SgdLaunch& L, int tiles, int dtype, hipStream_t s) {
+  PNN_LAUNCH_T(sgd_kernel, L, tiles, dtype, s);
 }
 int launch_colstat(const ColStatLaunch& L, int tiles, int dtype, hipStream_t s) {
   PNN_LAUNCH_T(colstat_kernel, L, tiles, dtype, s);

@@ -1173,6 +1173,63 @@ pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps
   return e ? PNN_ERR_HIP : PNN_OK;
 }
 
+pnn_status pnn_sgd_step(pnn_plan* plan, int part, void* const* params, const float* const* grads,
+                        float* const* momentum, float lr, float mu, float weight_decay, int nesterov,
+                        void* stream) {
+  if (plan == nullptr || params == nullptr || grads == nullptr || momentum == nullptr) return PNN_ERR_NULL;
+  if (part < 0 || part > 3) return PNN_ERR_INDEX;
+  const hipStream_t st = (hipStream_t)stream;
+  // tensors of the part, segment by segment: (segment, parameter offset, gradient offset, count, f32)
+  struct T { int seg; size_t po, go; long cnt; bool f32; };
+  std::vector<T> ts;
+  if (part == 3) {
+    const SegP& S = plan->fine[plan->N - 1];
+    const long C = S.slots[S.out].C;
+    ts.push_back({0, 0, 0, (long)plan->classes * C + plan->classes, true});
+  } else {
+    const std::vector<SegP>& segs = part == 0 ? plan->pre : part == 1 ? plan->fine : plan->coarse;
+    for (size_t j = 0; j < segs.size(); ++j) {
+      const SegP& S = segs[j];
+      for (const NodeP& n : S.nodes)
+        if (n.op == PNN_OP_CONV) ts.push_back({(int)j, n.w_off, n.gw_off, (long)n.cout * n.k * n.k * n.cin, false});
+      for (const BnP& b : S.bns) ts.push_back({(int)j, b.p_off, b.gp_off, 2L * b.C, true});
+    }
+  }
+  for (const T& t : ts)
+    if (params[t.seg] == nullptr || grads[t.seg] == nullptr || momentum[t.seg] == nullptr) return PNN_ERR_NULL;
+  // launches of at most SGD_MAXT tensors from at most SGD_MAXS consecutive segments
+  size_t i = 0;
+  while (i < ts.size()) {
+    SgdLaunch L;
+    std::memset(&L, 0, sizeof(L));
+    L.lr = lr;
+    L.mu = mu;
+    L.wd = weight_decay;
+    L.nesterov = nesterov != 0;
+    const int seg0 = ts[i].seg;
+    int chunks = 0;
+    while (i < ts.size() && L.nt < SGD_MAXT && ts[i].seg - seg0 < SGD_MAXS) {
+      const T& t = ts[i++];
+      if (t.cnt <= 0) continue;
+      if (t.po > 0xffffffffu || t.go > 0xffffffffu || t.cnt > 0x7fffffffL) return PNN_ERR_UNSUPPORTED;
+      const int ls = t.seg - seg0;
+      L.p[ls] = params[t.seg];
+      L.g[ls] = grads[t.seg];
+      L.v[ls] = momentum[t.seg];
+      SgdEnt& e = L.e[L.nt++];
+      e.p_off = (uint32_t)t.po;
+      e.g_off = (uint32_t)t.go;
+      e.count = (uint32_t)t.cnt;
+      e.chunk0 = (uint32_t)chunks;
+      e.seg = (uint16_t)ls;
+      e.f32 = t.f32 ? 1 : 0;
+      chunks += (int)cdiv(t.cnt, SGD_CHUNK);
+    }
+    if (L.nt > 0 && launch_sgd(L, chunks, plan->dtype, st)) return PNN_ERR_HIP;
+  }
+  return PNN_OK;
+}
+
 pnn_status coarse_bwd(pnn_plan* plan, int j, const void* D_next, const void* rt_j, const void* eta_j,
                       const void* saved, void* D_j, float* deta_j, void* scratch, void* stream) {
   if (!ok_ctx(plan, const_cast<void*>(saved), scratch)) return PNN_ERR_NULL;

@@ -201,6 +201,26 @@ struct AxpyLaunch {
   AxpyProb p[PNN_MAXG];
 };
 
+// SGD with momentum over a list of parameter tensors.  Entry e covers count elements at byte
+// offset p_off of params[seg] and g_off of grads[seg] / momentum[seg]; workgroups
+// [chunk0, chunk0 + ceil(count / SGD_CHUNK)) of the launch update it.
+struct SgdEnt {
+  uint32_t p_off, g_off, count, chunk0;
+  uint16_t seg, f32;     // f32: parameters stored as float (else the plan's storage type)
+};
+constexpr int SGD_MAXT = 180;      // entries per launch
+constexpr int SGD_MAXS = 8;        // segments per launch
+constexpr int SGD_CHUNK = 2048;    // elements per workgroup
+struct SgdLaunch {
+  int nt, nesterov;
+  float lr, mu, wd;
+  void* p[SGD_MAXS];
+  const float* g[SGD_MAXS];
+  float* v[SGD_MAXS];
+  SgdEnt e[SGD_MAXT];
+};
+int launch_sgd(const SgdLaunch& L, int tiles, int dtype, hipStream_t s);
+
 // gk: 0 = pointwise (1x1, stride 1, pad 0), 1 = vector gather, 2 = element-wise gather,
 //     3 = 3x3 / stride 1 / pad 1 through an LDS halo tile;
 // wn: 16-column sub-tiles per wave (1, 2, 4) shared by every problem of the launch

@@ -184,3 +184,21 @@ class ParaRealGPU:
     def step(self, s=None):
         self.forward(s)
         self.backward(s)
+
+    # -- parameter update (SGD with momentum; include/pnn.h pnn_sgd_step) -------------------------
+    def sgd_init(self):
+        """Zeroed momentum buffers laid out like the gradient buffers."""
+        torch = _torch()
+        self.mom = [[torch.zeros_like(b, dtype=torch.uint8) for b in bufs]
+                    for bufs in (self.ddelta, self.dphi, self.deta)]
+        self.mom.append([torch.zeros_like(self.deps)])
+
+    def sgd_step(self, lr, mu=0.9, weight_decay=1e-4, nesterov=True, s=None):
+        s = self.stream() if s is None else s
+        if not hasattr(self, "mom"):
+            self.sgd_init()
+        parts = ((self.delta, self.ddelta), (self.phi, self.dphi), (self.eta, self.deta), ([self.eps], [self.deps]))
+        for part, (pb, gb) in enumerate(parts):
+            if not pb:
+                continue
+            B.pnn_sgd_step(self.plan, part, pb, gb, self.mom[part], lr, mu, weight_decay, nesterov, s)

@@ -478,3 +478,53 @@ def test_bf16_storage_model():
     assert max(rel(a, b) for a, b in zip(ba["dx"], bb["dx"])) > 2e-2
     bc = b16.backward(fa, f64.head(fa["ytilde"], labels))     # exact forward, rounded backward
     assert max(rel(a, b) for a, b in zip(ba["dx"], bc["dx"])) < 2e-2
+
+
+# ------------------------------------------------------------------------------------------------
+# parameter update (Sec. 4 training setup): SGD with momentum and weight decay
+# ------------------------------------------------------------------------------------------------
+
+def test_sgd_plain_descent_on_a_quadratic():
+    """mu = 0 on f(w) = a w^2 / 2 with decay wd: w_k = (1 - lr (a + wd))^k w_0 (closed form)."""
+    from oracle.sgd import sgd_step
+    a, lr, wd = 3.0, 0.05, 1e-2
+    w0 = np.array([1.5, -2.0, 0.25])
+    w, v = w0.copy(), np.zeros(3)
+    for k in range(1, 8):
+        w, v = sgd_step(w, a * w, v, lr, 0.0, wd, nesterov=True)
+        assert np.allclose(w, (1 - lr * (a + wd)) ** k * w0, rtol=1e-14, atol=0)
+
+
+@pytest.mark.parametrize("nesterov", [True, False])
+def test_sgd_momentum_decay_without_gradient(nesterov):
+    """Zero gradient and decay: v_k = mu^k v_0 and w_k = w_0 - lr c mu (1 - mu^k) / (1 - mu) v_0 with
+    c = mu (Nesterov's look-ahead) or 1 (closed form of the geometric series)."""
+    from oracle.sgd import sgd_step
+    lr, mu = 0.1, 0.9
+    v0 = np.array([0.5, -1.0])
+    w0 = np.array([2.0, 3.0])
+    w, v = w0.copy(), v0.copy()
+    c = mu if nesterov else 1.0
+    for k in range(1, 10):
+        w, v = sgd_step(w, np.zeros(2), v, lr, mu, 0.0, nesterov)
+        assert np.allclose(v, mu ** k * v0, rtol=1e-14)
+        assert np.allclose(w, w0 - lr * c * mu * (1 - mu ** k) / (1 - mu) * v0, rtol=1e-13)
+
+
+@pytest.mark.parametrize("nesterov", [True, False])
+def test_sgd_matches_torch_optim(nesterov):
+    """The same steps as torch.optim.SGD (momentum 0.9, weight decay, float64), an implementation
+    written independently of this one."""
+    import torch
+    from oracle.sgd import sgd_step
+    rng = np.random.default_rng(5)
+    w0 = rng.standard_normal((7, 5))
+    p = torch.nn.Parameter(torch.from_numpy(w0.copy()))
+    opt = torch.optim.SGD([p], lr=0.03, momentum=0.9, weight_decay=5e-4, nesterov=nesterov)
+    w, v = w0.copy(), np.zeros_like(w0)
+    for _ in range(6):
+        g = rng.standard_normal(w0.shape)
+        p.grad = torch.from_numpy(g.copy())
+        opt.step()
+        w, v = sgd_step(w, g, v, 0.03, 0.9, 5e-4, nesterov)
+        assert np.allclose(p.detach().numpy(), w, rtol=1e-13, atol=1e-15)
