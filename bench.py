@@ -236,12 +236,21 @@ def main():
         fam[name] = {"ms": ms, "launches": n, "flops": fl, "bytes": by}
     dom = max(fam, key=lambda k: fam[k]["ms"])
     d = fam[dom]
+    # the family's bound: MFMA when its algorithmic intensity is above the ridge point
+    # (peak FLOP/s / peak bytes/s), else HBM
+    peak_f = PEAK_BF16_TFLOPS if net.dtype == "bf16" else PEAK_F32_TFLOPS
+    mfma = d["flops"] / max(d["bytes"], 1.0) > peak_f * 1e12 / (PEAK_HBM_GBS * 1e9)
+    tflops_dom = d["flops"] / (d["ms"] * 1e-3) / 1e12
     achieved = d["bytes"] / (d["ms"] * 1e-3) / 1e9
-    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": stored_traffic(dom),
+    roof = {"bound": "mfma" if mfma else "hbm",
+            "achieved": round(tflops_dom if mfma else achieved, 2 if mfma else 1),
+            "peak": peak_f if mfma else PEAK_HBM_GBS, "unit": "TFLOP/s" if mfma else "GB/s",
+            "frac": round((tflops_dom / peak_f) if mfma else (achieved / PEAK_HBM_GBS), 4),
+            "traffic": stored_traffic(dom) if args.config == 3 and args.coarse == "config" else None,
             "algorithmic_bytes_per_launch": round(d["bytes"] / max(d["launches"], 1)),
+            "algorithmic_flops_per_launch": round(d["flops"] / max(d["launches"], 1)),
             "kernel": dom, "avg_launch_us": round(d["ms"] * 1e3 / max(d["launches"], 1), 2),
-            "mfma_tflops": round(d["flops"] / (d["ms"] * 1e-3) / 1e12, 2)}
+            "hbm_gbs": round(achieved, 1), "mfma_tflops": round(tflops_dom, 2)}
 
     # the parameter update (SGD, Nesterov momentum; not part of the step the metric times)
     g.sgd_init()

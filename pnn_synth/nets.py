@@ -339,7 +339,7 @@ def tiny_parareal(name="tiny-basic-n2", batch=4, hw=32, ch=16, n_sub=2, classes=
 # ----------------------------------------------------------------------------------------------
 
 def config(idx: int, batch: Optional[int] = None, coarse: str = "config") -> Net:
-    """Workload ``idx`` (0..4); ``batch`` overrides the batch size (smaller parity cases);
+    """Workload ``idx`` (0..5); ``batch`` overrides the batch size (smaller parity cases);
     ``coarse="paper"`` replaces the coarse blocks F^j of the VGG / ResNet workloads by the paper's
     own coarse networks (ResNet: ceil(12/N) two-3x3 residual units per F^j, Sec. 4.2.1; VGG: two
     3x3 convolutions and a max pool, Sec. 4.1.1)."""
@@ -358,7 +358,12 @@ def config(idx: int, batch: Optional[int] = None, coarse: str = "config") -> Net
     if idx == 4:
         return resnet_parareal("resnet1001-parareal-n8-64px" + sfx, batch or 128, 64, 8, 200, "bf16",
                                (5001, 5002, 5003), coarse=coarse)
+    if idx == 5:
+        # ImageNet-shaped Parareal VGG-16-4 (Sec. 4.1.1, Table gradvgg): 224x224x3, 1000 classes,
+        # the paper's coarse blocks
+        return vgg_parareal("vgg16-parareal-n4-224px", batch or 128, 224, 1000, "bf16",
+                            (6001, 6002, 6003), coarse="paper")
     raise ValueError(idx)
 
 
-CONFIG_NAMES = [config(i, 1).name for i in range(5)]
+CONFIG_NAMES = [config(i, 1).name for i in range(6)]

@@ -29,7 +29,7 @@ def test_header_declarations_are_exported():
         assert hasattr(L, name), name
 
 
-@pytest.mark.parametrize("idx,coarse", [(i, "config") for i in range(5)] +
+@pytest.mark.parametrize("idx,coarse", [(i, "config") for i in range(6)] +
                          [(i, "paper") for i in range(1, 5)])
 def test_plans_and_layouts(idx, coarse):
     _lib_or_skip()
