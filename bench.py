@@ -160,6 +160,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, help="workload index 0..4")
+    ap.add_argument("--partition", default="contiguous",
+                    choices=("contiguous", "per_stage", "balanced", "balanced_flops"),
+                    help="split of the ResNet units into sub-networks")
     ap.add_argument("--coarse", default="config", choices=("config", "paper"),
                     help="coarse blocks F^j: the workload's (one unit) or the paper's own networks")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -197,7 +200,7 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    net = S.config(args.config, coarse=args.coarse)
+    net = S.config(args.config, coarse=args.coarse, partition=args.partition)
     x, labels, params = S.make_all(net)
     g = ParaRealGPU(net, params)
     g.load_input(x, labels)
@@ -246,7 +249,8 @@ def main():
             "achieved": round(tflops_dom if mfma else achieved, 2 if mfma else 1),
             "peak": peak_f if mfma else PEAK_HBM_GBS, "unit": "TFLOP/s" if mfma else "GB/s",
             "frac": round((tflops_dom / peak_f) if mfma else (achieved / PEAK_HBM_GBS), 4),
-            "traffic": stored_traffic(dom) if args.config == 3 and args.coarse == "config" else None,
+            "traffic": (stored_traffic(dom) if (args.config, args.coarse, args.partition) == (3, "config", "contiguous")
+                        else None),
             "algorithmic_bytes_per_launch": round(d["bytes"] / max(d["launches"], 1)),
             "algorithmic_flops_per_launch": round(d["flops"] / max(d["launches"], 1)),
             "kernel": dom, "avg_launch_us": round(d["ms"] * 1e3 / max(d["launches"], 1), 2),

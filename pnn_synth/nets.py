@@ -26,6 +26,8 @@ This module is shared input data: it holds no part of the method's arithmetic.
 from __future__ import annotations
 
 import math
+
+import numpy as np
 from dataclasses import dataclass, field
 from typing import List, Optional, Tuple
 
@@ -199,6 +201,48 @@ def partition_units(n_units, n_sub):
     return bounds
 
 
+def unit_cost(unit, kind="bytes"):
+    """Cost of one residual unit (cin, cout, stride, out_hw) for partitioning: "flops" = forward
+    multiply-adds of its convolutions, "bytes" = elements its convolutions read and write (what
+    bounds a layer-at-a-time schedule on a bandwidth-bound device).  Per image."""
+    cin, cout, stride, hw = unit
+    hin, mid = hw * stride, cout // 4
+    convs = [(hin, cin, hin, mid, 1), (hin, mid, hw, mid, 3), (hw, mid, hw, cout, 1)]   # (in_hw, cin, out_hw, cout, k)
+    if cin != cout or stride != 1:
+        convs.append((hin, cin, hw, cout, 1))
+    if kind == "flops":
+        return float(sum(o * o * co * ci * k * k for (i, ci, o, co, k) in convs))
+    return float(sum(i * i * ci + o * o * co for (i, ci, o, co, k) in convs) + hw * hw * cout)
+
+
+def partition_balanced(costs, n_sub):
+    """Contiguous split of units with costs ``costs`` into ``n_sub`` non-empty sub-networks that
+    minimises the largest sub-network cost (the decomposition by computational cost the paper
+    suggests in the Remark after Table grad).  Exact dynamic programme over prefix sums; ties go to
+    the earliest cut."""
+    n = len(costs)
+    assert 1 <= n_sub <= n
+    S = np.concatenate([[0.0], np.cumsum(np.asarray(costs, dtype=np.float64))])
+    INF = np.inf
+    best = np.full((n_sub + 1, n + 1), INF)
+    arg = np.zeros((n_sub + 1, n + 1), dtype=np.int64)
+    best[0, 0] = 0.0
+    for k in range(1, n_sub + 1):
+        for i in range(k, n - (n_sub - k) + 1):
+            j = np.arange(k - 1, i)
+            v = np.maximum(best[k - 1, j], S[i] - S[j])
+            a = int(np.argmin(v))
+            best[k, i] = v[a]
+            arg[k, i] = j[a]
+    bounds = []
+    i = n
+    for k in range(n_sub, 0, -1):
+        j = int(arg[k, i])
+        bounds.append((j, i))
+        i = j
+    return bounds[::-1]
+
+
 def partition_per_stage(units_per_stage, n_stages, n_sub):
     """The paper's split for N = 3 N_0 (Sec. 4.2.1): every stage cut into N_0 sub-networks of
     ceil(111 / N_0) units, the remainder to the stage's last one, so X_j is constant per stage."""
@@ -216,10 +260,14 @@ def resnet_parareal(name, batch, img_hw, n_sub, classes, dtype, seeds, coarse="c
                     partition="contiguous"):
     """Parareal ResNet-N (Sec. 4.2.1).  ``units_per_stage`` / ``widths`` / ``stem`` give smaller
     nets of the same form for tests.  ``partition``: "contiguous" chunks of ceil(333/N) units
-    (any N) or the paper's "per_stage" split (N a multiple of 3)."""
+    (any N), the paper's "per_stage" split (N a multiple of 3), or "balanced" / "balanced_flops":
+    equal cost per sub-network by unit_cost "bytes" / "flops"."""
     units = resnet_units(img_hw, units_per_stage, widths, stem)
     if partition == "per_stage":
         bounds = partition_per_stage(units_per_stage, len(widths), n_sub)
+    elif partition in ("balanced", "balanced_flops"):
+        kind = "flops" if partition == "balanced_flops" else "bytes"
+        bounds = partition_balanced([unit_cost(u, kind) for u in units], n_sub)
     else:
         bounds = partition_units(len(units), n_sub)
     # X_0 = stem output (``stem`` channels at full resolution), X_j = shape after g^j
@@ -338,12 +386,13 @@ def tiny_parareal(name="tiny-basic-n2", batch=4, hw=32, ch=16, n_sub=2, classes=
 # the five workloads
 # ----------------------------------------------------------------------------------------------
 
-def config(idx: int, batch: Optional[int] = None, coarse: str = "config") -> Net:
+def config(idx: int, batch: Optional[int] = None, coarse: str = "config", partition: str = "contiguous") -> Net:
     """Workload ``idx`` (0..5); ``batch`` overrides the batch size (smaller parity cases);
     ``coarse="paper"`` replaces the coarse blocks F^j of the VGG / ResNet workloads by the paper's
     own coarse networks (ResNet: ceil(12/N) two-3x3 residual units per F^j, Sec. 4.2.1; VGG: two
-    3x3 convolutions and a max pool, Sec. 4.1.1)."""
-    sfx = "" if coarse == "config" else "-papercoarse"
+    3x3 convolutions and a max pool, Sec. 4.1.1); ``partition`` splits the ResNet units
+    (resnet_parareal)."""
+    sfx = ("" if coarse == "config" else "-papercoarse") + ("" if partition == "contiguous" else "-" + partition)
     if idx == 0:
         return tiny_parareal(batch=batch or 4)
     if idx == 1:
@@ -351,13 +400,13 @@ def config(idx: int, batch: Optional[int] = None, coarse: str = "config") -> Net
                             coarse=coarse)
     if idx == 2:
         return resnet_parareal("resnet1001-parareal-n4" + sfx, batch or 64, 32, 4, 100, "bf16",
-                               (3001, 3002, 3003), coarse=coarse)
+                               (3001, 3002, 3003), coarse=coarse, partition=partition)
     if idx == 3:
         return resnet_parareal("resnet1001-parareal-n16" + sfx, batch or 128, 32, 16, 100, "bf16",
-                               (4001, 4002, 4003), coarse=coarse)
+                               (4001, 4002, 4003), coarse=coarse, partition=partition)
     if idx == 4:
         return resnet_parareal("resnet1001-parareal-n8-64px" + sfx, batch or 128, 64, 8, 200, "bf16",
-                               (5001, 5002, 5003), coarse=coarse)
+                               (5001, 5002, 5003), coarse=coarse, partition=partition)
     if idx == 5:
         # ImageNet-shaped Parareal VGG-16-4 (Sec. 4.1.1, Table gradvgg): 224x224x3, 1000 classes,
         # the paper's coarse blocks

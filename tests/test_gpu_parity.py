@@ -93,9 +93,10 @@ def _assert_tol(err, tol):
     assert not bad, sorted(bad.items(), key=lambda kv: -kv[1])[:10]
 
 
-def mini_resnet(n_sub, ups, batch, dtype="f32", hw=16, coarse="config"):
+def mini_resnet(n_sub, ups, batch, dtype="f32", hw=16, coarse="config", partition="contiguous"):
     return resnet_parareal(f"mini-resnet-u{ups}-n{n_sub}", batch, hw, n_sub, 10, dtype, (7, 8, 9),
-                           units_per_stage=ups, widths=(64, 128, 256), stem=16, coarse=coarse)
+                           units_per_stage=ups, widths=(64, 128, 256), stem=16, coarse=coarse,
+                           partition=partition)
 
 
 def test_tiny_workload_fp32():
@@ -115,6 +116,13 @@ def test_resnet_paper_coarse_fp32(n_sub, ups, batch):
     """The paper's own coarse network (ceil(12/N) two-3x3 residual units per F^j, the first strided
     with a projection at stage changes, Sec. 4.2.1): every tensor to 1e-4."""
     _assert_tol(run_net(mini_resnet(n_sub, ups, batch, coarse="paper")), 1e-4)
+
+
+@pytest.mark.parametrize("partition", ["balanced", "balanced_flops"])
+def test_resnet_balanced_partition_fp32(partition):
+    """Sub-networks of unequal unit counts from the cost-balanced decomposition: every tensor to
+    1e-4."""
+    _assert_tol(run_net(mini_resnet(4, 4, 2, partition=partition)), 1e-4)
 
 
 def test_vgg_paper_coarse_fp32():

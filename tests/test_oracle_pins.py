@@ -528,3 +528,43 @@ def test_sgd_matches_torch_optim(nesterov):
         opt.step()
         w, v = sgd_step(w, g, v, 0.03, 0.9, 5e-4, nesterov)
         assert np.allclose(p.detach().numpy(), w, rtol=1e-13, atol=1e-15)
+
+
+# ------------------------------------------------------------------------------------------------
+# cost-balanced decomposition (Remark after Table grad): contiguous, min-max cost
+# ------------------------------------------------------------------------------------------------
+
+def _all_splits(n, k):
+    """Every split of range(n) into k non-empty contiguous parts (brute force)."""
+    import itertools
+    for cuts in itertools.combinations(range(1, n), k - 1):
+        b = (0,) + cuts + (n,)
+        yield [(b[i], b[i + 1]) for i in range(k)]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_balanced_partition_is_the_brute_force_optimum(seed):
+    from pnn_synth.nets import partition_balanced
+    rng = np.random.default_rng(seed)
+    n, k = int(rng.integers(4, 11)), int(rng.integers(1, 5))
+    costs = rng.uniform(0.1, 3.0, n)
+    b = partition_balanced(costs, k)
+    assert b[0][0] == 0 and b[-1][1] == n and all(e > s for s, e in b)
+    assert all(b[i][1] == b[i + 1][0] for i in range(k - 1))
+    got = max(costs[s:e].sum() for s, e in b)
+    best = min(max(costs[s:e].sum() for s, e in sp) for sp in _all_splits(n, k))
+    assert np.isclose(got, best, rtol=1e-12)
+
+
+def test_balanced_partition_special_cases():
+    """Equal costs give sizes differing by at most one; one sub-network takes everything; as many
+    sub-networks as units gives one unit each; ResNet-1001's bottlenecks have (near) equal FLOPs, so
+    the FLOP-balanced split of 333 units into 16 is 20-21 units each."""
+    from pnn_synth.nets import partition_balanced, resnet_units, unit_cost
+    for n, k in ((12, 4), (13, 4), (333, 16)):
+        sizes = [e - s for s, e in partition_balanced(np.ones(n), k)]
+        assert max(sizes) - min(sizes) <= 1 and sum(sizes) == n
+    assert partition_balanced(np.ones(5), 1) == [(0, 5)]
+    assert partition_balanced(np.arange(1.0, 6.0), 5) == [(i, i + 1) for i in range(5)]
+    sizes = [e - s for s, e in partition_balanced([unit_cost(u, "flops") for u in resnet_units(32)], 16)]
+    assert set(sizes) <= {20, 21, 22}
