@@ -817,6 +817,178 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
 }
 
 // ------------------------------------------------------------------------------------------------
+// weight gradient of a 3x3 / stride 1 / pad 1 convolution through an LDS halo tile:
+// dW[co][(r,s)][c] = sum_m g[m][co] * act(in)[pixel(m) + (r - 1, s - 1)][c]
+//
+// A workgroup owns 16 output channels x one 16-channel input block x all 9 taps (9 MFMA column
+// tiles) over an m range (split-K in stages of W3_KC rows = whole image rows).  Each stage stages
+// the output-gradient rows m-major and the stage's input rows plus a one-pixel halo (BN prologue
+// applied when the loads land, zeros for padding) in LDS, once for all taps; the fragments of the
+// 8 consecutive m of a lane group are consecutive pixels of one halo row, read with the LDS
+// transpose read at the tap's pixel offset.  The four waves split each stage's K steps and are
+// summed in LDS in a fixed order at the end.
+// ------------------------------------------------------------------------------------------------
+template <typename T>
+struct W3Cfg {
+  static constexpr int VE = St<T>::VE;
+  static constexpr int KC = sizeof(T) == 2 ? 256 : 128;   // m rows per stage
+  static constexpr int PADE = 8 / sizeof(T);             // 8-byte row padding of the g tile
+  static constexpr int RSG = 16 + PADE;
+  static constexpr int GC = KC * 16 / VE / 256;          // g chunks per thread
+  static constexpr int HC = 4;                           // max halo chunks per thread
+  static constexpr int HALO = HC * 256 * VE;             // halo elements
+  static constexpr int STAGE_BYTES = (KC * RSG + HALO) * sizeof(T);
+  static constexpr int RED_BYTES = 3 * 9 * 256 * 4;      // waves 1..3 x 9 tiles x 16 x 16 floats
+  static constexpr int LDS_BYTES = STAGE_BYTES > RED_BYTES ? STAGE_BYTES : RED_BYTES;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void wgrad3_kernel(const WgradLaunch L) {
+  using C = W3Cfg<T>;
+  constexpr int VE = C::VE;
+  constexpr int KS = 4 * VE;
+  constexpr int KC = C::KC;
+  __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
+  __shared__ float2 pro_s[16];
+  T* lg = (T*)smem;
+  T* lh = lg + KC * C::RSG;
+
+  const int gi = find_group(L);
+  const WgradProb& P = L.p[gi];
+  const int local = blockIdx.x - P.tile_begin;
+  const int tcb = local % P.tiles_k;                // 16-channel input block
+  const int rest = local / P.tiles_k;
+  const int tco = rest % P.tiles_co;
+  const int split = rest / P.tiles_co;
+  const int co0 = tco * 16, c0 = tcb * 16;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int m_begin = split * P.mchunk;
+  const int m_end = min(P.M, m_begin + P.mchunk);
+  const int PQ = P.P * P.Q;
+  const int QH = P.Q + 2;
+  const bool multi = KC > PQ;
+  const int R = multi ? P.P : KC / P.Q;             // output rows per image in a stage
+  const int RH = R + 2;
+  const int nimg = multi ? KC / PQ : 1;
+  const int img_px = RH * QH;
+  constexpr int cpp = 16 / VE;                      // halo chunks per pixel
+  const int hchunks = nimg * img_px * cpp;
+
+  if (P.pro != nullptr && tid < 16) pro_s[tid] = make_float2(P.pro[c0 + tid], P.pro[P.Cg + c0 + tid]);
+  __syncthreads();
+
+  uint4 ga[C::GC], ha[C::HC];
+  int hoff[C::HC];
+  uint32_t hpend = 0;
+  const float r_img = 1.0f / img_px, r_qh = 1.0f / QH;
+
+  auto load_stage = [&](int mc) {
+#pragma unroll
+    for (int i = 0; i < C::GC; ++i) {
+      const int idx = tid + i * 256;
+      const int row = idx / (16 / VE), cc = (idx % (16 / VE)) * VE;
+      const int m = mc + row;
+      ga[i] = m < m_end ? *(const uint4*)((const T*)P.g + (long)m * P.Co + co0 + cc) : make_uint4(0, 0, 0, 0);
+    }
+    const int n_first = div_l2(mc, PQ, P.pq_log2);
+    const int p0 = multi ? 0 : div_l2(mc - n_first * PQ, P.Q, P.q_log2);
+    hpend = 0;
+#pragma unroll
+    for (int u = 0; u < C::HC; ++u) {
+      const int idx = tid + u * 256;
+      const int pix = idx / cpp, ch = idx % cpp;
+      int i, rem, y, x;
+      if (nimg > 1) divmod_small(pix, img_px, r_img, i, rem);
+      else { i = 0; rem = pix; }
+      divmod_small(rem, QH, r_qh, y, x);
+      const int n = n_first + i, ih = p0 - 1 + y, iw = x - 1;
+      const bool ok = idx < hchunks && n < P.B && (unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W;
+      hoff[u] = idx < hchunks ? pix * 16 + ch * VE : -1;
+      const long gofs = ok ? (((long)n * P.H + ih) * P.W + iw) * P.Cg + c0 + ch * VE : 0;
+      ha[u] = ok ? *(const uint4*)((const T*)P.in + gofs) : make_uint4(0, 0, 0, 0);
+      hpend |= ((ok && P.pro != nullptr) ? 1u : 0u) << u;
+    }
+  };
+  auto store_stage = [&]() {
+#pragma unroll
+    for (int i = 0; i < C::GC; ++i) {
+      const int idx = tid + i * 256;
+      const int row = idx / (16 / VE), cc = (idx % (16 / VE)) * VE;
+      lds_store8<T>(lg + row * C::RSG + cc, ga[i]);
+    }
+#pragma unroll
+    for (int u = 0; u < C::HC; ++u) {
+      if (hoff[u] < 0) continue;
+      uint4 w = ha[u];
+      if ((hpend >> u) & 1u) {
+        const int cb = hoff[u] & 15;            // channel offset within the block
+        Chunk<T> c;
+        unpack_chunk<T>(w, c);
+        float v[VE];
+#pragma unroll
+        for (int e = 0; e < VE; ++e) v[e] = fmaxf(fmaf(c.v[e], pro_s[cb + e].x, pro_s[cb + e].y), 0.0f);
+        store_chunk<T>(&w, 0, v);
+      }
+      *(uint4*)(lh + hoff[u]) = w;
+    }
+  };
+
+  f32x4 acc[9];
+#pragma unroll
+  for (int t = 0; t < 9; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (m_begin < m_end) load_stage(m_begin);
+  for (int mc = m_begin; mc < m_end; mc += KC) {
+    store_stage();
+    __syncthreads();
+    if (mc + KC < m_end) load_stage(mc + KC);
+    for (int st = wave; st < KC / KS; st += 4) {
+      const int row0 = st * KS + VE * grp;        // first of the lane group's VE rows of the stage
+      Frag<T> a;
+      lds_frag<T>(lg, row0, C::RSG, 0, r16, a);
+      const int i = multi ? div_l2(row0, PQ, P.pq_log2) : 0;
+      const int rem = row0 - i * PQ;
+      const int pl = div_l2(rem, P.Q, P.q_log2);
+      const int ql = rem - pl * P.Q;
+      const int pix0 = (i * RH + pl) * QH + ql;   // halo pixel of tap (0, 0)
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const int r = t / 3, s = t - 3 * (t / 3);
+        Frag<T> b;
+        lds_frag<T>(lh, pix0 + r * QH + s, 16, 0, r16, b);
+        mma(a, b, acc[t]);
+      }
+    }
+    __syncthreads();
+  }
+
+  // sum the four waves' K-step shares in wave order, then write the 16 x 144 partial tile
+  float* red = (float*)smem;
+  if (wave > 0) {
+#pragma unroll
+    for (int t = 0; t < 9; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[((wave - 1) * 9 + t) * 256 + (grp * 4 + i) * 16 + r16] = acc[t][i];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  for (int w = 0; w < 3; ++w)
+#pragma unroll
+    for (int t = 0; t < 9; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[t][i] += red[(w * 9 + t) * 256 + (grp * 4 + i) * 16 + r16];
+#pragma unroll
+  for (int t = 0; t < 9; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int co = co0 + grp * 4 + i;
+      P.part[((long)split * P.Co + co) * P.K + t * P.Cg + c0 + r16] = acc[t][i];
+    }
+}
+
+// ------------------------------------------------------------------------------------------------
 // launchers
 // ------------------------------------------------------------------------------------------------
 
@@ -848,6 +1020,14 @@ int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int
     if (mode == MODE_FWD) launch_conv_m<float, MODE_FWD>(L, tiles, gk, wn, s);
     else launch_conv_m<float, MODE_BWD>(L, tiles, gk, wn, s);
   }
+  return (int)hipGetLastError();
+}
+
+int launch_wgrad3(const WgradLaunch& L, int tiles, int dtype, hipStream_t s) {
+  if (dtype == 1)
+    hipLaunchKernelGGL((wgrad3_kernel<uint16_t>), dim3(tiles), dim3(256), 0, s, L);
+  else
+    hipLaunchKernelGGL((wgrad3_kernel<float>), dim3(tiles), dim3(256), 0, s, L);
   return (int)hipGetLastError();
 }
 

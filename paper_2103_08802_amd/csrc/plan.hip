@@ -73,6 +73,7 @@ struct SegP {
 
 struct WgradGeom {
   int wr, tiles_co, tiles_k, splits, mchunk;
+  bool halo3 = false;      // 3x3 / stride 1 / pad 1 through the halo kernel (tiles_k = Cg / 16)
 };
 
 }  // namespace
@@ -100,7 +101,39 @@ namespace {
 // plan construction
 // ------------------------------------------------------------------------------------------------
 
-// Weight-gradient tiling: (16 wr) x 64 dW tiles, split-K over m in multiples of 128 rows.
+// Weight-gradient tiling.  3x3 / stride 1 / pad 1 convolutions whose stages of W3 rows are whole
+// image rows go to the halo kernel: 16 output channels x one 16-channel input block x 9 taps per
+// workgroup, split-K in multiples of the stage.  Everything else: (16 wr) x 64 dW tiles, split-K
+// over m in multiples of 128 rows.
+WgradGeom wgrad_geom(int Co, int K, long M);
+
+WgradGeom wgrad_geom_node(const NodeP& n, int B, int es) {
+  const long M = (long)B * n.Ho * n.Wo;
+  const int K = n.k * n.k * n.cin;
+  const int kc = es == 2 ? 256 : 128;               // stage rows of the halo kernel (W3Cfg::KC)
+  const int ve = 16 / es;
+  const long pq = (long)n.Ho * n.Wo;
+  const bool whole_rows = kc % n.Wo == 0 && (pq % kc == 0 || kc % pq == 0);
+  if (n.k == 3 && n.stride == 1 && n.pad == 1 && n.H == n.Ho && n.W == n.Wo && n.Wo % 8 == 0 &&
+      n.cin % 16 == 0 && n.cout % 16 == 0 && whole_rows) {
+    const long nimg = kc > pq ? kc / pq : 1;
+    const long rows = kc > pq ? n.Ho : kc / n.Wo;
+    if (nimg * (rows + 2) * (n.Wo + 2) * (16 / ve) <= 1024) {      // W3Cfg::HC halo chunks / thread
+      WgradGeom g;
+      g.halo3 = true;
+      g.wr = 1;
+      g.tiles_co = n.cout / 16;
+      g.tiles_k = n.cin / 16;
+      const long base = (long)g.tiles_co * g.tiles_k;
+      long splits = std::max(1L, std::min(cdiv(M, 4L * kc), cdiv(256, base)));
+      g.mchunk = (int)(cdiv(cdiv(M, splits), kc) * kc);
+      g.splits = (int)cdiv(M, g.mchunk);
+      return g;
+    }
+  }
+  return wgrad_geom(n.cout, K, M);
+}
+
 WgradGeom wgrad_geom(int Co, int K, long M) {
   WgradGeom g;
   g.wr = (Co % 64 == 0) ? 4 : (Co % 32 == 0) ? 2 : 1;
@@ -329,7 +362,7 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
 }
 
 // wgrad partial bytes needed by one level of a set of segments run together
-size_t wgrad_level_bytes(const std::vector<SegP>& segs, int B) {
+size_t wgrad_level_bytes(const std::vector<SegP>& segs, int B, int es) {
   int maxL = 0;
   for (auto& s : segs) maxL = std::max(maxL, s.max_level);
   size_t best = 0;
@@ -338,9 +371,8 @@ size_t wgrad_level_bytes(const std::vector<SegP>& segs, int B) {
     for (auto& s : segs)
       for (auto& n : s.nodes) {
         if (n.level != L || n.op != PNN_OP_CONV) continue;
-        const long M = (long)B * n.Ho * n.Wo;
         const int K = n.k * n.k * n.cin;
-        WgradGeom g = wgrad_geom(n.cout, K, M);
+        WgradGeom g = wgrad_geom_node(n, B, es);
         tot = align256(tot + (size_t)g.splits * n.cout * K * 4);
       }
     best = std::max(best, tot);
@@ -791,7 +823,7 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
       if (e) return e;
     }
     // B + C: weight gradients
-    std::vector<WgradProb> wg_vec, wg_gen;
+    std::vector<WgradProb> wg_vec, wg_gen, wg_h3;
     std::vector<ColRedProb> red;
     size_t woff = 0;
     for (size_t i = 0; i < segs.size(); ++i) {
@@ -808,14 +840,14 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
         p.k = n.k; p.stride = n.stride; p.pad = n.pad;
         p.M = B * n.Ho * n.Wo;
         p.K = n.k * n.k * n.cin;
-        WgradGeom g = wgrad_geom(p.Co, p.K, p.M);
+        WgradGeom g = wgrad_geom_node(n, B, es);
         p.wr = g.wr; p.tiles_co = g.tiles_co; p.tiles_k = g.tiles_k; p.splits = g.splits; p.mchunk = g.mchunk;
         p.cg_log2 = log2_or(p.Cg);
         p.q_log2 = log2_or(p.Q);
         p.pq_log2 = log2_or(p.P * p.Q);
         p.part = (float*)(wpart + woff);
         woff = align256(woff + (size_t)g.splits * p.Co * p.K * 4);
-        (n.cin % (16 / es) == 0 ? wg_vec : wg_gen).push_back(p);
+        (g.halo3 ? wg_h3 : n.cin % (16 / es) == 0 ? wg_vec : wg_gen).push_back(p);
         ColRedProb r;
         std::memset(&r, 0, sizeof(r));
         r.part = p.part;
@@ -827,8 +859,8 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
         red.push_back(r);
       }
     }
-    for (int v = 0; v < 2; ++v) {
-      auto& list = v == 0 ? wg_vec : wg_gen;
+    for (int v = 0; v < 3; ++v) {
+      auto& list = v == 0 ? wg_vec : v == 1 ? wg_gen : wg_h3;
       int e = grouped<WgradLaunch>(
           list, [](const WgradProb& p) { return p.tiles_co * p.tiles_k * p.splits; },
           [&](const WgradLaunch& Lx, int tiles, size_t) {
@@ -839,7 +871,8 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
               by += (double)p.M * p.Co * es + (double)p.B * p.H * p.W * p.Cg * es + (double)p.Co * p.K * 4;
             }
             Timer t(plan, 2, c.stream);
-            int e2 = launch_wgrad(Lx, tiles, plan->dtype, v == 0, c.stream);
+            int e2 = v == 2 ? launch_wgrad3(Lx, tiles, plan->dtype, c.stream)
+                            : launch_wgrad(Lx, tiles, plan->dtype, v == 0, c.stream);
             t.done(c.stream, fl, by);
             return e2;
           });
@@ -1001,9 +1034,9 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
       sv = align256(sv + s.saved_bytes);
     }
   p->saved_bytes = sv;
-  size_t wp = wgrad_level_bytes(p->fine, p->B);
-  wp = std::max(wp, wgrad_level_bytes(p->pre, p->B));
-  for (auto& s : p->coarse) wp = std::max(wp, wgrad_level_bytes(std::vector<SegP>{s}, p->B));
+  size_t wp = wgrad_level_bytes(p->fine, p->B, p->es);
+  wp = std::max(wp, wgrad_level_bytes(p->pre, p->B, p->es));
+  for (auto& s : p->coarse) wp = std::max(wp, wgrad_level_bytes(std::vector<SegP>{s}, p->B, p->es));
   size_t sc = 0;
   p->wpart_off = sc;
   p->wpart_bytes = wp;

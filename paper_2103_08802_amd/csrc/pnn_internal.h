@@ -226,6 +226,8 @@ int launch_sgd(const SgdLaunch& L, int tiles, int dtype, hipStream_t s);
 // wn: 16-column sub-tiles per wave (1, 2, 4) shared by every problem of the launch
 int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, hipStream_t s);
 int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s);
+// 3x3 / stride 1 / pad 1 through an LDS halo tile: tiles_co = Co / 16, tiles_k = Cg / 16 blocks
+int launch_wgrad3(const WgradLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_colred(const ColRedLaunch& L, int tiles, hipStream_t s);
 int launch_colstat(const ColStatLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_bn_apply(const BnApplyLaunch& L, int tiles, int dtype, hipStream_t s);
