@@ -118,14 +118,18 @@ __device__ __forceinline__ void mma(const Frag<float>& a, const Frag<float>& b, 
   for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[e], b.v[e], acc, 0, 0, 0);
 }
 
-// Problem of this workgroup in a grouped launch: the last p with p.tile_begin <= blockIdx.x.
+// Problem of this workgroup in a grouped launch: the last p with p.tile_begin <= blockIdx.x
+// (tile_begin is non-decreasing; problems without tiles share the next one's begin).
 template <typename Launch>
 __device__ __forceinline__ int find_group(const Launch& L) {
-  int g = 0;
   const int t = blockIdx.x;
-  for (int i = 1; i < L.n; ++i)
-    if (L.p[i].tile_begin <= t) g = i;
-  return g;
+  int lo = 0, hi = L.n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (L.p[mid].tile_begin <= t) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
 }
 
 // x / d and x % d for a divisor given with log2(d) (>= 0) or as a plain value (lg < 0)

@@ -67,28 +67,33 @@ __global__ __launch_bounds__(1024) void colred_kernel(const ColRedLaunch L) {
   const int col = c0 + cl;
   double acc = 0.0;
   if (col < P.ncols) {
+    // row lane rl sums rows rl, rl + S, ... with eight loads in flight (eight interleaved partial
+    // sums, combined in a fixed order)
     const float* p = P.part + col;
-    int r = rl;
-    double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
     constexpr int S = RED_LANES;
-    for (; r + 3 * S < P.rows; r += 4 * S) {
-      a0 += (double)p[(long)r * P.ncols];
-      a1 += (double)p[(long)(r + S) * P.ncols];
-      a2 += (double)p[(long)(r + 2 * S) * P.ncols];
-      a3 += (double)p[(long)(r + 3 * S) * P.ncols];
+    double a[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) a[u] = 0.0;
+    int r = rl;
+    for (; r + 7 * S < P.rows; r += 8 * S) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = p[(long)(r + u * S) * P.ncols];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) a[u] += (double)v[u];
     }
-    for (; r < P.rows; r += S) a0 += (double)p[(long)r * P.ncols];
-    acc = (a0 + a1) + (a2 + a3);
+    for (; r < P.rows; r += S) a[0] += (double)p[(long)r * P.ncols];
+    acc = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
   }
   red[rl][cl] = acc;
   __syncthreads();
-  double tot = 0.0;
-  if (rl == 0) {
-    tot = red[0][cl];
+  // pairwise tree over the row lanes (fixed pairing)
 #pragma unroll
-    for (int k = 1; k < RED_LANES; ++k) tot += red[k][cl];
-    sum[cl] = tot;
+  for (int h = RED_LANES / 2; h >= 1; h >>= 1) {
+    if (rl < h) red[rl][cl] += red[rl + h][cl];
+    __syncthreads();
   }
+  if (rl == 0) sum[cl] = red[0][cl];
   __syncthreads();
   if (rl != 0 || col >= P.ncols) return;
   // BN modes: column 2c holds the first sum of channel c, column 2c+1 the second

@@ -464,7 +464,7 @@ int grouped(std::vector<Prob>& probs, TilesOf tiles_of, Fire fire) {
     L.n = 0;
     int tiles = 0;
     size_t first = i;
-    while (i < probs.size() && L.n < PNN_MAXG) {
+    while (i < probs.size() && L.n < (int)(sizeof(L.p) / sizeof(L.p[0]))) {
       Prob pr = probs[i];
       pr.tile_begin = tiles;
       tiles += tiles_of(pr);

@@ -1,9 +1,10 @@
 // Internal declarations of libpnn: grouped-launch problem descriptors shared by the host plan
 // code and the gfx950 kernels, plus the launchers.
 //
-// A grouped launch carries up to PNN_MAXG independent problems by value in its kernel
-// arguments (the N fine sub-networks of one depth level are the groups of one launch).  Every
-// problem owns a contiguous range [tile_begin, tile_begin + tiles) of the launch's workgroups.
+// A grouped launch carries up to PNN_MAXG (for small problem records more, within the 4 KB of
+// kernel arguments) independent problems by value in its kernel arguments (the N fine
+// sub-networks of one depth level are the groups of one launch).  Every problem owns a contiguous
+// range [tile_begin, tile_begin + tiles) of the launch's workgroups.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -101,7 +102,7 @@ struct ColRedProb {
 };
 struct ColRedLaunch {
   int n;
-  ColRedProb p[PNN_MAXG];
+  ColRedProb p[40];
 };
 constexpr int RED_COLS = 32;       // columns per column-reduce workgroup
 constexpr int RED_LANES = 32;      // row lanes per column (1024 threads)
@@ -143,7 +144,7 @@ struct BnApplyProb {
 };
 struct BnApplyLaunch {
   int n;
-  BnApplyProb p[PNN_MAXG];
+  BnApplyProb p[60];
 };
 
 // bnact: out = pool(ReLU(z * scale + shift)) [+ res] [+ ext]  (pool 0 or 2x2/2)
@@ -185,7 +186,7 @@ struct TransposeProb {   // wt[c][r][s][o] = w[o][r][s][c]
 };
 struct TransposeLaunch {
   int n;
-  TransposeProb p[PNN_MAXG];
+  TransposeProb p[120];
 };
 
 struct AxpyProb {        // out = a - b (rounded to storage); partial sum of squares (nullable)
@@ -224,6 +225,10 @@ int launch_sgd(const SgdLaunch& L, int tiles, int dtype, hipStream_t s);
 // gk: 0 = pointwise (1x1, stride 1, pad 0), 1 = vector gather, 2 = element-wise gather,
 //     3 = 3x3 / stride 1 / pad 1 through an LDS halo tile;
 // wn: 16-column sub-tiles per wave (1, 2, 4) shared by every problem of the launch
+// every launch record fits the 4 KB of kernel arguments
+static_assert(sizeof(ConvLaunch) <= 4096 && sizeof(WgradLaunch) <= 4096 && sizeof(ColRedLaunch) <= 4096 &&
+              sizeof(BnApplyLaunch) <= 4096 && sizeof(TransposeLaunch) <= 4096 && sizeof(SgdLaunch) <= 4096,
+              "kernel argument size");
 int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, hipStream_t s);
 int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s);
 // 3x3 / stride 1 / pad 1 through an LDS halo tile: tiles_co = Co / 16, tiles_k = Cg / 16 blocks
