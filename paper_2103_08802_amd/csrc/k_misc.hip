@@ -129,19 +129,59 @@ __global__ __launch_bounds__(1024) void colred_kernel(const ColRedLaunch L) {
 // Column sums / sums of squares of a stored tensor [M][C], COLSTAT_ROWS rows per workgroup.
 template <typename T>
 __global__ __launch_bounds__(256) void colstat_kernel(const ColStatLaunch L) {
+  // thread = (row lane, 16-byte column chunk); a lane sums its rows in order, lanes are added in
+  // lane order through LDS
+  constexpr int VE = St<T>::VE;
+  __shared__ float2 red[256 * VE];
   const int gi = find_group(L);
   const ColStatProb& P = L.p[gi];
   const int tile = blockIdx.x - P.tile_begin;
   const long r0 = (long)tile * COLSTAT_ROWS;
   const long r1 = min(P.M, r0 + COLSTAT_ROWS);
-  for (int c = threadIdx.x; c < P.C; c += 256) {
-    float s = 0.f, s2 = 0.f;
-    for (long r = r0; r < r1; ++r) {
-      const float v = St<T>::ld(P.x, r * P.C + c);
-      s += v;
-      s2 += v * v;
+  const int ncc = P.C / VE;
+  const int RL = 256 / ncc;
+  const int cc = threadIdx.x % ncc, rl = threadIdx.x / ncc;
+  float s1[VE], s2[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) s1[e] = s2[e] = 0.f;
+  if (rl < RL) {
+    long r = r0 + rl;
+    for (; r + 3 * RL < r1; r += 4 * RL) {
+      uint4 u[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) u[k] = *(const uint4*)((const T*)P.x + (r + k * RL) * P.C + cc * VE);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        Chunk<T> c;
+        unpack_chunk<T>(u[k], c);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          s1[e] += c.v[e];
+          s2[e] += c.v[e] * c.v[e];
+        }
+      }
     }
-    ((float2*)P.part)[(long)tile * P.C + c] = make_float2(s, s2);
+    for (; r < r1; r += RL) {
+      Chunk<T> c;
+      load_chunk<T>(P.x, r * P.C + cc * VE, c);
+#pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        s1[e] += c.v[e];
+        s2[e] += c.v[e] * c.v[e];
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < VE; ++e) red[rl * P.C + cc * VE + e] = make_float2(s1[e], s2[e]);
+  }
+  __syncthreads();
+  for (int c = threadIdx.x; c < P.C; c += 256) {
+    float a = 0.f, b = 0.f;
+    for (int k = 0; k < RL; ++k) {
+      const float2 v = red[k * P.C + c];
+      a += v.x;
+      b += v.y;
+    }
+    ((float2*)P.part)[(long)tile * P.C + c] = make_float2(a, b);
   }
 }
 
