@@ -145,16 +145,16 @@ __device__ __forceinline__ void load_b(const ConvProb& P, int col, int k0, Frag<
 // channels are followed by 0, 1 or 2 unused 16-byte chunks (conv_halo_pad) so that each half-wave's
 // A reads (16 pixels x an aligned chunk pair) fall on distinct LDS banks.  Wave w
 // owns column sub-tile w % WN and WM * WN row sub-tiles; its filter fragments for all K steps (at most
-// CONV_HALO_NKB) are loaded into registers before the LDS fill completes.  Steps past K read a
+// conv_halo_nkb(WN)) are loaded into registers before the LDS fill completes.  Steps past K read a
 // valid A position; the filter fragment there is zero.
-template <typename T, int MODE, int WM, int WN>
+template <typename T, int MODE, int WM, int WN, typename F>
 __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, T* halo, int tm, int n0,
-                                          f32x4 (&acc)[WM][WN]) {
+                                          f32x4 (&acc)[WM][WN], F&& before_compute) {
   constexpr int VE = St<T>::VE;
   constexpr int KS = 4 * VE;
   constexpr int BM = 64 * WM;
   constexpr int NT = WM * WN;                 // row sub-tiles per wave
-  constexpr int NKB = CONV_HALO_NKB;
+  constexpr int NKB = conv_halo_nkb(WN);
   constexpr int NL = 8;                      // halo chunks in flight per thread
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
@@ -222,7 +222,7 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
     }
   }
 
-  int rb[8];
+  int rb[NT];
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     const int lm = (rg * NT + t) * 16 + r16;
@@ -233,6 +233,7 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
     rb[t] = (i * RH + pl) * QH + ql;
   }
   __syncthreads();
+  before_compute();                           // the epilogue's early loads overlap the K loop
 
 #pragma unroll
   for (int s = 0; s < NKB; ++s) {
@@ -326,13 +327,16 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
                    : ((P.flags & EPI_STORE_F32) ? nullptr : (bnmask ? P.zsrc : P.res));
   const void* pf2 = (MODE == MODE_FWD) ? P.ext : (bnapply ? P.res : nullptr);
   uint4 pre[NCH], pre2[NCH];
+  auto load_epi = [&]() {
 #pragma unroll
-  for (int k = 0; k < NCH; ++k) {
-    const int m = tm * BM + tid / ncc + k * rpp;
-    const long o = (long)m * P.ncol + n0 + c0;
-    pre[k] = (pf != nullptr && m < P.M) ? *(const uint4*)((const T*)pf + o) : make_uint4(0, 0, 0, 0);
-    pre2[k] = (pf2 != nullptr && m < P.M) ? *(const uint4*)((const T*)pf2 + o) : make_uint4(0, 0, 0, 0);
-  }
+    for (int k = 0; k < NCH; ++k) {
+      const int m = tm * BM + tid / ncc + k * rpp;
+      const long o = (long)m * P.ncol + n0 + c0;
+      pre[k] = (pf != nullptr && m < P.M) ? *(const uint4*)((const T*)pf + o) : make_uint4(0, 0, 0, 0);
+      pre2[k] = (pf2 != nullptr && m < P.M) ? *(const uint4*)((const T*)pf2 + o) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  if constexpr (GK != GK_HALO) load_epi();
   uint4 a0raw[WM];
   Frag<T> b0[WN];
   if constexpr (GK == GK_POINT) {
@@ -383,7 +387,7 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
     kstart = KS;
   }
 
-  if constexpr (GK == GK_HALO) conv_halo<T, MODE, WM, WN>(P, pro_s, (T*)acc_s, tm, n0, acc);
+  if constexpr (GK == GK_HALO) conv_halo<T, MODE, WM, WN>(P, pro_s, (T*)acc_s, tm, n0, acc, load_epi);
   for (int kk = kstart; kk < P.K && GK != GK_HALO; kk += KS) {
     const int k0 = kk + VE * grp;
     Frag<T> a[WM];

@@ -535,11 +535,11 @@ int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk, i
 }
 
 // A 3x3 / stride 1 / pad 1 problem whose row tiles are whole image rows, whose input rows plus
-// halo fit CONV_HALO_BYTES of LDS and whose filter columns fit CONV_HALO_NKB K steps of registers.
+// halo fit CONV_HALO_BYTES of LDS and whose filter columns fit conv_halo_nkb(wn) K steps of registers.
 bool halo_ok(const ConvProb& p, int es) {
   if (p.k != 3 || p.stride != 1 || p.pad != 1 || p.H != p.P || p.W != p.Q) return false;
   const int ve = 16 / es;
-  if (p.K > 4 * ve * CONV_HALO_NKB) return false;
+  if (p.K > 4 * ve * conv_halo_nkb(p.wn)) return false;
   const int bm = 64 * (CONV_SUBTILES / p.wn);
   const int pq = p.P * p.Q;
   if (bm % p.Q != 0 || (pq % bm != 0 && bm % pq != 0)) return false;

@@ -256,7 +256,9 @@ constexpr int ELT_TILE = 2048;     // elements per workgroup of elementwise kern
 constexpr int COLSTAT_ROWS = 128;  // rows per column-statistics workgroup
 constexpr int BNACT_PIX = 32;      // output pixels per bnact workgroup
 constexpr int CONV_HALO_BYTES = 40960;  // LDS of a 3x3 halo tile (input rows + halo, padded pixels)
-constexpr int CONV_HALO_NKB = 18;       // K steps whose filter fragments a wave keeps in registers
+// K steps whose filter fragments a wave keeps in registers, by column sub-tiles per wave (the
+// register budget of narrow tiles, which carry more row sub-tiles, is smaller)
+__host__ __device__ constexpr int conv_halo_nkb(int wn) { return wn == 1 ? 5 : wn == 2 ? 9 : 18; }
 // unused 16-byte chunks after the cpp channel chunks of a halo pixel (output width Q)
 __host__ __device__ inline int conv_halo_pad(int cpp, int Q) { return cpp >= 4 ? (Q >= 16 ? 2 : 1) : 0; }
 
