@@ -267,8 +267,10 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   constexpr int STAT_WORDS = 2 * 256 * VE + 512;   // BN sums reduce (epilogue)
   constexpr int ACC_WORDS0 = BM * LDA > STAT_WORDS ? BM * LDA : STAT_WORDS;
   constexpr int ACC_WORDS = (GK == GK_HALO && CONV_HALO_BYTES / 4 > ACC_WORDS0) ? CONV_HALO_BYTES / 4 : ACC_WORDS0;
-  __shared__ float2 pro_s[CONV_PRO_MAXC];
-  __shared__ __attribute__((aligned(16))) float bn_s[7][64];   // mean, invstd, scale, shift; A, B, K
+  // BN prologue constants (forward only) and BN statistics / apply coefficients (data gradient
+  // only): each mode allocates only its own, which keeps four workgroups resident per CU
+  __shared__ float2 pro_s[MODE == MODE_FWD ? CONV_PRO_MAXC : 1];
+  __shared__ __attribute__((aligned(16))) float bn_s[MODE == MODE_BWD ? 7 : 1][64];   // mean, invstd, scale, shift; A, B, K
   __shared__ __attribute__((aligned(16))) float acc_s[ACC_WORDS];
 
   const int gi = find_group(L);
