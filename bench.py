@@ -205,12 +205,12 @@ def main():
     g = ParaRealGPU(net, params)
     g.load_input(x, labels)
     s = torch.cuda.current_stream()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(8)] for _ in range(args.steps)]
 
     def step(k=None):
         e = ev[k] if k is not None else None
-        g.forward(fine_events=(e[0], e[1]) if e else None)
-        g.backward(fine_events=(e[2], e[3]) if e else None)
+        g.forward(fine_events=(e[0], e[1]) if e else None, coarse_events=(e[4], e[5]) if e else None)
+        g.backward(fine_events=(e[2], e[3]) if e else None, coarse_events=(e[6], e[7]) if e else None)
 
     for _ in range(args.warmup):
         step()
@@ -222,6 +222,8 @@ def main():
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
     fine_ms = sum(e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev) / args.steps
+    coarse_ms = (sum(e[4].elapsed_time(e[5]) + e[6].elapsed_time(e[7]) for e in ev) / args.steps
+                 if net.n_sub > 1 else 0.0)
     ff = fine_flops(net)
     tflops = ff / (fine_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if net.dtype == "bf16" else PEAK_F32_TFLOPS
@@ -292,6 +294,7 @@ def main():
         "pct_bf16_mfma_peak": round(100.0 * tflops / peak, 3),
         "fine_ms_per_step": round(fine_ms, 3),
         "fine_gflop_per_step": round(ff / 1e9, 1),
+        "coarse_ms_per_step": round(coarse_ms, 3),
         "sgd_ms_per_step": round(sgd_ms, 3),
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -171,6 +171,14 @@ pnn_status coarse_bwd(pnn_plan* plan, int j, const void* D_next, const void* rt_
                       const void* eta_j, const void* saved, void* D_j, float* deta_j,
                       void* scratch, void* stream);
 
+/* The whole coarse chain at once: for j = N-2 .. 0 the data gradients D_j as coarse_bwd computes
+ * them, then every deta_j (the weight gradients do not feed the chain, Alg. para3) in grouped
+ * launches.  D[N-1] = D_N is read, D[0..N-2] are written (D[j] must not alias D[j+1]); rt[j],
+ * eta[j], deta[j] for j = 0..N-2.  Same results as the N-1 coarse_bwd calls. */
+pnn_status coarse_bwd_all(pnn_plan* plan, void* const* D, const void* const* rt,
+                          const void* const* eta, const void* saved, float* const* deta,
+                          void* scratch, void* stream);
+
 /* For all j at once (Alg. para3, parallel loop; dL/dy_j = D_j by eq. (ingredient1)):
  * dphi[j] = D_j . dg^j/dphi_j (gradient buffer, overwritten) and dx[j] = D_j . dg^j/dx_j
  * (X_{j-1} shaped).  dy[j] = D_j. */

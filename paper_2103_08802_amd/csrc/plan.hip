@@ -361,6 +361,18 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
   return PNN_OK;
 }
 
+// wgrad partial bytes needed by every level of a set of segments at once (deferred weight gradients)
+size_t wgrad_all_bytes(const std::vector<SegP>& segs, int B, int es) {
+  size_t tot = 0;
+  for (auto& s : segs)
+    for (auto& n : s.nodes) {
+      if (n.op != PNN_OP_CONV) continue;
+      WgradGeom g = wgrad_geom_node(n, B, es);
+      tot = align256(tot + (size_t)g.splits * n.cout * n.k * n.k * n.cin * 4);
+    }
+  return tot;
+}
+
 // wgrad partial bytes needed by one level of a set of segments run together
 size_t wgrad_level_bytes(const std::vector<SegP>& segs, int B, int es) {
   int maxL = 0;
@@ -775,7 +787,74 @@ int fire_finalize(const Ctx& c, std::vector<ColRedProb>& fin, std::vector<BnAppl
   return fire_conv(c, rec, MODE_BWD);
 }
 
-int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
+// Weight gradients of the convolutions at level L (every level when L < 0) of a set of segments,
+// grouped by kernel variant; their split-K partial sums are appended to ``red`` (RED_SUM).
+int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs, int L,
+                std::vector<ColRedProb>& red) {
+  pnn_plan* plan = c.plan;
+  const int B = plan->B, es = plan->es;
+  char* wpart = c.scratch + plan->wpart_off;
+  std::vector<WgradProb> wg_vec, wg_gen, wg_h3;
+  size_t woff = 0;
+  for (size_t i = 0; i < segs.size(); ++i) {
+    const SegP& S = *segs[i];
+    const Ptrs& P = ptrs[i];
+    for (const NodeP& n : S.nodes) {
+      if ((L >= 0 && n.level != L) || n.op != PNN_OP_CONV) continue;
+      WgradProb p;
+      std::memset(&p, 0, sizeof(p));
+      p.g = grad_ptr(c, S, P, n.dst);
+      p.in = slot_ptr(c, S, P, n.src);
+      p.pro = n.bn >= 0 ? stats_ptr(c, S, n.bn) + 2 * S.bns[n.bn].C : nullptr;
+      p.B = B; p.H = n.H; p.W = n.W; p.Cg = n.cin; p.P = n.Ho; p.Q = n.Wo; p.Co = n.cout;
+      p.k = n.k; p.stride = n.stride; p.pad = n.pad;
+      p.M = B * n.Ho * n.Wo;
+      p.K = n.k * n.k * n.cin;
+      WgradGeom g = wgrad_geom_node(n, B, es);
+      p.wr = g.wr; p.tiles_co = g.tiles_co; p.tiles_k = g.tiles_k; p.splits = g.splits; p.mchunk = g.mchunk;
+      p.cg_log2 = log2_or(p.Cg);
+      p.q_log2 = log2_or(p.Q);
+      p.pq_log2 = log2_or(p.P * p.Q);
+      p.part = (float*)(wpart + woff);
+      woff = align256(woff + (size_t)g.splits * p.Co * p.K * 4);
+      (g.halo3 ? wg_h3 : n.cin % (16 / es) == 0 ? wg_vec : wg_gen).push_back(p);
+      ColRedProb r;
+      std::memset(&r, 0, sizeof(r));
+      r.part = p.part;
+      r.dst = (float*)(cp(P.grads) + n.gw_off);
+      r.rows = g.splits;
+      r.ncols = p.Co * p.K;
+      r.mode = RED_SUM;
+      r.rl_log2 = red_sum_rl_log2(r.rows);
+      red.push_back(r);
+    }
+  }
+  for (int v = 0; v < 3; ++v) {
+    auto& list = v == 0 ? wg_vec : v == 1 ? wg_gen : wg_h3;
+    int e = grouped<WgradLaunch>(
+        list, [](const WgradProb& p) { return p.tiles_co * p.tiles_k * p.splits; },
+        [&](const WgradLaunch& Lx, int tiles, size_t) {
+          double fl = 0, by = 0;
+          for (int i = 0; i < Lx.n; ++i) {
+            const WgradProb& p = Lx.p[i];
+            fl += 2.0 * p.M * (double)p.Co * p.K;
+            by += (double)p.M * p.Co * es + (double)p.B * p.H * p.W * p.Cg * es + (double)p.Co * p.K * 4;
+          }
+          Timer t(plan, 2, c.stream);
+          int e2 = v == 2 ? launch_wgrad3(Lx, tiles, plan->dtype, c.stream)
+                          : launch_wgrad(Lx, tiles, plan->dtype, v == 0, c.stream);
+          t.done(c.stream, fl, by);
+          return e2;
+        });
+    if (e) return e;
+  }
+  return PNN_OK;
+}
+
+// Backward of a set of segments run together, level by level.  wgrad = false leaves the weight
+// gradients to a later fire_wgrads (the coarse chain defers them).
+int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
+            bool wgrad = true) {
   pnn_plan* plan = c.plan;
   const int B = plan->B, es = plan->es;
   // filters of the data-gradient convolutions, [c_in][k][k][c_out]
@@ -804,7 +883,6 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
   // split-K weight-gradient sums of level L are reduced in the same launch as the BN backward
   // finalisation of level L - 1 (independent of it); level L - 1's weight gradient reuses the
   // partial region only after that launch (stream order)
-  char* wpart = c.scratch + plan->wpart_off;
   std::vector<ColRedProb> pending;
   for (int L = maxL; L >= 1; --L) {
     // A: gradients of the slots produced at this level (+ the previous level's split-K sums)
@@ -823,59 +901,9 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
       if (e) return e;
     }
     // B + C: weight gradients
-    std::vector<WgradProb> wg_vec, wg_gen, wg_h3;
     std::vector<ColRedProb> red;
-    size_t woff = 0;
-    for (size_t i = 0; i < segs.size(); ++i) {
-      const SegP& S = *segs[i];
-      const Ptrs& P = ptrs[i];
-      for (const NodeP& n : S.nodes) {
-        if (n.level != L || n.op != PNN_OP_CONV) continue;
-        WgradProb p;
-        std::memset(&p, 0, sizeof(p));
-        p.g = grad_ptr(c, S, P, n.dst);
-        p.in = slot_ptr(c, S, P, n.src);
-        p.pro = n.bn >= 0 ? stats_ptr(c, S, n.bn) + 2 * S.bns[n.bn].C : nullptr;
-        p.B = B; p.H = n.H; p.W = n.W; p.Cg = n.cin; p.P = n.Ho; p.Q = n.Wo; p.Co = n.cout;
-        p.k = n.k; p.stride = n.stride; p.pad = n.pad;
-        p.M = B * n.Ho * n.Wo;
-        p.K = n.k * n.k * n.cin;
-        WgradGeom g = wgrad_geom_node(n, B, es);
-        p.wr = g.wr; p.tiles_co = g.tiles_co; p.tiles_k = g.tiles_k; p.splits = g.splits; p.mchunk = g.mchunk;
-        p.cg_log2 = log2_or(p.Cg);
-        p.q_log2 = log2_or(p.Q);
-        p.pq_log2 = log2_or(p.P * p.Q);
-        p.part = (float*)(wpart + woff);
-        woff = align256(woff + (size_t)g.splits * p.Co * p.K * 4);
-        (g.halo3 ? wg_h3 : n.cin % (16 / es) == 0 ? wg_vec : wg_gen).push_back(p);
-        ColRedProb r;
-        std::memset(&r, 0, sizeof(r));
-        r.part = p.part;
-        r.dst = (float*)(cp(P.grads) + n.gw_off);
-        r.rows = g.splits;
-        r.ncols = p.Co * p.K;
-        r.mode = RED_SUM;
-        r.rl_log2 = red_sum_rl_log2(r.rows);
-        red.push_back(r);
-      }
-    }
-    for (int v = 0; v < 3; ++v) {
-      auto& list = v == 0 ? wg_vec : v == 1 ? wg_gen : wg_h3;
-      int e = grouped<WgradLaunch>(
-          list, [](const WgradProb& p) { return p.tiles_co * p.tiles_k * p.splits; },
-          [&](const WgradLaunch& Lx, int tiles, size_t) {
-            double fl = 0, by = 0;
-            for (int i = 0; i < Lx.n; ++i) {
-              const WgradProb& p = Lx.p[i];
-              fl += 2.0 * p.M * (double)p.Co * p.K;
-              by += (double)p.M * p.Co * es + (double)p.B * p.H * p.W * p.Cg * es + (double)p.Co * p.K * 4;
-            }
-            Timer t(plan, 2, c.stream);
-            int e2 = v == 2 ? launch_wgrad3(Lx, tiles, plan->dtype, c.stream)
-                            : launch_wgrad(Lx, tiles, plan->dtype, v == 0, c.stream);
-            t.done(c.stream, fl, by);
-            return e2;
-          });
+    if (wgrad) {
+      int e = fire_wgrads(c, segs, ptrs, L, red);
       if (e) return e;
     }
     pending = std::move(red);
@@ -1037,6 +1065,7 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
   size_t wp = wgrad_level_bytes(p->fine, p->B, p->es);
   wp = std::max(wp, wgrad_level_bytes(p->pre, p->B, p->es));
   for (auto& s : p->coarse) wp = std::max(wp, wgrad_level_bytes(std::vector<SegP>{s}, p->B, p->es));
+  wp = std::max(wp, wgrad_all_bytes(p->coarse, p->B, p->es));     // coarse_bwd_all
   size_t sc = 0;
   p->wpart_off = sc;
   p->wpart_bytes = wp;
@@ -1278,6 +1307,38 @@ pnn_status coarse_bwd(pnn_plan* plan, int j, const void* D_next, const void* rt_
   p.gout = D_next;
   p.gin = D_j;
   return run_bwd(c, {&plan->coarse[j]}, {p});
+}
+
+pnn_status coarse_bwd_all(pnn_plan* plan, void* const* D, const void* const* rt, const void* const* eta,
+                          const void* saved, float* const* deta, void* scratch, void* stream) {
+  if (!ok_ctx(plan, const_cast<void*>(saved), scratch)) return PNN_ERR_NULL;
+  if (D == nullptr || rt == nullptr || eta == nullptr || deta == nullptr) return PNN_ERR_NULL;
+  const int N = plan->N;
+  if (N < 2) return PNN_OK;
+  for (int j = 0; j < N; ++j)
+    if (D[j] == nullptr) return PNN_ERR_NULL;
+  for (int j = 0; j < N - 1; ++j)
+    if (rt[j] == nullptr || eta[j] == nullptr || deta[j] == nullptr) return PNN_ERR_NULL;
+  Ctx c{plan, (char*)const_cast<void*>(saved), (char*)scratch, (hipStream_t)stream};
+  std::vector<const SegP*> segs;
+  std::vector<Ptrs> ptrs;
+  for (int j = N - 2; j >= 0; --j) {
+    Ptrs p;
+    p.in = rt[j];
+    p.params = eta[j];
+    p.grads = deta[j];
+    p.gout = D[j + 1];
+    p.gin = D[j];
+    if (D[j] == D[j + 1]) return PNN_ERR_SHAPE;
+    int e = run_bwd(c, {&plan->coarse[j]}, {p}, false);
+    if (e) return e;
+    segs.push_back(&plan->coarse[j]);
+    ptrs.push_back(p);
+  }
+  std::vector<ColRedProb> red;
+  int e = fire_wgrads(c, segs, ptrs, -1, red);
+  if (e) return e;
+  return fire_colred(red, c.stream) ? PNN_ERR_HIP : PNN_OK;
 }
 
 pnn_status parareal_fine_bwd(pnn_plan* plan, const void* const* dy, const void* const* x,

@@ -25,6 +25,7 @@ class ParaRealGPU:
             raise RuntimeError("ParaRealGPU needs a GPU (HIP device)")
         self.net = net
         self.plan = B.Plan(net)
+        self.coarse_chain_all = True      # coarse_bwd_all (deferred coarse weight gradients)
         self.dev = torch.device(device)
         self.sdt = torch.bfloat16 if net.dtype == "bf16" else torch.float32
         N, Bt = net.n_sub, net.batch
@@ -134,9 +135,10 @@ class ParaRealGPU:
     def stream(self):
         return _torch().cuda.current_stream().cuda_stream
 
-    def forward(self, s=None, rnorm=False, fine_events=None):
-        """Alg. para2 and the head (loss, D_N).  ``fine_events``: a pair of torch.cuda.Event
-        recorded (on torch's current stream) around parareal_fine_fwd."""
+    def forward(self, s=None, rnorm=False, fine_events=None, coarse_events=None):
+        """Alg. para2 and the head (loss, D_N).  ``fine_events`` / ``coarse_events``: pairs of
+        torch.cuda.Event recorded (on torch's current stream) around parareal_fine_fwd / the
+        coarse chain."""
         s = self.stream() if s is None else s
         p, N = self.plan, self.net.n_sub
         B.pnn_pre_fwd(p, self.image, self.x, self.delta, self.saved, self.scratch, s)
@@ -148,26 +150,38 @@ class ParaRealGPU:
         if N > 1:
             B.parareal_combine_fwd(p, self.y, self.x, self.r, self.rnorm2 if rnorm else None,
                                    self.scratch, s)
+            if coarse_events:
+                coarse_events[0].record()
             for j in range(N - 1):
                 last = j + 1 == N - 1
                 add = self.y[N - 1] if last else self.r[j + 1]
                 out = self.ytilde if last else self.rt[j + 1]
                 B.coarse_fwd(p, j, self.rt[j], self.eta[j], add, out, self.saved, self.scratch, s)
+            if coarse_events:
+                coarse_events[1].record()
         B.pnn_head_fwd_bwd(p, self.ytilde, self.eps, self.labels, self.logits, self.loss,
                            self.D[N - 1], self.deps, self.scratch, s)
 
-    def backward(self, s=None, fine_events=None):
-        """Alg. para3.  ``fine_events`` as in ``forward``, around parareal_fine_bwd."""
-        self.backward_coarse_fine(s, fine_events)
+    def backward(self, s=None, fine_events=None, coarse_events=None):
+        """Alg. para3.  ``fine_events`` / ``coarse_events`` as in ``forward``, around
+        parareal_fine_bwd / the coarse chain."""
+        self.backward_coarse_fine(s, fine_events, coarse_events)
         self.backward_pre(s)
 
-    def backward_coarse_fine(self, s=None, fine_events=None):
+    def backward_coarse_fine(self, s=None, fine_events=None, coarse_events=None):
         """The coarse chain D_j (j = N-1..1) and the fine sub-networks' gradients."""
         s = self.stream() if s is None else s
         p, N = self.plan, self.net.n_sub
-        for j in range(N - 2, -1, -1):
-            B.coarse_bwd(p, j, self.D[j + 1], self.rt[j], self.eta[j], self.saved, self.D[j],
-                         self.deta[j], self.scratch, s)
+        if coarse_events:
+            coarse_events[0].record()
+        if N > 1 and self.coarse_chain_all:
+            B.coarse_bwd_all(p, self.D, self.rt, self.eta, self.saved, self.deta, self.scratch, s)
+        else:
+            for j in range(N - 2, -1, -1):
+                B.coarse_bwd(p, j, self.D[j + 1], self.rt[j], self.eta[j], self.saved, self.D[j],
+                             self.deta[j], self.scratch, s)
+        if coarse_events:
+            coarse_events[1].record()
         if fine_events:
             fine_events[0].record()
         B.parareal_fine_bwd(p, self.D, self.x, self.phi, self.saved, self.dx, self.dphi, self.scratch, s)

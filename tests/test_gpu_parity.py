@@ -146,3 +146,23 @@ def test_vgg_workload_bf16_forward():
     err = run_net(S.config(1, 32))
     fw = {k: v for k, v in err.items() if k[0] in "xyrl" or k == "ytilde"}
     _assert_tol(fw, 2e-2)
+
+
+def test_coarse_bwd_all_equals_per_block_calls():
+    """coarse_bwd_all (coarse weight gradients deferred into grouped launches) gives bit-identical
+    D_j and deta_j to the N - 1 coarse_bwd calls."""
+    import torch
+    from paper_2103_08802_amd.step import ParaRealGPU
+    net = S.config(2, 2)
+    x, labels, params = S.make_all(net)
+    out = []
+    for chain_all in (False, True):
+        g = ParaRealGPU(net, params)
+        g.coarse_chain_all = chain_all
+        g.load_input(x, labels)
+        g.forward()
+        g.backward_coarse_fine()
+        torch.cuda.synchronize()
+        out.append(([t.clone() for t in g.D], [t.clone() for t in g.deta]))
+    for a, b in zip(out[0][0] + out[0][1], out[1][0] + out[1][1]):
+        assert torch.equal(a, b)
