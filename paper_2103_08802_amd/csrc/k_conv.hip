@@ -339,16 +339,22 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
     }
   };
   if constexpr (GK != GK_HALO) load_epi();
-  uint4 a0raw[WM];
-  Frag<T> b0[WN];
+  // K steps whose operands are loaded before the barrier: two for the tall 16-column tiles
+  // (their 1x1 problems have K = 64 = two steps), one otherwise
+  constexpr int ES = (GK == GK_POINT && WM >= 8) ? 2 : 1;
+  uint4 a0raw[ES][WM];
+  Frag<T> b0[ES][WN];
   if constexpr (GK == GK_POINT) {
-    const int k0 = VE * grp;
 #pragma unroll
-    for (int wm = 0; wm < WM; ++wm)
-      a0raw[wm] = (rv[wm] && k0 < P.K) ? *(const uint4*)((const T*)P.in + (long)rm[wm] * P.Cg + k0)
-                                       : make_uint4(0, 0, 0, 0);
+    for (int es = 0; es < ES; ++es) {
+      const int k0 = es * KS + VE * grp;
 #pragma unroll
-    for (int j = 0; j < WN; ++j) load_b<T, true>(P, n0 + j * 16 + r16, k0, b0[j]);
+      for (int wm = 0; wm < WM; ++wm)
+        a0raw[es][wm] = (rv[wm] && k0 < P.K) ? *(const uint4*)((const T*)P.in + (long)rm[wm] * P.Cg + k0)
+                                             : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int j = 0; j < WN; ++j) load_b<T, true>(P, n0 + j * 16 + r16, k0, b0[es][j]);
+    }
   }
 
   if (MODE == MODE_FWD && P.pro != nullptr)
@@ -366,27 +372,30 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
 
   int kstart = 0;
   if constexpr (GK == GK_POINT) {
-    // first K step from the early loads; the BN prologue (scale, shift from LDS) applies now.
-    // Rows past M and columns past K are zeros of the activated operand.
-    const int k0 = VE * grp;
-    Frag<T> a[WM];
+    // the early K steps; the BN prologue (scale, shift from LDS) applies now.  Rows past M and
+    // columns past K are zeros of the activated operand.
 #pragma unroll
-    for (int wm = 0; wm < WM; ++wm) {
-      if (MODE == MODE_FWD && P.pro != nullptr && rv[wm] && k0 < P.K) {
-        Chunk<T> c;
-        unpack_chunk<T>(a0raw[wm], c);
+    for (int es = 0; es < ES; ++es) {
+      const int k0 = es * KS + VE * grp;
+      Frag<T> a[WM];
 #pragma unroll
-        for (int e = 0; e < VE; ++e) c.v[e] = fmaxf(fmaf(c.v[e], pro_s[k0 + e].x, pro_s[k0 + e].y), 0.0f);
-        a[wm].from_chunk(c);
-      } else {
-        a[wm].from_raw(a0raw[wm]);
+      for (int wm = 0; wm < WM; ++wm) {
+        if (MODE == MODE_FWD && P.pro != nullptr && rv[wm] && k0 < P.K) {
+          Chunk<T> c;
+          unpack_chunk<T>(a0raw[es][wm], c);
+#pragma unroll
+          for (int e = 0; e < VE; ++e) c.v[e] = fmaxf(fmaf(c.v[e], pro_s[k0 + e].x, pro_s[k0 + e].y), 0.0f);
+          a[wm].from_chunk(c);
+        } else {
+          a[wm].from_raw(a0raw[es][wm]);
+        }
       }
+#pragma unroll
+      for (int j = 0; j < WN; ++j)
+#pragma unroll
+        for (int wm = 0; wm < WM; ++wm) mma(a[wm], b0[es][j], acc[wm][j]);
     }
-#pragma unroll
-    for (int j = 0; j < WN; ++j)
-#pragma unroll
-      for (int wm = 0; wm < WM; ++wm) mma(a[wm], b0[j], acc[wm][j]);
-    kstart = KS;
+    kstart = ES * KS;
   }
 
   if constexpr (GK == GK_HALO) conv_halo<T, MODE, WM, WN>(P, pro_s, (T*)acc_s, tm, n0, acc, load_epi);
