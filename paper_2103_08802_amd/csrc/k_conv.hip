@@ -1004,6 +1004,152 @@ __global__ __launch_bounds__(256) void wgrad3_kernel(const WgradLaunch L) {
 }
 
 // ------------------------------------------------------------------------------------------------
+// BN backward sums of a 1x1 convolution's input BN without forming its data gradient in HBM:
+// per row m and column c, v = sum_o g[m][o] W[o][c] (transposed filter wmat[c][o]), dbn =
+// rnd(v * [ReLU(BN(z)) > 0]), sums of dbn and dbn * xhat.  A workgroup owns 64 columns and
+// BNSUM_ROWS rows and streams them in tiles of BNSUM_TR rows: g (contiguous, BNSUM_TR * K
+// elements) and z (BNSUM_TR rows of 64 columns) go through LDS with whole-workgroup 16-byte loads,
+// the next tile's loads in flight while the current one is computed.  Wave w owns columns
+// [16 w, 16 w + 16); its MFMA takes the filter as the row operand and 16 gradient rows as the
+// column operand, so a lane's results are four consecutive columns of one row.  One partial row
+// [rows / BNSUM_ROWS][ncol][2] per workgroup; nothing else is stored.
+// ------------------------------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void bnsum_kernel(const ConvLaunch L) {
+  constexpr int VE = St<T>::VE;
+  constexpr int KS = 4 * VE;
+  constexpr int NOS = BNSUM_MAXK / KS;                // K steps over the gradient's channels
+  constexpr int TR = BNSUM_TR;
+  constexpr int ST = 64 + VE;                         // LDS row stride of both tiles (elements)
+  constexpr int NLD = TR * 64 / VE / 256;             // 16-byte loads per thread for a full tile
+  __shared__ __attribute__((aligned(16))) T gs[TR * ST];
+  __shared__ __attribute__((aligned(16))) T zs[TR * ST];
+
+  const int gi = find_group(L);
+  const ConvProb& P = L.p[gi];
+  const int local = blockIdx.x - P.tile_begin;
+  const int tm = local / P.tiles_n;
+  const int tn = local - tm * P.tiles_n;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int K = P.K, ncol = P.ncol;
+  const int c0 = tn * 64;
+  const int ncl = min(64, ncol - c0);                 // columns of this tile (16, 32, 48 or 64)
+  const int m_begin = tm * BNSUM_ROWS;
+  const int m_end = min(P.M, m_begin + BNSUM_ROWS);
+  const int gch = K / VE;                             // 16-byte chunks per gradient row
+  const T* __restrict__ g = (const T*)P.in;
+  const T* __restrict__ z = (const T*)P.zsrc;
+  const bool active = wave * 16 < ncl;                // the wave has columns
+
+  // filter fragments (column c0 + 16 wave + r16, gradient channels os * KS + VE * grp ..) and the
+  // BN parameters of the lane's result columns c0 + 16 wave + 4 grp + i
+  Frag<T> wf[NOS];
+  float mu[4], is[4], sc[4], sh[4];
+  {
+    const int c = wave * 16 + r16;
+#pragma unroll
+    for (int os = 0; os < NOS; ++os) {
+      const int o0 = os * KS + VE * grp;
+      if (o0 < K && c < ncl) wf[os].from_raw(*(const uint4*)((const T*)P.wmat + (long)(c0 + c) * K + o0));
+      else wf[os].zero();
+    }
+    const int cl = wave * 16 + grp * 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool cv = cl + i < ncl;
+      mu[i] = cv ? P.bnst[c0 + cl + i] : 0.f;
+      is[i] = cv ? P.bnst[ncol + c0 + cl + i] : 0.f;
+      sc[i] = cv ? P.bnst[2 * ncol + c0 + cl + i] : 0.f;
+      sh[i] = cv ? P.bnst[3 * ncol + c0 + cl + i] : 0.f;
+    }
+  }
+
+  // chunk u of the g tile is row u / gch, channels VE * (u % gch); chunk u of the z tile is row
+  // u / (64 / VE), columns VE * (u % (64 / VE))
+  uint4 gr[NLD], zr[NLD];
+  auto fetch = [&](int mt) {
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int u = i * 256 + tid;
+      const int row = u / gch;
+      gr[i] = (row < TR && mt + row < m_end) ? *(const uint4*)(g + (long)mt * K + (long)u * VE)
+                                              : make_uint4(0, 0, 0, 0);
+      const int zrow = u / (64 / VE), zc = (u % (64 / VE)) * VE;
+      zr[i] = (mt + zrow < m_end && zc < ncl) ? *(const uint4*)(z + (long)(mt + zrow) * ncol + c0 + zc)
+                                               : make_uint4(0, 0, 0, 0);
+    }
+  };
+
+  float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
+  fetch(m_begin);
+  for (int mt = m_begin; mt < m_end; mt += TR) {
+#pragma unroll
+    for (int i = 0; i < NLD; ++i) {
+      const int u = i * 256 + tid;
+      const int row = u / gch;
+      if (row < TR) *(uint4*)(gs + row * ST + (u - row * gch) * VE) = gr[i];
+      const int zrow = u / (64 / VE);
+      *(uint4*)(zs + zrow * ST + (u % (64 / VE)) * VE) = zr[i];
+    }
+    __syncthreads();
+    if (mt + TR < m_end) fetch(mt + TR);
+    if (active) {
+#pragma unroll
+      for (int sub = 0; sub < TR / 16; ++sub) {
+        const int row = sub * 16 + r16;
+        f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int os = 0; os < NOS; ++os) {
+          const int o0 = os * KS + VE * grp;
+          if (os * KS < K) {
+            Frag<T> gf;
+            if (o0 < K) gf.from_raw(*(const uint4*)(gs + row * ST + o0));
+            else gf.zero();
+            mma(wf[os], gf, v);
+          }
+        }
+        float zv[4];
+        const int cl = wave * 16 + grp * 4;
+        if constexpr (sizeof(T) == 2) {
+          const uint2 u = *(const uint2*)(zs + row * ST + cl);
+          zv[0] = __uint_as_float(u.x << 16);
+          zv[1] = __uint_as_float(u.x & 0xffff0000u);
+          zv[2] = __uint_as_float(u.y << 16);
+          zv[3] = __uint_as_float(u.y & 0xffff0000u);
+        } else {
+          const float4 u = *(const float4*)(zs + row * ST + cl);
+          zv[0] = u.x; zv[1] = u.y; zv[2] = u.z; zv[3] = u.w;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float d = fmaf(zv[i], sc[i], sh[i]) > 0.f ? v[i] : 0.f;
+          const float dr = St<T>::rnd(d);
+          s1[i] += dr;
+          s2[i] += dr * ((zv[i] - mu[i]) * is[i]);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // sum over the 16 rows of a lane group (lanes r16); lane r16 == 0 holds four columns
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      s1[i] += __shfl_xor(s1[i], o, 64);
+      s2[i] += __shfl_xor(s2[i], o, 64);
+    }
+  if (active && r16 == 0) {
+    const int cl = wave * 16 + grp * 4;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (cl + i < ncl) ((float2*)P.part)[(long)tm * ncol + c0 + cl + i] = make_float2(s1[i], s2[i]);
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
 // launchers
 // ------------------------------------------------------------------------------------------------
 
@@ -1035,6 +1181,12 @@ int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int
     if (mode == MODE_FWD) launch_conv_m<float, MODE_FWD>(L, tiles, gk, wn, s);
     else launch_conv_m<float, MODE_BWD>(L, tiles, gk, wn, s);
   }
+  return (int)hipGetLastError();
+}
+
+int launch_bnsum(const ConvLaunch& L, int tiles, int dtype, hipStream_t s) {
+  if (dtype == 1) hipLaunchKernelGGL((bnsum_kernel<uint16_t>), dim3(tiles), dim3(256), 0, s, L);
+  else hipLaunchKernelGGL((bnsum_kernel<float>), dim3(tiles), dim3(256), 0, s, L);
   return (int)hipGetLastError();
 }
 

@@ -55,6 +55,7 @@ struct BnP {
   size_t dbn_off = NONE, coef_off = NONE, datmp_off = NONE;
   bool bnact_consumer = false;
   bool defer_apply = false;  // dbn not stored: the apply pass recomputes it (see build_segment)
+  bool bnsum = false;        // its backward sums come from bnsum_kernel (no data-gradient tile)
 };
 
 struct SegP {
@@ -286,6 +287,7 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
     if (n.op != PNN_OP_CONV || !n.dgrad || n.k != 1 || n.stride != 1 || n.pad != 0) continue;
     if (n.cout % (16 / es) != 0 || n.cout >= 2 * n.cin) continue;
     b.defer_apply = true;
+    b.bnsum = n.cout <= BNSUM_MAXK && n.cin % 16 == 0;
   }
   // parameter / gradient layout
   size_t po = 0, go = 0;
@@ -325,7 +327,7 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
     const long M = (long)B * sl.H * sl.W;
     b.C = sl.C;
     b.fwd_tiles = (int)cdiv(M, b.slot == 0 ? COLSTAT_ROWS : conv_bm(b.C));
-    b.bwd_tiles = (int)cdiv(M, conv_bm(b.C));
+    b.bwd_tiles = (int)cdiv(M, b.bnsum ? BNSUM_ROWS : conv_bm(b.C));
     if (b.bnact_consumer) {
       const NodeP& c = S.nodes[sl.bn_consumers[0]];
       b.bwd_tiles = (int)cdiv((long)B * c.Ho * c.Wo, BNACT_PIX);
@@ -909,7 +911,7 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
     pending = std::move(red);
     // D + E: data gradients (first of two BN consumers, then the rest) and bnact backward
     for (int phase = 0; phase < 2; ++phase) {
-      std::vector<ConvProb> dg;
+      std::vector<ConvProb> dg, bs;
       std::vector<BnActProb> ba;
       for (size_t i = 0; i < segs.size(); ++i) {
         const SegP& S = *segs[i];
@@ -940,6 +942,15 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
               p.out32 = (float*)(c.scratch + S.scr_base + b.datmp_off);
             } else {
               p.flags = EPI_BN_MASK | (b.defer_apply ? EPI_NO_STORE : 0);
+              if (b.bnsum) {           // sums only, by the streaming BN-sum kernel
+                p.zsrc = slot_ptr(c, S, P, n.src);
+                p.bnst = stats_ptr(c, S, n.bn);
+                p.part = part_ptr(c, S, n.bn);
+                p.tiles_m = (int)cdiv(p.M, BNSUM_ROWS);
+                p.tiles_n = (int)cdiv(p.ncol, 64);
+                bs.push_back(p);
+                continue;
+              }
               p.out = b.defer_apply ? nullptr : c.scratch + S.scr_base + b.dbn_off;
               p.zsrc = slot_ptr(c, S, P, n.src);
               p.bnst = stats_ptr(c, S, n.bn);
@@ -958,6 +969,18 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
         }
       }
       int e = fire_conv(c, dg, MODE_BWD);
+      if (e) return e;
+      e = grouped<ConvLaunch>(
+          bs, [](const ConvProb& p) { return p.tiles_m * p.tiles_n; },
+          [&](const ConvLaunch& Lx, int tiles, size_t) {
+            double by = 0;
+            for (int j = 0; j < Lx.n; ++j)
+              by += (double)Lx.p[j].M * (Lx.p[j].K + Lx.p[j].ncol) * plan->es;
+            Timer t(plan, 1, c.stream);
+            int r = launch_bnsum(Lx, tiles, plan->dtype, c.stream);
+            t.done(c.stream, 0, by);
+            return r;
+          });
       if (e) return e;
       e = grouped<BnActLaunch>(
           ba, [](const BnActProb& p) { return (int)cdiv(p.n_out, BNACT_PIX); },

@@ -231,6 +231,9 @@ static_assert(sizeof(ConvLaunch) <= 4096 && sizeof(WgradLaunch) <= 4096 && sizeo
               "kernel argument size");
 int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, hipStream_t s);
 int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s);
+// BN backward sums of a 1x1 convolution's input BN (EPI_BN_MASK | EPI_NO_STORE problems):
+// tiles_m = ceil(M / BNSUM_ROWS), tiles_n = ceil(ncol / 64); K <= BNSUM_MAXK
+int launch_bnsum(const ConvLaunch& L, int tiles, int dtype, hipStream_t s);
 // 3x3 / stride 1 / pad 1 through an LDS halo tile: tiles_co = Co / 16, tiles_k = Cg / 16 blocks
 int launch_wgrad3(const WgradLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_colred(const ColRedLaunch& L, int tiles, hipStream_t s);
@@ -253,6 +256,9 @@ constexpr int CONV_SUBTILES = 8;
 inline int conv_wn(int ncol) { return (ncol % 64 == 0) ? 4 : (ncol % 32 == 0) ? 2 : 1; }
 inline int conv_bm(int ncol) { return 64 * (CONV_SUBTILES / conv_wn(ncol)); }
 constexpr int ELT_TILE = 2048;     // elements per workgroup of elementwise kernels
+constexpr int BNSUM_ROWS = 512;    // rows per BN-sum workgroup
+constexpr int BNSUM_MAXK = 64;     // gradient channels of a BN-sum problem
+constexpr int BNSUM_TR = 64;       // rows per LDS tile of bnsum_kernel
 constexpr int COLSTAT_ROWS = 128;  // rows per column-statistics workgroup
 constexpr int BNACT_PIX = 32;      // output pixels per bnact workgroup
 constexpr int CONV_HALO_BYTES = 40960;  // LDS of a 3x3 halo tile (input rows + halo, padded pixels)
