@@ -574,10 +574,10 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
 // 16-byte global loads; the MFMA fragments (8 consecutive m per lane) are read column-wise from
 // rows padded to 8 bytes past a 16-byte multiple, which keeps the four m-groups of a wave on
 // disjoint banks.  wr waves cover the tile's rows; the other 4 / wr wave groups split each LDS
-// stage's m-steps and are summed in LDS at the end.  Global loads of the next stage are issued
-// before the current stage is consumed.
+// stage's m-steps and are summed in LDS at the end.  Two register buffers keep the global loads
+// of the next two stages in flight while a stage is consumed.
 // ------------------------------------------------------------------------------------------------
-constexpr int WG_KC = 128;                 // m rows per LDS stage
+constexpr int WG_KC = 64;                  // m rows per LDS stage
 constexpr int WG_TK = 64;                  // dW columns per workgroup tile
 
 template <typename T>
@@ -611,28 +611,40 @@ __device__ __forceinline__ WgCol wg_col(const WgradProb& P, int kidx) {
 }
 
 // One 16-byte activation chunk of row m at the thread's filter column.  VEC: the raw stored values
-// (pending = true when the BN prologue still has to be applied, once the load has landed, so that a
-// stage's loads stay in flight across the previous stage's MMAs); padding chunks are zeros of the
-// activated tensor (pending = false).  Element-wise gather: final values.
+// (pending = true when the BN prologue still has to be applied, valid = false for padding chunks,
+// which are zeros of the activated tensor; both are applied once the load has landed, so that a
+// stage's loads stay in flight across the previous stage's MMAs).  Element-wise gather: final
+// values (valid = true, pending = false).
 template <typename T, bool VEC>
 __device__ __forceinline__ uint4 wg_gather(const WgradProb& P, const float2* pro, int m, const WgCol& cl,
-                                           int col, bool& pending) {
+                                           int col, bool& valid, bool& pending) {
   constexpr int VE = St<T>::VE;
   const int PQ = P.P * P.Q;
   uint4 zero = make_uint4(0, 0, 0, 0);
+  valid = true;
   pending = false;
-  if (m >= P.M || cl.kidx >= P.K) return zero;
-  const int n = div_l2(m, PQ, P.pq_log2);
-  const int rem = m - n * PQ;
-  const int p = div_l2(rem, P.Q, P.q_log2);
-  const int q = rem - p * P.Q;
   if constexpr (VEC) {
+    // branch-free: every lane issues its load (padding lanes read the tensor's first chunk and
+    // drop it once it has landed: valid = false), so the number of loads in flight is the same on
+    // every path
+    const bool mv = m < P.M && cl.kidx < P.K;
+    const int mm = mv ? m : 0;
+    const int n = div_l2(mm, PQ, P.pq_log2);
+    const int rem = mm - n * PQ;
+    const int p = div_l2(rem, P.Q, P.q_log2);
+    const int q = rem - p * P.Q;
     const int ih = p * P.stride + cl.r - P.pad, iw = q * P.stride + cl.s - P.pad;
-    if ((unsigned)ih >= (unsigned)P.H || (unsigned)iw >= (unsigned)P.W) return zero;
-    const long idx = (((long)n * P.H + ih) * P.W + iw) * P.Cg + cl.c0;
-    pending = P.pro != nullptr;
+    const bool v = mv && (unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W;
+    const long idx = v ? (((long)n * P.H + ih) * P.W + iw) * P.Cg + cl.c0 : 0;
+    valid = v;
+    pending = v && P.pro != nullptr;
     return *(const uint4*)((const T*)P.in + idx);
   } else {
+    if (m >= P.M || cl.kidx >= P.K) return zero;
+    const int n = div_l2(m, PQ, P.pq_log2);
+    const int rem = m - n * PQ;
+    const int p = div_l2(rem, P.Q, P.q_log2);
+    const int q = rem - p * P.Q;
     float v[VE];
 #pragma unroll
     for (int e = 0; e < VE; ++e) {
@@ -670,12 +682,8 @@ __device__ __forceinline__ void lds_frag(const T* base, int row0, int rs, int cb
     const T* p0 = base + (row0 + (r16 >> 2)) * rs + cbase + 4 * (r16 & 3);
     const v4s16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s16*)p0);
     const v4s16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s16*)(p0 + 4 * rs));
-    uint4 u;
-    u.x = (uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16);
-    u.y = (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16);
-    u.z = (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16);
-    u.w = (uint32_t)(uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16);
-    f.from_raw(u);
+    const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+    f.from_raw(make_uint4(l2.x, l2.y, h2.x, h2.y));
   } else {
     constexpr int VE = St<T>::VE;
     T tmp[VE];
@@ -687,14 +695,18 @@ __device__ __forceinline__ void lds_frag(const T* base, int row0, int rs, int cb
   }
 }
 
-template <typename T, bool VEC>
+template <typename T, int GA>
 __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
   using C = WgCfg<T>;
   constexpr int VE = C::VE;
   constexpr int KS = 4 * VE;
-  __shared__ T lg[WG_KC * (64 + C::PADE)];
-  __shared__ T la[WG_KC * C::RSA];
+  constexpr int LG = WG_KC * (64 + C::PADE);          // output-gradient tile (elements)
+  constexpr int LA = WG_KC * C::RSA;                  // activation tile
+  constexpr int SMEM = (LG + LA) * (int)sizeof(T) > 16384 ? (LG + LA) * (int)sizeof(T) : 16384;
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];   // the two tiles; the final reduce
   __shared__ float2 pro_s[WG_TK];
+  T* lg = (T*)smem;
+  T* la = lg + LG;
 
   const int gi = find_group(L);
   const WgradProb& P = L.p[gi];
@@ -729,45 +741,68 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
   static_assert(256 % acpr == 0, "a thread keeps one activation column");
   const int acol = (tid % acpr) * VE;
   const WgCol wcol = wg_col(P, kk0 + acol);
-  uint4 ga[C::GC], aa[C::AC];
-  uint32_t apend = 0;                  // bit i: aa[i] still needs the BN prologue
+  // per-thread chunk geometry, fixed over the stages: stage row, element offset in the global
+  // tensor relative to the stage's first row, LDS offset (rows past the tile: row = 1 << 29)
+  int grow[C::GC], goff[C::GC], gls[C::GC];
+#pragma unroll
+  for (int i = 0; i < C::GC; ++i) {
+    const int idx = tid + i * 256;
+    const int row = idx / gcpr, cc = (idx - row * gcpr) * VE;
+    const bool in = idx < gchunks;
+    grow[i] = in ? row : (1 << 29);
+    goff[i] = in ? row * P.Co + co0 + cc : 0;
+    gls[i] = in ? row * RSG + cc : -1;
+  }
+  int arow[C::AC], aoff[C::AC];
+  const bool acv = kk0 + acol < P.K;   // the thread's activation column exists
+#pragma unroll
+  for (int i = 0; i < C::AC; ++i) {
+    arow[i] = (tid + i * 256) / acpr;
+    aoff[i] = arow[i] * P.Cg + kk0 + acol;   // pointwise gather: row-major [M][Cg] input
+  }
+  uint4 ga0[C::GC], aa0[C::AC], ga1[C::GC], aa1[C::AC];
+  // per stage buffer: bit i of the low byte: ga[i] valid; bit 8 + i: aa[i] valid; bit 16 + i:
+  // aa[i] still needs the BN prologue.  Invalid chunks are zeroed when they are written to LDS.
+  uint32_t bits0 = 0, bits1 = 0;
+  static_assert(C::GC <= 8 && C::AC <= 8, "stage bits");
+  const bool has_pro = P.pro != nullptr;
 
-  auto load_stage = [&](int mc) {
+  auto load_stage = [&](uint4 (&ga)[C::GC], uint4 (&aa)[C::AC], uint32_t& bits, int mc) {
+    bits = 0;
+    const T* gs = (const T*)P.g + (long)mc * P.Co;
 #pragma unroll
     for (int i = 0; i < C::GC; ++i) {
-      const int idx = tid + i * 256;
-      ga[i] = make_uint4(0, 0, 0, 0);
-      if (idx < gchunks) {
-        const int row = idx / gcpr, cc = (idx - row * gcpr) * VE;
-        const int m = mc + row;
-        if (m < m_end) ga[i] = *(const uint4*)((const T*)P.g + (long)m * P.Co + co0 + cc);
-      }
+      // branch-free like wg_gather: invalid chunks load the tensor's first chunk
+      const bool v = mc + grow[i] < m_end;
+      ga[i] = *(const uint4*)(v ? gs + goff[i] : (const T*)P.g);
+      bits |= (v ? 1u : 0u) << i;
     }
-    apend = 0;
+    if constexpr (GA == WG_PW) {
+      const T* as = (const T*)P.in + (long)mc * P.Cg;
 #pragma unroll
-    for (int i = 0; i < C::AC; ++i) {
-      const int row = (tid + i * 256) / acpr;    // the thread's column acol is the same for every i
-      const int m = mc + row;
-      bool pend = false;
-      aa[i] = m < m_end ? wg_gather<T, VEC>(P, pro_s, m, wcol, acol, pend) : make_uint4(0, 0, 0, 0);
-      apend |= (pend ? 1u : 0u) << i;
+      for (int i = 0; i < C::AC; ++i) {
+        const bool v = acv && mc + arow[i] < m_end;
+        aa[i] = *(const uint4*)(v ? as + aoff[i] : (const T*)P.in);
+        bits |= ((v ? 1u : 0u) << (8 + i)) | ((v && has_pro ? 1u : 0u) << (16 + i));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < C::AC; ++i) {
+        const int m = mc + arow[i];
+        bool valid = true, pend = false;
+        aa[i] = wg_gather<T, GA == WG_VEC>(P, pro_s, m < m_end ? m : P.M, wcol, acol, valid, pend);
+        bits |= ((valid ? 1u : 0u) << (8 + i)) | ((pend ? 1u : 0u) << (16 + i));
+      }
     }
   };
-  auto store_stage = [&]() {
+  auto store_stage = [&](const uint4 (&ga)[C::GC], const uint4 (&aa)[C::AC], uint32_t bits) {
 #pragma unroll
-    for (int i = 0; i < C::GC; ++i) {
-      const int idx = tid + i * 256;
-      if (idx < gchunks) {
-        const int row = idx / gcpr, cc = (idx - row * gcpr) * VE;
-        lds_store8<T>(lg + row * RSG + cc, ga[i]);
-      }
-    }
+    for (int i = 0; i < C::GC; ++i)
+      if (gls[i] >= 0) lds_store8<T>(lg + gls[i], ((bits >> i) & 1u) ? ga[i] : make_uint4(0, 0, 0, 0));
 #pragma unroll
     for (int i = 0; i < C::AC; ++i) {
-      const int idx = tid + i * 256;
-      const int row = idx / acpr, cc = (idx - row * acpr) * VE;
-      uint4 u = aa[i];
-      if ((apend >> i) & 1u) {
+      uint4 u = ((bits >> (8 + i)) & 1u) ? aa[i] : make_uint4(0, 0, 0, 0);
+      if ((bits >> (16 + i)) & 1u) {
         Chunk<T> c;
         unpack_chunk<T>(u, c);
         float v[VE];
@@ -775,20 +810,18 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
         for (int e = 0; e < VE; ++e) v[e] = fmaxf(fmaf(c.v[e], pro_s[acol + e].x, pro_s[acol + e].y), 0.0f);
         store_chunk<T>(&u, 0, v);
       }
-      lds_store8<T>(la + row * C::RSA + cc, u);
+      lds_store8<T>(la + arow[i] * C::RSA + acol, u);
     }
   };
 
   f32x4 acc[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  if (m_begin < m_end) load_stage(m_begin);
-  for (int mc = m_begin; mc < m_end; mc += WG_KC) {
-    store_stage();
-    __syncthreads();
-    if (mc + WG_KC < m_end) load_stage(mc + WG_KC);
-    for (int st = msi; st < WG_KC / KS; st += ms) {
+  // m-step st of stage si goes to wave group (si * steps + st) mod ms
+  auto compute = [&](int si) {
+#pragma unroll
+    for (int st = 0; st < WG_KC / KS; ++st) {
+      if (((si * (WG_KC / KS) + st) & (ms - 1)) != msi) continue;
       const int row0 = st * KS + VE * grp;
       Frag<T> a;
       lds_frag<T>(lg, row0, RSG, sr * 16, r16, a);
@@ -799,11 +832,30 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradLaunch L) {
         mma(a, b, acc[j]);
       }
     }
+  };
+
+  // stages alternate between the two register buffers; the loads of stage i + 2 are issued as soon
+  // as stage i has been written to LDS.  Every stage's loads are issued, also past m_end (all
+  // chunks invalid: zeros), so that the loads in flight are the same on every path and the waits
+  // before a stage's LDS stores only cover that stage.
+  load_stage(ga0, aa0, bits0, m_begin);
+  __builtin_amdgcn_sched_barrier(0);   // keep the two stages' loads in order (the waits count on it)
+  load_stage(ga1, aa1, bits1, m_begin + WG_KC);
+  for (int mc = m_begin, si = 0; mc < m_end; mc += 2 * WG_KC, si += 2) {
+    store_stage(ga0, aa0, bits0);
+    __syncthreads();
+    load_stage(ga0, aa0, bits0, mc + 2 * WG_KC);
+    compute(si);
+    __syncthreads();
+    store_stage(ga1, aa1, bits1);
+    __syncthreads();
+    load_stage(ga1, aa1, bits1, mc + 3 * WG_KC);
+    compute(si + 1);
     __syncthreads();
   }
 
   // combine the m-split wave groups (fixed order) and write the partial tile
-  float* red = (float*)la;             // ms x wr x 16 x 64 floats <= 16 KB
+  float* red = (float*)smem;           // ms x wr x 16 x 64 floats <= 16 KB
   if (ms > 1) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
@@ -1198,17 +1250,18 @@ int launch_wgrad3(const WgradLaunch& L, int tiles, int dtype, hipStream_t s) {
   return (int)hipGetLastError();
 }
 
-int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s) {
+template <typename T>
+static void launch_wgrad_t(const WgradLaunch& L, int tiles, int gather, hipStream_t s) {
+  if (gather == WG_PW) hipLaunchKernelGGL((wgrad_kernel<T, WG_PW>), dim3(tiles), dim3(256), 0, s, L);
+  else if (gather == WG_VEC) hipLaunchKernelGGL((wgrad_kernel<T, WG_VEC>), dim3(tiles), dim3(256), 0, s, L);
+  else hipLaunchKernelGGL((wgrad_kernel<T, WG_GEN>), dim3(tiles), dim3(256), 0, s, L);
+}
+
+int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, int gather, hipStream_t s) {
   if (dtype == 1) {
-    if (vec)
-      hipLaunchKernelGGL((wgrad_kernel<uint16_t, true>), dim3(tiles), dim3(256), 0, s, L);
-    else
-      hipLaunchKernelGGL((wgrad_kernel<uint16_t, false>), dim3(tiles), dim3(256), 0, s, L);
+    launch_wgrad_t<uint16_t>(L, tiles, gather, s);
   } else {
-    if (vec)
-      hipLaunchKernelGGL((wgrad_kernel<float, true>), dim3(tiles), dim3(256), 0, s, L);
-    else
-      hipLaunchKernelGGL((wgrad_kernel<float, false>), dim3(tiles), dim3(256), 0, s, L);
+    launch_wgrad_t<float>(L, tiles, gather, s);
   }
   return (int)hipGetLastError();
 }

@@ -796,7 +796,7 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
   pnn_plan* plan = c.plan;
   const int B = plan->B, es = plan->es;
   char* wpart = c.scratch + plan->wpart_off;
-  std::vector<WgradProb> wg_vec, wg_gen, wg_h3;
+  std::vector<WgradProb> wg_vec, wg_gen, wg_h3, wg_pw;
   size_t woff = 0;
   for (size_t i = 0; i < segs.size(); ++i) {
     const SegP& S = *segs[i];
@@ -819,7 +819,9 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
       p.pq_log2 = log2_or(p.P * p.Q);
       p.part = (float*)(wpart + woff);
       woff = align256(woff + (size_t)g.splits * p.Co * p.K * 4);
-      (g.halo3 ? wg_h3 : n.cin % (16 / es) == 0 ? wg_vec : wg_gen).push_back(p);
+      const bool vec = n.cin % (16 / es) == 0;
+      const bool pw = vec && n.k == 1 && n.stride == 1 && n.pad == 0;
+      (g.halo3 ? wg_h3 : pw ? wg_pw : vec ? wg_vec : wg_gen).push_back(p);
       ColRedProb r;
       std::memset(&r, 0, sizeof(r));
       r.part = p.part;
@@ -831,8 +833,8 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
       red.push_back(r);
     }
   }
-  for (int v = 0; v < 3; ++v) {
-    auto& list = v == 0 ? wg_vec : v == 1 ? wg_gen : wg_h3;
+  for (int v = 0; v < 4; ++v) {
+    auto& list = v == 0 ? wg_vec : v == 1 ? wg_gen : v == 2 ? wg_h3 : wg_pw;
     int e = grouped<WgradLaunch>(
         list, [](const WgradProb& p) { return p.tiles_co * p.tiles_k * p.splits; },
         [&](const WgradLaunch& Lx, int tiles, size_t) {
@@ -844,7 +846,8 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
           }
           Timer t(plan, 2, c.stream);
           int e2 = v == 2 ? launch_wgrad3(Lx, tiles, plan->dtype, c.stream)
-                          : launch_wgrad(Lx, tiles, plan->dtype, v == 0, c.stream);
+                          : launch_wgrad(Lx, tiles, plan->dtype, v == 0 ? WG_VEC : v == 1 ? WG_GEN : WG_PW,
+                                         c.stream);
           t.done(c.stream, fl, by);
           return e2;
         });

@@ -230,7 +230,10 @@ static_assert(sizeof(ConvLaunch) <= 4096 && sizeof(WgradLaunch) <= 4096 && sizeo
               sizeof(BnApplyLaunch) <= 4096 && sizeof(TransposeLaunch) <= 4096 && sizeof(SgdLaunch) <= 4096,
               "kernel argument size");
 int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, hipStream_t s);
-int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, bool vec, hipStream_t s);
+// activation gather of wgrad_kernel: element-wise (any channel count), 16-byte chunks through the
+// filter taps (Cg a multiple of the chunk), or pointwise (1x1 / stride 1 / pad 0: input row m)
+enum { WG_GEN = 0, WG_VEC = 1, WG_PW = 2 };
+int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, int gather, hipStream_t s);
 // BN backward sums of a 1x1 convolution's input BN (EPI_BN_MASK | EPI_NO_STORE problems):
 // tiles_m = ceil(M / BNSUM_ROWS), tiles_n = ceil(ncol / 64); K <= BNSUM_MAXK
 int launch_bnsum(const ConvLaunch& L, int tiles, int dtype, hipStream_t s);
