@@ -27,8 +27,13 @@
  *     activation gradients and filters as bfloat16 bit patterns (uint16_t) and keep BN
  *     parameters, every parameter gradient, the head and the loss in float.  Arithmetic is fp32
  *     (bf16 MFMA operands with fp32 accumulation).
- *   - Entry points never allocate, free or synchronise.  All work is enqueued on the given
- *     stream, in stream order.  Only pnn_plan_create allocates (host memory only).
+ *   - Entry points never allocate memory, free or synchronise.  All work is ordered on the given
+ *     stream.  parareal_fine_fwd / parareal_fine_bwd may run groups of sub-networks on up to
+ *     pnn_set_streams() streams: the given one and internal streams of the plan (default
+ *     priority), which first wait for the work enqueued on the given stream before the call; the
+ *     given stream waits for all of them before the call returns.  The first call that uses a
+ *     second stream creates the plan's internal streams and events (no memory);
+ *     pnn_plan_destroy releases them.  Only pnn_plan_create allocates (host memory only).
  *   - Workspaces: the caller allocates one "saved" buffer (activations kept from the forward for
  *     the backward; pnn_workspace_size(PNN_WS_SAVED)) and one "scratch" buffer (temporaries;
  *     PNN_WS_SCRATCH), both at least 256-byte aligned, and passes the same ones to every call of a
@@ -229,6 +234,13 @@ pnn_status pnn_sgd_step(pnn_plan* plan, int part, void* const* params, const flo
 pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx, size_t* offset);
 
 const char* pnn_status_string(pnn_status s);
+
+/* Number of streams (1 .. 4, default 4) over which parareal_fine_fwd / parareal_fine_bwd may run
+ * their sub-networks: the sub-networks are grouped by input width (one group per ResNet stage
+ * they start in; at most `streams` groups) and each group's level-by-level launches go to a stream
+ * of its own.  1 keeps every launch on the call's stream.  Results do not depend on it (every
+ * group's launches are the same; no reduction crosses groups).  PNN_ERR_INDEX outside 1 .. 4. */
+pnn_status pnn_set_streams(pnn_plan* plan, int streams);
 
 /* Per-kernel-family GPU time accounting with HIP events recorded on the call's stream around
  * every launch of one family (0 = off).  Families: 1 = grouped conv forward / data-gradient

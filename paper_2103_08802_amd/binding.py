@@ -24,7 +24,7 @@ EXPORTS = ["pnn_plan_create", "pnn_plan_destroy", "pnn_workspace_size", "pnn_par
            "pnn_tensor_shape", "pnn_pre_fwd", "parareal_fine_fwd", "parareal_combine_fwd",
            "coarse_fwd", "pnn_head_fwd_bwd", "coarse_bwd", "parareal_fine_bwd",
            "parareal_combine_bwd", "pnn_pre_bwd", "pnn_status_string", "pnn_inspect",
-           "pnn_timing_enable", "pnn_timing_read", "pnn_sgd_step", "coarse_bwd_all"]
+           "pnn_timing_enable", "pnn_timing_read", "pnn_sgd_step", "coarse_bwd_all", "pnn_set_streams"]
 
 
 class PnnError(RuntimeError):
@@ -85,6 +85,7 @@ def lib():
     L.pnn_status_string.restype = ctypes.c_char_p
     L.pnn_inspect.argtypes = [_vp, i, i, i, i, ctypes.POINTER(sz)]
     L.pnn_timing_enable.argtypes = [_vp, i]
+    L.pnn_set_streams.argtypes = [_vp, i]
     L.pnn_timing_read.argtypes = [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong),
                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     L.coarse_bwd_all.argtypes = [_vp, _PP, _PP, _PP, _vp, _PP, _vp, _vp]
@@ -279,6 +280,10 @@ def pnn_pre_bwd(plan, image, g, delta, saved, ddelta, scratch, stream):
     a3, k3 = _arr(ddelta)
     _check(lib().pnn_pre_bwd(plan.handle, _ptr(image), a1, a2, _ptr(saved), a3, _ptr(scratch), stream),
            "pnn_pre_bwd")
+
+
+def pnn_set_streams(plan, streams):
+    _check(lib().pnn_set_streams(plan.handle, streams), "pnn_set_streams")
 
 
 def pnn_timing_enable(plan, family):

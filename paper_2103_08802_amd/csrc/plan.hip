@@ -88,6 +88,13 @@ struct pnn_plan {
   size_t wpart_off = 0, wpart_bytes = 0;
   size_t head_off = 0, head_bytes = 0;
   size_t sq_off = 0, sq_bytes = 0;
+  // independent chains of the fine sub-networks: up to `streams` streams, the call's stream and
+  // internal ones created by the first call that needs them (default priority, non-blocking)
+  int streams = PNN_MAX_CHAINS;
+  std::vector<hipStream_t> side;
+  std::vector<hipEvent_t> fj;          // fork / join events (no timing), used round robin
+  size_t fj_next = 0;
+  size_t wpart_stride = 0;             // one split-K partial region per chain
   // timing of one kernel family
   int timing_family = 0;
   std::vector<hipEvent_t> ev;
@@ -418,6 +425,7 @@ struct Ctx {
   char* saved;
   char* scratch;
   hipStream_t stream;
+  char* wpart = nullptr;   // split-K weight-gradient partials (nullptr: the plan's first region)
 };
 
 inline char* cp(const void* p) { return (char*)const_cast<void*>(p); }
@@ -611,7 +619,15 @@ void set_tiles(ConvProb& p) {
 // ------------------------------------------------------------------------------------------------
 // forward of a set of segments
 // ------------------------------------------------------------------------------------------------
-int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
+int seg_max_level(const std::vector<const SegP*>& segs) {
+  int maxL = 0;
+  for (auto* s : segs) maxL = std::max(maxL, s->max_level);
+  return maxL;
+}
+
+// Forward of a set of segments: run_fwd_begin (identity segments, statistics of BNs on the segment
+// inputs), then run_fwd_level for L = 1 .. max level.
+int run_fwd_begin(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
   pnn_plan* plan = c.plan;
   const int B = plan->B, es = plan->es;
   // identity segments
@@ -647,9 +663,13 @@ int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
     if (e) return e;
     if (fire_colred(fw, c.stream)) return PNN_ERR_HIP;
   }
-  int maxL = 0;
-  for (auto* s : segs) maxL = std::max(maxL, s->max_level);
-  for (int L = 1; L <= maxL; ++L) {
+  return PNN_OK;
+}
+
+int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs, int L) {
+  pnn_plan* plan = c.plan;
+  const int B = plan->B, es = plan->es;
+  {
     std::vector<ConvProb> cv_vec, cv_gen;
     std::vector<BnActProb> ba;
     std::vector<MaxPool3Prob> mp;
@@ -719,6 +739,12 @@ int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
     if (fire_colred(fw, c.stream)) return PNN_ERR_HIP;
   }
   return PNN_OK;
+}
+
+int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
+  int e = run_fwd_begin(c, segs, ptrs);
+  for (int L = 1, maxL = seg_max_level(segs); e == PNN_OK && L <= maxL; ++L) e = run_fwd_level(c, segs, ptrs, L);
+  return e;
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -795,7 +821,7 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
                 std::vector<ColRedProb>& red) {
   pnn_plan* plan = c.plan;
   const int B = plan->B, es = plan->es;
-  char* wpart = c.scratch + plan->wpart_off;
+  char* wpart = c.wpart != nullptr ? c.wpart : c.scratch + plan->wpart_off;
   std::vector<WgradProb> wg_vec, wg_gen, wg_h3, wg_pw;
   size_t woff = 0;
   for (size_t i = 0; i < segs.size(); ++i) {
@@ -858,10 +884,13 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
 
 // Backward of a set of segments run together, level by level.  wgrad = false leaves the weight
 // gradients to a later fire_wgrads (the coarse chain defers them).
-int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
-            bool wgrad = true) {
+// Backward of a set of segments: run_bwd_begin (transposed filters), run_bwd_level for L = max
+// level .. 1, run_bwd_end (gradient of the segment inputs).  The split-K weight-gradient sums of
+// level L are reduced in the same launch as the BN backward finalisation of level L - 1
+// (independent of it; `pending` carries them); level L - 1's weight gradient reuses the partial
+// region only after that launch (stream order).
+int run_bwd_begin(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
   pnn_plan* plan = c.plan;
-  const int B = plan->B, es = plan->es;
   // filters of the data-gradient convolutions, [c_in][k][k][c_out]
   {
     std::vector<TransposeProb> tp;
@@ -883,13 +912,14 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
         [&](const TransposeLaunch& L, int tiles, size_t) { return launch_transpose(L, tiles, plan->dtype, c.stream); });
     if (e) return e;
   }
-  int maxL = 0;
-  for (auto* s : segs) maxL = std::max(maxL, s->max_level);
-  // split-K weight-gradient sums of level L are reduced in the same launch as the BN backward
-  // finalisation of level L - 1 (independent of it); level L - 1's weight gradient reuses the
-  // partial region only after that launch (stream order)
-  std::vector<ColRedProb> pending;
-  for (int L = maxL; L >= 1; --L) {
+  return PNN_OK;
+}
+
+int run_bwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs, int L,
+                  bool wgrad, std::vector<ColRedProb>& pending) {
+  pnn_plan* plan = c.plan;
+  const int B = plan->B;
+  {
     // A: gradients of the slots produced at this level (+ the previous level's split-K sums)
     {
       std::vector<ColRedProb> fin;
@@ -991,6 +1021,11 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
       if (e) return e;
     }
   }
+  return PNN_OK;
+}
+
+int run_bwd_end(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
+                std::vector<ColRedProb>& pending) {
   // gradient of the segment inputs (+ the last level's split-K sums)
   {
     std::vector<ColRedProb> fin = std::move(pending);
@@ -1005,6 +1040,109 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
     if (e) return e;
   }
   return PNN_OK;
+}
+
+int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
+            bool wgrad = true) {
+  std::vector<ColRedProb> pending;
+  int e = run_bwd_begin(c, segs, ptrs);
+  for (int L = seg_max_level(segs); e == PNN_OK && L >= 1; --L) e = run_bwd_level(c, segs, ptrs, L, wgrad, pending);
+  return e == PNN_OK ? run_bwd_end(c, segs, ptrs, pending) : e;
+}
+
+// ------------------------------------------------------------------------------------------------
+// independent chains
+// ------------------------------------------------------------------------------------------------
+// The level schedule only orders nodes of one segment; segments are independent.  The fine
+// segments are grouped by input width (the ResNet stage they start in), so that each group's
+// levels launch one kernel variant, and each group runs its levels on a stream of its own: level
+// L of every group is enqueued before level L + 1, and the small launches of one group overlap
+// the others'.  One fork (the side streams wait for the call's stream) and one join (the call's
+// stream waits for them) per call.  Timed runs keep one stream.
+struct Chains {
+  std::vector<std::vector<const SegP*>> segs;
+  std::vector<std::vector<Ptrs>> ptrs;
+  std::vector<Ctx> ctx;
+};
+
+int chains_fork(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
+                Chains& ch) {
+  pnn_plan* p = c.plan;
+  const int maxg = p->timing_family != 0 ? 1 : p->streams;
+  std::vector<int> widths;
+  for (size_t i = 0; i < segs.size(); ++i) {
+    const int w = segs[i]->slots[0].C;
+    size_t g = std::find(widths.begin(), widths.end(), w) - widths.begin();
+    if (g == widths.size()) widths.push_back(w);
+    g %= (size_t)maxg;
+    if (g >= ch.segs.size()) {
+      ch.segs.resize(g + 1);
+      ch.ptrs.resize(g + 1);
+    }
+    ch.segs[g].push_back(segs[i]);
+    ch.ptrs[g].push_back(ptrs[i]);
+  }
+  const int G = (int)ch.segs.size();
+  for (int g = 0; g < G; ++g) {
+    Ctx d = c;
+    d.wpart = c.scratch + p->wpart_off + (size_t)g * p->wpart_stride;
+    ch.ctx.push_back(d);
+  }
+  if (G <= 1) return PNN_OK;
+  while (p->side.size() < (size_t)(PNN_MAX_CHAINS - 1)) {
+    hipStream_t st;
+    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return PNN_ERR_HIP;
+    p->side.push_back(st);
+  }
+  while (p->fj.size() < 16) {
+    hipEvent_t e;
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return PNN_ERR_HIP;
+    p->fj.push_back(e);
+  }
+  hipEvent_t e = p->fj[p->fj_next++ % p->fj.size()];
+  if (hipEventRecord(e, c.stream) != hipSuccess) return PNN_ERR_HIP;
+  for (int g = 1; g < G; ++g) {
+    ch.ctx[g].stream = p->side[g - 1];
+    if (hipStreamWaitEvent(ch.ctx[g].stream, e, 0) != hipSuccess) return PNN_ERR_HIP;
+  }
+  return PNN_OK;
+}
+
+int chains_join(const Ctx& c, const Chains& ch) {
+  pnn_plan* p = c.plan;
+  int st = PNN_OK;
+  for (size_t g = 1; g < ch.ctx.size(); ++g) {
+    hipEvent_t e = p->fj[p->fj_next++ % p->fj.size()];
+    if (hipEventRecord(e, ch.ctx[g].stream) != hipSuccess || hipStreamWaitEvent(c.stream, e, 0) != hipSuccess)
+      st = PNN_ERR_HIP;
+  }
+  return st;
+}
+
+int run_fwd_chains(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
+  Chains ch;
+  int e = chains_fork(c, segs, ptrs, ch);
+  const int G = (int)ch.segs.size();
+  for (int g = 0; e == PNN_OK && g < G; ++g) e = run_fwd_begin(ch.ctx[g], ch.segs[g], ch.ptrs[g]);
+  for (int L = 1, maxL = seg_max_level(segs); e == PNN_OK && L <= maxL; ++L)
+    for (int g = 0; e == PNN_OK && g < G; ++g)
+      if (L <= seg_max_level(ch.segs[g])) e = run_fwd_level(ch.ctx[g], ch.segs[g], ch.ptrs[g], L);
+  const int ej = chains_join(c, ch);
+  return e != PNN_OK ? e : ej;
+}
+
+int run_bwd_chains(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
+  Chains ch;
+  int e = chains_fork(c, segs, ptrs, ch);
+  const int G = (int)ch.segs.size();
+  std::vector<std::vector<ColRedProb>> pending(G);
+  for (int g = 0; e == PNN_OK && g < G; ++g) e = run_bwd_begin(ch.ctx[g], ch.segs[g], ch.ptrs[g]);
+  for (int L = seg_max_level(segs); e == PNN_OK && L >= 1; --L)
+    for (int g = 0; e == PNN_OK && g < G; ++g)
+      if (L <= seg_max_level(ch.segs[g])) e = run_bwd_level(ch.ctx[g], ch.segs[g], ch.ptrs[g], L, true, pending[g]);
+  for (int g = 0; e == PNN_OK && g < G; ++g) e = run_bwd_end(ch.ctx[g], ch.segs[g], ch.ptrs[g], pending[g]);
+  const int ej = chains_join(c, ch);
+  return e != PNN_OK ? e : ej;
 }
 
 bool ok_ctx(pnn_plan* plan, void* saved, void* scratch) {
@@ -1095,7 +1233,8 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
   size_t sc = 0;
   p->wpart_off = sc;
   p->wpart_bytes = wp;
-  sc = align256(sc + wp);
+  p->wpart_stride = align256(wp);
+  sc = align256(sc + p->wpart_stride * PNN_MAX_CHAINS);
   const SlotP& yo = p->fine[N - 1].slots[p->fine[N - 1].out];
   p->head_off = sc;
   p->head_bytes = (size_t)p->B * (yo.C + p->classes + 1) * 4;
@@ -1118,6 +1257,8 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
 void pnn_plan_destroy(pnn_plan* plan) {
   if (plan == nullptr) return;
   for (auto e : plan->ev) hipEventDestroy(e);
+  for (auto e : plan->fj) hipEventDestroy(e);
+  for (auto st : plan->side) hipStreamDestroy(st);
   delete plan;
 }
 
@@ -1193,7 +1334,7 @@ pnn_status parareal_fine_fwd(pnn_plan* plan, const void* const* x, const void* c
     segs.push_back(&plan->fine[j]);
     ptrs.push_back(p);
   }
-  return run_fwd(c, segs, ptrs);
+  return run_fwd_chains(c, segs, ptrs);
 }
 
 pnn_status parareal_combine_fwd(pnn_plan* plan, const void* const* y, const void* const* x, void* const* r,
@@ -1387,7 +1528,7 @@ pnn_status parareal_fine_bwd(pnn_plan* plan, const void* const* dy, const void* 
     segs.push_back(&plan->fine[j]);
     ptrs.push_back(p);
   }
-  return run_bwd(c, segs, ptrs);
+  return run_bwd_chains(c, segs, ptrs);
 }
 
 pnn_status parareal_combine_bwd(pnn_plan* plan, void* const* dx, const void* const* D, void* stream) {
@@ -1465,6 +1606,13 @@ pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx,
     return PNN_OK;
   }
   return PNN_ERR_INDEX;
+}
+
+pnn_status pnn_set_streams(pnn_plan* plan, int streams) {
+  if (plan == nullptr) return PNN_ERR_NULL;
+  if (streams < 1 || streams > PNN_MAX_CHAINS) return PNN_ERR_INDEX;
+  plan->streams = streams;
+  return PNN_OK;
 }
 
 pnn_status pnn_timing_enable(pnn_plan* plan, int family) {

@@ -259,6 +259,7 @@ constexpr int CONV_SUBTILES = 8;
 inline int conv_wn(int ncol) { return (ncol % 64 == 0) ? 4 : (ncol % 32 == 0) ? 2 : 1; }
 inline int conv_bm(int ncol) { return 64 * (CONV_SUBTILES / conv_wn(ncol)); }
 constexpr int ELT_TILE = 2048;     // elements per workgroup of elementwise kernels
+constexpr int PNN_MAX_CHAINS = 4;  // streams the fine forward / backward may spread its segment groups over
 constexpr int BNSUM_ROWS = 512;    // rows per BN-sum workgroup
 constexpr int BNSUM_MAXK = 64;     // gradient channels of a BN-sum problem
 constexpr int BNSUM_TR = 64;       // rows per LDS tile of bnsum_kernel

@@ -166,3 +166,30 @@ def test_coarse_bwd_all_equals_per_block_calls():
         out.append(([t.clone() for t in g.D], [t.clone() for t in g.deta]))
     for a, b in zip(out[0][0] + out[0][1], out[1][0] + out[1][1]):
         assert torch.equal(a, b)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("idx,batch", [(2, 2), (3, 4)])
+def test_streams_do_not_change_results(idx, batch):
+    """Running the fine sub-network groups on separate streams gives bit-identical loss, logits and
+    parameter gradients to running every launch on the call's stream (also on a second step,
+    which reuses the plan's streams and events)."""
+    import torch
+    from paper_2103_08802_amd import binding as B
+    from paper_2103_08802_amd.step import ParaRealGPU
+    net = S.config(idx, batch)
+    x, labels, params = S.make_all(net)
+    out = []
+    for streams in (1, 4):
+        g = ParaRealGPU(net, params)
+        B.pnn_set_streams(g.plan, streams)
+        g.load_input(x, labels)
+        res = []
+        for _ in range(2):
+            g.forward()
+            g.backward()
+            torch.cuda.synchronize()
+            res += [t.clone() for t in [g.loss, g.logits, g.deps] + g.ddelta + g.dphi + g.deta]
+        out.append(res)
+    for a, b in zip(out[0], out[1]):
+        assert torch.equal(a, b)
