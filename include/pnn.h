@@ -236,9 +236,9 @@ pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx,
 const char* pnn_status_string(pnn_status s);
 
 /* Number of streams (1 .. 4, default 4) over which parareal_fine_fwd / parareal_fine_bwd may run
- * their sub-networks: the sub-networks are grouped by input width (one group per ResNet stage
- * they start in; at most `streams` groups) and each group's level-by-level launches go to a stream
- * of its own.  1 keeps every launch on the call's stream.  Results do not depend on it (every
+ * their sub-networks: the sub-networks are grouped by the spatial size of their input (the
+ * ResNet stage they start in), the group with the most work is halved while streams are left, and
+ * each group's level-by-level launches go to a stream of its own.  1 keeps every launch on the call's stream.  Results do not depend on it (every
  * group's launches are the same; no reduction crosses groups).  PNN_ERR_INDEX outside 1 .. 4. */
 pnn_status pnn_set_streams(pnn_plan* plan, int streams);
 

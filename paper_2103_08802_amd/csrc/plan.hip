@@ -1054,11 +1054,12 @@ int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vecto
 // independent chains
 // ------------------------------------------------------------------------------------------------
 // The level schedule only orders nodes of one segment; segments are independent.  The fine
-// segments are grouped by input width (the ResNet stage they start in), so that each group's
-// levels launch one kernel variant, and each group runs its levels on a stream of its own: level
-// L of every group is enqueued before level L + 1, and the small launches of one group overlap
-// the others'.  One fork (the side streams wait for the call's stream) and one join (the call's
-// stream waits for them) per call.  Timed runs keep one stream.
+// segments are grouped by the spatial size of their input (the ResNet stage they start in), so
+// that each group's levels launch one kernel variant; while streams are left, the group with the
+// most work is halved.  Each group runs its levels on a stream of its own: level L of every group
+// is enqueued before level L + 1, and the small launches of one group overlap the others'.  One
+// fork (the side streams wait for the call's stream) and one join (the call's stream waits for
+// them) per call.  Timed runs keep one stream.
 struct Chains {
   std::vector<std::vector<const SegP*>> segs;
   std::vector<std::vector<Ptrs>> ptrs;
@@ -1069,11 +1070,11 @@ int chains_fork(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
                 Chains& ch) {
   pnn_plan* p = c.plan;
   const int maxg = p->timing_family != 0 ? 1 : p->streams;
-  std::vector<int> widths;
+  std::vector<long> keys;
   for (size_t i = 0; i < segs.size(); ++i) {
-    const int w = segs[i]->slots[0].C;
-    size_t g = std::find(widths.begin(), widths.end(), w) - widths.begin();
-    if (g == widths.size()) widths.push_back(w);
+    const long key = (long)segs[i]->slots[0].H << 20 | segs[i]->slots[0].W;   // the stage
+    size_t g = std::find(keys.begin(), keys.end(), key) - keys.begin();
+    if (g == keys.size()) keys.push_back(key);
     g %= (size_t)maxg;
     if (g >= ch.segs.size()) {
       ch.segs.resize(g + 1);
@@ -1081,6 +1082,23 @@ int chains_fork(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
     }
     ch.segs[g].push_back(segs[i]);
     ch.ptrs[g].push_back(ptrs[i]);
+  }
+  // streams left over: halve the group with the most saved activation bytes (its work)
+  auto work = [&](size_t g) {
+    size_t w = 0;
+    for (auto* sp : ch.segs[g]) w += sp->saved_bytes;
+    return w;
+  };
+  while ((int)ch.segs.size() < maxg) {
+    size_t big = 0;
+    for (size_t g = 1; g < ch.segs.size(); ++g)
+      if (work(g) > work(big)) big = g;
+    const size_t n = ch.segs[big].size();
+    if (n < 2) break;
+    ch.segs.emplace_back(ch.segs[big].begin() + n / 2, ch.segs[big].end());
+    ch.ptrs.emplace_back(ch.ptrs[big].begin() + n / 2, ch.ptrs[big].end());
+    ch.segs[big].resize(n / 2);
+    ch.ptrs[big].resize(n / 2);
   }
   const int G = (int)ch.segs.size();
   for (int g = 0; g < G; ++g) {
