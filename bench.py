@@ -165,6 +165,9 @@ def main():
                     help="split of the ResNet units into sub-networks")
     ap.add_argument("--coarse", default="config", choices=("config", "paper"),
                     help="coarse blocks F^j: the workload's (one unit) or the paper's own networks")
+    ap.add_argument("--streams", type=int, default=4,
+                    help="streams the fine forward / backward may spread its sub-network groups over "
+                         "(1: everything on one stream, as the per-kernel timing passes run)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 256 MiB device copy first (reference for HBM byte counters)")
@@ -203,6 +206,7 @@ def main():
     net = S.config(args.config, coarse=args.coarse, partition=args.partition)
     x, labels, params = S.make_all(net)
     g = ParaRealGPU(net, params)
+    B.pnn_set_streams(g.plan, args.streams)
     g.load_input(x, labels)
     s = torch.cuda.current_stream()
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(8)] for _ in range(args.steps)]
@@ -229,7 +233,8 @@ def main():
     peak = PEAK_BF16_TFLOPS if net.dtype == "bf16" else PEAK_F32_TFLOPS
 
     # per-kernel-family GPU time (HIP events around every launch of that family, same stream),
-    # over the same number of steps right after the timed region
+    # over the same number of steps right after the timed region; these passes run every launch on
+    # one stream, so that each launch is timed alone
     fam = {}
     for f, name in ((1, "conv_kernel"), (2, "wgrad_kernel")):
         B.pnn_timing_enable(g.plan, f)
@@ -289,7 +294,8 @@ def main():
         "config": {"workload": f"{net.name}: batch {net.batch}, {net.in_shape[0]}x{net.in_shape[1]}x"
                                f"{net.in_shape[2]} input, N={net.n_sub} fine sub-networks, "
                                f"{net.classes} classes",
-                   "batch": net.batch, "n_sub": net.n_sub, "parallelism": "single GPU, N sub-networks grouped"},
+                   "batch": net.batch, "n_sub": net.n_sub,
+                   "parallelism": f"single GPU, N sub-networks grouped, {args.streams} stream(s)"},
         "images_per_s": round(net.batch / (ms_step * 1e-3), 1),
         "pct_bf16_mfma_peak": round(100.0 * tflops / peak, 3),
         "fine_ms_per_step": round(fine_ms, 3),
