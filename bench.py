@@ -7,6 +7,8 @@ Prints ONE JSON line.  ``value`` is the metric's first part: fine-sub-network co
 i.e. 3 x (forward conv FLOPs of all N sub-networks, projections included) / GPU time of
 parareal_fine_fwd + parareal_fine_bwd, averaged over the timed steps.  ``images_per_s`` is
 batch / whole-step time (preprocessing, fine, combine, coarse, head and all backward parts).
+``--graph`` times replays of the step captured in HIP graphs (one graph per part, so that the
+fine and coarse parts are timed between replays) instead of eager library calls.
 """
 from __future__ import annotations
 
@@ -168,6 +170,8 @@ def main():
     ap.add_argument("--streams", type=int, default=4,
                     help="streams the fine forward / backward may spread its sub-network groups over "
                          "(1: everything on one stream, as the per-kernel timing passes run)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of the step captured in HIP graphs instead of eager library calls")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 256 MiB device copy first (reference for HBM byte counters)")
@@ -211,17 +215,24 @@ def main():
     s = torch.cuda.current_stream()
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(8)] for _ in range(args.steps)]
 
-    def step(k=None):
+    def step(k=None, graph=False):
         e = ev[k] if k is not None else None
-        g.forward(fine_events=(e[0], e[1]) if e else None, coarse_events=(e[4], e[5]) if e else None)
-        g.backward(fine_events=(e[2], e[3]) if e else None, coarse_events=(e[6], e[7]) if e else None)
+        fwd, bwd = (g.replay_forward, g.replay_backward) if graph else (g.forward, g.backward)
+        fwd(fine_events=(e[0], e[1]) if e else None, coarse_events=(e[4], e[5]) if e else None)
+        bwd(fine_events=(e[2], e[3]) if e else None, coarse_events=(e[6], e[7]) if e else None)
 
+    use_graph = args.graph
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if use_graph:
+        g.capture()             # the timed steps replay the captured step (all its launches)
+        for _ in range(args.warmup):
+            step(graph=True)
+        torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
-        step(k)
+        step(k, graph=use_graph)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
@@ -295,7 +306,8 @@ def main():
                                f"{net.in_shape[2]} input, N={net.n_sub} fine sub-networks, "
                                f"{net.classes} classes",
                    "batch": net.batch, "n_sub": net.n_sub,
-                   "parallelism": f"single GPU, N sub-networks grouped, {args.streams} stream(s)"},
+                   "parallelism": f"single GPU, N sub-networks grouped, {args.streams} stream(s), "
+                                  f"{'HIP graph replay' if args.graph else 'eager launches'}"},
         "images_per_s": round(net.batch / (ms_step * 1e-3), 1),
         "pct_bf16_mfma_peak": round(100.0 * tflops / peak, 3),
         "fine_ms_per_step": round(fine_ms, 3),

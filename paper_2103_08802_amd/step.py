@@ -199,6 +199,92 @@ class ParaRealGPU:
         self.forward(s)
         self.backward(s)
 
+    # -- HIP graphs ---------------------------------------------------------------------------
+    def _parts(self):
+        """The step's library calls in order, as parts that are captured one graph each (so that
+        the fine and coarse parts can still be timed between replays)."""
+        p, N = self.plan, self.net.n_sub
+        st = self.stream
+
+        def coarse_fwd():
+            for j in range(N - 1):
+                last = j + 1 == N - 1
+                add = self.y[N - 1] if last else self.r[j + 1]
+                out = self.ytilde if last else self.rt[j + 1]
+                B.coarse_fwd(p, j, self.rt[j], self.eta[j], add, out, self.saved, self.scratch, st())
+
+        def coarse_bwd():
+            if self.coarse_chain_all:
+                B.coarse_bwd_all(p, self.D, self.rt, self.eta, self.saved, self.deta, self.scratch, st())
+            else:
+                for j in range(N - 2, -1, -1):
+                    B.coarse_bwd(p, j, self.D[j + 1], self.rt[j], self.eta[j], self.saved, self.D[j],
+                                 self.deta[j], self.scratch, st())
+
+        parts = {
+            "pre_fwd": lambda: B.pnn_pre_fwd(p, self.image, self.x, self.delta, self.saved, self.scratch, st()),
+            "fine_fwd": lambda: B.parareal_fine_fwd(p, self.x, self.phi, self.y, self.saved, self.scratch, st()),
+            "combine_fwd": lambda: B.parareal_combine_fwd(p, self.y, self.x, self.r, None, self.scratch, st()),
+            "coarse_fwd": coarse_fwd,
+            "head": lambda: B.pnn_head_fwd_bwd(p, self.ytilde, self.eps, self.labels, self.logits, self.loss,
+                                               self.D[N - 1], self.deps, self.scratch, st()),
+            "coarse_bwd": coarse_bwd,
+            "fine_bwd": lambda: B.parareal_fine_bwd(p, self.D, self.x, self.phi, self.saved, self.dx, self.dphi,
+                                                    self.scratch, st()),
+            "pre_bwd": lambda: self.backward_pre(st()),
+        }
+        if N == 1:
+            for k in ("combine_fwd", "coarse_fwd", "coarse_bwd"):
+                del parts[k]
+        return parts
+
+    def capture(self):
+        """Capture one training step (forward and backward, as ``forward`` + ``backward`` run it)
+        into HIP graphs, one per part.  Run at least one eager step first (it creates the plan's
+        internal streams and events).  A replay repeats the step on what the buffers hold then."""
+        torch = _torch()
+        self.graphs = {}
+        for name, fn in self._parts().items():
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                fn()
+            self.graphs[name] = g
+        torch.cuda.synchronize()
+
+    def replay_forward(self, fine_events=None, coarse_events=None):
+        """``forward`` from the captured graphs; the events as in ``forward``."""
+        G = self.graphs
+        G["pre_fwd"].replay()
+        if fine_events:
+            fine_events[0].record()
+        G["fine_fwd"].replay()
+        if fine_events:
+            fine_events[1].record()
+        if "coarse_fwd" in G:
+            G["combine_fwd"].replay()
+            if coarse_events:
+                coarse_events[0].record()
+            G["coarse_fwd"].replay()
+            if coarse_events:
+                coarse_events[1].record()
+        G["head"].replay()
+
+    def replay_backward(self, fine_events=None, coarse_events=None):
+        """``backward`` from the captured graphs; the events as in ``backward``."""
+        G = self.graphs
+        if coarse_events:
+            coarse_events[0].record()
+        if "coarse_bwd" in G:
+            G["coarse_bwd"].replay()
+        if coarse_events:
+            coarse_events[1].record()
+        if fine_events:
+            fine_events[0].record()
+        G["fine_bwd"].replay()
+        if fine_events:
+            fine_events[1].record()
+        G["pre_bwd"].replay()
+
     # -- parameter update (SGD with momentum; include/pnn.h pnn_sgd_step) -------------------------
     def sgd_init(self):
         """Zeroed momentum buffers laid out like the gradient buffers."""
