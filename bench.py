@@ -5,10 +5,13 @@ the last 18), batch 128 of 3x32x32 synthetic N(0,1) images, 100 classes, bf16 st
 
 Prints ONE JSON line.  ``value`` is the metric's first part: fine-sub-network convolution TFLOP/s,
 i.e. 3 x (forward conv FLOPs of all N sub-networks, projections included) / GPU time of
-parareal_fine_fwd + parareal_fine_bwd, averaged over the timed steps.  ``images_per_s`` is
-batch / whole-step time (preprocessing, fine, combine, coarse, head and all backward parts).
+parareal_fine_fwd + parareal_fine_bwd, averaged over as many steps as are timed.  ``images_per_s``
+is batch / whole-step time (preprocessing, fine, combine, coarse, head and all backward parts).
 ``--graph`` times replays of the step captured in HIP graphs (one graph per part, so that the
-fine and coarse parts are timed between replays) instead of eager library calls.
+fine and coarse parts are timed between replays) instead of eager library calls.  The timed steps
+run the backward as parareal_bwd (coarse chain overlapped with the fine sub-networks; ``--no-overlap``:
+the two separate calls); the fine and coarse GPU times (and so ``value``) then come from the same
+number of steps with the separate calls, run right after the timed region.
 """
 from __future__ import annotations
 
@@ -170,6 +173,9 @@ def main():
     ap.add_argument("--streams", type=int, default=4,
                     help="streams the fine forward / backward may spread its sub-network groups over "
                          "(1: everything on one stream, as the per-kernel timing passes run)")
+    ap.add_argument("--no-overlap", action="store_true",
+                    help="timed steps call coarse_bwd_all and parareal_fine_bwd one after the other "
+                         "instead of parareal_bwd (the coarse chain overlapped with the fine backward)")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of the step captured in HIP graphs instead of eager library calls")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -222,6 +228,7 @@ def main():
         bwd(fine_events=(e[2], e[3]) if e else None, coarse_events=(e[6], e[7]) if e else None)
 
     use_graph = args.graph
+    g.overlap_bwd = not args.no_overlap and not args.graph    # the graphs capture the separate calls
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -236,6 +243,20 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
+    overlapped = g.overlap_bwd and net.n_sub > 1
+    # backward of the timed steps: coarse chain + fine sub-networks (one span when overlapped)
+    bwd_ms = sum(e[2].elapsed_time(e[3]) + (0.0 if overlapped else e[6].elapsed_time(e[7]))
+                 for e in ev) / args.steps
+    if overlapped:
+        # the fine and coarse parts of the overlapped backward are not separable: time them from
+        # the same number of steps with the separate calls, right after the timed region
+        g.overlap_bwd = False
+        for _ in range(args.warmup):
+            step()
+        for k in range(args.steps):
+            step(k)
+        torch.cuda.synchronize()
+        g.overlap_bwd = True
     fine_ms = sum(e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev) / args.steps
     coarse_ms = (sum(e[4].elapsed_time(e[5]) + e[6].elapsed_time(e[7]) for e in ev) / args.steps
                  if net.n_sub > 1 else 0.0)
@@ -313,6 +334,8 @@ def main():
         "fine_ms_per_step": round(fine_ms, 3),
         "fine_gflop_per_step": round(ff / 1e9, 1),
         "coarse_ms_per_step": round(coarse_ms, 3),
+        "bwd_ms_per_step": round(bwd_ms, 3),
+        "bwd_overlapped": overlapped,
         "sgd_ms_per_step": round(sgd_ms, 3),
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -191,6 +191,16 @@ pnn_status parareal_fine_bwd(pnn_plan* plan, const void* const* dy, const void* 
                              const void* const* phi, const void* saved, void* const* dx,
                              float* const* dphi, void* scratch, void* stream);
 
+/* coarse_bwd_all followed by parareal_fine_bwd (dy = D) in one call, with the same results: the
+ * coarse chain runs on the given stream, and each group of fine sub-networks (as grouped by
+ * pnn_set_streams) starts on its own stream as soon as the chain has produced the last D_j it
+ * needs (the chain produces D_{N-2} first and D_0 last); the coarse weight gradients follow on a
+ * side stream.  Arguments as in those two calls. */
+pnn_status parareal_bwd(pnn_plan* plan, void* const* D, const void* const* rt, const void* const* eta,
+                        float* const* deta, const void* const* x, const void* const* phi,
+                        void* const* dx, float* const* dphi, const void* saved, void* scratch,
+                        void* stream);
+
 /* dx[j] -= D_{j-1} in place for j = 1..N-1 (eq. (deltaj), the -D_{j-1} term; D_0 = 0). */
 pnn_status parareal_combine_bwd(pnn_plan* plan, void* const* dx, const void* const* D,
                                 void* stream);

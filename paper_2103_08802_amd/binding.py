@@ -24,7 +24,8 @@ EXPORTS = ["pnn_plan_create", "pnn_plan_destroy", "pnn_workspace_size", "pnn_par
            "pnn_tensor_shape", "pnn_pre_fwd", "parareal_fine_fwd", "parareal_combine_fwd",
            "coarse_fwd", "pnn_head_fwd_bwd", "coarse_bwd", "parareal_fine_bwd",
            "parareal_combine_bwd", "pnn_pre_bwd", "pnn_status_string", "pnn_inspect",
-           "pnn_timing_enable", "pnn_timing_read", "pnn_sgd_step", "coarse_bwd_all", "pnn_set_streams"]
+           "pnn_timing_enable", "pnn_timing_read", "pnn_sgd_step", "coarse_bwd_all", "pnn_set_streams",
+           "parareal_bwd"]
 
 
 class PnnError(RuntimeError):
@@ -89,6 +90,7 @@ def lib():
     L.pnn_timing_read.argtypes = [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong),
                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     L.coarse_bwd_all.argtypes = [_vp, _PP, _PP, _PP, _vp, _PP, _vp, _vp]
+    L.parareal_bwd.argtypes = [_vp, _PP, _PP, _PP, _PP, _PP, _PP, _PP, _PP, _vp, _vp, _vp]
     f = ctypes.c_float
     L.pnn_sgd_step.argtypes = [_vp, i, _PP, _PP, _PP, f, f, f, i, _vp]
     for name in EXPORTS:
@@ -264,6 +266,19 @@ def coarse_bwd_all(plan, D, rt, eta, saved, deta, scratch, stream):
     a4, k4 = _arr(deta)
     _check(lib().coarse_bwd_all(plan.handle, a1, a2, a3, _ptr(saved), a4, _ptr(scratch), stream),
            "coarse_bwd_all")
+
+
+def parareal_bwd(plan, D, rt, eta, deta, x, phi, dx, dphi, saved, scratch, stream):
+    a1, k1 = _arr(D)
+    a2, k2 = _arr(rt)
+    a3, k3 = _arr(eta)
+    a4, k4 = _arr(deta)
+    a5, k5 = _arr(x)
+    a6, k6 = _arr(phi)
+    a7, k7 = _arr(dx)
+    a8, k8 = _arr(dphi)
+    _check(lib().parareal_bwd(plan.handle, a1, a2, a3, a4, a5, a6, a7, a8, _ptr(saved), _ptr(scratch), stream),
+           "parareal_bwd")
 
 
 def pnn_sgd_step(plan, part, params, grads, momentum, lr, mu, weight_decay, nesterov, stream):

@@ -1066,8 +1066,10 @@ struct Chains {
   std::vector<Ctx> ctx;
 };
 
-int chains_fork(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
-                Chains& ch) {
+// Groups and their contexts: group g runs on the call's stream (g = 0) or side stream g - 1 and
+// uses split-K partial region g + 1 (region 0 stays with the calls that do not chain).
+int chains_group(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
+                 Chains& ch) {
   pnn_plan* p = c.plan;
   const int maxg = p->timing_family != 0 ? 1 : p->streams;
   std::vector<long> keys;
@@ -1103,7 +1105,7 @@ int chains_fork(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
   const int G = (int)ch.segs.size();
   for (int g = 0; g < G; ++g) {
     Ctx d = c;
-    d.wpart = c.scratch + p->wpart_off + (size_t)g * p->wpart_stride;
+    d.wpart = c.scratch + p->wpart_off + (size_t)(g + 1) * p->wpart_stride;
     ch.ctx.push_back(d);
   }
   if (G <= 1) return PNN_OK;
@@ -1117,13 +1119,25 @@ int chains_fork(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
     if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return PNN_ERR_HIP;
     p->fj.push_back(e);
   }
+  for (int g = 1; g < G; ++g) ch.ctx[g].stream = p->side[g - 1];
+  return PNN_OK;
+}
+
+// Side streams of groups [g0, g1) wait for everything enqueued on the call's stream so far.
+int chains_wait(const Ctx& c, const Chains& ch, int g0, int g1) {
+  if (g1 <= g0 || ch.ctx.size() <= 1) return PNN_OK;
+  pnn_plan* p = c.plan;
   hipEvent_t e = p->fj[p->fj_next++ % p->fj.size()];
   if (hipEventRecord(e, c.stream) != hipSuccess) return PNN_ERR_HIP;
-  for (int g = 1; g < G; ++g) {
-    ch.ctx[g].stream = p->side[g - 1];
+  for (int g = std::max(g0, 1); g < g1; ++g)
     if (hipStreamWaitEvent(ch.ctx[g].stream, e, 0) != hipSuccess) return PNN_ERR_HIP;
-  }
   return PNN_OK;
+}
+
+int chains_fork(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
+                Chains& ch) {
+  int e = chains_group(c, segs, ptrs, ch);
+  return e ? e : chains_wait(c, ch, 1, (int)ch.ctx.size());
 }
 
 int chains_join(const Ctx& c, const Chains& ch) {
@@ -1252,7 +1266,7 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
   p->wpart_off = sc;
   p->wpart_bytes = wp;
   p->wpart_stride = align256(wp);
-  sc = align256(sc + p->wpart_stride * PNN_MAX_CHAINS);
+  sc = align256(sc + p->wpart_stride * (PNN_MAX_CHAINS + 1));
   const SlotP& yo = p->fine[N - 1].slots[p->fine[N - 1].out];
   p->head_off = sc;
   p->head_bytes = (size_t)p->B * (yo.C + p->classes + 1) * 4;
@@ -1547,6 +1561,90 @@ pnn_status parareal_fine_bwd(pnn_plan* plan, const void* const* dy, const void* 
     ptrs.push_back(p);
   }
   return run_bwd_chains(c, segs, ptrs);
+}
+
+pnn_status parareal_bwd(pnn_plan* plan, void* const* D, const void* const* rt, const void* const* eta,
+                        float* const* deta, const void* const* x, const void* const* phi, void* const* dx,
+                        float* const* dphi, const void* saved, void* scratch, void* stream) {
+  if (!ok_ctx(plan, const_cast<void*>(saved), scratch)) return PNN_ERR_NULL;
+  if (D == nullptr || x == nullptr || phi == nullptr || dx == nullptr || dphi == nullptr) return PNN_ERR_NULL;
+  const int N = plan->N;
+  if (N > 1 && (rt == nullptr || eta == nullptr || deta == nullptr)) return PNN_ERR_NULL;
+  for (int j = 0; j < N; ++j)
+    if (D[j] == nullptr || x[j] == nullptr || phi[j] == nullptr || dx[j] == nullptr || dphi[j] == nullptr)
+      return PNN_ERR_NULL;
+  for (int j = 0; j + 1 < N; ++j) {
+    if (rt[j] == nullptr || eta[j] == nullptr || deta[j] == nullptr) return PNN_ERR_NULL;
+    if (D[j] == D[j + 1]) return PNN_ERR_SHAPE;
+  }
+  Ctx c{plan, (char*)const_cast<void*>(saved), (char*)scratch, (hipStream_t)stream};
+  std::vector<const SegP*> segs;
+  std::vector<Ptrs> ptrs;
+  for (int j = 0; j < N; ++j) {
+    Ptrs p;
+    p.in = x[j];
+    p.params = phi[j];
+    p.grads = dphi[j];
+    p.gout = D[j];
+    p.gin = dx[j];
+    segs.push_back(&plan->fine[j]);
+    ptrs.push_back(p);
+  }
+  Chains ch;
+  int e = chains_group(c, segs, ptrs, ch);
+  if (e) return e;
+  const int G = (int)ch.ctx.size();
+  // the lowest sub-network index of a group: the last D_j of the chain the group needs
+  std::vector<int> need(G, N - 1);
+  for (int g = 0; g < G; ++g)
+    for (auto* sp : ch.segs[g]) need[g] = std::min(need[g], sp->index);
+  // side streams: after the work enqueued before the call, their filter transposes (independent
+  // of the chain); group 0 runs on the call's stream after the chain
+  e = chains_wait(c, ch, 1, G);
+  std::vector<std::vector<ColRedProb>> pending(G);
+  for (int g = 0; e == PNN_OK && g < G; ++g) e = run_bwd_begin(ch.ctx[g], ch.segs[g], ch.ptrs[g]);
+  // the coarse chain's data gradients on the call's stream; a group starts once its D_j is out
+  std::vector<const SegP*> csegs;
+  std::vector<Ptrs> cptrs;
+  for (int j = N - 2; e == PNN_OK && j >= 0; --j) {
+    Ptrs p;
+    p.in = rt[j];
+    p.params = eta[j];
+    p.grads = deta[j];
+    p.gout = D[j + 1];
+    p.gin = D[j];
+    e = run_bwd(c, {&plan->coarse[j]}, {p}, false);
+    csegs.push_back(&plan->coarse[j]);
+    cptrs.push_back(p);
+    for (int g = 1; e == PNN_OK && g < G; ++g)
+      if (need[g] == j) e = chains_wait(c, ch, g, g + 1);
+  }
+  // the coarse weight gradients (split-K region 0) wait for the chain on the side stream of the
+  // group that starts first, after its own levels; without side streams on the call's stream
+  hipEvent_t chain_done = nullptr;
+  if (e == PNN_OK && G > 1 && N > 1) {
+    chain_done = plan->fj[plan->fj_next++ % plan->fj.size()];
+    if (hipEventRecord(chain_done, c.stream) != hipSuccess) e = PNN_ERR_HIP;
+  }
+  for (int L = seg_max_level(segs); e == PNN_OK && L >= 1; --L)
+    for (int g = 0; e == PNN_OK && g < G; ++g)
+      if (L <= seg_max_level(ch.segs[g])) e = run_bwd_level(ch.ctx[g], ch.segs[g], ch.ptrs[g], L, true, pending[g]);
+  for (int g = 0; e == PNN_OK && g < G; ++g) e = run_bwd_end(ch.ctx[g], ch.segs[g], ch.ptrs[g], pending[g]);
+  if (e == PNN_OK && N > 1) {
+    Ctx cw = c;
+    if (G > 1) {
+      int gw = 1;
+      for (int g = 2; g < G; ++g)
+        if (need[g] > need[gw]) gw = g;
+      cw.stream = ch.ctx[gw].stream;
+      if (hipStreamWaitEvent(cw.stream, chain_done, 0) != hipSuccess) e = PNN_ERR_HIP;
+    }
+    std::vector<ColRedProb> red;
+    if (e == PNN_OK) e = fire_wgrads(cw, csegs, cptrs, -1, red);
+    if (e == PNN_OK && fire_colred(red, cw.stream)) e = PNN_ERR_HIP;
+  }
+  const int ej = chains_join(c, ch);
+  return e != PNN_OK ? e : ej;
 }
 
 pnn_status parareal_combine_bwd(pnn_plan* plan, void* const* dx, const void* const* D, void* stream) {

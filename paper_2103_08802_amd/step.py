@@ -26,6 +26,7 @@ class ParaRealGPU:
         self.net = net
         self.plan = B.Plan(net)
         self.coarse_chain_all = True      # coarse_bwd_all (deferred coarse weight gradients)
+        self.overlap_bwd = False          # parareal_bwd: the coarse chain overlapped with the fine backward
         self.dev = torch.device(device)
         self.sdt = torch.bfloat16 if net.dtype == "bf16" else torch.float32
         N, Bt = net.n_sub, net.batch
@@ -169,9 +170,20 @@ class ParaRealGPU:
         self.backward_pre(s)
 
     def backward_coarse_fine(self, s=None, fine_events=None, coarse_events=None):
-        """The coarse chain D_j (j = N-1..1) and the fine sub-networks' gradients."""
+        """The coarse chain D_j (j = N-1..1) and the fine sub-networks' gradients.  With
+        ``overlap_bwd`` (and N > 1) both run in one parareal_bwd call, which starts each group of
+        fine sub-networks as soon as the chain has produced its D_j; ``fine_events`` then bracket
+        that call and ``coarse_events`` are not recorded."""
         s = self.stream() if s is None else s
         p, N = self.plan, self.net.n_sub
+        if self.overlap_bwd and N > 1:
+            if fine_events:
+                fine_events[0].record()
+            B.parareal_bwd(p, self.D, self.rt, self.eta, self.deta, self.x, self.phi, self.dx, self.dphi,
+                           self.saved, self.scratch, s)
+            if fine_events:
+                fine_events[1].record()
+            return
         if coarse_events:
             coarse_events[0].record()
         if N > 1 and self.coarse_chain_all:

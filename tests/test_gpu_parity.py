@@ -232,3 +232,29 @@ def test_graph_replay_matches_eager(idx, batch, streams):
         torch.cuda.synchronize()
         for a, b in zip(outputs(), ref):
             assert torch.equal(a, b)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("idx,batch,streams", [(2, 2, 4), (3, 4, 4), (3, 4, 1)])
+def test_parareal_bwd_equals_separate_calls(idx, batch, streams):
+    """parareal_bwd (coarse chain overlapped with the fine backward) gives bit-identical D_j,
+    coarse and fine parameter gradients and input gradients to coarse_bwd_all followed by
+    parareal_fine_bwd."""
+    import torch
+    from paper_2103_08802_amd import binding as B
+    from paper_2103_08802_amd.step import ParaRealGPU
+    net = S.config(idx, batch)
+    x, labels, params = S.make_all(net)
+    out = []
+    for overlap in (False, True, True):
+        g = ParaRealGPU(net, params)
+        B.pnn_set_streams(g.plan, streams)
+        g.overlap_bwd = overlap
+        g.load_input(x, labels)
+        g.forward()
+        g.backward()
+        torch.cuda.synchronize()
+        out.append([t.clone() for t in [g.loss, g.deps] + g.D + g.deta + g.dphi + g.ddelta + g.dx])
+    for run in out[1:]:
+        for a, b in zip(out[0], run):
+            assert torch.equal(a, b)
