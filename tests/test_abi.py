@@ -82,5 +82,16 @@ def test_error_codes():
     assert L.pnn_param_layout(p.handle, 1, 5, 0, None, ctypes.byref(v)) == -7  # PNN_ERR_INDEX
     assert L.coarse_fwd(p.handle, 3, 1, 1, 1, 2, 1, 1, None) == -7
     assert L.parareal_fine_fwd(p.handle, None, None, None, 1, 1, None) == -1
+    assert L.pnn_set_streams(p.handle, 0) == -7                                # 1 .. 4 streams
+    assert L.pnn_set_streams(p.handle, 5) == -7
+    assert L.pnn_set_streams(p.handle, 1) == 0 and L.pnn_set_streams(p.handle, 4) == 0
+    assert L.pnn_set_streams(None, 2) == -1
+    # parareal_bwd: NULL arrays and aliased D_j / D_{j+1} are rejected before anything is enqueued
+    assert L.parareal_bwd(p.handle, None, None, None, None, None, None, None, None, 1, 1, None) == -1
+    N = S.config(0).n_sub
+    arr = lambda vals: (ctypes.c_void_p * len(vals))(*vals)
+    D = arr([16] * N)                                                          # D_0 aliases D_1
+    ok = arr([16 * (i + 1) for i in range(N)])
+    assert L.parareal_bwd(p.handle, D, ok, ok, ok, ok, ok, ok, ok, 1, 1, None) == -2
     assert B.pnn_status_string(-5) == "network form not supported by this library"
     p.close()
