@@ -257,7 +257,7 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
 }
 
 // WM row sub-tiles of 16 per wave, WN column sub-tiles: a workgroup owns a (64 WM) x (16 WN) tile
-// (WM * WN = CONV_SUBTILES, so narrow problems get taller tiles).
+// (tall tiles: WM * WN = CONV_SUBTILES, so narrow problems get taller tiles; short tiles: 2 or 4).
 template <typename T, int MODE, int GK, int WM, int WN>
 __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   constexpr int VE = St<T>::VE;
@@ -1205,9 +1205,8 @@ __global__ __launch_bounds__(256) void bnsum_kernel(const ConvLaunch L) {
 // launchers
 // ------------------------------------------------------------------------------------------------
 
-template <typename T, int MODE, int WN>
-static void launch_conv_w(const ConvLaunch& L, int tiles, int gk, hipStream_t s) {
-  constexpr int WM = CONV_SUBTILES / WN;
+template <typename T, int MODE, int WM, int WN>
+static void launch_conv_v(const ConvLaunch& L, int tiles, int gk, hipStream_t s) {
   if (gk == GK_POINT)
     hipLaunchKernelGGL((conv_kernel<T, MODE, GK_POINT, WM, WN>), dim3(tiles), dim3(256), 0, s, L);
   else if (gk == GK_VEC)
@@ -1218,22 +1217,28 @@ static void launch_conv_w(const ConvLaunch& L, int tiles, int gk, hipStream_t s)
     hipLaunchKernelGGL((conv_kernel<T, MODE, GK_SCALAR, WM, WN>), dim3(tiles), dim3(256), 0, s, L);
 }
 
+// tile variants: (wn, wm) = (1, 8), (2, 4), (4, 2) tall; (1, 2), (2, 1), (4, 1) short
 template <typename T, int MODE>
-static void launch_conv_m(const ConvLaunch& L, int tiles, int gk, int wn, hipStream_t s) {
-  if (wn == 1) launch_conv_w<T, MODE, 1>(L, tiles, gk, s);
-  else if (wn == 2) launch_conv_w<T, MODE, 2>(L, tiles, gk, s);
-  else launch_conv_w<T, MODE, 4>(L, tiles, gk, s);
+static int launch_conv_m(const ConvLaunch& L, int tiles, int gk, int wn, int wm, hipStream_t s) {
+  if (wn == 1 && wm == 8) launch_conv_v<T, MODE, 8, 1>(L, tiles, gk, s);
+  else if (wn == 2 && wm == 4) launch_conv_v<T, MODE, 4, 2>(L, tiles, gk, s);
+  else if (wn == 4 && wm == 2) launch_conv_v<T, MODE, 2, 4>(L, tiles, gk, s);
+  else if (wn == 1 && wm == 2) launch_conv_v<T, MODE, 2, 1>(L, tiles, gk, s);
+  else if (wn == 2 && wm == 1) launch_conv_v<T, MODE, 1, 2>(L, tiles, gk, s);
+  else if (wn == 4 && wm == 1) launch_conv_v<T, MODE, 1, 4>(L, tiles, gk, s);
+  else return (int)hipErrorInvalidValue;
+  return 0;
 }
 
-int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, hipStream_t s) {
-  if (dtype == 1) {
-    if (mode == MODE_FWD) launch_conv_m<uint16_t, MODE_FWD>(L, tiles, gk, wn, s);
-    else launch_conv_m<uint16_t, MODE_BWD>(L, tiles, gk, wn, s);
-  } else {
-    if (mode == MODE_FWD) launch_conv_m<float, MODE_FWD>(L, tiles, gk, wn, s);
-    else launch_conv_m<float, MODE_BWD>(L, tiles, gk, wn, s);
-  }
-  return (int)hipGetLastError();
+int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, int wm, hipStream_t s) {
+  int e;
+  if (dtype == 1)
+    e = mode == MODE_FWD ? launch_conv_m<uint16_t, MODE_FWD>(L, tiles, gk, wn, wm, s)
+                         : launch_conv_m<uint16_t, MODE_BWD>(L, tiles, gk, wn, wm, s);
+  else
+    e = mode == MODE_FWD ? launch_conv_m<float, MODE_FWD>(L, tiles, gk, wn, wm, s)
+                         : launch_conv_m<float, MODE_BWD>(L, tiles, gk, wn, wm, s);
+  return e ? e : (int)hipGetLastError();
 }
 
 int launch_bnsum(const ConvLaunch& L, int tiles, int dtype, hipStream_t s) {

@@ -60,6 +60,7 @@ struct BnP {
 
 struct SegP {
   int part = 0, index = 0;
+  bool short_tiles = false;   // convolutions in short tiles (the coarse blocks: one problem a launch)
   int in_h = 0, in_w = 0, in_c = 0;
   std::vector<NodeP> nodes;
   std::vector<SlotP> slots;
@@ -159,6 +160,7 @@ WgradGeom wgrad_geom(int Co, int K, long M) {
 pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, int es, SegP& S) {
   S.part = part;
   S.index = index;
+  S.short_tiles = part == 2;
   S.in_h = d.in_h;
   S.in_w = d.in_w;
   S.in_c = d.in_c;
@@ -333,8 +335,15 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
     const SlotP& sl = S.slots[b.slot];
     const long M = (long)B * sl.H * sl.W;
     b.C = sl.C;
-    b.fwd_tiles = (int)cdiv(M, b.slot == 0 ? COLSTAT_ROWS : conv_bm(b.C));
-    b.bwd_tiles = (int)cdiv(M, b.bnsum ? BNSUM_ROWS : conv_bm(b.C));
+    // partial rows = tiles of the producing convolution: the forward one writing the slot, the
+    // data gradient of the consumer that reduces the BN sums (the second of two)
+    int kf = 1, kb = 1;
+    if (sl.producer >= 0 && S.nodes[sl.producer].op == PNN_OP_CONV) kf = S.nodes[sl.producer].k;
+    for (int ci : sl.bn_consumers)
+      if (!S.nodes[ci].first_of_two) kb = S.nodes[ci].k;
+    const bool sh = S.short_tiles;
+    b.fwd_tiles = (int)cdiv(M, b.slot == 0 ? COLSTAT_ROWS : 64 * conv_rows_wm(kf, M, b.C, sh));
+    b.bwd_tiles = (int)cdiv(M, b.bnsum ? BNSUM_ROWS : 64 * conv_rows_wm(kb, M, b.C, sh));
     if (b.bnact_consumer) {
       const NodeP& c = S.nodes[sl.bn_consumers[0]];
       b.bwd_tiles = (int)cdiv((long)B * c.Ho * c.Wo, BNACT_PIX);
@@ -539,7 +548,7 @@ double conv_bytes(const ConvProb& p, int es, int mode) {
   return b;
 }
 
-int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk, int wn) {
+int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk, int wn, int wm) {
   pnn_plan* plan = c.plan;
   return grouped<ConvLaunch>(
       probs, [](const ConvProb& p) { return p.tiles_m * p.tiles_n; },
@@ -550,7 +559,7 @@ int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk, i
           by += conv_bytes(L.p[i], plan->es, mode);
         }
         Timer t(plan, 1, c.stream);
-        int e = launch_conv(L, tiles, plan->dtype, mode, gk, wn, c.stream);
+        int e = launch_conv(L, tiles, plan->dtype, mode, gk, wn, wm, c.stream);
         t.done(c.stream, fl, by);
         return e;
       });
@@ -562,7 +571,7 @@ bool halo_ok(const ConvProb& p, int es) {
   if (p.k != 3 || p.stride != 1 || p.pad != 1 || p.H != p.P || p.W != p.Q) return false;
   const int ve = 16 / es;
   if (p.K > 4 * ve * conv_halo_nkb(p.wn)) return false;
-  const int bm = 64 * (CONV_SUBTILES / p.wn);
+  const int bm = 64 * p.wm;
   const int pq = p.P * p.Q;
   if (bm % p.Q != 0 || (pq % bm != 0 && bm % pq != 0)) return false;
   const long nimg = bm > pq ? bm / pq : 1;
@@ -580,14 +589,20 @@ int gather_kind(const ConvProb& p, int es) {
   return 1;
 }
 
+// one grouped launch per (gather kind, column sub-tiles, tall / short tiles)
 int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode) {
-  std::vector<ConvProb> by[4][3];
-  for (auto& p : probs) by[gather_kind(p, c.plan->es)][p.wn == 1 ? 0 : p.wn == 2 ? 1 : 2].push_back(p);
+  std::vector<ConvProb> by[4][3][2];
+  for (auto& p : probs) {
+    const int w = p.wn == 1 ? 0 : p.wn == 2 ? 1 : 2;
+    by[gather_kind(p, c.plan->es)][w][p.wm == conv_wm(p.wn, false) ? 0 : 1].push_back(p);
+  }
   for (int gk = 0; gk < 4; ++gk)
-    for (int w = 0; w < 3; ++w) {
-      int e = fire_conv_gk(c, by[gk][w], mode, gk, 1 << w);
-      if (e) return e;
-    }
+    for (int w = 0; w < 3; ++w)
+      for (int t = 0; t < 2; ++t) {
+        if (by[gk][w][t].empty()) continue;
+        int e = fire_conv_gk(c, by[gk][w][t], mode, gk, 1 << w, conv_wm(1 << w, t == 1));
+        if (e) return e;
+      }
   return PNN_OK;
 }
 
@@ -607,12 +622,13 @@ int log2_or(int v) {
   return l;
 }
 
-void set_tiles(ConvProb& p) {
+void set_tiles(ConvProb& p, bool short_tiles) {
   p.cg_log2 = log2_or(p.Cg);
   p.q_log2 = log2_or(p.Q);
   p.pq_log2 = log2_or(p.P * p.Q);
-  p.tiles_m = (int)cdiv(p.M, conv_bm(p.ncol));
   p.wn = conv_wn(p.ncol);
+  p.wm = conv_rows_wm(p.k, p.M, p.ncol, short_tiles);
+  p.tiles_m = (int)cdiv(p.M, 64 * p.wm);
   p.tiles_n = p.ncol / (16 * p.wn);
 }
 
@@ -697,7 +713,7 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
           p.P = n.Ho; p.Q = n.Wo; p.ncol = n.cout;
           p.M = B * n.Ho * n.Wo;
           p.K = n.k * n.k * n.cin;
-          set_tiles(p);
+          set_tiles(p, S.short_tiles);
           (n.cin % (16 / es) == 0 ? cv_vec : cv_gen).push_back(p);
         } else if (n.op == PNN_OP_BNACT) {
           BnActProb p;
@@ -789,7 +805,7 @@ void bn_bwd_finalize(const Ctx& c, const SegP& S, const Ptrs& P, int s, std::vec
     p.coef = f.coef;
     p.out = grad_ptr(c, S, P, s);
     p.res = skip_ptr(c, S, P, s);
-    set_tiles(p);
+    set_tiles(p, S.short_tiles);
     rec.push_back(p);
     return;
   }
@@ -997,7 +1013,7 @@ int run_bwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
             p.out = grad_ptr(c, S, P, n.src);
             p.res = skip_ptr(c, S, P, n.src);
           }
-          set_tiles(p);
+          set_tiles(p, S.short_tiles);
           dg.push_back(p);
         }
       }

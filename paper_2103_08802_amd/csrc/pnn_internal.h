@@ -50,7 +50,7 @@ struct ConvProb {
   int ncol;
   int k, stride, pad;   // forward convolution geometry (BWD gathers through its transpose)
   int M, K;
-  int tiles_m, tiles_n, wn;
+  int tiles_m, tiles_n, wn, wm;   // tiles; column and row sub-tiles per wave
   int flags;
   int cg_log2;          // log2(Cg) when Cg is a power of two, else -1
   int q_log2, pq_log2;  // log2(Q), log2(P*Q) when powers of two, else -1
@@ -229,7 +229,7 @@ int launch_sgd(const SgdLaunch& L, int tiles, int dtype, hipStream_t s);
 static_assert(sizeof(ConvLaunch) <= 4096 && sizeof(WgradLaunch) <= 4096 && sizeof(ColRedLaunch) <= 4096 &&
               sizeof(BnApplyLaunch) <= 4096 && sizeof(TransposeLaunch) <= 4096 && sizeof(SgdLaunch) <= 4096,
               "kernel argument size");
-int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, hipStream_t s);
+int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, int wm, hipStream_t s);
 // activation gather of wgrad_kernel: element-wise (any channel count), 16-byte chunks through the
 // filter taps (Cg a multiple of the chunk), or pointwise (1x1 / stride 1 / pad 0: input row m)
 enum { WG_GEN = 0, WG_VEC = 1, WG_PW = 2 };
@@ -255,9 +255,22 @@ int launch_head(const void* yt, const float* eps, const int32_t* labels, float* 
 // tile sizes shared by host and device code
 // conv workgroup tile: 16 x 16 sub-tiles per wave (row sub-tiles x column sub-tiles); a problem with
 // ncol output columns takes wn = 4, 2 or 1 column sub-tiles and 64 x (CONV_SUBTILES / wn) rows of M
+// (tall tiles) or 64 x conv_wm(wn, true) rows (short tiles)
 constexpr int CONV_SUBTILES = 8;
 inline int conv_wn(int ncol) { return (ncol % 64 == 0) ? 4 : (ncol % 32 == 0) ? 2 : 1; }
 inline int conv_bm(int ncol) { return 64 * (CONV_SUBTILES / conv_wn(ncol)); }
+// short tiles (single-problem launches such as the coarse chain's, which need more workgroups than
+// tall tiles give): 2 sub-tiles per wave for 16- and 32-column tiles, 4 for 64-column tiles
+inline int conv_wm(int wn, bool short_tiles) { return short_tiles ? (wn == 1 ? 2 : 1) : CONV_SUBTILES / wn; }
+constexpr int SHORT_TILES_BELOW = 512;   // workgroups of a tall tiling below which short tiles pay
+// row sub-tiles per wave of a k x k convolution problem with M rows and ncol columns in a segment
+// that allows short tiles: short for 1x1 problems with few tall tiles (3x3 keep tall tiles)
+inline int conv_rows_wm(int k, long M, int ncol, bool short_ok) {
+  const int wn = conv_wn(ncol), tall = CONV_SUBTILES / wn;
+  if (!short_ok || k != 1) return tall;
+  const long tiles = (M + 64 * tall - 1) / (64 * tall) * (ncol / (16 * wn));
+  return tiles < SHORT_TILES_BELOW ? conv_wm(wn, true) : tall;
+}
 constexpr int ELT_TILE = 2048;     // elements per workgroup of elementwise kernels
 constexpr int PNN_MAX_CHAINS = 4;  // streams the fine forward / backward may spread its segment groups over
 constexpr int BNSUM_ROWS = 512;    // rows per BN-sum workgroup
