@@ -268,7 +268,7 @@ def main():
     # over the same number of steps right after the timed region; these passes run every launch on
     # one stream, so that each launch is timed alone
     fam = {}
-    for f, name in ((1, "conv_kernel"), (2, "wgrad_kernel")):
+    for f, name in ((1, "conv_kernel"), (2, "wgrad_kernel"), (3, "pw_kernel")):
         B.pnn_timing_enable(g.plan, f)
         for _ in range(args.steps):
             step()

@@ -254,7 +254,8 @@ pnn_status pnn_set_streams(pnn_plan* plan, int streams);
 
 /* Per-kernel-family GPU time accounting with HIP events recorded on the call's stream around
  * every launch of one family (0 = off).  Families: 1 = grouped conv forward / data-gradient
- * kernel, 2 = weight-gradient kernel.  pnn_timing_read synchronises on the recorded events and
+ * kernel, 2 = weight-gradient kernels, 3 = streaming pointwise kernels (narrow 1x1 forward and
+ * data gradients; BN sums of deferred-apply BNs).  pnn_timing_read synchronises on the recorded events and
  * returns the summed milliseconds, the launch count, and the summed multiply-add count
  * (2 x MACs = FLOPs) and minimum HBM bytes of those launches; it resets the accumulators. */
 pnn_status pnn_timing_enable(pnn_plan* plan, int family);

@@ -1202,6 +1202,226 @@ __global__ __launch_bounds__(256) void bnsum_kernel(const ConvLaunch L) {
 }
 
 // ------------------------------------------------------------------------------------------------
+// Streaming pointwise convolution (1x1, stride 1, pad 0, K <= MAXK), used for narrow problems
+// (16-column tiles), where it keeps more loads in flight than the 512-row conv tile:
+//   FWD: out[m][c] = sum_k act(x[m][k]) W[c][k], act = ReLU(x * scale + shift) (P.pro) or identity;
+//        stored rounded; EPI_STATS: column sums of the stored value and of its square -> part.
+//   BWD (EPI_BN_MASK): v[m][c] = sum_o g[m][o] Wt[c][o]; dbn = rnd(v * [ReLU(BN(z)) > 0]), stored
+//        unless EPI_NO_STORE; sums of dbn and dbn * xhat -> part.
+// A workgroup owns 16 CW columns and P.wm tiles of PW_TR rows, streamed one tile after the other: the input rows
+// (contiguous, PW_TR * K elements; the FWD prologue applied as they are written) and for BWD the BN
+// input go through LDS with whole-workgroup 16-byte loads, the next tile's loads in flight while the
+// current one is computed.  Waves: CW columns of 16 times 4 / CW row groups.  A wave's MFMA takes
+// its 16 filter rows as the row operand and 16 input rows as the column operand, so a lane's
+// results are four consecutive columns of one row.  One partial row [tiles_m][ncol][2] per workgroup.
+// ------------------------------------------------------------------------------------------------
+template <typename T, int MODE, int CW, int MAXK>
+__global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
+  constexpr int VE = St<T>::VE;
+  constexpr int KS = 4 * VE;
+  constexpr int NOS = MAXK / KS;                      // K steps
+  constexpr int TR = PW_TR;
+  constexpr int NC = 16 * CW;                         // columns of the workgroup tile
+  constexpr int WR = 4 / CW;                          // wave row groups
+  constexpr int SZ = NC + VE;                         // LDS row stride of the BN-input tile
+  constexpr int NLA = TR * MAXK / VE / 256;           // 16-byte input loads per thread
+  constexpr int NLZ = (TR * NC / VE + 255) / 256;     // 16-byte BN-input loads per thread
+  __shared__ __attribute__((aligned(16))) T xs[TR * (MAXK + VE)];
+  __shared__ __attribute__((aligned(16))) T zs[MODE == MODE_BWD ? TR * SZ : 8];
+  __shared__ float2 pro_s[MODE == MODE_FWD ? MAXK : 1];
+  __shared__ float2 red[WR][NC];
+
+  const int gi = find_group(L);
+  const ConvProb& P = L.p[gi];
+  const int local = blockIdx.x - P.tile_begin;
+  const int tm = local / P.tiles_n;
+  const int tn = local - tm * P.tiles_n;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int wr = wave / CW, wc = wave % CW;
+  const int K = P.K, ncol = P.ncol;
+  const int c0 = tn * NC;
+  const int ncl = min(NC, ncol - c0);                 // columns of this tile (a multiple of 16)
+  const int m_begin = tm * (P.wm * TR);               // P.wm tiles of TR rows per workgroup
+  const int m_end = min(P.M, m_begin + P.wm * TR);
+  const int gch = K / VE;                             // 16-byte chunks per input row
+  const int SA = K + VE;                              // LDS row stride of the input tile (elements)
+  const T* __restrict__ xin = (const T*)P.in;
+  const T* __restrict__ z = (const T*)P.zsrc;
+  const bool active = wc * 16 < ncl;                  // the wave's 16 columns exist
+  const bool pro = MODE == MODE_FWD && P.pro != nullptr;
+  const bool stats = MODE == MODE_FWD ? (P.flags & EPI_STATS) != 0 : true;
+  const bool store = MODE == MODE_FWD || !(P.flags & EPI_NO_STORE);
+
+  if constexpr (MODE == MODE_FWD) {
+    if (pro)
+      for (int k = tid; k < K; k += 256) pro_s[k] = make_float2(P.pro[k], P.pro[P.Cg + k]);
+  }
+  // filter fragments (column c0 + 16 wc + r16, channels os * KS + VE * grp ..) and the BN
+  // parameters of the lane's result columns c0 + 16 wc + 4 grp + i
+  Frag<T> wf[NOS];
+  const int cl = wc * 16 + grp * 4;
+  float mu[4], is[4], sc[4], sh[4];
+  {
+    const int c = wc * 16 + r16;
+#pragma unroll
+    for (int os = 0; os < NOS; ++os) {
+      const int o0 = os * KS + VE * grp;
+      if (o0 < K && c < ncl) wf[os].from_raw(*(const uint4*)((const T*)P.wmat + (long)(c0 + c) * K + o0));
+      else wf[os].zero();
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool cv = MODE == MODE_BWD && cl + i < ncl;
+      mu[i] = cv ? P.bnst[c0 + cl + i] : 0.f;
+      is[i] = cv ? P.bnst[ncol + c0 + cl + i] : 0.f;
+      sc[i] = cv ? P.bnst[2 * ncol + c0 + cl + i] : 0.f;
+      sh[i] = cv ? P.bnst[3 * ncol + c0 + cl + i] : 0.f;
+    }
+  }
+
+  // chunk u of the input tile is row u / gch, channels VE * (u % gch); chunk u of the BN-input tile
+  // is row u / (NC / VE), columns VE * (u % (NC / VE))
+  uint4 xr[NLA], zr[NLZ];
+  auto fetch = [&](int mt) {
+#pragma unroll
+    for (int i = 0; i < NLA; ++i) {
+      const int u = i * 256 + tid;
+      const int row = u / gch;
+      xr[i] = (row < TR && mt + row < m_end) ? *(const uint4*)(xin + (long)mt * K + (long)u * VE)
+                                              : make_uint4(0, 0, 0, 0);
+    }
+    if constexpr (MODE == MODE_BWD) {
+#pragma unroll
+      for (int i = 0; i < NLZ; ++i) {
+        const int u = i * 256 + tid;
+        const int zrow = u / (NC / VE), zc = (u % (NC / VE)) * VE;
+        zr[i] = (zrow < TR && mt + zrow < m_end && zc < ncl)
+                    ? *(const uint4*)(z + (long)(mt + zrow) * ncol + c0 + zc) : make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+
+  float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
+  fetch(m_begin);
+  __syncthreads();                                    // pro_s
+  for (int mt = m_begin; mt < m_end; mt += TR) {
+#pragma unroll
+    for (int i = 0; i < NLA; ++i) {
+      const int u = i * 256 + tid;
+      const int row = u / gch;
+      if (row >= TR) continue;
+      const int ch = (u - row * gch) * VE;
+      uint4 w = xr[i];
+      if (pro && mt + row < m_end) {
+        Chunk<T> cx;
+        unpack_chunk<T>(w, cx);
+        float f[VE];
+#pragma unroll
+        for (int e = 0; e < VE; ++e) f[e] = fmaxf(fmaf(cx.v[e], pro_s[ch + e].x, pro_s[ch + e].y), 0.0f);
+        store_chunk<T>(&w, 0, f);
+      }
+      *(uint4*)(xs + row * SA + ch) = w;
+    }
+    if constexpr (MODE == MODE_BWD) {
+#pragma unroll
+      for (int i = 0; i < NLZ; ++i) {
+        const int u = i * 256 + tid;
+        const int zrow = u / (NC / VE);
+        if (zrow < TR) *(uint4*)(zs + zrow * SZ + (u % (NC / VE)) * VE) = zr[i];
+      }
+    }
+    __syncthreads();
+    if (mt + TR < m_end) fetch(mt + TR);
+    if (active) {
+#pragma unroll
+      for (int b = 0; b < CW; ++b) {
+        const int row = (wr * CW + b) * 16 + r16;
+        const int m = mt + row;
+        f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int os = 0; os < NOS; ++os) {
+          if (os * KS < K) {
+            const int o0 = os * KS + VE * grp;
+            Frag<T> xf;
+            if (o0 < K) xf.from_raw(*(const uint4*)(xs + row * SA + o0));
+            else xf.zero();
+            mma(wf[os], xf, v);
+          }
+        }
+        const bool mv = m < m_end;
+        float o[4];
+        if constexpr (MODE == MODE_FWD) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            o[i] = v[i];
+            const float vr = St<T>::rnd(v[i]);
+            if (stats && mv) {
+              s1[i] += vr;
+              s2[i] += vr * vr;
+            }
+          }
+        } else {
+          float zv[4];
+          if constexpr (sizeof(T) == 2) {
+            const uint2 u = *(const uint2*)(zs + row * SZ + cl);
+            zv[0] = __uint_as_float(u.x << 16);
+            zv[1] = __uint_as_float(u.x & 0xffff0000u);
+            zv[2] = __uint_as_float(u.y << 16);
+            zv[3] = __uint_as_float(u.y & 0xffff0000u);
+          } else {
+            const float4 u = *(const float4*)(zs + row * SZ + cl);
+            zv[0] = u.x; zv[1] = u.y; zv[2] = u.z; zv[3] = u.w;
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float d = fmaf(zv[i], sc[i], sh[i]) > 0.f ? v[i] : 0.f;
+            const float dr = St<T>::rnd(d);
+            o[i] = d;
+            s1[i] += dr;
+            s2[i] += dr * ((zv[i] - mu[i]) * is[i]);
+          }
+        }
+        if (store && mv) {
+          T* dst = (T*)P.out + (long)m * ncol + c0 + cl;
+          if constexpr (sizeof(T) == 2) {
+            *(uint2*)dst = make_uint2((uint32_t)f2bf(o[0]) | ((uint32_t)f2bf(o[1]) << 16),
+                                      (uint32_t)f2bf(o[2]) | ((uint32_t)f2bf(o[3]) << 16));
+          } else {
+            *(float4*)dst = make_float4(o[0], o[1], o[2], o[3]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (!stats) return;
+  // sum over the 16 rows of a lane group (lanes r16), then over the wave row groups in order
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      s1[i] += __shfl_xor(s1[i], o, 64);
+      s2[i] += __shfl_xor(s2[i], o, 64);
+    }
+  if (active && r16 == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wr][cl + i] = make_float2(s1[i], s2[i]);
+  }
+  __syncthreads();
+  if (tid < ncl) {
+    float a = 0.f, b = 0.f;
+#pragma unroll
+    for (int w = 0; w < WR; ++w) {
+      a += red[w][tid].x;
+      b += red[w][tid].y;
+    }
+    ((float2*)P.part)[(long)tm * ncol + c0 + tid] = make_float2(a, b);
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
 // launchers
 // ------------------------------------------------------------------------------------------------
 
@@ -1239,6 +1459,17 @@ int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int
     e = mode == MODE_FWD ? launch_conv_m<float, MODE_FWD>(L, tiles, gk, wn, wm, s)
                          : launch_conv_m<float, MODE_BWD>(L, tiles, gk, wn, wm, s);
   return e ? e : (int)hipGetLastError();
+}
+
+int launch_pw(const ConvLaunch& L, int tiles, int dtype, int mode, hipStream_t s) {
+  if (dtype == 1) {
+    if (mode == MODE_FWD) hipLaunchKernelGGL((pw_kernel<uint16_t, MODE_FWD, 1, PW_MAXK>), dim3(tiles), dim3(256), 0, s, L);
+    else hipLaunchKernelGGL((pw_kernel<uint16_t, MODE_BWD, 1, PW_MAXK>), dim3(tiles), dim3(256), 0, s, L);
+  } else {
+    if (mode == MODE_FWD) hipLaunchKernelGGL((pw_kernel<float, MODE_FWD, 1, PW_MAXK>), dim3(tiles), dim3(256), 0, s, L);
+    else hipLaunchKernelGGL((pw_kernel<float, MODE_BWD, 1, PW_MAXK>), dim3(tiles), dim3(256), 0, s, L);
+  }
+  return (int)hipGetLastError();
 }
 
 int launch_bnsum(const ConvLaunch& L, int tiles, int dtype, hipStream_t s) {

@@ -157,6 +157,26 @@ WgradGeom wgrad_geom(int Co, int K, long M) {
 }
 
 
+// Problems of the streaming pointwise kernel: narrow (16-column tiles) forward 1x1 / stride 1 /
+// pad 0 convolutions without a residual or an addend, and data gradients of such convolutions that
+// store dbn and reduce the sums of their input BN when that BN has no other consumer (K <= PW_MAXK).
+// The deferred-apply BNs' sums-only passes go to the BN-sum kernel.
+bool pw_fwd_node(const SegP& S, const NodeP& n, int es) {
+  return n.op == PNN_OP_CONV && n.k == 1 && n.stride == 1 && n.pad == 0 && n.cin % (16 / es) == 0 &&
+         n.cin <= PW_MAXK && n.res < 0 && n.dst != S.out && n.cout % 16 == 0 && conv_wn(n.cout) == 1;
+}
+bool pw_bwd_node(const SegP& S, const NodeP& n, int es) {
+  return n.op == PNN_OP_CONV && n.dgrad && n.k == 1 && n.stride == 1 && n.pad == 0 && n.bn >= 0 &&
+         !S.bns[n.bn].defer_apply && S.slots[n.src].bn_consumers.size() == 1 && n.cout % (16 / es) == 0 &&
+         n.cout <= PW_MAXK && n.cin % 16 == 0 && conv_wn(n.cin) == 1;
+}
+// 64-row tiles per streaming pointwise workgroup: 8, or 2 for short-tile segments when 8 would give
+// under SHORT_TILES_BELOW workgroups
+int pw_wm(long M, int ncol, bool short_ok) {
+  const long tiles = (M + 64 * 8 - 1) / (64 * 8) * (ncol / 16);
+  return short_ok && tiles < SHORT_TILES_BELOW ? 2 : 8;
+}
+
 pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, int es, SegP& S) {
   S.part = part;
   S.index = index;
@@ -338,12 +358,20 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
     // partial rows = tiles of the producing convolution: the forward one writing the slot, the
     // data gradient of the consumer that reduces the BN sums (the second of two)
     int kf = 1, kb = 1;
-    if (sl.producer >= 0 && S.nodes[sl.producer].op == PNN_OP_CONV) kf = S.nodes[sl.producer].k;
+    bool pwf = false, pwb = false;
+    if (sl.producer >= 0 && S.nodes[sl.producer].op == PNN_OP_CONV) {
+      kf = S.nodes[sl.producer].k;
+      pwf = pw_fwd_node(S, S.nodes[sl.producer], es);
+    }
     for (int ci : sl.bn_consumers)
-      if (!S.nodes[ci].first_of_two) kb = S.nodes[ci].k;
+      if (!S.nodes[ci].first_of_two) {
+        kb = S.nodes[ci].k;
+        pwb = pw_bwd_node(S, S.nodes[ci], es);
+      }
     const bool sh = S.short_tiles;
-    b.fwd_tiles = (int)cdiv(M, b.slot == 0 ? COLSTAT_ROWS : 64 * conv_rows_wm(kf, M, b.C, sh));
-    b.bwd_tiles = (int)cdiv(M, b.bnsum ? BNSUM_ROWS : 64 * conv_rows_wm(kb, M, b.C, sh));
+    const int pw_rows = 64 * pw_wm(M, b.C, sh);
+    b.fwd_tiles = (int)cdiv(M, b.slot == 0 ? COLSTAT_ROWS : pwf ? pw_rows : 64 * conv_rows_wm(kf, M, b.C, sh));
+    b.bwd_tiles = (int)cdiv(M, b.bnsum ? BNSUM_ROWS : pwb ? pw_rows : 64 * conv_rows_wm(kb, M, b.C, sh));
     if (b.bnact_consumer) {
       const NodeP& c = S.nodes[sl.bn_consumers[0]];
       b.bwd_tiles = (int)cdiv((long)B * c.Ho * c.Wo, BNACT_PIX);
@@ -606,6 +634,31 @@ int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode) {
   return PNN_OK;
 }
 
+// streaming pointwise problems: one grouped launch
+int fire_pw(const Ctx& c, std::vector<ConvProb>& probs, int mode) {
+  pnn_plan* plan = c.plan;
+  return grouped<ConvLaunch>(
+      probs, [](const ConvProb& p) { return p.tiles_m * p.tiles_n; },
+      [&](const ConvLaunch& L, int tiles, size_t) {
+        double fl = 0, by = 0;
+        for (int i = 0; i < L.n; ++i) {
+          fl += conv_flops(L.p[i]);
+          by += conv_bytes(L.p[i], plan->es, mode);
+        }
+        Timer t(plan, 3, c.stream);
+        int r = launch_pw(L, tiles, plan->dtype, mode, c.stream);
+        t.done(c.stream, fl, by);
+        return r;
+      });
+}
+
+void set_pw_tiles(ConvProb& p, bool short_tiles) {
+  p.wn = 1;
+  p.wm = pw_wm(p.M, p.ncol, short_tiles);
+  p.tiles_m = (int)cdiv(p.M, 64 * p.wm);
+  p.tiles_n = p.ncol / 16;
+}
+
 ConvProb conv_common(const pnn_plan* plan, const NodeP& n) {
   ConvProb p;
   std::memset(&p, 0, sizeof(p));
@@ -686,7 +739,7 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
   pnn_plan* plan = c.plan;
   const int B = plan->B, es = plan->es;
   {
-    std::vector<ConvProb> cv_vec, cv_gen;
+    std::vector<ConvProb> cv_vec, cv_gen, cv_pw;
     std::vector<BnActProb> ba;
     std::vector<MaxPool3Prob> mp;
     std::vector<ColRedProb> fw;
@@ -713,8 +766,13 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
           p.P = n.Ho; p.Q = n.Wo; p.ncol = n.cout;
           p.M = B * n.Ho * n.Wo;
           p.K = n.k * n.k * n.cin;
-          set_tiles(p, S.short_tiles);
-          (n.cin % (16 / es) == 0 ? cv_vec : cv_gen).push_back(p);
+          if (pw_fwd_node(S, n, es)) {
+            set_pw_tiles(p, S.short_tiles);
+            cv_pw.push_back(p);
+          } else {
+            set_tiles(p, S.short_tiles);
+            (n.cin % (16 / es) == 0 ? cv_vec : cv_gen).push_back(p);
+          }
         } else if (n.op == PNN_OP_BNACT) {
           BnActProb p;
           std::memset(&p, 0, sizeof(p));
@@ -744,6 +802,7 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
     int e;
     if ((e = fire_conv(c, cv_vec, MODE_FWD))) return e;
     if ((e = fire_conv(c, cv_gen, MODE_FWD))) return e;
+    if ((e = fire_pw(c, cv_pw, MODE_FWD))) return e;
     e = grouped<BnActLaunch>(
         ba, [](const BnActProb& p) { return (int)cdiv(p.n_out, BNACT_PIX); },
         [&](const BnActLaunch& Lx, int tiles, size_t) { return launch_bnact_fwd(Lx, tiles, plan->dtype, c.stream); });
@@ -960,7 +1019,7 @@ int run_bwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
     pending = std::move(red);
     // D + E: data gradients (first of two BN consumers, then the rest) and bnact backward
     for (int phase = 0; phase < 2; ++phase) {
-      std::vector<ConvProb> dg, bs;
+      std::vector<ConvProb> dg, bs, pw;
       std::vector<BnActProb> ba;
       for (size_t i = 0; i < segs.size(); ++i) {
         const SegP& S = *segs[i];
@@ -1000,6 +1059,15 @@ int run_bwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
                 bs.push_back(p);
                 continue;
               }
+              if (pw_bwd_node(S, n, plan->es)) {   // narrow: the streaming pointwise kernel
+                p.out = c.scratch + S.scr_base + b.dbn_off;
+                p.zsrc = slot_ptr(c, S, P, n.src);
+                p.bnst = stats_ptr(c, S, n.bn);
+                p.part = part_ptr(c, S, n.bn);
+                set_pw_tiles(p, S.short_tiles);
+                pw.push_back(p);
+                continue;
+              }
               p.out = b.defer_apply ? nullptr : c.scratch + S.scr_base + b.dbn_off;
               p.zsrc = slot_ptr(c, S, P, n.src);
               p.bnst = stats_ptr(c, S, n.bn);
@@ -1025,11 +1093,13 @@ int run_bwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
             double by = 0;
             for (int j = 0; j < Lx.n; ++j)
               by += (double)Lx.p[j].M * (Lx.p[j].K + Lx.p[j].ncol) * plan->es;
-            Timer t(plan, 1, c.stream);
+            Timer t(plan, 3, c.stream);
             int r = launch_bnsum(Lx, tiles, plan->dtype, c.stream);
             t.done(c.stream, 0, by);
             return r;
           });
+      if (e) return e;
+      e = fire_pw(c, pw, MODE_BWD);
       if (e) return e;
       e = grouped<BnActLaunch>(
           ba, [](const BnActProb& p) { return (int)cdiv(p.n_out, BNACT_PIX); },
@@ -1749,7 +1819,7 @@ pnn_status pnn_set_streams(pnn_plan* plan, int streams) {
 
 pnn_status pnn_timing_enable(pnn_plan* plan, int family) {
   if (plan == nullptr) return PNN_ERR_NULL;
-  if (family < 0 || family > 2) return PNN_ERR_INDEX;
+  if (family < 0 || family > 3) return PNN_ERR_INDEX;
   plan->timing_family = family;
   if (family != 0 && plan->ev.empty()) {
     plan->ev.resize(16384);

@@ -234,6 +234,11 @@ int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int
 // filter taps (Cg a multiple of the chunk), or pointwise (1x1 / stride 1 / pad 0: input row m)
 enum { WG_GEN = 0, WG_VEC = 1, WG_PW = 2 };
 int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, int gather, hipStream_t s);
+// Streaming pointwise convolution of narrow problems (1x1 / stride 1 / pad 0, ncol % 32 != 0,
+// K <= PW_MAXK): FWD with an optional BN prologue and EPI_STATS (no residual or addend); BWD with
+// EPI_BN_MASK.  16-column workgroup tiles; wm = tiles of PW_TR rows per workgroup;
+// tiles_m = ceil(M / (PW_TR wm)), tiles_n = ncol / 16.
+int launch_pw(const ConvLaunch& L, int tiles, int dtype, int mode, hipStream_t s);
 // BN backward sums of a 1x1 convolution's input BN (EPI_BN_MASK | EPI_NO_STORE problems):
 // tiles_m = ceil(M / BNSUM_ROWS), tiles_n = ceil(ncol / 64); K <= BNSUM_MAXK
 int launch_bnsum(const ConvLaunch& L, int tiles, int dtype, hipStream_t s);
@@ -273,6 +278,8 @@ inline int conv_rows_wm(int k, long M, int ncol, bool short_ok) {
 }
 constexpr int ELT_TILE = 2048;     // elements per workgroup of elementwise kernels
 constexpr int PNN_MAX_CHAINS = 4;  // streams the fine forward / backward may spread its segment groups over
+constexpr int PW_TR = 64;          // rows per LDS tile of the streaming pointwise kernel
+constexpr int PW_MAXK = 64;        // largest K of a streaming pointwise problem
 constexpr int BNSUM_ROWS = 512;    // rows per BN-sum workgroup
 constexpr int BNSUM_MAXK = 64;     // gradient channels of a BN-sum problem
 constexpr int BNSUM_TR = 64;       // rows per LDS tile of bnsum_kernel
