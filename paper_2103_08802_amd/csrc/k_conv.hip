@@ -183,6 +183,11 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
   }
 
   const float r_cpp = 1.0f / cpp, r_img = 1.0f / img_px, r_qh = 1.0f / QH;
+  // one image per tile and a power-of-two chunk count per pixel (the usual case): shifts for the
+  // chunk / pixel split and 32-bit offsets from the image's first element
+  const int cpp_l2 = P.cg_log2 - (VE == 8 ? 3 : 2);
+  const bool fast = nimg == 1 && cpp_l2 >= 0 && (long)P.H * P.W * P.Cg < (1L << 31);
+  const T* img0 = (const T*)P.in + (long)n_first * P.H * P.W * P.Cg;
   for (int base = 0; base < total; base += 256 * NL) {
     uint4 v[NL];
     int off[NL], cv[NL];
@@ -190,6 +195,18 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
 #pragma unroll
     for (int u = 0; u < NL; ++u) {
       const int idx = base + u * 256 + tid;
+      if (fast) {
+        const int ch = idx & (cpp - 1), pix = idx >> cpp_l2;
+        int y, x;
+        divmod_small(pix, QH, r_qh, y, x);
+        const int ih = p0 - 1 + y, iw = x - 1;
+        ok[u] = idx < total && (unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W;
+        off[u] = idx < total ? pix * PS + ch * VE : -1;
+        cv[u] = ch * VE;
+        const int g = ok[u] ? ((ih * P.W + iw) << P.cg_log2) + ch * VE : 0;
+        v[u] = *(const uint4*)(img0 + g);
+        continue;
+      }
       int pix, ch, i, rem, y, x;
       divmod_small(idx, cpp, r_cpp, pix, ch);
       if (nimg > 1) divmod_small(pix, img_px, r_img, i, rem);
@@ -222,7 +239,7 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
     }
   }
 
-  int rb[NT];
+  int rb[NT];                                  // LDS element offset of the sub-tile row's pixel
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     const int lm = (rg * NT + t) * 16 + r16;
@@ -230,7 +247,7 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
     const int rem = lm - i * R * P.Q;
     const int pl = div_l2(rem, P.Q, P.q_log2);
     const int ql = rem - pl * P.Q;
-    rb[t] = (i * RH + pl) * QH + ql;
+    rb[t] = ((i * RH + pl) * QH + ql) * PS;
   }
   __syncthreads();
   before_compute();                           // the epilogue's early loads overlap the K loop
@@ -244,11 +261,11 @@ __device__ __forceinline__ void conv_halo(const ConvProb& P, const float2* pro, 
       const int c0 = k0 - tap * P.Cg;
       int r, q;
       tap_rs(tap, 3, r, q);
-      const int toff = (MODE == MODE_FWD) ? (r * QH + q) : ((2 - r) * QH + (2 - q));
+      const int toff = ((MODE == MODE_FWD) ? (r * QH + q) : ((2 - r) * QH + (2 - q))) * PS + c0;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         Frag<T> a;
-        a.from_raw(*(const uint4*)(halo + (rb[t] + toff) * PS + c0));
+        a.from_raw(*(const uint4*)(halo + rb[t] + toff));
         mma(a, bq[s], acc[t / WN][t % WN]);
       }
     }
