@@ -258,3 +258,31 @@ def test_parareal_bwd_equals_separate_calls(idx, batch, streams):
     for run in out[1:]:
         for a, b in zip(out[0], run):
             assert torch.equal(a, b)
+
+
+@pytest.mark.gpu
+def test_bench_configuration_full_size():
+    """The launch configuration bench.py times (4 streams, coarse chain overlapped with the fine
+    backward) at the full ResNet-1001 N=16 batch-128 workload gives bit-identical loss, logits and
+    every parameter and input gradient to one stream with the separate calls (the path the
+    node-level parity checks run at full size)."""
+    import torch
+    from paper_2103_08802_amd import binding as B
+    from paper_2103_08802_amd.step import ParaRealGPU
+    net = S.config(3)
+    x, labels, params = S.make_all(net)
+    out = []
+    for streams, overlap in ((1, False), (4, True)):
+        g = ParaRealGPU(net, params)
+        B.pnn_set_streams(g.plan, streams)
+        g.overlap_bwd = overlap
+        g.load_input(x, labels)
+        g.forward()
+        g.backward()
+        torch.cuda.synchronize()
+        out.append([t.clone() for t in [g.loss, g.logits, g.deps] + g.ddelta + g.dphi + g.deta + g.dx])
+        del g
+        torch.cuda.empty_cache()
+    assert torch.isfinite(out[0][0]).all()
+    for a, b in zip(out[0], out[1]):
+        assert torch.equal(a, b)
