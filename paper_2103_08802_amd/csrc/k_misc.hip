@@ -408,22 +408,51 @@ __global__ __launch_bounds__(256) void transpose_kernel(const TransposeLaunch L)
   }
 }
 
-// out = a - b (rounded to storage); optional per-tile partial of sum(out^2)
+// out = a - b (rounded to storage); optional per-tile partial of sum(out^2).  SUB_TILE elements per
+// workgroup; a whole tile goes as 16-byte chunks with every load issued before the first store, a
+// ragged last tile element by element.
 template <typename T>
 __global__ __launch_bounds__(256) void sub_kernel(const AxpyLaunch L) {
+  constexpr int VE = St<T>::VE;
+  constexpr int NCH = SUB_TILE / (256 * VE);          // chunks per thread
   __shared__ float red[4];
   const int gi = find_group(L);
   const AxpyProb& P = L.p[gi];
   const int tile = blockIdx.x - P.tile_begin;
-  const long base = (long)tile * ELT_TILE;
+  const long base = (long)tile * SUB_TILE;
   float sq = 0.f;
-  for (int t = threadIdx.x; t < ELT_TILE; t += 256) {
-    const long i = base + t;
-    if (i >= P.n) break;
-    const float v = St<T>::ld(P.a, i) - St<T>::ld(P.b, i);
-    St<T>::st(P.out, i, v);
-    const float vr = St<T>::rnd(v);
-    sq += vr * vr;
+  if (base + SUB_TILE <= P.n) {
+    uint4 ua[NCH], ub[NCH];
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) {
+      const long i = base + (long)(k * 256 + threadIdx.x) * VE;
+      ua[k] = *(const uint4*)((const T*)P.a + i);
+      ub[k] = *(const uint4*)((const T*)P.b + i);
+    }
+#pragma unroll
+    for (int k = 0; k < NCH; ++k) {
+      const long i = base + (long)(k * 256 + threadIdx.x) * VE;
+      Chunk<T> ca, cb;
+      unpack_chunk<T>(ua[k], ca);
+      unpack_chunk<T>(ub[k], cb);
+      float v[VE];
+#pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        v[e] = ca.v[e] - cb.v[e];
+        const float vr = St<T>::rnd(v[e]);
+        sq += vr * vr;
+      }
+      store_chunk<T>(P.out, i, v);
+    }
+  } else {
+    for (int t = threadIdx.x; t < SUB_TILE; t += 256) {
+      const long i = base + t;
+      if (i >= P.n) break;
+      const float v = St<T>::ld(P.a, i) - St<T>::ld(P.b, i);
+      St<T>::st(P.out, i, v);
+      const float vr = St<T>::rnd(v);
+      sq += vr * vr;
+    }
   }
   if (P.sq_part != nullptr) {
     sq = wave_sum(sq);

@@ -1358,7 +1358,7 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
   p->head_bytes = (size_t)p->B * (yo.C + p->classes + 1) * 4;
   sc = align256(sc + p->head_bytes);
   long sqt = 0;
-  for (int j = 0; j + 1 < N; ++j) sqt += cdiv(p->fine[j].slots[p->fine[j].out].elems, ELT_TILE);
+  for (int j = 0; j + 1 < N; ++j) sqt += cdiv(p->fine[j].slots[p->fine[j].out].elems, SUB_TILE);
   p->sq_off = sc;
   p->sq_bytes = (size_t)sqt * 4;
   sc = align256(sc + p->sq_bytes);
@@ -1473,17 +1473,17 @@ pnn_status parareal_combine_fwd(pnn_plan* plan, const void* const* y, const void
     p.out = r[j];
     p.n = plan->fine[j].slots[plan->fine[j].out].elems;
     p.sq_part = sq ? sq + off : nullptr;
-    off += cdiv(p.n, ELT_TILE);
+    off += cdiv(p.n, SUB_TILE);
     pr.push_back(p);
   }
   int e = grouped<AxpyLaunch>(
-      pr, [](const AxpyProb& p) { return (int)cdiv(p.n, ELT_TILE); },
+      pr, [](const AxpyProb& p) { return (int)cdiv(p.n, SUB_TILE); },
       [&](const AxpyLaunch& L, int tiles, size_t) { return launch_sub(L, tiles, plan->dtype, s); });
   if (e) return e;
   if (sq) {
     off = 0;
     for (int j = 0; j + 1 < plan->N; ++j) {
-      const int t = (int)cdiv(pr[j].n, ELT_TILE);
+      const int t = (int)cdiv(pr[j].n, SUB_TILE);
       if (launch_sumsq(sq + off, t, rnorm2 + j, s)) return PNN_ERR_HIP;
       off += t;
     }
@@ -1750,7 +1750,7 @@ pnn_status parareal_combine_bwd(pnn_plan* plan, void* const* dx, const void* con
   }
   hipStream_t s = (hipStream_t)stream;
   return grouped<AxpyLaunch>(
-      pr, [](const AxpyProb& p) { return (int)cdiv(p.n, ELT_TILE); },
+      pr, [](const AxpyProb& p) { return (int)cdiv(p.n, SUB_TILE); },
       [&](const AxpyLaunch& L, int tiles, size_t) { return launch_sub(L, tiles, plan->dtype, s); });
 }
 

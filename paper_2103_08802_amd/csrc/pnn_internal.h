@@ -277,6 +277,7 @@ inline int conv_rows_wm(int k, long M, int ncol, bool short_ok) {
   return tiles < SHORT_TILES_BELOW ? conv_wm(wn, true) : tall;
 }
 constexpr int ELT_TILE = 2048;     // elements per workgroup of elementwise kernels
+constexpr int SUB_TILE = 8192;     // elements per workgroup of the combine (sub_kernel)
 constexpr int PNN_MAX_CHAINS = 4;  // streams the fine forward / backward may spread its segment groups over
 constexpr int PW_TR = 64;          // rows per LDS tile of the streaming pointwise kernel
 constexpr int PW_MAXK = 64;        // largest K of a streaming pointwise problem

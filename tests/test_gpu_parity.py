@@ -286,3 +286,24 @@ def test_bench_configuration_full_size():
     assert torch.isfinite(out[0][0]).all()
     for a, b in zip(out[0], out[1]):
         assert torch.equal(a, b)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("idx,batch", [(0, 4), (1, 2), (3, 4)])
+def test_combine_fwd_and_rnorm2(idx, batch):
+    """parareal_combine_fwd: r_j = y_j - x_{j+1} rounded to storage, bit for bit (eq. (rk)), and the
+    optional ||r_j||^2 equals the sum of squares of the stored r_j; whole and ragged tiles (the VGG
+    workload at batch 2 has a 4096-element interface)."""
+    import torch
+    from paper_2103_08802_amd.step import ParaRealGPU
+    net = S.config(idx, batch)
+    x, labels, params = S.make_all(net)
+    g = ParaRealGPU(net, params)
+    g.load_input(x, labels)
+    g.forward(rnorm=True)
+    torch.cuda.synchronize()
+    for j in range(net.n_sub - 1):
+        ref = (g.y[j].float() - g.x[j + 1].float()).to(g.r[j].dtype)
+        assert torch.equal(g.r[j], ref)
+        ss = float((g.r[j].double() ** 2).sum())
+        assert abs(float(g.rnorm2[j]) - ss) <= 1e-5 * max(ss, 1e-30)
