@@ -162,7 +162,8 @@ pnn_status coarse_fwd(pnn_plan* plan, int j, const void* rt_j, const void* eta_j
 /* Postprocessing h and the loss, forward and backward (Alg. para3, first line): logits =
  * mean_{h,w}(ytilde) W^T + b (eps = [W (classes x C) | b (classes)] float), loss = mean softmax
  * cross-entropy over the batch.  Writes logits[B][classes] (float, nullable), *loss (float,
- * device), D_N = dL/dytilde (X_N shaped) and deps = [dW | db] (float). labels: int32[B]. */
+ * device), D_N = dL/dytilde (X_N shaped) and deps = [dW | db] (float). labels: int32[B]; a label
+ * outside [0, classes) makes that sample's loss term, and so *loss, NaN. */
 pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps,
                             const int32_t* labels, float* logits, float* loss, void* D_N,
                             float* deps, void* scratch, void* stream);

@@ -1076,12 +1076,12 @@ __global__ __launch_bounds__(256) void wgrad3_kernel(const WgradLaunch L) {
 // BN backward sums of a 1x1 convolution's input BN without forming its data gradient in HBM:
 // per row m and column c, v = sum_o g[m][o] W[o][c] (transposed filter wmat[c][o]), dbn =
 // rnd(v * [ReLU(BN(z)) > 0]), sums of dbn and dbn * xhat.  A workgroup owns 64 columns and
-// BNSUM_ROWS rows and streams them in tiles of BNSUM_TR rows: g (contiguous, BNSUM_TR * K
+// P.wm * BNSUM_TR rows and streams them in tiles of BNSUM_TR rows: g (contiguous, BNSUM_TR * K
 // elements) and z (BNSUM_TR rows of 64 columns) go through LDS with whole-workgroup 16-byte loads,
 // the next tile's loads in flight while the current one is computed.  Wave w owns columns
 // [16 w, 16 w + 16); its MFMA takes the filter as the row operand and 16 gradient rows as the
 // column operand, so a lane's results are four consecutive columns of one row.  One partial row
-// [rows / BNSUM_ROWS][ncol][2] per workgroup; nothing else is stored.
+// [tiles_m][ncol][2] per workgroup; nothing else is stored.
 // ------------------------------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void bnsum_kernel(const ConvLaunch L) {
@@ -1105,8 +1105,8 @@ __global__ __launch_bounds__(256) void bnsum_kernel(const ConvLaunch L) {
   const int K = P.K, ncol = P.ncol;
   const int c0 = tn * 64;
   const int ncl = min(64, ncol - c0);                 // columns of this tile (16, 32, 48 or 64)
-  const int m_begin = tm * BNSUM_ROWS;
-  const int m_end = min(P.M, m_begin + BNSUM_ROWS);
+  const int m_begin = tm * (P.wm * TR);
+  const int m_end = min(P.M, m_begin + P.wm * TR);
   const int gch = K / VE;                             // 16-byte chunks per gradient row
   const T* __restrict__ g = (const T*)P.in;
   const T* __restrict__ z = (const T*)P.zsrc;

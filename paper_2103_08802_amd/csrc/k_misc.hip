@@ -361,50 +361,74 @@ __global__ __launch_bounds__(256) void bnact_bwd_kernel(const BnActLaunch L) {
   }
 }
 
-// 3x3 / stride 2 / pad 1 max pool (preprocessing operators C^j, Sec. 4.1.1 and 4.2.1)
+// 3x3 / stride 2 / pad 1 max pool (preprocessing operators C^j, Sec. 4.1.1 and 4.2.1).  Each thread
+// computes P.ve consecutive outputs of one pixel: a 16-byte chunk of channels (P.ve = elements per
+// chunk; the host checks the channel count and alignment), or one element (P.ve = 1).
 template <typename T>
 __global__ __launch_bounds__(256) void maxpool3_kernel(const MaxPool3Launch L) {
+  constexpr int VE = St<T>::VE;
   const int gi = find_group(L);
   const MaxPool3Prob& P = L.p[gi];
   const long n_out = (long)P.B * P.Ho * P.Wo * P.C;
-  const long base = (long)(blockIdx.x - P.tile_begin) * ELT_TILE;
-  for (int t = threadIdx.x; t < ELT_TILE; t += 256) {
-    const long i = base + t;
-    if (i >= n_out) break;
-    const int c = (int)(i % P.C);
-    const long px = i / P.C;
-    const int q = (int)(px % P.Wo);
-    const int p = (int)((px / P.Wo) % P.Ho);
-    const int n = (int)(px / ((long)P.Wo * P.Ho));
-    float m = -INFINITY;
-    for (int a = 0; a < 3; ++a) {
-      const int ih = 2 * p + a - 1;
-      if (ih < 0 || ih >= P.H) continue;
-      for (int b = 0; b < 3; ++b) {
-        const int iw = 2 * q + b - 1;
-        if (iw < 0 || iw >= P.W) continue;
-        m = fmaxf(m, St<T>::ld(P.x, (((long)n * P.H + ih) * P.W + iw) * P.C + c));
+  const bool vec = P.ve == VE;
+  const long i = ((long)(blockIdx.x - P.tile_begin) * 256 + threadIdx.x) * P.ve;
+  if (i >= n_out) return;
+  const int c = (int)(i % P.C);
+  const long px = i / P.C;
+  const int q = (int)(px % P.Wo);
+  const long np = px / P.Wo;
+  const int p = (int)(np % P.Ho);
+  const int n = (int)(np / P.Ho);
+  float m[VE];
+#pragma unroll
+  for (int v = 0; v < VE; ++v) m[v] = -INFINITY;
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+    const int ih = 2 * p + a - 1;
+#pragma unroll
+    for (int b = 0; b < 3; ++b) {
+      const int iw = 2 * q + b - 1;
+      if (ih < 0 || ih >= P.H || iw < 0 || iw >= P.W) continue;
+      const long src = (((long)n * P.H + ih) * P.W + iw) * P.C + c;
+      if (vec) {
+        Chunk<T> ch;
+        load_chunk<T>(P.x, src, ch);
+#pragma unroll
+        for (int v = 0; v < VE; ++v) m[v] = fmaxf(m[v], ch.v[v]);
+      } else {
+        m[0] = fmaxf(m[0], St<T>::ld(P.x, src));
       }
     }
-    St<T>::st(P.y, i, m);
   }
+  if (vec)
+    store_chunk<T>(P.y, i, m);
+  else
+    St<T>::st(P.y, i, m[0]);
 }
 
-// wt[c][t][o] = w[o][t][c]  (filter layout of the data-gradient convolution)
+// wt[c][t][o] = w[o][t][c]  (filter layout of the data-gradient convolution): per tap, 64 x 64
+// tiles of [o][c] through LDS so that reads and writes are both coalesced.  Tiles of a problem:
+// T * ceil(O / 64) * ceil(C / 64), tap fastest.
 template <typename T>
 __global__ __launch_bounds__(256) void transpose_kernel(const TransposeLaunch L) {
+  __shared__ T tile[64][65];
   const int gi = find_group(L);
   const TransposeProb& P = L.p[gi];
-  const long n = (long)P.O * P.T * P.C;
-  const long base = (long)(blockIdx.x - P.tile_begin) * ELT_TILE;
-  for (int t = threadIdx.x; t < ELT_TILE; t += 256) {
-    const long i = base + t;   // index into wt
-    if (i >= n) break;
-    const int o = (int)(i % P.O);
-    const long ct = i / P.O;
-    const int tp = (int)(ct % P.T);
-    const int c = (int)(ct / P.T);
-    ((T*)P.wt)[i] = ((const T*)P.w)[((long)o * P.T + tp) * P.C + c];
+  const int lt = blockIdx.x - P.tile_begin;
+  const int tp = lt % P.T;
+  const int rest = lt / P.T;
+  const int tiles_o = (P.O + 63) / 64;
+  const int o0 = (rest % tiles_o) * 64, c0 = (rest / tiles_o) * 64;
+  const T* w = (const T*)P.w;
+  T* wt = (T*)P.wt;
+  for (int k = threadIdx.x; k < 64 * 64; k += 256) {
+    const int r = k >> 6, cc = k & 63;       // read w[o0 + r][tp][c0 + cc]
+    if (o0 + r < P.O && c0 + cc < P.C) tile[r][cc] = w[((long)(o0 + r) * P.T + tp) * P.C + c0 + cc];
+  }
+  __syncthreads();
+  for (int k = threadIdx.x; k < 64 * 64; k += 256) {
+    const int r = k >> 6, oo = k & 63;       // write wt[c0 + r][tp][o0 + oo]
+    if (c0 + r < P.C && o0 + oo < P.O) wt[((long)(c0 + r) * P.T + tp) * P.O + o0 + oo] = tile[oo][r];
   }
 }
 
@@ -472,82 +496,169 @@ __global__ void sumsq_kernel(const float* part, int n, float* out) {
 
 // ------------------------------------------------------------------------------------------------
 // head h: logits = mean_{hw}(ytilde) W^T + b, softmax cross-entropy (mean over the batch), and
-// D_N = dL/dytilde.  Kernel 1: one workgroup per sample.  Kernel 2: dW, db, loss (fixed order).
+// D_N = dL/dytilde.  Kernel 1: one workgroup per sample.  Kernel 2: dW, db, loss.  Every sum runs
+// in an order fixed by the shapes alone, so repeated calls give identical bits.
 // scratch: pooled [B][C], dlogits [B][K], loss_n [B]
 // ------------------------------------------------------------------------------------------------
+// G > 0: 16-byte chunks (C a multiple of the chunk), the pixels split over G row groups, each
+// summing its pixels into part[g][C]; G = 0: one element per load, one row group.
 template <typename T>
 __global__ __launch_bounds__(256) void head_sample_kernel(const void* yt, const float* eps,
                                                           const int32_t* labels, float* logits,
                                                           void* D_N, float* scratch, int B, int HW,
-                                                          int C, int K) {
-  extern __shared__ float sh[];  // pooled [C], z [K], dpooled [C]
+                                                          int C, int K, int G) {
+  extern __shared__ float sh[];  // pooled [C], z (then dlogits) [K], part [G][C] when G > 1
+  constexpr int VE = St<T>::VE;
   float* pooled = sh;
   float* z = sh + C;
-  __shared__ float red[2];
-  const int n = blockIdx.x;
+  float* part = G > 1 ? z + K : pooled;
+  __shared__ float red[1];
+  const int n = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const float* W = eps;
   const float* bias = eps + (long)K * C;
-  for (int c = threadIdx.x; c < C; c += 256) {
-    float s = 0.f;
-    for (int h = 0; h < HW; ++h) s += St<T>::ld(yt, ((long)n * HW + h) * C + c);
-    pooled[c] = s / (float)HW;
+  const long base = (long)n * HW * C;
+  const int GG = G > 0 ? G : 1;
+  if (G > 0) {
+    const int nch = C / VE;
+    for (int i = t; i < G * nch; i += 256) {
+      const int q = i % nch, g = i / nch;
+      float acc[VE];
+#pragma unroll
+      for (int v = 0; v < VE; ++v) acc[v] = 0.f;
+#pragma unroll 8
+      for (int h = g; h < HW; h += G) {
+        Chunk<T> ch;
+        load_chunk<T>(yt, base + (long)h * C + q * VE, ch);
+#pragma unroll
+        for (int v = 0; v < VE; ++v) acc[v] += ch.v[v];
+      }
+#pragma unroll
+      for (int v = 0; v < VE; ++v) part[g * C + q * VE + v] = acc[v];
+    }
+  } else {
+    for (int c = t; c < C; c += 256) {
+      float acc = 0.f;
+      for (int h = 0; h < HW; ++h) acc += St<T>::ld(yt, base + (long)h * C + c);
+      part[c] = acc;
+    }
+  }
+  __syncthreads();
+  for (int c = t; c < C; c += 256) {
+    float acc = 0.f;
+    for (int g = 0; g < GG; ++g) acc += part[g * C + c];
+    pooled[c] = acc / (float)HW;
     scratch[(long)n * C + c] = pooled[c];
   }
   __syncthreads();
-  for (int k = threadIdx.x; k < K; k += 256) {
-    float s = bias[k];
-    for (int c = 0; c < C; ++c) s += W[(long)k * C + c] * pooled[c];
-    z[k] = s;
-    if (logits) logits[(long)n * K + k] = s;
+  // logits: wave w takes the classes 8 w .. 8 w + 7 (mod 32), its lanes stride over the channels
+  for (int k0 = 8 * wave; k0 < K; k0 += 32) {
+    float acc[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc[u] = 0.f;
+#pragma unroll 4
+    for (int c = lane; c < C; c += 64) {
+      const float pc = pooled[c];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (k0 + u < K) acc[u] += W[(long)(k0 + u) * C + c] * pc;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) acc[u] += __shfl_xor(acc[u], o);
+    if (lane == 0)
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (k0 + u < K) {
+          z[k0 + u] = acc[u] + bias[k0 + u];
+          if (logits) logits[(long)n * K + k0 + u] = acc[u] + bias[k0 + u];
+        }
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (wave == 0) {  // log-sum-exp, the exponentials summed in double
     float mx = -INFINITY;
-    for (int k = 0; k < K; ++k) mx = fmaxf(mx, z[k]);
+    for (int k = lane; k < K; k += 64) mx = fmaxf(mx, z[k]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
     double se = 0.0;
-    for (int k = 0; k < K; ++k) se += exp((double)(z[k] - mx));
-    red[0] = mx + (float)log(se);
+    for (int k = lane; k < K; k += 64) se += exp((double)(z[k] - mx));
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) se += __shfl_xor(se, o);
+    if (lane == 0) red[0] = mx + (float)log(se);
   }
   __syncthreads();
   const float lse = red[0];
   const int lab = labels[n];
+  const bool lab_ok = lab >= 0 && lab < K;  // a label outside [0, K) gives a NaN loss
+  if (t == 0) scratch[(long)B * C + (long)B * K + n] = lab_ok ? lse - z[lab] : NAN;
+  __syncthreads();
   float* dlog = scratch + (long)B * C;
-  for (int k = threadIdx.x; k < K; k += 256) {
-    const float pk = expf(z[k] - lse);
-    const float d = (pk - (k == lab ? 1.f : 0.f)) / (float)B;
+  for (int k = t; k < K; k += 256) {
+    const float d = (expf(z[k] - lse) - (k == lab ? 1.f : 0.f)) / (float)B;
+    z[k] = d;
     dlog[(long)n * K + k] = d;
   }
-  if (threadIdx.x == 0) scratch[(long)B * C + (long)B * K + n] = lse - z[lab];
   __syncthreads();
-  for (int c = threadIdx.x; c < C; c += 256) {
-    float s = 0.f;
-    for (int k = 0; k < K; ++k) s += dlog[(long)n * K + k] * W[(long)k * C + c];
-    const float d = s / (float)HW;
-    for (int h = 0; h < HW; ++h) St<T>::st(D_N, ((long)n * HW + h) * C + c, d);
+  // D_N[n, h, c] = (sum_k dlogits[k] W[k, c]) / HW for every pixel h: per channel once (into the
+  // pooled array, no longer needed), then stored over the pixels
+  for (int c = t; c < C; c += 256) {
+    float acc = 0.f;
+#pragma unroll 32
+    for (int k = 0; k < K; ++k) acc += z[k] * W[(long)k * C + c];
+    pooled[c] = acc / (float)HW;
+  }
+  __syncthreads();
+  if (G > 0) {
+    const int nch = C / VE;
+    for (int i = t; i < G * nch; i += 256) {
+      const int q = i % nch, g = i / nch;
+      float d[VE];
+#pragma unroll
+      for (int v = 0; v < VE; ++v) d[v] = pooled[q * VE + v];
+      for (int h = g; h < HW; h += G) store_chunk<T>(D_N, base + (long)h * C + q * VE, d);
+    }
+  } else {
+    for (int c = t; c < C; c += 256) {
+      const float d = pooled[c];
+      for (int h = 0; h < HW; ++h) St<T>::st(D_N, base + (long)h * C + c, d);
+    }
   }
 }
 
+// 64 outputs of [dW | db | loss] per workgroup; wave w sums the samples of its quarter of the
+// batch, the four partial sums are added in wave order.
 __global__ __launch_bounds__(256) void head_reduce_kernel(const float* scratch, float* deps,
                                                           float* loss, int B, int C, int K) {
+  __shared__ float rs[4][64];
+  __shared__ double rl[4];
   const float* pooled = scratch;
   const float* dlog = scratch + (long)B * C;
+  const float* ln = dlog + (long)B * K;
   const long nW = (long)K * C;
-  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const long i = (long)blockIdx.x * 64 + lane;
+  const int nb = (B + 3) / 4, n0 = wave * nb, n1 = min(B, n0 + nb);
+  float acc = 0.f;
   if (i < nW) {
     const int k = (int)(i / C), c = (int)(i % C);
-    float s = 0.f;
-    for (int n = 0; n < B; ++n) s += dlog[(long)n * K + k] * pooled[(long)n * C + c];
-    deps[i] = s;
+#pragma unroll 16
+    for (int n = n0; n < n1; ++n) acc += dlog[(long)n * K + k] * pooled[(long)n * C + c];
   } else if (i < nW + K) {
     const int k = (int)(i - nW);
-    float s = 0.f;
-    for (int n = 0; n < B; ++n) s += dlog[(long)n * K + k];
-    deps[i] = s;
+#pragma unroll 8
+    for (int n = n0; n < n1; ++n) acc += dlog[(long)n * K + k];
   } else if (i == nW + K) {
-    const float* ln = scratch + (long)B * C + (long)B * K;
-    double s = 0.0;
-    for (int n = 0; n < B; ++n) s += ln[n];
-    *loss = (float)(s / (double)B);
+    double sl = 0.0;
+    for (int n = n0; n < n1; ++n) sl += ln[n];
+    rl[wave] = sl;
+  }
+  rs[wave][lane] = acc;
+  __syncthreads();
+  if (wave == 0) {
+    if (i < nW + K)
+      deps[i] = ((rs[0][lane] + rs[1][lane]) + rs[2][lane]) + rs[3][lane];
+    else if (i == nW + K)
+      *loss = (float)((((rl[0] + rl[1]) + rl[2]) + rl[3]) / (double)B);
   }
 }
 
@@ -599,17 +710,24 @@ int launch_sumsq(const float* part, int n, float* out, hipStream_t s) {
 int launch_head(const void* yt, const float* eps, const int32_t* labels, float* logits, float* loss,
                 void* D_N, float* deps, float* scratch, int B, int HW, int C, int K, int dtype,
                 hipStream_t s) {
-  const size_t shm = sizeof(float) * (size_t)(C + K);
+  const int es = dtype == 1 ? 2 : 4, ve = 16 / es;
+  const bool vec = C % ve == 0 && ((uintptr_t)yt % 16) == 0 && ((uintptr_t)D_N % 16) == 0;
+  int G = 0;
+  if (vec) {
+    const int nch = C / ve;
+    G = nch >= 256 ? 1 : std::max(1, std::min(256 / nch, HW));
+  }
+  const size_t shm = sizeof(float) * ((size_t)C + K + (G > 1 ? (size_t)G * C : 0));
   if (dtype == 1)
     hipLaunchKernelGGL(head_sample_kernel<uint16_t>, dim3(B), dim3(256), shm, s, yt, eps, labels,
-                       logits, D_N, scratch, B, HW, C, K);
+                       logits, D_N, scratch, B, HW, C, K, G);
   else
     hipLaunchKernelGGL(head_sample_kernel<float>, dim3(B), dim3(256), shm, s, yt, eps, labels,
-                       logits, D_N, scratch, B, HW, C, K);
+                       logits, D_N, scratch, B, HW, C, K, G);
   int e = (int)hipGetLastError();
   if (e) return e;
   const long n = (long)K * C + K + 1;
-  hipLaunchKernelGGL(head_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+  hipLaunchKernelGGL(head_reduce_kernel, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, s,
                      scratch, deps, loss, B, C, K);
   return (int)hipGetLastError();
 }

@@ -172,6 +172,15 @@ bool pw_bwd_node(const SegP& S, const NodeP& n, int es) {
 }
 // 64-row tiles per streaming pointwise workgroup: 8, or 2 for short-tile segments when 8 would give
 // under SHORT_TILES_BELOW workgroups
+// bnsum_kernel rows per workgroup in tiles of BNSUM_TR: BNSUM_ROWS, or in short-tile segments
+// halved while the launch has fewer than SHORT_TILES_BELOW workgroups
+int bnsum_wm(long M, int ncol, bool short_ok) {
+  int wm = BNSUM_ROWS / BNSUM_TR;
+  if (short_ok)
+    while (wm > 1 && cdiv(M, (long)BNSUM_TR * wm) * cdiv(ncol, 64) < SHORT_TILES_BELOW) wm >>= 1;
+  return wm;
+}
+
 int pw_wm(long M, int ncol, bool short_ok) {
   const long tiles = (M + 64 * 8 - 1) / (64 * 8) * (ncol / 16);
   return short_ok && tiles < SHORT_TILES_BELOW ? 2 : 8;
@@ -371,7 +380,7 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
     const bool sh = S.short_tiles;
     const int pw_rows = 64 * pw_wm(M, b.C, sh);
     b.fwd_tiles = (int)cdiv(M, b.slot == 0 ? COLSTAT_ROWS : pwf ? pw_rows : 64 * conv_rows_wm(kf, M, b.C, sh));
-    b.bwd_tiles = (int)cdiv(M, b.bnsum ? BNSUM_ROWS : pwb ? pw_rows : 64 * conv_rows_wm(kb, M, b.C, sh));
+    b.bwd_tiles = (int)cdiv(M, b.bnsum ? BNSUM_TR * bnsum_wm(M, b.C, sh) : pwb ? pw_rows : 64 * conv_rows_wm(kb, M, b.C, sh));
     if (b.bnact_consumer) {
       const NodeP& c = S.nodes[sl.bn_consumers[0]];
       b.bwd_tiles = (int)cdiv((long)B * c.Ho * c.Wo, BNACT_PIX);
@@ -789,6 +798,8 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
           p.x = slot_ptr(c, S, P, n.src);
           p.y = slot_ptr(c, S, P, n.dst);
           p.B = B; p.H = n.H; p.W = n.W; p.C = n.cin; p.Ho = n.Ho; p.Wo = n.Wo;
+          const int ve = 16 / es;
+          p.ve = (p.C % ve == 0 && (((uintptr_t)p.x | (uintptr_t)p.y) & 15) == 0) ? ve : 1;
           mp.push_back(p);
         }
         if (so.bn >= 0) {
@@ -808,7 +819,7 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
         [&](const BnActLaunch& Lx, int tiles, size_t) { return launch_bnact_fwd(Lx, tiles, plan->dtype, c.stream); });
     if (e) return e;
     e = grouped<MaxPool3Launch>(
-        mp, [](const MaxPool3Prob& p) { return (int)cdiv((long)p.B * p.Ho * p.Wo * p.C, ELT_TILE); },
+        mp, [](const MaxPool3Prob& p) { return (int)cdiv((long)p.B * p.Ho * p.Wo * p.C, 256L * p.ve); },
         [&](const MaxPool3Launch& Lx, int tiles, size_t) { return launch_maxpool3(Lx, tiles, plan->dtype, c.stream); });
     if (e) return e;
     if (fire_colred(fw, c.stream)) return PNN_ERR_HIP;
@@ -983,7 +994,7 @@ int run_bwd_begin(const Ctx& c, const std::vector<const SegP*>& segs, const std:
       }
     }
     int e = grouped<TransposeLaunch>(
-        tp, [](const TransposeProb& p) { return (int)cdiv((long)p.O * p.T * p.C, ELT_TILE); },
+        tp, [](const TransposeProb& p) { return (int)(p.T * cdiv(p.O, 64) * cdiv(p.C, 64)); },
         [&](const TransposeLaunch& L, int tiles, size_t) { return launch_transpose(L, tiles, plan->dtype, c.stream); });
     if (e) return e;
   }
@@ -1054,7 +1065,8 @@ int run_bwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
                 p.zsrc = slot_ptr(c, S, P, n.src);
                 p.bnst = stats_ptr(c, S, n.bn);
                 p.part = part_ptr(c, S, n.bn);
-                p.tiles_m = (int)cdiv(p.M, BNSUM_ROWS);
+                p.wm = bnsum_wm(p.M, p.ncol, S.short_tiles);
+                p.tiles_m = (int)cdiv(p.M, (long)BNSUM_TR * p.wm);
                 p.tiles_n = (int)cdiv(p.ncol, 64);
                 bs.push_back(p);
                 continue;
@@ -1128,12 +1140,19 @@ int run_bwd_end(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
   return PNN_OK;
 }
 
-int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
-            bool wgrad = true) {
+// the levels and the input gradient, once run_bwd_begin's transposed filters are in place
+int run_bwd_body(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
+                 bool wgrad) {
   std::vector<ColRedProb> pending;
-  int e = run_bwd_begin(c, segs, ptrs);
+  int e = PNN_OK;
   for (int L = seg_max_level(segs); e == PNN_OK && L >= 1; --L) e = run_bwd_level(c, segs, ptrs, L, wgrad, pending);
   return e == PNN_OK ? run_bwd_end(c, segs, ptrs, pending) : e;
+}
+
+int run_bwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
+            bool wgrad = true) {
+  int e = run_bwd_begin(c, segs, ptrs);
+  return e == PNN_OK ? run_bwd_body(c, segs, ptrs, wgrad) : e;
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -1615,13 +1634,15 @@ pnn_status coarse_bwd_all(pnn_plan* plan, void* const* D, const void* const* rt,
     p.gout = D[j + 1];
     p.gin = D[j];
     if (D[j] == D[j + 1]) return PNN_ERR_SHAPE;
-    int e = run_bwd(c, {&plan->coarse[j]}, {p}, false);
-    if (e) return e;
     segs.push_back(&plan->coarse[j]);
     ptrs.push_back(p);
   }
+  // every block's transposed filters in one grouped launch, then the chain of data gradients
+  int e = run_bwd_begin(c, segs, ptrs);
+  for (size_t i = 0; e == PNN_OK && i < segs.size(); ++i) e = run_bwd_body(c, {segs[i]}, {ptrs[i]}, false);
+  if (e) return e;
   std::vector<ColRedProb> red;
-  int e = fire_wgrads(c, segs, ptrs, -1, red);
+  e = fire_wgrads(c, segs, ptrs, -1, red);
   if (e) return e;
   return fire_colred(red, c.stream) ? PNN_ERR_HIP : PNN_OK;
 }
@@ -1684,24 +1705,46 @@ pnn_status parareal_bwd(pnn_plan* plan, void* const* D, const void* const* rt, c
   std::vector<int> need(G, N - 1);
   for (int g = 0; g < G; ++g)
     for (auto* sp : ch.segs[g]) need[g] = std::min(need[g], sp->index);
-  // side streams: after the work enqueued before the call, their filter transposes (independent
-  // of the chain); group 0 runs on the call's stream after the chain
-  e = chains_wait(c, ch, 1, G);
-  std::vector<std::vector<ColRedProb>> pending(G);
-  for (int g = 0; e == PNN_OK && g < G; ++g) e = run_bwd_begin(ch.ctx[g], ch.segs[g], ch.ptrs[g]);
-  // the coarse chain's data gradients on the call's stream; a group starts once its D_j is out
   std::vector<const SegP*> csegs;
   std::vector<Ptrs> cptrs;
-  for (int j = N - 2; e == PNN_OK && j >= 0; --j) {
+  for (int j = N - 2; j >= 0; --j) {
     Ptrs p;
     p.in = rt[j];
     p.params = eta[j];
     p.grads = deta[j];
     p.gout = D[j + 1];
     p.gin = D[j];
-    e = run_bwd(c, {&plan->coarse[j]}, {p}, false);
     csegs.push_back(&plan->coarse[j]);
     cptrs.push_back(p);
+  }
+  // Filter transposes depend on the parameters only.  Side streams, after the work enqueued
+  // before the call: group 0's (first side stream; the call's stream waits for them after the
+  // chain), then each group's own.  The call's stream: every coarse block's in one grouped launch
+  // ahead of the chain (group 0's too when there is no side stream).
+  e = chains_wait(c, ch, 1, G);
+  hipEvent_t t0_done = nullptr;
+  if (e == PNN_OK && G > 1) {
+    Ctx t0 = ch.ctx[0];
+    t0.stream = ch.ctx[1].stream;
+    e = run_bwd_begin(t0, ch.segs[0], ch.ptrs[0]);
+    t0_done = plan->fj[plan->fj_next++ % plan->fj.size()];
+    if (e == PNN_OK && hipEventRecord(t0_done, t0.stream) != hipSuccess) e = PNN_ERR_HIP;
+  }
+  for (int g = 1; e == PNN_OK && g < G; ++g) e = run_bwd_begin(ch.ctx[g], ch.segs[g], ch.ptrs[g]);
+  if (e == PNN_OK) {
+    std::vector<const SegP*> ts = csegs;
+    std::vector<Ptrs> tp = cptrs;
+    if (G == 1) {
+      ts.insert(ts.end(), ch.segs[0].begin(), ch.segs[0].end());
+      tp.insert(tp.end(), ch.ptrs[0].begin(), ch.ptrs[0].end());
+    }
+    e = run_bwd_begin(c, ts, tp);
+  }
+  std::vector<std::vector<ColRedProb>> pending(G);
+  // the coarse chain's data gradients on the call's stream; a group starts once its D_j is out
+  for (size_t i = 0; e == PNN_OK && i < csegs.size(); ++i) {
+    const int j = N - 2 - (int)i;
+    e = run_bwd_body(c, {csegs[i]}, {cptrs[i]}, false);
     for (int g = 1; e == PNN_OK && g < G; ++g)
       if (need[g] == j) e = chains_wait(c, ch, g, g + 1);
   }
@@ -1712,6 +1755,7 @@ pnn_status parareal_bwd(pnn_plan* plan, void* const* D, const void* const* rt, c
     chain_done = plan->fj[plan->fj_next++ % plan->fj.size()];
     if (hipEventRecord(chain_done, c.stream) != hipSuccess) e = PNN_ERR_HIP;
   }
+  if (e == PNN_OK && t0_done != nullptr && hipStreamWaitEvent(c.stream, t0_done, 0) != hipSuccess) e = PNN_ERR_HIP;
   for (int L = seg_max_level(segs); e == PNN_OK && L >= 1; --L)
     for (int g = 0; e == PNN_OK && g < G; ++g)
       if (L <= seg_max_level(ch.segs[g])) e = run_bwd_level(ch.ctx[g], ch.segs[g], ch.ptrs[g], L, true, pending[g]);

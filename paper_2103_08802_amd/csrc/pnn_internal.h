@@ -167,10 +167,11 @@ struct BnActLaunch {
 };
 
 // Elementwise / small kernels.
-struct MaxPool3Prob {
+struct MaxPool3Prob {     // 256 * ve outputs per workgroup, ve per thread (1, or a 16-byte chunk)
   const void* x;
   void* y;
   int B, H, W, C, Ho, Wo;
+  int ve;
   int tile_begin;
 };
 struct MaxPool3Launch {
@@ -178,7 +179,7 @@ struct MaxPool3Launch {
   MaxPool3Prob p[PNN_MAXG];
 };
 
-struct TransposeProb {   // wt[c][r][s][o] = w[o][r][s][c]
+struct TransposeProb {   // wt[c][r][s][o] = w[o][r][s][c]; T * ceil(O / 64) * ceil(C / 64) tiles
   const void* w;
   void* wt;
   int O, T, C;           // T = k * k taps
@@ -240,7 +241,8 @@ int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, int gather, hipStre
 // tiles_m = ceil(M / (PW_TR wm)), tiles_n = ncol / 16.
 int launch_pw(const ConvLaunch& L, int tiles, int dtype, int mode, hipStream_t s);
 // BN backward sums of a 1x1 convolution's input BN (EPI_BN_MASK | EPI_NO_STORE problems):
-// tiles_m = ceil(M / BNSUM_ROWS), tiles_n = ceil(ncol / 64); K <= BNSUM_MAXK
+// wm = tiles of BNSUM_TR rows per workgroup (bnsum_wm); tiles_m = ceil(M / (BNSUM_TR wm)),
+// tiles_n = ceil(ncol / 64); K <= BNSUM_MAXK
 int launch_bnsum(const ConvLaunch& L, int tiles, int dtype, hipStream_t s);
 // 3x3 / stride 1 / pad 1 through an LDS halo tile: tiles_co = Co / 16, tiles_k = Cg / 16 blocks
 int launch_wgrad3(const WgradLaunch& L, int tiles, int dtype, hipStream_t s);
@@ -281,7 +283,7 @@ constexpr int SUB_TILE = 8192;     // elements per workgroup of the combine (sub
 constexpr int PNN_MAX_CHAINS = 4;  // streams the fine forward / backward may spread its segment groups over
 constexpr int PW_TR = 64;          // rows per LDS tile of the streaming pointwise kernel
 constexpr int PW_MAXK = 64;        // largest K of a streaming pointwise problem
-constexpr int BNSUM_ROWS = 512;    // rows per BN-sum workgroup
+constexpr int BNSUM_ROWS = 512;    // rows per BN-sum workgroup (short-tile segments: fewer, bnsum_wm)
 constexpr int BNSUM_MAXK = 64;     // gradient channels of a BN-sum problem
 constexpr int BNSUM_TR = 64;       // rows per LDS tile of bnsum_kernel
 constexpr int COLSTAT_ROWS = 128;  // rows per column-statistics workgroup

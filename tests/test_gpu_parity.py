@@ -307,3 +307,34 @@ def test_combine_fwd_and_rnorm2(idx, batch):
         assert torch.equal(g.r[j], ref)
         ss = float((g.r[j].double() ** 2).sum())
         assert abs(float(g.rnorm2[j]) - ss) <= 1e-5 * max(ss, 1e-30)
+
+
+@pytest.mark.parametrize("idx, batch", [(0, 4), (3, 3)])
+def test_head_repeatable_and_label_range(idx, batch):
+    """pnn_head_fwd_bwd: a second call on the same inputs gives the same bits (every sum of the head
+    runs in a fixed order), and a label outside [0, classes) makes the loss NaN while the other
+    samples' logits are unchanged."""
+    import torch
+    from paper_2103_08802_amd import binding as B
+    from paper_2103_08802_amd.step import ParaRealGPU
+    net = S.config(idx, batch)
+    x, labels, params = S.make_all(net)
+    g = ParaRealGPU(net, params)
+    g.load_input(x, labels)
+    g.forward()
+    torch.cuda.synchronize()
+    N = net.n_sub
+    first = [t.clone() for t in (g.loss, g.logits, g.D[N - 1], g.deps)]
+    B.pnn_head_fwd_bwd(g.plan, g.ytilde, g.eps, g.labels, g.logits, g.loss, g.D[N - 1], g.deps,
+                       g.scratch, None)
+    torch.cuda.synchronize()
+    for a, b in zip(first, (g.loss, g.logits, g.D[N - 1], g.deps)):
+        assert torch.equal(a, b)
+    assert torch.isfinite(g.loss).all()
+    bad = g.labels.clone()
+    bad[0] = net.classes
+    B.pnn_head_fwd_bwd(g.plan, g.ytilde, g.eps, bad, g.logits, g.loss, g.D[N - 1], g.deps,
+                       g.scratch, None)
+    torch.cuda.synchronize()
+    assert torch.isnan(g.loss).all()
+    assert torch.equal(g.logits, first[1])
