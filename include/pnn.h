@@ -28,10 +28,10 @@
  *     parameters, every parameter gradient, the head and the loss in float.  Arithmetic is fp32
  *     (bf16 MFMA operands with fp32 accumulation).
  *   - Entry points never allocate memory, free or synchronise.  All work is ordered on the given
- *     stream.  parareal_fine_fwd / parareal_fine_bwd may run groups of sub-networks on up to
- *     pnn_set_streams() streams: the given one and internal streams of the plan (default
- *     priority), which first wait for the work enqueued on the given stream before the call; the
- *     given stream waits for all of them before the call returns.  The first call that uses a
+ *     stream.  parareal_fine_fwd / parareal_fine_bwd / parareal_bwd may run groups of
+ *     sub-networks on up to pnn_set_streams() streams: the given one and internal streams of the
+ *     plan (default priority), which first wait for the work enqueued on the given stream before
+ *     the call; the given stream waits for all of them before the call returns.  The first call that uses a
  *     second stream creates the plan's internal streams and events (no memory);
  *     pnn_plan_destroy releases them.  Only pnn_plan_create allocates (host memory only).
  *   - Workspaces: the caller allocates one "saved" buffer (activations kept from the forward for
@@ -196,7 +196,9 @@ pnn_status parareal_fine_bwd(pnn_plan* plan, const void* const* dy, const void* 
  * coarse chain runs on the given stream, and each group of fine sub-networks (as grouped by
  * pnn_set_streams) starts on its own stream as soon as the chain has produced the last D_j it
  * needs (the chain produces D_{N-2} first and D_0 last); the coarse weight gradients follow on a
- * side stream.  Arguments as in those two calls. */
+ * side stream.  The transposed filters of the data gradients (parameters only) are formed first:
+ * the coarse blocks' on the given stream ahead of the chain, the fine groups' on the side
+ * streams.  Arguments as in those two calls. */
 pnn_status parareal_bwd(pnn_plan* plan, void* const* D, const void* const* rt, const void* const* eta,
                         float* const* deta, const void* const* x, const void* const* phi,
                         void* const* dx, float* const* dphi, const void* saved, void* scratch,
@@ -249,8 +251,9 @@ const char* pnn_status_string(pnn_status s);
 /* Number of streams (1 .. 4, default 4) over which parareal_fine_fwd / parareal_fine_bwd may run
  * their sub-networks: the sub-networks are grouped by the spatial size of their input (the
  * ResNet stage they start in), the group with the most work is halved while streams are left, and
- * each group's level-by-level launches go to a stream of its own.  1 keeps every launch on the call's stream.  Results do not depend on it (every
- * group's launches are the same; no reduction crosses groups).  PNN_ERR_INDEX outside 1 .. 4. */
+ * each group's level-by-level launches go to a stream of its own.  1 keeps every launch on the
+ * call's stream.  Results do not depend on it (every group's launches are the same; no reduction
+ * crosses groups).  PNN_ERR_INDEX outside 1 .. 4. */
 pnn_status pnn_set_streams(pnn_plan* plan, int streams);
 
 /* Per-kernel-family GPU time accounting with HIP events recorded on the call's stream around
