@@ -338,3 +338,30 @@ def test_head_repeatable_and_label_range(idx, batch):
     torch.cuda.synchronize()
     assert torch.isnan(g.loss).all()
     assert torch.equal(g.logits, first[1])
+
+
+def pooled_16ch_net(dtype, batch):
+    """Two sub-networks on a 16-channel 32x32 input, g^1 ending at 16x16: C^2 max-pools the
+    16-channel input (whole 16-byte channel chunks per thread) before its 1x1 convolution."""
+    from pnn_synth.nets import Net, _SegBuilder, _pre_pool_conv
+    ch = 16
+    img, half = (32, 32, ch), (16, 16, ch)
+    pre0 = _SegBuilder(img).done(0)
+    pre1 = _pre_pool_conv(img, half)
+    b = _SegBuilder(img)
+    z = b.conv(0, ch, 3, 2, 1, preact=True)
+    fine0 = b.done(b.conv(z, ch, 3, 1, 1, preact=True))
+    b = _SegBuilder(half)
+    z = b.conv(0, ch, 3, 1, 1, preact=True)
+    fine1 = b.done(b.conv(z, ch, 3, 1, 1, preact=True, res=0))
+    b = _SegBuilder(half)
+    coarse = [b.done(b.conv(0, ch, 3, 1, 1))]
+    return Net(f"pool16-{dtype}-b{batch}", dtype, batch, img, 10, [pre0, pre1], [fine0, fine1],
+               coarse, ch, (21, 22, 23))
+
+
+@pytest.mark.parametrize("dtype,batch,tol", [("f32", 3, 1e-4), ("bf16", 4, 2e-2)])
+def test_pooled_multichannel_input(dtype, batch, tol):
+    """C^j max-pooling a multi-channel input (the vectorised pool path; the workloads pool only the
+    3-channel image): every tensor within the fp32 / bf16 tolerance of the oracle."""
+    _assert_tol(run_net(pooled_16ch_net(dtype, batch)), tol)
