@@ -1231,6 +1231,10 @@ __global__ __launch_bounds__(256) void bnsum_kernel(const ConvLaunch L) {
 // current one is computed.  Waves: CW columns of 16 times 4 / CW row groups.  A wave's MFMA takes
 // its 16 filter rows as the row operand and 16 input rows as the column operand, so a lane's
 // results are four consecutive columns of one row.  One partial row [tiles_m][ncol][2] per workgroup.
+// BWD + EPI_PW_WGRAD (CW = 1): the same LDS tiles also give the convolution's weight gradient
+// dW[o][c] = sum_m g[m][o] ReLU(BN(z))[m][c]: wave w accumulates rows o = 16 w .. 16 w + 15 (the
+// gradient tile read column-wise as the row operand, the activated BN input as the column
+// operand) and writes them to the split-K partial row tm of out32 [tiles_m][K][ncol].
 // ------------------------------------------------------------------------------------------------
 template <typename T, int MODE, int CW, int MAXK>
 __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
@@ -1296,6 +1300,16 @@ __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
       sc[i] = cv ? P.bnst[2 * ncol + c0 + cl + i] : 0.f;
       sh[i] = cv ? P.bnst[3 * ncol + c0 + cl + i] : 0.f;
     }
+  }
+
+  // fused weight gradient: BN scale / shift of the lane's activation column c0 + r16
+  const bool wgr = MODE == MODE_BWD && CW == 1 && (P.flags & EPI_PW_WGRAD) != 0;
+  const bool wact = wgr && 16 * wave < K;
+  f32x4 dw = f32x4{0.f, 0.f, 0.f, 0.f};
+  float wsc = 0.f, wsh = 0.f;
+  if (wgr && r16 < ncl) {
+    wsc = P.bnst[2 * ncol + c0 + r16];
+    wsh = P.bnst[3 * ncol + c0 + r16];
   }
 
   // chunk u of the input tile is row u / gch, channels VE * (u % gch); chunk u of the BN-input tile
@@ -1411,7 +1425,32 @@ __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
         }
       }
     }
+    if constexpr (MODE == MODE_BWD && CW == 1) {
+      if (wact) {
+        // rows past m_end are zeros of g in the tile, so they add nothing
+#pragma unroll
+        for (int ms = 0; ms < TR / KS; ++ms) {
+          const int row0 = ms * KS + VE * grp;
+          Frag<T> gf, af;
+          lds_frag<T>(xs, row0, SA, 16 * wave, r16, gf);
+          lds_frag<T>(zs, row0, SZ, 0, r16, af);
+#pragma unroll
+          for (int e = 0; e < (int)(sizeof(af.v) / sizeof(af.v[0])); ++e) {
+            const float a = fmaxf(fmaf((float)af.v[e], wsc, wsh), 0.0f);
+            if constexpr (sizeof(T) == 2) af.v[e] = (__bf16)a;
+            else af.v[e] = a;
+          }
+          mma(gf, af, dw);
+        }
+      }
+    }
     __syncthreads();
+  }
+  if (wact && r16 < ncl) {
+    // lane (r16, grp) holds rows o = 16 wave + 4 grp + i of column c0 + r16
+    float* dst = P.out32 + (long)tm * K * ncol + c0 + r16;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dst[(long)(16 * wave + 4 * grp + i) * ncol] = dw[i];
   }
   if (!stats) return;
   // sum over the 16 rows of a lane group (lanes r16), then over the wave row groups in order

@@ -170,8 +170,6 @@ bool pw_bwd_node(const SegP& S, const NodeP& n, int es) {
          !S.bns[n.bn].defer_apply && S.slots[n.src].bn_consumers.size() == 1 && n.cout % (16 / es) == 0 &&
          n.cout <= PW_MAXK && n.cin % 16 == 0 && conv_wn(n.cin) == 1;
 }
-// 64-row tiles per streaming pointwise workgroup: 8, or 2 for short-tile segments when 8 would give
-// under SHORT_TILES_BELOW workgroups
 // bnsum_kernel rows per workgroup in tiles of BNSUM_TR: BNSUM_ROWS, or in short-tile segments
 // halved while the launch has fewer than SHORT_TILES_BELOW workgroups
 int bnsum_wm(long M, int ncol, bool short_ok) {
@@ -181,9 +179,22 @@ int bnsum_wm(long M, int ncol, bool short_ok) {
   return wm;
 }
 
+// 64-row tiles per streaming pointwise workgroup: 8, or 2 for short-tile segments when 8 would give
+// under SHORT_TILES_BELOW workgroups
 int pw_wm(long M, int ncol, bool short_ok) {
   const long tiles = (M + 64 * 8 - 1) / (64 * 8) * (ncol / 16);
   return short_ok && tiles < SHORT_TILES_BELOW ? 2 : 8;
+}
+
+// The weight gradient of a narrow pointwise data-gradient problem is formed by the same pw_kernel
+// launch (EPI_PW_WGRAD) when every output channel row is a whole 16-row MFMA tile and its split-K
+// partial rows (one per workgroup) fit the region reserved for the weight-gradient kernel's splits.
+bool pw_wgrad_fused(const SegP& S, const NodeP& n, int B, int es) {
+  if (!pw_bwd_node(S, n, es) || n.cout % 16 != 0) return false;
+  const long M = (long)B * n.Ho * n.Wo;
+  const long tiles_m = cdiv(M, (long)PW_TR * pw_wm(M, n.cin, S.short_tiles));
+  const WgradGeom g = wgrad_geom_node(n, B, es);
+  return !g.halo3 && tiles_m <= g.splits;
 }
 
 pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, int es, SegP& S) {
@@ -902,9 +913,13 @@ int fire_finalize(const Ctx& c, std::vector<ColRedProb>& fin, std::vector<BnAppl
 }
 
 // Weight gradients of the convolutions at level L (every level when L < 0) of a set of segments,
-// grouped by kernel variant; their split-K partial sums are appended to ``red`` (RED_SUM).
+// grouped by kernel variant; their split-K partial sums are appended to ``red`` (RED_SUM).  With
+// ``fused``, the convolutions whose weight gradient the narrow pointwise data-gradient launch forms
+// (pw_wgrad_fused) only get their partial region and their reduction; ``fused`` lists them with
+// that region.
+using FusedWgrad = std::vector<std::pair<const NodeP*, float*>>;
 int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs, int L,
-                std::vector<ColRedProb>& red) {
+                std::vector<ColRedProb>& red, FusedWgrad* fused = nullptr) {
   pnn_plan* plan = c.plan;
   const int B = plan->B, es = plan->es;
   char* wpart = c.wpart != nullptr ? c.wpart : c.scratch + plan->wpart_off;
@@ -931,14 +946,20 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
       p.pq_log2 = log2_or(p.P * p.Q);
       p.part = (float*)(wpart + woff);
       woff = align256(woff + (size_t)g.splits * p.Co * p.K * 4);
-      const bool vec = n.cin % (16 / es) == 0;
-      const bool pw = vec && n.k == 1 && n.stride == 1 && n.pad == 0;
-      (g.halo3 ? wg_h3 : pw ? wg_pw : vec ? wg_vec : wg_gen).push_back(p);
+      int rows = g.splits;
+      if (fused != nullptr && pw_wgrad_fused(S, n, B, es)) {
+        fused->push_back({&n, p.part});
+        rows = (int)cdiv(p.M, (long)PW_TR * pw_wm(p.M, n.cin, S.short_tiles));
+      } else {
+        const bool vec = n.cin % (16 / es) == 0;
+        const bool pw = vec && n.k == 1 && n.stride == 1 && n.pad == 0;
+        (g.halo3 ? wg_h3 : pw ? wg_pw : vec ? wg_vec : wg_gen).push_back(p);
+      }
       ColRedProb r;
       std::memset(&r, 0, sizeof(r));
       r.part = p.part;
       r.dst = (float*)(cp(P.grads) + n.gw_off);
-      r.rows = g.splits;
+      r.rows = rows;
       r.ncols = p.Co * p.K;
       r.mode = RED_SUM;
       r.rl_log2 = red_sum_rl_log2(r.rows);
@@ -1021,10 +1042,12 @@ int run_bwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
       int e = fire_finalize(c, fin, app, rec);
       if (e) return e;
     }
-    // B + C: weight gradients
+    // B + C: weight gradients (those of the narrow pointwise problems come with their data
+    // gradients below)
     std::vector<ColRedProb> red;
+    FusedWgrad fused;
     if (wgrad) {
-      int e = fire_wgrads(c, segs, ptrs, L, red);
+      int e = fire_wgrads(c, segs, ptrs, L, red, &fused);
       if (e) return e;
     }
     pending = std::move(red);
@@ -1076,6 +1099,11 @@ int run_bwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
                 p.zsrc = slot_ptr(c, S, P, n.src);
                 p.bnst = stats_ptr(c, S, n.bn);
                 p.part = part_ptr(c, S, n.bn);
+                for (const auto& f : fused)
+                  if (f.first == &n) {
+                    p.flags |= EPI_PW_WGRAD;
+                    p.out32 = f.second;
+                  }
                 set_pw_tiles(p, S.short_tiles);
                 pw.push_back(p);
                 continue;
