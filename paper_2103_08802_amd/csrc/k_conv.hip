@@ -1081,7 +1081,11 @@ __global__ __launch_bounds__(256) void wgrad3_kernel(const WgradLaunch L) {
 // the next tile's loads in flight while the current one is computed.  Wave w owns columns
 // [16 w, 16 w + 16); its MFMA takes the filter as the row operand and 16 gradient rows as the
 // column operand, so a lane's results are four consecutive columns of one row.  One partial row
-// [tiles_m][ncol][2] per workgroup; nothing else is stored.
+// [tiles_m][ncol][2] per workgroup; nothing else is stored.  EPI_PW_WGRAD: the same tiles also
+// give the convolution's weight gradient dW[o][c] = sum_m g[m][o] ReLU(BN(z))[m][c]: wave w forms
+// the columns c0 + 16 w .. c0 + 16 w + 15 of every 16-row block of o (the gradient tile read
+// column-wise as the row operand, the activated BN input as the column operand) and writes them to
+// the split-K partial row tm of out32 [tiles_m][K][ncol].
 // ------------------------------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void bnsum_kernel(const ConvLaunch L) {
@@ -1133,6 +1137,18 @@ __global__ __launch_bounds__(256) void bnsum_kernel(const ConvLaunch L) {
       sc[i] = cv ? P.bnst[2 * ncol + c0 + cl + i] : 0.f;
       sh[i] = cv ? P.bnst[3 * ncol + c0 + cl + i] : 0.f;
     }
+  }
+
+  // fused weight gradient: BN scale / shift of the lane's activation column c0 + 16 wave + r16
+  constexpr int NOB = BNSUM_MAXK / 16;                // 16-row blocks of o
+  const bool wgr = (P.flags & EPI_PW_WGRAD) != 0 && active;
+  f32x4 dw[NOB];
+#pragma unroll
+  for (int ob = 0; ob < NOB; ++ob) dw[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float wsc = 0.f, wsh = 0.f;
+  if (wgr && wave * 16 + r16 < ncl) {
+    wsc = P.bnst[2 * ncol + c0 + wave * 16 + r16];
+    wsh = P.bnst[3 * ncol + c0 + wave * 16 + r16];
   }
 
   // chunk u of the g tile is row u / gch, channels VE * (u % gch); chunk u of the z tile is row
@@ -1200,7 +1216,39 @@ __global__ __launch_bounds__(256) void bnsum_kernel(const ConvLaunch L) {
         }
       }
     }
+    if (wgr) {
+      // rows past m_end are zeros of g in the tile, so they add nothing
+#pragma unroll
+      for (int ms = 0; ms < TR / KS; ++ms) {
+        const int row0 = ms * KS + VE * grp;
+        Frag<T> af;
+        lds_frag<T>(zs, row0, ST, wave * 16, r16, af);
+#pragma unroll
+        for (int e = 0; e < (int)(sizeof(af.v) / sizeof(af.v[0])); ++e) {
+          const float a = fmaxf(fmaf((float)af.v[e], wsc, wsh), 0.0f);
+          if constexpr (sizeof(T) == 2) af.v[e] = (__bf16)a;
+          else af.v[e] = a;
+        }
+#pragma unroll
+        for (int ob = 0; ob < NOB; ++ob) {
+          if (ob * 16 < K) {
+            Frag<T> gf;
+            lds_frag<T>(gs, row0, ST, ob * 16, r16, gf);
+            mma(gf, af, dw[ob]);
+          }
+        }
+      }
+    }
     __syncthreads();
+  }
+  if (wgr && wave * 16 + r16 < ncl) {
+    // lane (r16, grp) holds rows o = 16 ob + 4 grp + i of column c0 + 16 wave + r16
+    float* dst = P.out32 + (long)tm * K * ncol + c0 + wave * 16 + r16;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+      if (ob * 16 < K)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dst[(long)(ob * 16 + 4 * grp + i) * ncol] = dw[ob][i];
   }
   // sum over the 16 rows of a lane group (lanes r16); lane r16 == 0 holds four columns
 #pragma unroll

@@ -189,12 +189,20 @@ int pw_wm(long M, int ncol, bool short_ok) {
 // The weight gradient of a narrow pointwise data-gradient problem is formed by the same pw_kernel
 // launch (EPI_PW_WGRAD) when every output channel row is a whole 16-row MFMA tile and its split-K
 // partial rows (one per workgroup) fit the region reserved for the weight-gradient kernel's splits.
-bool pw_wgrad_fused(const SegP& S, const NodeP& n, int B, int es) {
-  if (!pw_bwd_node(S, n, es) || n.cout % 16 != 0) return false;
+// Likewise the BN-sum pass of a deferred-apply BN (bnsum_kernel) for its consumer's weight gradient.
+// Returns the partial rows (the launch's row tiles), or 0 when the weight gradient is not fused.
+long wgrad_fused_rows(const SegP& S, const NodeP& n, int B, int es) {
+  if (n.op != PNN_OP_CONV || !n.dgrad || n.bn < 0 || n.cout % 16 != 0) return 0;
   const long M = (long)B * n.Ho * n.Wo;
-  const long tiles_m = cdiv(M, (long)PW_TR * pw_wm(M, n.cin, S.short_tiles));
+  long tiles_m = 0;
+  if (pw_bwd_node(S, n, es))
+    tiles_m = cdiv(M, (long)PW_TR * pw_wm(M, n.cin, S.short_tiles));
+  else if (S.bns[n.bn].bnsum && n.k == 1 && n.stride == 1 && n.pad == 0)
+    tiles_m = cdiv(M, (long)BNSUM_TR * bnsum_wm(M, n.cin, S.short_tiles));
+  else
+    return 0;
   const WgradGeom g = wgrad_geom_node(n, B, es);
-  return !g.halo3 && tiles_m <= g.splits;
+  return !g.halo3 && tiles_m <= g.splits ? tiles_m : 0;
 }
 
 pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, int es, SegP& S) {
@@ -914,9 +922,9 @@ int fire_finalize(const Ctx& c, std::vector<ColRedProb>& fin, std::vector<BnAppl
 
 // Weight gradients of the convolutions at level L (every level when L < 0) of a set of segments,
 // grouped by kernel variant; their split-K partial sums are appended to ``red`` (RED_SUM).  With
-// ``fused``, the convolutions whose weight gradient the narrow pointwise data-gradient launch forms
-// (pw_wgrad_fused) only get their partial region and their reduction; ``fused`` lists them with
-// that region.
+// ``fused``, the convolutions whose weight gradient their pointwise data-gradient or BN-sum launch
+// forms (wgrad_fused_rows) only get their partial region and their reduction; ``fused`` lists them
+// with that region.
 using FusedWgrad = std::vector<std::pair<const NodeP*, float*>>;
 int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs, int L,
                 std::vector<ColRedProb>& red, FusedWgrad* fused = nullptr) {
@@ -947,9 +955,10 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
       p.part = (float*)(wpart + woff);
       woff = align256(woff + (size_t)g.splits * p.Co * p.K * 4);
       int rows = g.splits;
-      if (fused != nullptr && pw_wgrad_fused(S, n, B, es)) {
+      const long frows = fused != nullptr ? wgrad_fused_rows(S, n, B, es) : 0;
+      if (frows > 0) {
         fused->push_back({&n, p.part});
-        rows = (int)cdiv(p.M, (long)PW_TR * pw_wm(p.M, n.cin, S.short_tiles));
+        rows = (int)frows;
       } else {
         const bool vec = n.cin % (16 / es) == 0;
         const bool pw = vec && n.k == 1 && n.stride == 1 && n.pad == 0;
@@ -1090,6 +1099,11 @@ int run_bwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
                 p.part = part_ptr(c, S, n.bn);
                 p.wm = bnsum_wm(p.M, p.ncol, S.short_tiles);
                 p.tiles_m = (int)cdiv(p.M, (long)BNSUM_TR * p.wm);
+                for (const auto& f : fused)
+                  if (f.first == &n) {
+                    p.flags |= EPI_PW_WGRAD;
+                    p.out32 = f.second;
+                  }
                 p.tiles_n = (int)cdiv(p.ncol, 64);
                 bs.push_back(p);
                 continue;

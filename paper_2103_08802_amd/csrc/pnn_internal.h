@@ -27,8 +27,9 @@ enum {
   EPI_NO_STORE = 16,  // BWD + EPI_BN_MASK: BN sums only, dbn is not stored
   EPI_BN_APPLY = 32,  // BWD: dbn = rnd(v * mask) as for EPI_BN_MASK, then the BN backward apply
                       // out = A dbn + B z + K [+ res] (coefficients coef [3][ncol]); no sums
-  EPI_PW_WGRAD = 64,  // pw_kernel BWD: also the convolution's weight gradient from the same tiles,
-                      // split-K partial row tm of out32 [tiles_m][K][ncol] (g^T . ReLU(BN(z)))
+  EPI_PW_WGRAD = 64,  // pw_kernel BWD / bnsum_kernel: also the convolution's weight gradient from
+                      // the same tiles, split-K partial row tm of out32 [tiles_m][K][ncol]
+                      // (g^T . ReLU(BN(z)))
 };
 
 // Implicit-GEMM convolution problem.  FWD: out[m][n] = sum_k A[m][k] wmat[n][k] with
