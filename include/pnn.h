@@ -159,6 +159,15 @@ pnn_status parareal_combine_fwd(pnn_plan* plan, const void* const* y, const void
 pnn_status coarse_fwd(pnn_plan* plan, int j, const void* rt_j, const void* eta_j, const void* add,
                       void* rt_next, void* saved, void* scratch, void* stream);
 
+/* The whole coarse chain, j = 0..N-2 in order (eq. (tilderk), (tildey)): rt[j + 1] = add[j] +
+ * F^j(rt[j]).  rt has N entries: rt[0] = r_0 is read, rt[1..N-2] = rt_1..rt_{N-2} and rt[N-1] =
+ * ytilde are written; add[j] = r_{j+1} for j < N-2 and add[N-2] = y_N; eta[j] as for coarse_fwd.
+ * rt[j + 1] must not alias rt[j].  Same arithmetic as the N-1 coarse_fwd calls, except that a
+ * block's input BN statistics are summed by the previous block's last convolution as it writes
+ * that input (one pass over rt_j fewer per block), in a different order. */
+pnn_status coarse_fwd_all(pnn_plan* plan, void* const* rt, const void* const* eta,
+                          const void* const* add, void* saved, void* scratch, void* stream);
+
 /* Postprocessing h and the loss, forward and backward (Alg. para3, first line): logits =
  * mean_{h,w}(ytilde) W^T + b (eps = [W (classes x C) | b (classes)] float), loss = mean softmax
  * cross-entropy over the batch.  Writes logits[B][classes] (float, nullable), *loss (float,

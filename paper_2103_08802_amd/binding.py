@@ -24,7 +24,8 @@ EXPORTS = ["pnn_plan_create", "pnn_plan_destroy", "pnn_workspace_size", "pnn_par
            "pnn_tensor_shape", "pnn_pre_fwd", "parareal_fine_fwd", "parareal_combine_fwd",
            "coarse_fwd", "pnn_head_fwd_bwd", "coarse_bwd", "parareal_fine_bwd",
            "parareal_combine_bwd", "pnn_pre_bwd", "pnn_status_string", "pnn_inspect",
-           "pnn_timing_enable", "pnn_timing_read", "pnn_sgd_step", "coarse_bwd_all", "pnn_set_streams",
+           "pnn_timing_enable", "pnn_timing_read", "pnn_sgd_step", "coarse_bwd_all", "coarse_fwd_all",
+           "pnn_set_streams",
            "parareal_bwd"]
 
 
@@ -90,6 +91,7 @@ def lib():
     L.pnn_timing_read.argtypes = [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong),
                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     L.coarse_bwd_all.argtypes = [_vp, _PP, _PP, _PP, _vp, _PP, _vp, _vp]
+    L.coarse_fwd_all.argtypes = [_vp, _PP, _PP, _PP, _vp, _vp, _vp]
     L.parareal_bwd.argtypes = [_vp, _PP, _PP, _PP, _PP, _PP, _PP, _PP, _PP, _vp, _vp, _vp]
     f = ctypes.c_float
     L.pnn_sgd_step.argtypes = [_vp, i, _PP, _PP, _PP, f, f, f, i, _vp]
@@ -257,6 +259,14 @@ def parareal_combine_bwd(plan, dx, D, stream):
     a1, k1 = _arr(dx)
     a2, k2 = _arr(D)
     _check(lib().parareal_combine_bwd(plan.handle, a1, a2, stream), "parareal_combine_bwd")
+
+
+def coarse_fwd_all(plan, rt, eta, add, saved, scratch, stream):
+    a1, k1 = _arr(rt)
+    a2, k2 = _arr(eta)
+    a3, k3 = _arr(add)
+    _check(lib().coarse_fwd_all(plan.handle, a1, a2, a3, _ptr(saved), _ptr(scratch), stream),
+           "coarse_fwd_all")
 
 
 def coarse_bwd_all(plan, D, rt, eta, saved, deta, scratch, stream):

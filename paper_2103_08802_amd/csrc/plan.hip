@@ -56,6 +56,8 @@ struct BnP {
   bool bnact_consumer = false;
   bool defer_apply = false;  // dbn not stored: the apply pass recomputes it (see build_segment)
   bool bnsum = false;        // its backward sums come from bnsum_kernel (no data-gradient tile)
+  int fwd_tiles_in = 0;      // coarse input BN: forward sums from the previous block's last
+                             // convolution (coarse_fwd_all), in its row tiles; 0 = not chained
 };
 
 struct SegP {
@@ -404,7 +406,10 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
       const NodeP& c = S.nodes[sl.bn_consumers[0]];
       b.bwd_tiles = (int)cdiv((long)B * c.Ho * c.Wo, BNACT_PIX);
     }
-    const int tiles = std::max(b.fwd_tiles, b.bwd_tiles);
+    int tiles = std::max(b.fwd_tiles, b.bwd_tiles);
+    // a coarse block's input BN may take its forward sums from the previous block's last
+    // convolution (coarse_fwd_all), in that convolution's row tiles of at least 64 rows
+    if (part == 2 && b.slot == 0) tiles = std::max(tiles, (int)cdiv(M, 64));
     b.part_off = sc;
     sc = align256(sc + (size_t)tiles * 2 * b.C * 4);
     b.coef_off = sc;
@@ -483,6 +488,9 @@ struct Ptrs {
   const void* ext = nullptr;
   const void* gout = nullptr;
   void* gin = nullptr;
+  bool in_sums = false;               // forward: the input BN's sums are already in its partial rows
+  const SegP* out_sums = nullptr;     // forward: the output's convolution also forms the sums of
+                                      // this segment's input BN (the next coarse block)
 };
 
 struct Ctx {
@@ -745,14 +753,15 @@ int run_fwd_begin(const Ctx& c, const std::vector<const SegP*>& segs, const std:
       const SlotP& s0 = S.slots[0];
       if (s0.bn < 0) continue;
       const BnP& b = S.bns[s0.bn];
+      const bool chained = ptrs[i].in_sums && b.fwd_tiles_in > 0;
       ColStatProb p;
       p.x = ptrs[i].in;
       p.part = part_ptr(c, S, s0.bn);
       p.M = (long)B * s0.H * s0.W;
       p.C = s0.C;
-      cs.push_back(p);
-      fw.push_back(bn_fwd_red(p.part, b.fwd_tiles, (const float*)(cp(ptrs[i].params) + b.p_off),
-                              stats_ptr(c, S, s0.bn), b.C, p.M));
+      if (!chained) cs.push_back(p);
+      fw.push_back(bn_fwd_red(p.part, chained ? b.fwd_tiles_in : b.fwd_tiles,
+                              (const float*)(cp(ptrs[i].params) + b.p_off), stats_ptr(c, S, s0.bn), b.C, p.M));
     }
     int e = grouped<ColStatLaunch>(
         cs, [](const ColStatProb& p) { return (int)cdiv(p.M, COLSTAT_ROWS); },
@@ -788,6 +797,10 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
           p.pro = n.bn >= 0 ? stats_ptr(c, S, n.bn) + 2 * S.bns[n.bn].C : nullptr;
           if (so.bn >= 0) {
             p.part = part_ptr(c, S, so.bn);
+            p.flags = EPI_STATS;
+          } else if (n.dst == S.out && P.out_sums != nullptr) {
+            const SegP& nx = *P.out_sums;
+            p.part = part_ptr(c, nx, nx.slots[0].bn);
             p.flags = EPI_STATS;
           }
           p.B = B; p.H = n.H; p.W = n.W; p.Cg = n.cin;
@@ -1397,6 +1410,24 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
     delete p;
     return st;
   }
+  // coarse_fwd_all: the last convolution of block j - 1 also forms the forward sums of block j's
+  // input BN (the same tensor), in that convolution's row tiles
+  for (int j = 1; j + 1 < N; ++j) {
+    SegP& nx = p->coarse[j];
+    const SegP& pv = p->coarse[j - 1];
+    const int bn = nx.slots[0].bn;
+    if (bn < 0 || pv.slots[pv.out].bn >= 0) continue;
+    const NodeP* prod = nullptr;
+    for (const NodeP& n : pv.nodes)
+      if (n.dst == pv.out) prod = &n;
+    if (prod == nullptr || prod->op != PNN_OP_CONV || pw_fwd_node(pv, *prod, p->es)) continue;
+    ConvProb t;
+    std::memset(&t, 0, sizeof(t));
+    t.k = prod->k; t.Cg = prod->cin; t.P = prod->Ho; t.Q = prod->Wo; t.ncol = prod->cout;
+    t.M = p->B * prod->Ho * prod->Wo;
+    set_tiles(t, pv.short_tiles);
+    if (t.ncol == nx.bns[bn].C && t.tiles_m <= cdiv(t.M, 64)) nx.bns[bn].fwd_tiles_in = t.tiles_m;
+  }
   // workspace layout: saved = [pre | fine | coarse]; scratch = [shared | per segment]
   size_t sv = 0;
   for (auto* v : {&p->pre, &p->fine, &p->coarse})
@@ -1565,6 +1596,37 @@ pnn_status coarse_fwd(pnn_plan* plan, int j, const void* rt_j, const void* eta_j
   p.params = eta_j;
   p.ext = add;
   return run_fwd(c, {&plan->coarse[j]}, {p});
+}
+
+pnn_status coarse_fwd_all(pnn_plan* plan, void* const* rt, const void* const* eta, const void* const* add,
+                          void* saved, void* scratch, void* stream) {
+  if (!ok_ctx(plan, saved, scratch)) return PNN_ERR_NULL;
+  if (rt == nullptr || eta == nullptr || add == nullptr) return PNN_ERR_NULL;
+  const int N = plan->N;
+  if (N < 2) return PNN_OK;
+  for (int j = 0; j < N; ++j)
+    if (rt[j] == nullptr) return PNN_ERR_NULL;
+  for (int j = 0; j + 1 < N; ++j) {
+    if (eta[j] == nullptr || add[j] == nullptr) return PNN_ERR_NULL;
+    if (rt[j] == rt[j + 1]) return PNN_ERR_SHAPE;
+  }
+  Ctx c{plan, (char*)saved, (char*)scratch, (hipStream_t)stream};
+  auto chained = [&](int j) {   // block j's input BN takes its sums from block j - 1
+    const SegP& S = plan->coarse[j];
+    return j > 0 && S.slots[0].bn >= 0 && S.bns[S.slots[0].bn].fwd_tiles_in > 0;
+  };
+  for (int j = 0; j + 1 < N; ++j) {
+    Ptrs p;
+    p.in = rt[j];
+    p.out = rt[j + 1];
+    p.params = eta[j];
+    p.ext = add[j];
+    p.in_sums = chained(j);
+    p.out_sums = (j + 2 < N && chained(j + 1)) ? &plan->coarse[j + 1] : nullptr;
+    const int e = run_fwd(c, {&plan->coarse[j]}, {p});
+    if (e) return e;
+  }
+  return PNN_OK;
 }
 
 pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps, const int32_t* labels,

@@ -27,6 +27,7 @@ class ParaRealGPU:
         self.plan = B.Plan(net)
         self.coarse_chain_all = True      # coarse_bwd_all (deferred coarse weight gradients)
         self.overlap_bwd = False          # parareal_bwd: the coarse chain overlapped with the fine backward
+        self.coarse_fwd_chain = True      # coarse_fwd_all (input BN sums from the previous block)
         self.dev = torch.device(device)
         self.sdt = torch.bfloat16 if net.dtype == "bf16" else torch.float32
         N, Bt = net.n_sub, net.batch
@@ -153,15 +154,22 @@ class ParaRealGPU:
                                    self.scratch, s)
             if coarse_events:
                 coarse_events[0].record()
-            for j in range(N - 1):
-                last = j + 1 == N - 1
-                add = self.y[N - 1] if last else self.r[j + 1]
-                out = self.ytilde if last else self.rt[j + 1]
-                B.coarse_fwd(p, j, self.rt[j], self.eta[j], add, out, self.saved, self.scratch, s)
+            self._coarse_forward(s)
             if coarse_events:
                 coarse_events[1].record()
         B.pnn_head_fwd_bwd(p, self.ytilde, self.eps, self.labels, self.logits, self.loss,
                            self.D[N - 1], self.deps, self.scratch, s)
+
+    def _coarse_forward(self, s):
+        """The coarse chain rt_{j+1} = add_j + F^j(rt_j), j = 0..N-2 (ytilde last)."""
+        p, N = self.plan, self.net.n_sub
+        adds = [self.r[j + 1] for j in range(N - 2)] + [self.y[N - 1]]
+        outs = [self.rt[j + 1] for j in range(N - 2)] + [self.ytilde]
+        if self.coarse_fwd_chain:
+            B.coarse_fwd_all(p, [self.rt[0]] + outs, self.eta, adds, self.saved, self.scratch, s)
+        else:
+            for j in range(N - 1):
+                B.coarse_fwd(p, j, self.rt[j], self.eta[j], adds[j], outs[j], self.saved, self.scratch, s)
 
     def backward(self, s=None, fine_events=None, coarse_events=None):
         """Alg. para3.  ``fine_events`` / ``coarse_events`` as in ``forward``, around
@@ -219,11 +227,7 @@ class ParaRealGPU:
         st = self.stream
 
         def coarse_fwd():
-            for j in range(N - 1):
-                last = j + 1 == N - 1
-                add = self.y[N - 1] if last else self.r[j + 1]
-                out = self.ytilde if last else self.rt[j + 1]
-                B.coarse_fwd(p, j, self.rt[j], self.eta[j], add, out, self.saved, self.scratch, st())
+            self._coarse_forward(st())
 
         def coarse_bwd():
             if self.coarse_chain_all:

@@ -93,5 +93,9 @@ def test_error_codes():
     D = arr([16] * N)                                                          # D_0 aliases D_1
     ok = arr([16 * (i + 1) for i in range(N)])
     assert L.parareal_bwd(p.handle, D, ok, ok, ok, ok, ok, ok, ok, 1, 1, None) == -2
+    # coarse_fwd_all: NULL arrays and aliased rt_j / rt_{j+1} are rejected the same way
+    assert L.coarse_fwd_all(p.handle, None, None, None, 1, 1, None) == -1
+    assert L.coarse_fwd_all(p.handle, D, ok, ok, 1, 1, None) == -2
+    assert L.coarse_fwd_all(p.handle, ok, ok, ok, None, 1, None) == -1
     assert B.pnn_status_string(-5) == "network form not supported by this library"
     p.close()

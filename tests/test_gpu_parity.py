@@ -365,3 +365,48 @@ def test_pooled_multichannel_input(dtype, batch, tol):
     """C^j max-pooling a multi-channel input (the vectorised pool path; the workloads pool only the
     3-channel image): every tensor within the fp32 / bf16 tolerance of the oracle."""
     _assert_tol(run_net(pooled_16ch_net(dtype, batch)), tol)
+
+
+@pytest.mark.parametrize("n_sub,ups,batch", [(3, 2, 2), (4, 4, 3)])
+def test_coarse_fwd_all_equals_per_block_calls(n_sub, ups, batch):
+    """coarse_fwd_all (each block's input BN sums formed by the previous block's last convolution)
+    against the N - 1 coarse_fwd calls, fp32: rt_j and ytilde agree to 1e-5 (the BN sums are the
+    same numbers summed in another order)."""
+    import torch
+    from paper_2103_08802_amd.step import ParaRealGPU
+    net = mini_resnet(n_sub, ups, batch)
+    x, labels, params = S.make_all(net)
+    out = []
+    for chain in (False, True):
+        g = ParaRealGPU(net, params)
+        g.coarse_fwd_chain = chain
+        g.load_input(x, labels)
+        g.forward()
+        torch.cuda.synchronize()
+        out.append([g.to_np(t) for t in g.rt[1:] + [g.ytilde]])
+    for a, b in zip(*out):
+        assert rel_inf(b, a) <= 1e-5
+
+
+def test_coarse_fwd_all_bf16_full_size():
+    """The full-size bf16 workload: ytilde from coarse_fwd_all against the per-block calls.  The BN
+    sums differ only in summation order, but the values they move across a bf16 rounding boundary
+    change by one ulp (2^-8 relative) and feed the next block, 15 times: the two agree to about one
+    bf16 ulp in L2 (measured 4.0e-3), bounded here by 1e-2, half the oracle tolerance that each of
+    them meets block by block (test_gpu_nodes)."""
+    import torch
+    from paper_2103_08802_amd.step import ParaRealGPU
+    net = S.config(3)
+    x, labels, params = S.make_all(net)
+    out = []
+    for chain in (False, True):
+        g = ParaRealGPU(net, params)
+        g.coarse_fwd_chain = chain
+        g.load_input(x, labels)
+        g.forward()
+        torch.cuda.synchronize()
+        out.append(g.to_np(g.ytilde))
+        del g
+    err = rel_2(out[1], out[0])
+    _say(f"[coarse_fwd_all] bf16 full size: ytilde L2 relative difference {err:.3e}")
+    assert err <= 1e-2
