@@ -1440,6 +1440,7 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
   wp = std::max(wp, wgrad_level_bytes(p->pre, p->B, p->es));
   for (auto& s : p->coarse) wp = std::max(wp, wgrad_level_bytes(std::vector<SegP>{s}, p->B, p->es));
   wp = std::max(wp, wgrad_all_bytes(p->coarse, p->B, p->es));     // coarse_bwd_all
+  wp = std::max(wp, wgrad_all_bytes(p->pre, p->B, p->es));        // pnn_pre_bwd, every level at once
   size_t sc = 0;
   p->wpart_off = sc;
   p->wpart_bytes = wp;
@@ -1922,7 +1923,20 @@ pnn_status pnn_pre_bwd(pnn_plan* plan, const void* image, const void* const* g, 
     ptrs.push_back(p);
   }
   if (segs.empty()) return PNN_OK;
-  return run_bwd(c, segs, ptrs);
+  // Without BN instances and data gradients (max pools and a convolution on the image) the
+  // backward is only the weight gradients, which do not depend on each other: every level in one
+  // grouped launch and one column reduce
+  bool wgrad_only = true;
+  for (auto* sp : segs) {
+    if (!sp->bns.empty()) wgrad_only = false;
+    for (const NodeP& n : sp->nodes)
+      if (n.op == PNN_OP_BNACT || (n.op == PNN_OP_CONV && (n.dgrad || n.dst != sp->out))) wgrad_only = false;
+  }
+  if (!wgrad_only) return run_bwd(c, segs, ptrs);
+  std::vector<ColRedProb> red;
+  const int e = fire_wgrads(c, segs, ptrs, -1, red);
+  if (e) return e;
+  return fire_colred(red, c.stream) ? PNN_ERR_HIP : PNN_OK;
 }
 
 pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx, size_t* offset) {
