@@ -196,7 +196,7 @@ def main():
         summarize_trace(*args.summarize_trace, args.title, args.cmd)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs the whole parareal network on ONE GPU (all N "
+        print(json.dumps({"error": "this library runs the whole parareal network on ONE GPU (all N "
                           "fine sub-networks as grouped launches); --gpus must be 1"}))
         sys.exit(2)
 
