@@ -132,6 +132,52 @@ def summarize_pmc(fetch_csv, write_csv, kernel, cmd):
     print(json.dumps(rec))
 
 
+def summarize_families(fetch_csv, write_csv, trace_csv, out_md, cmd):
+    """Per kernel family: HBM bytes per launch from the two --pmc runs (each counter scaled by what
+    it reads for the calibration copy), average duration from a --kernel-trace run of the same
+    build and workload, and the HBM bandwidth they give."""
+    import csv
+
+    def load(p):
+        per, copy = {}, None
+        for r in csv.DictReader(open(p)):
+            v = float(r["Counter_Value"]) * 1024.0
+            n = _short(r["Kernel_Name"])
+            if n == "__amd_rocclr_copyBuffer":
+                copy = max(copy or 0.0, v)
+            per.setdefault(n, []).append(v)
+        return per, copy
+
+    fe, fcopy = load(fetch_csv)
+    wr, wcopy = load(write_csv)
+    ffac, wfac = COPY_BYTES / fcopy, COPY_BYTES / wcopy
+    dur = {}
+    for r in csv.DictReader(open(trace_csv)):
+        dur.setdefault(_short(r["Kernel_Name"]), []).append(
+            (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    rows = []
+    for n in fe:
+        if n not in wr or n not in dur or n.startswith("__amd") or n.startswith("at::"):
+            continue
+        fb = sum(fe[n]) / len(fe[n]) * ffac
+        wb = sum(wr[n]) / len(wr[n]) * wfac
+        us = sum(dur[n]) / len(dur[n])
+        rows.append((n, len(dur[n]), fb / 1e6, wb / 1e6, us, (fb + wb) / (us * 1e3)))
+    rows.sort(key=lambda r: -r[1] * r[4])
+    with open(out_md, "w") as f:
+        f.write("# HBM traffic per kernel family: parareal ResNet-1001, N=16, batch 128, bf16 (one "
+                "stream)\n\nCommands (from the repository root, on one MI355X):\n\n```\n"
+                f"{cmd}\n```\n\n")
+        f.write(f"FETCH_SIZE scaled by {ffac:.4f}, WRITE_SIZE by {wfac:.4f} (what each reads for one "
+                f"{COPY_BYTES >> 20} MiB device copy).  Bytes per launch are averages over the PMC "
+                "runs' dispatches, durations over the kernel-trace run's; both runs use the same "
+                "launches per step.\n\n")
+        f.write("| family | launches (trace) | fetched MB | written MB | avg us | HBM GB/s |\n"
+                "|---|---:|---:|---:|---:|---:|\n")
+        for n, c, fm, wm, us, gbs in rows:
+            f.write(f"| `{n}` | {c} | {fm:.1f} | {wm:.1f} | {us:.2f} | {gbs:.0f} |\n")
+
+
 def summarize_trace(stats_csv, trace_csv, out_md, title, cmd):
     """Markdown summary of a rocprofv3 --kernel-trace --stats run: the per-instantiation statistics
     and, per kernel family, the average duration over all its dispatches."""
@@ -185,6 +231,8 @@ def main():
                     help="no GPU work: store HBM bytes per launch of --kernel from two PMC runs")
     ap.add_argument("--summarize-trace", nargs=3, metavar=("STATS_CSV", "TRACE_CSV", "OUT_MD"),
                     help="no GPU work: write a markdown summary of a kernel-trace run")
+    ap.add_argument("--summarize-families", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "TRACE_CSV", "OUT_MD"),
+                    help="no GPU work: HBM bytes, duration and bandwidth per kernel family")
     ap.add_argument("--kernel", default="conv_kernel")
     ap.add_argument("--title", default="")
     ap.add_argument("--cmd", default="", help="command that produced the CSVs (recorded)")
@@ -194,6 +242,9 @@ def main():
         return
     if args.summarize_trace:
         summarize_trace(*args.summarize_trace, args.title, args.cmd)
+        return
+    if args.summarize_families:
+        summarize_families(*args.summarize_families, args.cmd)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this library runs the whole parareal network on ONE GPU (all N "
