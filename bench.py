@@ -178,6 +178,39 @@ def summarize_families(fetch_csv, write_csv, trace_csv, out_md, cmd):
             f.write(f"| `{n}` | {c} | {fm:.1f} | {wm:.1f} | {us:.2f} | {gbs:.0f} |\n")
 
 
+def summarize_sq(csv_path, out_md, cmd):
+    """Per kernel instantiation, ratios of one rocprofv3 --pmc run of SQ counters (SQ_WAVES,
+    SQ_WAVE_CYCLES, SQ_BUSY_CYCLES, SQ_WAIT_ANY, SQ_WAIT_INST_LDS, SQ_ACTIVE_INST_LDS,
+    SQ_VALU_MFMA_BUSY_CYCLES, SQ_LDS_BANK_CONFLICT), summed over its dispatches."""
+    import csv
+    tot, disp = {}, {}
+    for r in csv.DictReader(open(csv_path)):
+        n = r["Kernel_Name"].split("(")[0].replace("void ", "")
+        tot.setdefault(n, {}).setdefault(r["Counter_Name"], 0.0)
+        tot[n][r["Counter_Name"]] += float(r["Counter_Value"])
+        disp.setdefault(n, set()).add(r["Dispatch_Id"])
+    rows = sorted(tot.items(), key=lambda kv: -kv[1].get("SQ_WAVE_CYCLES", 0.0))
+    with open(out_md, "w") as f:
+        f.write("# SQ counters per conv_kernel instantiation: parareal ResNet-1001, N=16, batch 128, "
+                "bf16 (one stream)\n\nCommand (from the repository root, on one MI355X):\n\n```\n"
+                f"{cmd}\n```\n\nwave cycles = SQ_WAVE_CYCLES / SQ_WAVES; the waits and LDS activity as "
+                "fractions of SQ_WAVE_CYCLES; MFMA busy per SQ busy cycle; LDS bank-conflict cycles per "
+                "LDS-active cycle.\n\n")
+        f.write("| kernel | dispatches | waves / dispatch | cycles / wave | wait any | wait LDS | "
+                "LDS active | MFMA busy / busy | bank conflicts / LDS active |\n"
+                "|---|---:|---:|---:|---:|---:|---:|---:|---:|\n")
+        for n, c in rows:
+            w, wc = c.get("SQ_WAVES", 0.0), c.get("SQ_WAVE_CYCLES", 0.0)
+            if w <= 0 or wc <= 0:
+                continue
+            lds = max(c.get("SQ_ACTIVE_INST_LDS", 0.0), 1.0)
+            f.write(f"| `{n}` | {len(disp[n])} | {w / len(disp[n]):.0f} | {wc / w:.0f} | "
+                    f"{c.get('SQ_WAIT_ANY', 0.0) / wc:.2f} | {c.get('SQ_WAIT_INST_LDS', 0.0) / wc:.2f} | "
+                    f"{c.get('SQ_ACTIVE_INST_LDS', 0.0) / wc:.2f} | "
+                    f"{c.get('SQ_VALU_MFMA_BUSY_CYCLES', 0.0) / max(c.get('SQ_BUSY_CYCLES', 0.0), 1.0):.2f} | "
+                    f"{c.get('SQ_LDS_BANK_CONFLICT', 0.0) / lds:.2f} |\n")
+
+
 def summarize_trace(stats_csv, trace_csv, out_md, title, cmd):
     """Markdown summary of a rocprofv3 --kernel-trace --stats run: the per-instantiation statistics
     and, per kernel family, the average duration over all its dispatches."""
@@ -233,6 +266,8 @@ def main():
                     help="no GPU work: write a markdown summary of a kernel-trace run")
     ap.add_argument("--summarize-families", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "TRACE_CSV", "OUT_MD"),
                     help="no GPU work: HBM bytes, duration and bandwidth per kernel family")
+    ap.add_argument("--summarize-sq", nargs=2, metavar=("PMC_CSV", "OUT_MD"),
+                    help="no GPU work: SQ counter ratios per kernel instantiation")
     ap.add_argument("--kernel", default="conv_kernel")
     ap.add_argument("--title", default="")
     ap.add_argument("--cmd", default="", help="command that produced the CSVs (recorded)")
@@ -245,6 +280,9 @@ def main():
         return
     if args.summarize_families:
         summarize_families(*args.summarize_families, args.cmd)
+        return
+    if args.summarize_sq:
+        summarize_sq(*args.summarize_sq, args.cmd)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this library runs the whole parareal network on ONE GPU (all N "
