@@ -8,17 +8,21 @@
  *   x_j = C^j(x),  y_j = g^j(x_j)                    (eq. (xjyj), Alg. para2)      pnn_pre_fwd,
  *                                                                                  parareal_fine_fwd
  *   r_j = y_j - x_{j+1} (j < N), r_N = 0             (eq. (rk))                    parareal_combine_fwd
- *   rt_1 = r_1, rt_{j+1} = r_{j+1} + F^j(rt_j)       (eq. (tilderk))               coarse_fwd
+ *   rt_1 = r_1, rt_{j+1} = r_{j+1} + F^j(rt_j)       (eq. (tilderk))               coarse_fwd,
+ *                                                                                  coarse_fwd_all
  *   ytilde = y_N + rt_N                              (eq. (tildey))                coarse_fwd (j = N-1)
  *   logits = h(ytilde), loss, D_N = dL/dytilde       (Alg. para3, first line)      pnn_head_fwd_bwd
- *   D_j = D_{j+1} . dF^j/drt_j, dL/deta_j            (Alg. para3, eq. (etak))      coarse_bwd
+ *   D_j = D_{j+1} . dF^j/drt_j, dL/deta_j            (Alg. para3, eq. (etak))      coarse_bwd,
+ *                                                                                  coarse_bwd_all
  *   dL/dphi_j = D_j . dg^j/dphi_j, D_j . dg^j/dx_j   (Alg. para3, eq. (phij))      parareal_fine_bwd
+ *   (the last two together, overlapped)                                            parareal_bwd
  *   dL/dx_j = D_j . dg^j/dx_j - D_{j-1}              (eq. (deltaj))                parareal_combine_bwd
  *   dL/ddelta_j                                       (eq. (deltaj))                pnn_pre_bwd
  *
  * All N fine sub-networks g^j run in the same kernel launches (grouped convolutions over N
- * independent weight sets).  The coarse network is sequential by definition (Sec. 3.1) and runs
- * one block F^j per call.
+ * independent weight sets).  The coarse network is sequential by definition (Sec. 3.1): one block
+ * F^j per call (coarse_fwd / coarse_bwd) or the whole chain in order (coarse_fwd_all /
+ * coarse_bwd_all / parareal_bwd).
  *
  * Conventions for every entry point
  *   - Every tensor pointer is a DEVICE pointer owned by the caller.  Activations are NHWC and
@@ -31,8 +35,8 @@
  *     stream.  parareal_fine_fwd / parareal_fine_bwd / parareal_bwd may run groups of
  *     sub-networks on up to pnn_set_streams() streams: the given one and internal streams of the
  *     plan (default priority), which first wait for the work enqueued on the given stream before
- *     the call; the given stream waits for all of them before the call returns.  The first call that uses a
- *     second stream creates the plan's internal streams and events (no memory);
+ *     the call; the given stream waits for all of them before the call returns.  The first call
+ *     that uses a second stream creates the plan's internal streams and events (no memory);
  *     pnn_plan_destroy releases them.  Only pnn_plan_create allocates (host memory only).
  *   - Workspaces: the caller allocates one "saved" buffer (activations kept from the forward for
  *     the backward; pnn_workspace_size(PNN_WS_SAVED)) and one "scratch" buffer (temporaries;
