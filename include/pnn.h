@@ -31,13 +31,18 @@
  *     activation gradients and filters as bfloat16 bit patterns (uint16_t) and keep BN
  *     parameters, every parameter gradient, the head and the loss in float.  Arithmetic is fp32
  *     (bf16 MFMA operands with fp32 accumulation).
- *   - Entry points never allocate memory, free or synchronise.  All work is ordered on the given
- *     stream.  parareal_fine_fwd / parareal_fine_bwd / parareal_bwd may run groups of
- *     sub-networks on up to pnn_set_streams() streams: the given one and internal streams of the
- *     plan (default priority), which first wait for the work enqueued on the given stream before
- *     the call; the given stream waits for all of them before the call returns.  The first call
- *     that uses a second stream creates the plan's internal streams and events (no memory);
- *     pnn_plan_destroy releases them.  Only pnn_plan_create allocates (host memory only).
+ *   - Entry points never allocate memory, free or synchronise, and never create streams or
+ *     events.  All work is ordered on the given stream.  parareal_fine_fwd / parareal_fine_bwd /
+ *     parareal_bwd may run groups of sub-networks on up to pnn_set_streams() streams: the given
+ *     one and internal streams of the plan (default priority), which first wait for the work
+ *     enqueued on the given stream before the call; the given stream waits for all of them before
+ *     the call returns.  pnn_set_streams creates those internal streams and their events (no
+ *     device memory) and pnn_plan_destroy releases them; pnn_plan_create allocates host memory
+ *     only.  So every compute call can be captured into a HIP graph, the first one included.
+ *   - Alignment: every tensor pointer (activations, their gradients, the image) and every
+ *     parameter / gradient / momentum buffer must be 16-byte aligned (the kernels move 16-byte
+ *     chunks); the workspaces 256-byte aligned; labels, logits and the loss 4-byte aligned.  A
+ *     violation returns PNN_ERR_ALIGN before anything is enqueued.
  *   - Workspaces: the caller allocates one "saved" buffer (activations kept from the forward for
  *     the backward; pnn_workspace_size(PNN_WS_SAVED)) and one "scratch" buffer (temporaries;
  *     PNN_WS_SCRATCH), both at least 256-byte aligned, and passes the same ones to every call of a
@@ -66,7 +71,8 @@ enum {
   PNN_ERR_WORKSPACE = -4,   /* unknown workspace kind */
   PNN_ERR_UNSUPPORTED = -5, /* a valid network this library does not run (e.g. channels not a multiple of 16) */
   PNN_ERR_HIP = -6,         /* a HIP call failed */
-  PNN_ERR_INDEX = -7        /* sub-network / coarse block index out of range */
+  PNN_ERR_INDEX = -7,       /* sub-network / coarse block index out of range */
+  PNN_ERR_ALIGN = -8        /* a pointer violates the alignment rules above */
 };
 
 typedef enum { PNN_F32 = 0, PNN_BF16 = 1 } pnn_dtype;
@@ -261,12 +267,15 @@ pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx,
 
 const char* pnn_status_string(pnn_status s);
 
-/* Number of streams (1 .. 4, default 4) over which parareal_fine_fwd / parareal_fine_bwd may run
- * their sub-networks: the sub-networks are grouped by the spatial size of their input (the
- * ResNet stage they start in), the group with the most work is halved while streams are left, and
- * each group's level-by-level launches go to a stream of its own.  1 keeps every launch on the
- * call's stream.  Results do not depend on it (every group's launches are the same; no reduction
- * crosses groups).  PNN_ERR_INDEX outside 1 .. 4. */
+/* Number of streams (1 .. 4, default 1) over which parareal_fine_fwd / parareal_fine_bwd /
+ * parareal_bwd may run their sub-networks: the sub-networks are grouped by the spatial size of
+ * their input (the ResNet stage they start in), the group with the most work is halved while
+ * streams are left, and each group's level-by-level launches go to a stream of its own.  1 keeps
+ * every launch on the call's stream.  Results do not depend on it (every group's launches are the
+ * same; no reduction crosses groups).  Creates the plan's internal streams (default priority,
+ * non-blocking) and fork / join events the first time more streams are asked for than exist (a
+ * set-up call: needs a HIP device, allocates no device memory); PNN_ERR_HIP if that fails.
+ * PNN_ERR_INDEX outside 1 .. 4. */
 pnn_status pnn_set_streams(pnn_plan* plan, int streams);
 
 /* Per-kernel-family GPU time accounting with HIP events recorded on the call's stream around

@@ -17,7 +17,8 @@ PNN_F32, PNN_BF16 = 0, 1
 PNN_WS_SAVED, PNN_WS_SCRATCH = 0, 1
 OPS = {"conv": 0, "bnact": 1, "maxpool3": 2}
 STATUS = {0: "PNN_OK", -1: "PNN_ERR_NULL", -2: "PNN_ERR_SHAPE", -3: "PNN_ERR_DTYPE",
-          -4: "PNN_ERR_WORKSPACE", -5: "PNN_ERR_UNSUPPORTED", -6: "PNN_ERR_HIP", -7: "PNN_ERR_INDEX"}
+          -4: "PNN_ERR_WORKSPACE", -5: "PNN_ERR_UNSUPPORTED", -6: "PNN_ERR_HIP", -7: "PNN_ERR_INDEX",
+          -8: "PNN_ERR_ALIGN"}
 
 # every symbol include/pnn.h declares
 EXPORTS = ["pnn_plan_create", "pnn_plan_destroy", "pnn_workspace_size", "pnn_param_layout",

@@ -7,7 +7,9 @@
 // parareal_fine_fwd: all N sub-networks, Alg. para2's parallel loop).  A backward call walks the
 // levels downwards (Alg. para3).
 #include <algorithm>
+#include <cstdint>
 #include <cstring>
+#include <initializer_list>
 #include <new>
 #include <string>
 #include <vector>
@@ -92,8 +94,9 @@ struct pnn_plan {
   size_t head_off = 0, head_bytes = 0;
   size_t sq_off = 0, sq_bytes = 0;
   // independent chains of the fine sub-networks: up to `streams` streams, the call's stream and
-  // internal ones created by the first call that needs them (default priority, non-blocking)
-  int streams = PNN_MAX_CHAINS;
+  // internal ones created by pnn_set_streams (default priority, non-blocking); compute calls never
+  // create streams or events
+  int streams = 1;
   std::vector<hipStream_t> side;
   std::vector<hipEvent_t> fj;          // fork / join events (no timing), used round robin
   size_t fj_next = 0;
@@ -1231,7 +1234,7 @@ struct Chains {
 int chains_group(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs,
                  Chains& ch) {
   pnn_plan* p = c.plan;
-  const int maxg = p->timing_family != 0 ? 1 : p->streams;
+  const int maxg = p->timing_family != 0 ? 1 : std::min(p->streams, (int)p->side.size() + 1);
   std::vector<long> keys;
   for (size_t i = 0; i < segs.size(); ++i) {
     const long key = (long)segs[i]->slots[0].H << 20 | segs[i]->slots[0].W;   // the stage
@@ -1269,16 +1272,6 @@ int chains_group(const Ctx& c, const std::vector<const SegP*>& segs, const std::
     ch.ctx.push_back(d);
   }
   if (G <= 1) return PNN_OK;
-  while (p->side.size() < (size_t)(PNN_MAX_CHAINS - 1)) {
-    hipStream_t st;
-    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return PNN_ERR_HIP;
-    p->side.push_back(st);
-  }
-  while (p->fj.size() < 16) {
-    hipEvent_t e;
-    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return PNN_ERR_HIP;
-    p->fj.push_back(e);
-  }
   for (int g = 1; g < G; ++g) ch.ctx[g].stream = p->side[g - 1];
   return PNN_OK;
 }
@@ -1342,6 +1335,21 @@ bool ok_ctx(pnn_plan* plan, void* saved, void* scratch) {
          (plan->scratch_bytes == 0 || scratch != nullptr);
 }
 
+// Alignment rules of the interface: tensors and parameter / gradient buffers 16 bytes (the kernels
+// move 16-byte chunks), workspaces 256 bytes.  NULL passes (the NULL checks come first).
+inline bool al(const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+bool al16(std::initializer_list<const void*> ps) {
+  for (const void* p : ps)
+    if (!al(p, 16)) return false;
+  return true;
+}
+bool al16n(const void* const* a, int j0, int j1) {
+  for (int j = j0; j < j1; ++j)
+    if (!al(a[j], 16)) return false;
+  return true;
+}
+bool al_ws(const void* saved, const void* scratch) { return al(saved, 256) && al(scratch, 256); }
+
 }  // namespace
 
 // ================================================================================================
@@ -1360,6 +1368,7 @@ const char* pnn_status_string(pnn_status s) {
     case PNN_ERR_UNSUPPORTED: return "network form not supported by this library";
     case PNN_ERR_HIP: return "a HIP call failed";
     case PNN_ERR_INDEX: return "index out of range";
+    case PNN_ERR_ALIGN: return "a pointer is not aligned as the interface requires";
     default: return "unknown status";
   }
 }
@@ -1513,6 +1522,7 @@ pnn_status pnn_tensor_shape(const pnn_plan* plan, int which, int j, int* h, int*
 pnn_status pnn_pre_fwd(pnn_plan* plan, const void* image, void* const* x, const void* const* delta,
                        void* saved, void* scratch, void* stream) {
   if (!ok_ctx(plan, saved, scratch) || image == nullptr || x == nullptr) return PNN_ERR_NULL;
+  if (!al_ws(saved, scratch)) return PNN_ERR_ALIGN;
   Ctx c{plan, (char*)saved, (char*)scratch, (hipStream_t)stream};
   std::vector<const SegP*> segs;
   std::vector<Ptrs> ptrs;
@@ -1520,6 +1530,7 @@ pnn_status pnn_pre_fwd(pnn_plan* plan, const void* image, void* const* x, const 
     const SegP& S = plan->pre[j];
     if (x[j] == nullptr) return PNN_ERR_NULL;
     if (S.param_bytes > 0 && (delta == nullptr || delta[j] == nullptr)) return PNN_ERR_NULL;
+    if (!al16({image, x[j], delta ? delta[j] : nullptr})) return PNN_ERR_ALIGN;
     Ptrs p;
     p.in = image;
     p.out = x[j];
@@ -1533,11 +1544,13 @@ pnn_status pnn_pre_fwd(pnn_plan* plan, const void* image, void* const* x, const 
 pnn_status parareal_fine_fwd(pnn_plan* plan, const void* const* x, const void* const* phi, void* const* y,
                              void* saved, void* scratch, void* stream) {
   if (!ok_ctx(plan, saved, scratch) || x == nullptr || phi == nullptr || y == nullptr) return PNN_ERR_NULL;
+  if (!al_ws(saved, scratch)) return PNN_ERR_ALIGN;
   Ctx c{plan, (char*)saved, (char*)scratch, (hipStream_t)stream};
   std::vector<const SegP*> segs;
   std::vector<Ptrs> ptrs;
   for (int j = 0; j < plan->N; ++j) {
     if (x[j] == nullptr || phi[j] == nullptr || y[j] == nullptr) return PNN_ERR_NULL;
+    if (!al16({x[j], phi[j], y[j]})) return PNN_ERR_ALIGN;
     Ptrs p;
     p.in = x[j];
     p.out = y[j];
@@ -1554,12 +1567,14 @@ pnn_status parareal_combine_fwd(pnn_plan* plan, const void* const* y, const void
   if (plan->N == 1) return PNN_OK;
   if (y == nullptr || x == nullptr || r == nullptr) return PNN_ERR_NULL;
   if (rnorm2 != nullptr && scratch == nullptr) return PNN_ERR_NULL;
+  if (!al(rnorm2, 4) || !al(scratch, 256)) return PNN_ERR_ALIGN;
   hipStream_t s = (hipStream_t)stream;
   std::vector<AxpyProb> pr;
   float* sq = rnorm2 ? (float*)((char*)scratch + plan->sq_off) : nullptr;
   long off = 0;
   for (int j = 0; j + 1 < plan->N; ++j) {
     if (y[j] == nullptr || x[j + 1] == nullptr || r[j] == nullptr) return PNN_ERR_NULL;
+    if (!al16({y[j], x[j + 1], r[j]})) return PNN_ERR_ALIGN;
     AxpyProb p;
     p.a = y[j];
     p.b = x[j + 1];
@@ -1590,6 +1605,7 @@ pnn_status coarse_fwd(pnn_plan* plan, int j, const void* rt_j, const void* eta_j
   if (j < 0 || j >= plan->N - 1) return PNN_ERR_INDEX;
   if (rt_j == nullptr || eta_j == nullptr || add == nullptr || rt_next == nullptr) return PNN_ERR_NULL;
   if (rt_j == rt_next) return PNN_ERR_SHAPE;
+  if (!al16({rt_j, eta_j, add, rt_next}) || !al_ws(saved, scratch)) return PNN_ERR_ALIGN;
   Ctx c{plan, (char*)saved, (char*)scratch, (hipStream_t)stream};
   Ptrs p;
   p.in = rt_j;
@@ -1611,6 +1627,8 @@ pnn_status coarse_fwd_all(pnn_plan* plan, void* const* rt, const void* const* et
     if (eta[j] == nullptr || add[j] == nullptr) return PNN_ERR_NULL;
     if (rt[j] == rt[j + 1]) return PNN_ERR_SHAPE;
   }
+  if (!al16n(rt, 0, N) || !al16n(eta, 0, N - 1) || !al16n(add, 0, N - 1) || !al_ws(saved, scratch))
+    return PNN_ERR_ALIGN;
   Ctx c{plan, (char*)saved, (char*)scratch, (hipStream_t)stream};
   auto chained = [&](int j) {   // block j's input BN takes its sums from block j - 1
     const SegP& S = plan->coarse[j];
@@ -1635,6 +1653,8 @@ pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps
   if (plan == nullptr || ytilde == nullptr || eps == nullptr || labels == nullptr || loss == nullptr ||
       D_N == nullptr || deps == nullptr || scratch == nullptr)
     return PNN_ERR_NULL;
+  if (!al16({ytilde, eps, D_N, deps}) || !al(labels, 4) || !al(logits, 4) || !al(loss, 4) || !al(scratch, 256))
+    return PNN_ERR_ALIGN;
   const SegP& S = plan->fine[plan->N - 1];
   const SlotP& yo = S.slots[S.out];
   if (plan->classes > 4096 || yo.C > 8192) return PNN_ERR_UNSUPPORTED;
@@ -1668,6 +1688,8 @@ pnn_status pnn_sgd_step(pnn_plan* plan, int part, void* const* params, const flo
   }
   for (const T& t : ts)
     if (params[t.seg] == nullptr || grads[t.seg] == nullptr || momentum[t.seg] == nullptr) return PNN_ERR_NULL;
+  for (const T& t : ts)
+    if (!al16({params[t.seg], grads[t.seg], momentum[t.seg]})) return PNN_ERR_ALIGN;
   // launches of at most SGD_MAXT tensors from at most SGD_MAXS consecutive segments
   size_t i = 0;
   while (i < ts.size()) {
@@ -1708,6 +1730,7 @@ pnn_status coarse_bwd(pnn_plan* plan, int j, const void* D_next, const void* rt_
   if (D_next == nullptr || rt_j == nullptr || eta_j == nullptr || D_j == nullptr || deta_j == nullptr)
     return PNN_ERR_NULL;
   if (D_j == D_next) return PNN_ERR_SHAPE;
+  if (!al16({D_next, rt_j, eta_j, D_j, deta_j}) || !al_ws(saved, scratch)) return PNN_ERR_ALIGN;
   Ctx c{plan, (char*)const_cast<void*>(saved), (char*)scratch, (hipStream_t)stream};
   Ptrs p;
   p.in = rt_j;
@@ -1728,6 +1751,9 @@ pnn_status coarse_bwd_all(pnn_plan* plan, void* const* D, const void* const* rt,
     if (D[j] == nullptr) return PNN_ERR_NULL;
   for (int j = 0; j < N - 1; ++j)
     if (rt[j] == nullptr || eta[j] == nullptr || deta[j] == nullptr) return PNN_ERR_NULL;
+  if (!al16n(D, 0, N) || !al16n(rt, 0, N - 1) || !al16n(eta, 0, N - 1) ||
+      !al16n((const void* const*)deta, 0, N - 1) || !al_ws(saved, scratch))
+    return PNN_ERR_ALIGN;
   Ctx c{plan, (char*)const_cast<void*>(saved), (char*)scratch, (hipStream_t)stream};
   std::vector<const SegP*> segs;
   std::vector<Ptrs> ptrs;
@@ -1757,12 +1783,14 @@ pnn_status parareal_fine_bwd(pnn_plan* plan, const void* const* dy, const void* 
                              void* scratch, void* stream) {
   if (!ok_ctx(plan, const_cast<void*>(saved), scratch)) return PNN_ERR_NULL;
   if (dy == nullptr || x == nullptr || phi == nullptr || dx == nullptr || dphi == nullptr) return PNN_ERR_NULL;
+  if (!al_ws(saved, scratch)) return PNN_ERR_ALIGN;
   Ctx c{plan, (char*)const_cast<void*>(saved), (char*)scratch, (hipStream_t)stream};
   std::vector<const SegP*> segs;
   std::vector<Ptrs> ptrs;
   for (int j = 0; j < plan->N; ++j) {
     if (dy[j] == nullptr || x[j] == nullptr || phi[j] == nullptr || dx[j] == nullptr || dphi[j] == nullptr)
       return PNN_ERR_NULL;
+    if (!al16({dy[j], x[j], phi[j], dx[j], dphi[j]})) return PNN_ERR_ALIGN;
     Ptrs p;
     p.in = x[j];
     p.params = phi[j];
@@ -1789,6 +1817,11 @@ pnn_status parareal_bwd(pnn_plan* plan, void* const* D, const void* const* rt, c
     if (rt[j] == nullptr || eta[j] == nullptr || deta[j] == nullptr) return PNN_ERR_NULL;
     if (D[j] == D[j + 1]) return PNN_ERR_SHAPE;
   }
+  for (int j = 0; j < N; ++j)
+    if (!al16({D[j], x[j], phi[j], dx[j], dphi[j]})) return PNN_ERR_ALIGN;
+  for (int j = 0; j + 1 < N; ++j)
+    if (!al16({rt[j], eta[j], deta[j]})) return PNN_ERR_ALIGN;
+  if (!al_ws(saved, scratch)) return PNN_ERR_ALIGN;
   Ctx c{plan, (char*)const_cast<void*>(saved), (char*)scratch, (hipStream_t)stream};
   std::vector<const SegP*> segs;
   std::vector<Ptrs> ptrs;
@@ -1889,6 +1922,7 @@ pnn_status parareal_combine_bwd(pnn_plan* plan, void* const* dx, const void* con
   std::vector<AxpyProb> pr;
   for (int j = 1; j < plan->N; ++j) {
     if (dx[j] == nullptr || D[j - 1] == nullptr) return PNN_ERR_NULL;
+    if (!al16({dx[j], D[j - 1]})) return PNN_ERR_ALIGN;
     AxpyProb p;
     p.a = dx[j];
     p.b = D[j - 1];
@@ -1906,6 +1940,7 @@ pnn_status parareal_combine_bwd(pnn_plan* plan, void* const* dx, const void* con
 pnn_status pnn_pre_bwd(pnn_plan* plan, const void* image, const void* const* g, const void* const* delta,
                        const void* saved, float* const* ddelta, void* scratch, void* stream) {
   if (!ok_ctx(plan, const_cast<void*>(saved), scratch) || image == nullptr || g == nullptr) return PNN_ERR_NULL;
+  if (!al_ws(saved, scratch)) return PNN_ERR_ALIGN;
   Ctx c{plan, (char*)const_cast<void*>(saved), (char*)scratch, (hipStream_t)stream};
   std::vector<const SegP*> segs;
   std::vector<Ptrs> ptrs;
@@ -1913,6 +1948,7 @@ pnn_status pnn_pre_bwd(pnn_plan* plan, const void* image, const void* const* g, 
     const SegP& S = plan->pre[j];
     if (S.grad_bytes == 0 || ddelta == nullptr || ddelta[j] == nullptr) continue;
     if (g[j] == nullptr || delta == nullptr || delta[j] == nullptr) return PNN_ERR_NULL;
+    if (!al16({image, g[j], delta[j], ddelta[j]})) return PNN_ERR_ALIGN;
     Ptrs p;
     p.in = image;
     p.params = delta[j];
@@ -1975,6 +2011,17 @@ pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx,
 pnn_status pnn_set_streams(pnn_plan* plan, int streams) {
   if (plan == nullptr) return PNN_ERR_NULL;
   if (streams < 1 || streams > PNN_MAX_CHAINS) return PNN_ERR_INDEX;
+  // the side streams and the fork / join events, created once (kept for the plan's lifetime)
+  while (plan->side.size() + 1 < (size_t)streams) {
+    hipStream_t st;
+    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return PNN_ERR_HIP;
+    plan->side.push_back(st);
+  }
+  while (streams > 1 && plan->fj.size() < 16) {
+    hipEvent_t e;
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) return PNN_ERR_HIP;
+    plan->fj.push_back(e);
+  }
   plan->streams = streams;
   return PNN_OK;
 }

@@ -16,6 +16,16 @@ def _torch():
     return torch
 
 
+def bf16_bits(f):
+    """float32 array -> bfloat16 bit patterns (uint16), rounded to nearest even; NaN stays NaN."""
+    u = np.ascontiguousarray(f, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    nan = np.isnan(f)
+    if nan.any():
+        r[nan] = 0x7FC0
+    return r
+
+
 class ParaRealGPU:
     """Device state of one parareal network (``pnn_synth.Net``) and its training step."""
 
@@ -25,6 +35,7 @@ class ParaRealGPU:
             raise RuntimeError("ParaRealGPU needs a GPU (HIP device)")
         self.net = net
         self.plan = B.Plan(net)
+        B.pnn_set_streams(self.plan, 4)   # the fine sub-network groups on up to 4 streams
         self.coarse_chain_all = True      # coarse_bwd_all (deferred coarse weight gradients)
         self.overlap_bwd = False          # parareal_bwd: the coarse chain overlapped with the fine backward
         self.coarse_fwd_chain = True      # coarse_fwd_all (input BN sums from the previous block)
@@ -78,10 +89,7 @@ class ParaRealGPU:
             if w is None:
                 continue
             f = np.ascontiguousarray(w, dtype=np.float32)
-            if self.net.dtype == "bf16":
-                raw = (f.view(np.uint32) >> 16).astype(np.uint16).tobytes()
-            else:
-                raw = f.tobytes()
+            raw = bf16_bits(f).tobytes() if self.net.dtype == "bf16" else f.tobytes()
             buf[offs[i]:offs[i] + len(raw)] = np.frombuffer(raw, dtype=np.uint8)
         for b in range(len(seg.bns)):
             for k, key in enumerate(("gamma", "beta")):
@@ -256,8 +264,8 @@ class ParaRealGPU:
 
     def capture(self):
         """Capture one training step (forward and backward, as ``forward`` + ``backward`` run it)
-        into HIP graphs, one per part.  Run at least one eager step first (it creates the plan's
-        internal streams and events).  A replay repeats the step on what the buffers hold then."""
+        into HIP graphs, one per part (no eager step is needed first: the library's calls create
+        nothing).  A replay repeats the step on what the buffers hold then."""
         torch = _torch()
         self.graphs = {}
         for name, fn in self._parts().items():

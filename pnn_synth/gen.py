@@ -8,7 +8,10 @@ in the storage type the GPU path uses (bf16 or fp32), so that both sides consume
 * labels    ~ U{0 .. classes-1};
 * conv filters: He-normal, std sqrt(2 / fan_in), fan_in = c_in * k * k (Sec. 4: initialisation of
   He et al.), drawn directly in [c_out][k][k][c_in] order;
-* BN: gamma = 1, beta = 0;  linear head: He-normal weight [classes][C], bias 0.
+* BN: gamma = 1, beta = 0 (``net.bn_init == "unit"``, the initial state of training), or, with
+  ``net.bn_init == "random"``, gamma ~ U(0.5, 1.5) and beta ~ N(0, 0.2^2) drawn from their own
+  PCG64 stream (seed: the weight seed + 7919), as BN parameters look once training has moved them;
+  linear head: He-normal weight [classes][C], bias 0 (``"random"``: bias ~ N(0, 0.1^2)).
 
 Tensors are drawn from one PCG64 stream per config in a fixed order: pre segments j = 1..N,
 fine segments j = 1..N, coarse segments j = 1..N-1, then the head.
@@ -52,8 +55,9 @@ def segment_shapes(seg: Segment):
     return shapes
 
 
-def init_segment(seg: Segment, rng: np.random.Generator, dtype: str):
-    """Parameters of one segment: {'conv': [W per conv node or None], 'gamma': [...], 'beta': [...]}."""
+def init_segment(seg: Segment, rng: np.random.Generator, dtype: str, bn_rng=None):
+    """Parameters of one segment: {'conv': [W per conv node or None], 'gamma': [...], 'beta': [...]}.
+    ``bn_rng``: generator of random BN parameters (None: gamma = 1, beta = 0)."""
     shapes = segment_shapes(seg)
     conv = []
     for n in seg.nodes:
@@ -64,20 +68,34 @@ def init_segment(seg: Segment, rng: np.random.Generator, dtype: str):
             conv.append(to_storage(w, dtype))
         else:
             conv.append(None)
-    gamma = [np.ones(shapes[s][2]) for s in seg.bns]
-    beta = [np.zeros(shapes[s][2]) for s in seg.bns]
+    if bn_rng is None:
+        gamma = [np.ones(shapes[s][2]) for s in seg.bns]
+        beta = [np.zeros(shapes[s][2]) for s in seg.bns]
+    else:
+        gamma, beta = [], []
+        for s in seg.bns:
+            C = shapes[s][2]
+            gamma.append(to_storage(bn_rng.uniform(0.5, 1.5, C), "f32"))
+            beta.append(to_storage(0.2 * bn_rng.standard_normal(C), "f32"))
     return {"conv": conv, "gamma": gamma, "beta": beta}
 
 
 def init_params(net: Net):
     rng = np.random.Generator(np.random.PCG64(net.seeds[0]))
+    if net.bn_init == "random":
+        bn_rng = np.random.Generator(np.random.PCG64(net.seeds[0] + 7919))
+    elif net.bn_init == "unit":
+        bn_rng = None
+    else:
+        raise ValueError(net.bn_init)
     p = {
-        "pre": [init_segment(s, rng, net.dtype) for s in net.pre],
-        "fine": [init_segment(s, rng, net.dtype) for s in net.fine],
-        "coarse": [init_segment(s, rng, net.dtype) for s in net.coarse],
+        "pre": [init_segment(s, rng, net.dtype, bn_rng) for s in net.pre],
+        "fine": [init_segment(s, rng, net.dtype, bn_rng) for s in net.fine],
+        "coarse": [init_segment(s, rng, net.dtype, bn_rng) for s in net.coarse],
     }
     w = rng.standard_normal((net.classes, net.head_cin)) * np.sqrt(2.0 / net.head_cin)
-    p["head"] = {"w": to_storage(w, "f32"), "b": np.zeros(net.classes)}
+    b = np.zeros(net.classes) if bn_rng is None else to_storage(0.1 * bn_rng.standard_normal(net.classes), "f32")
+    p["head"] = {"w": to_storage(w, "f32"), "b": b}
     return p
 
 

@@ -74,6 +74,7 @@ class Net:
     head_cin: int
     seeds: Tuple[int, int, int]      # (weights, input, labels)
     input_layout: str = "nchw->nhwc"
+    bn_init: str = "unit"            # "unit": gamma = 1, beta = 0; "random": seeded gamma, beta
 
     @property
     def n_sub(self) -> int:

@@ -84,7 +84,7 @@ def test_error_codes():
     assert L.parareal_fine_fwd(p.handle, None, None, None, 1, 1, None) == -1
     assert L.pnn_set_streams(p.handle, 0) == -7                                # 1 .. 4 streams
     assert L.pnn_set_streams(p.handle, 5) == -7
-    assert L.pnn_set_streams(p.handle, 1) == 0 and L.pnn_set_streams(p.handle, 4) == 0
+    assert L.pnn_set_streams(p.handle, 1) == 0
     assert L.pnn_set_streams(None, 2) == -1
     # parareal_bwd: NULL arrays and aliased D_j / D_{j+1} are rejected before anything is enqueued
     assert L.parareal_bwd(p.handle, None, None, None, None, None, None, None, None, 1, 1, None) == -1
@@ -98,4 +98,39 @@ def test_error_codes():
     assert L.coarse_fwd_all(p.handle, D, ok, ok, 1, 1, None) == -2
     assert L.coarse_fwd_all(p.handle, ok, ok, ok, None, 1, None) == -1
     assert B.pnn_status_string(-5) == "network form not supported by this library"
+    p.close()
+
+
+def test_alignment_rules():
+    """Tensor pointers must be 16-byte aligned and workspaces 256-byte aligned: a violation is
+    rejected with PNN_ERR_ALIGN before anything is enqueued (checked here without a GPU: the
+    pointers are never dereferenced)."""
+    L = _lib_or_skip()
+    net = S.config(3, 2)
+    p = B.Plan(net)
+    N = net.n_sub
+    arr = lambda vals: (ctypes.c_void_p * len(vals))(*vals)
+    base = 1 << 30
+    ok = [base + (1 << 20) * (i + 1) for i in range(N)]
+    ws, ws2 = base, base + (1 << 28)
+    bad = list(ok)
+    bad[3] += 8                                                                # one x_j off by 8 bytes
+    A_ok, A_bad = arr(ok), arr(bad)
+    assert L.parareal_fine_fwd(p.handle, A_bad, A_ok, A_ok, ws, ws2, None) == -8
+    assert L.parareal_fine_fwd(p.handle, A_ok, A_ok, A_ok, ws + 128, ws2, None) == -8   # workspace
+    assert L.parareal_fine_bwd(p.handle, A_ok, A_ok, A_ok, ws, A_bad, A_ok, ws2, None) == -8
+    assert L.parareal_bwd(p.handle, A_bad, A_ok, A_ok, A_ok, A_ok, A_ok, A_ok, A_ok, ws, ws2, None) == -8
+    assert L.parareal_combine_fwd(p.handle, A_ok, A_bad, A_ok, None, None, None) == -8
+    assert L.parareal_combine_bwd(p.handle, A_bad, A_ok, None) == -8
+    assert L.coarse_fwd(p.handle, 0, ok[0] + 4, ok[1], ok[2], ok[3], ws, ws2, None) == -8
+    assert L.coarse_fwd_all(p.handle, A_ok, A_bad, A_ok, ws, ws2, None) == -8
+    assert L.coarse_bwd(p.handle, 0, ok[0], ok[1], ok[2], ws, ok[3] + 2, ok[4], ws2, None) == -8
+    assert L.coarse_bwd_all(p.handle, A_bad, A_ok, A_ok, ws, A_ok, ws2, None) == -8
+    assert L.pnn_pre_fwd(p.handle, base + 1 + (1 << 29), A_ok, A_ok, ws, ws2, None) == -8
+    assert L.pnn_pre_bwd(p.handle, base + (1 << 29), A_ok, A_ok, ws, A_bad, ws2, None) == -8
+    assert L.pnn_head_fwd_bwd(p.handle, ok[0], ok[1], ok[2], None, ok[3] + 2, ok[4], ok[5], ws2, None) == -8
+    assert L.pnn_head_fwd_bwd(p.handle, ok[0] + 8, ok[1], ok[2], None, ok[3], ok[4], ok[5], ws2, None) == -8
+    assert L.pnn_sgd_step(p.handle, 1, A_bad, A_ok, A_ok, ctypes.c_float(0.1), ctypes.c_float(0.9),
+                          ctypes.c_float(5e-4), 1, None) == -8
+    assert B.pnn_status_string(-8) == "a pointer is not aligned as the interface requires"
     p.close()

@@ -92,6 +92,15 @@ def test_unit_sample_reduced_batch(idx, batch):
     _assert(*check_net(S.config(idx, batch), node_subset=True))
 
 
+@pytest.mark.parametrize("idx,batch", [(1, 3), (3, 3)])
+def test_random_bn_nodes(idx, batch):
+    """bf16 node checks with seeded non-trivial BN gamma / beta (every node of the VGG workload; the
+    sampled units of the ResNet N = 16 workload)."""
+    net = S.config(idx, batch)
+    net.bn_init = "random"
+    _assert(*check_net(net, node_subset=idx != 1))
+
+
 @pytest.mark.parametrize("idx,fine_subset", [(1, None), (2, [0, 1, 3]), (3, [0, 5, 10, 15]), (4, [0, 2, 5, 7])])
 def test_sampled_nodes_full_size(idx, fine_subset):
     _assert(*check_net(S.config(idx), sample=256, fine_subset=fine_subset))

@@ -99,9 +99,14 @@ def mini_resnet(n_sub, ups, batch, dtype="f32", hw=16, coarse="config", partitio
                            partition=partition)
 
 
-def test_tiny_workload_fp32():
-    """The tiny workload itself (N = 2 basic blocks, batch 4, fp32): every tensor to 1e-4."""
-    _assert_tol(run_net(S.config(0)), 1e-4)
+@pytest.mark.parametrize("bn_init", ["unit", "random"])
+def test_tiny_workload_fp32(bn_init):
+    """The tiny workload itself (N = 2 basic blocks, batch 4, fp32): every tensor to 1e-4; also with
+    seeded non-trivial BN gamma / beta and head bias (the affine paths of the BN forward, the BN
+    backward coefficients and the ReLU mask of the data-gradient epilogue)."""
+    net = S.config(0)
+    net.bn_init = bn_init
+    _assert_tol(run_net(net), 1e-4)
 
 
 @pytest.mark.parametrize("n_sub,ups,batch", [(1, 2, 2), (2, 2, 3), (3, 2, 2), (4, 4, 3), (5, 3, 2)])
@@ -109,6 +114,14 @@ def test_resnet_forms_fp32(n_sub, ups, batch):
     """Bottleneck ResNets with strided projected units, N not a multiple of 3 (sub-networks
     straddle stages), ragged tiles: every tensor to 1e-4."""
     _assert_tol(run_net(mini_resnet(n_sub, ups, batch)), 1e-4)
+
+
+def test_resnet_forms_fp32_random_bn():
+    """A bottleneck ResNet (N = 4, strided projected units, straddling sub-networks) with seeded
+    non-trivial BN gamma / beta: every tensor to 1e-4."""
+    net = mini_resnet(4, 4, 3)
+    net.bn_init = "random"
+    _assert_tol(run_net(net), 1e-4)
 
 
 @pytest.mark.parametrize("n_sub,ups,batch", [(2, 2, 3), (3, 2, 2), (4, 4, 2)])
@@ -133,10 +146,13 @@ def test_vgg_paper_coarse_fp32():
     _assert_tol(run_net(net), 1e-4)
 
 
-def test_vgg_workload_structure_fp32():
-    """The VGG-16 workload's network (all 13 convolutions, 2x2 pools, N = 4) in fp32 at batch 3."""
+@pytest.mark.parametrize("bn_init", ["unit", "random"])
+def test_vgg_workload_structure_fp32(bn_init):
+    """The VGG-16 workload's network (all 13 convolutions, 2x2 pools, N = 4) in fp32 at batch 3,
+    also with seeded non-trivial BN gamma / beta."""
     net = S.config(1, 3)
     net.dtype = "f32"
+    net.bn_init = bn_init
     _assert_tol(run_net(net), 1e-4)
 
 
