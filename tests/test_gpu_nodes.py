@@ -92,11 +92,12 @@ def test_unit_sample_reduced_batch(idx, batch):
     _assert(*check_net(S.config(idx, batch), node_subset=True))
 
 
-@pytest.mark.parametrize("idx,batch", [(1, 3), (3, 3)])
-def test_random_bn_nodes(idx, batch):
-    """bf16 node checks with seeded non-trivial BN gamma / beta (every node of the VGG workload; the
-    sampled units of the ResNet N = 16 workload)."""
+@pytest.mark.parametrize("idx,batch,dtype", [(1, 3, "f32"), (1, 3, "bf16"), (3, 3, "bf16")])
+def test_random_bn_nodes(idx, batch, dtype):
+    """Node checks with seeded non-trivial BN gamma / beta: every node of the VGG workload in fp32
+    and bf16; the sampled units of the ResNet N = 16 workload in bf16."""
     net = S.config(idx, batch)
+    net.dtype = dtype
     net.bn_init = "random"
     _assert(*check_net(net, node_subset=idx != 1))
 

@@ -146,13 +146,14 @@ def test_vgg_paper_coarse_fp32():
     _assert_tol(run_net(net), 1e-4)
 
 
-@pytest.mark.parametrize("bn_init", ["unit", "random"])
-def test_vgg_workload_structure_fp32(bn_init):
-    """The VGG-16 workload's network (all 13 convolutions, 2x2 pools, N = 4) in fp32 at batch 3,
-    also with seeded non-trivial BN gamma / beta."""
+def test_vgg_workload_structure_fp32():
+    """The VGG-16 workload's network (all 13 convolutions, 2x2 pools, N = 4) in fp32 at batch 3.
+    (With seeded non-trivial BN gamma / beta the same network has a 2x2 pool window in g^2 whose two
+    largest activations differ by 7.7e-6 relative, within reach of fp32 rounding, so the pool's
+    gradient routing can flip end to end; that form is checked node by node, teacher-forced, in
+    test_gpu_nodes.py::test_random_bn_nodes.)"""
     net = S.config(1, 3)
     net.dtype = "f32"
-    net.bn_init = bn_init
     _assert_tol(run_net(net), 1e-4)
 
 
@@ -214,9 +215,9 @@ def test_streams_do_not_change_results(idx, batch):
 @pytest.mark.gpu
 @pytest.mark.parametrize("idx,batch,streams", [(2, 2, 4), (3, 4, 4), (3, 4, 1)])
 def test_graph_replay_matches_eager(idx, batch, streams):
-    """The step captured into HIP graphs (one per part) and replayed gives bit-identical loss,
-    logits, parameter gradients and input gradients to the eager step, on every replay, with eager
-    steps, output clearing and synchronisations in between."""
+    """The step captured into HIP graphs (one per part, captured before any eager call) and replayed
+    gives bit-identical loss, logits, parameter gradients and input gradients to the eager step, on
+    every replay, with eager steps, output clearing and synchronisations in between."""
     import torch
     from paper_2103_08802_amd import binding as B
     from paper_2103_08802_amd.step import ParaRealGPU
@@ -229,11 +230,18 @@ def test_graph_replay_matches_eager(idx, batch, streams):
     def outputs():
         return [t.clone() for t in [g.loss, g.logits, g.deps] + g.ddelta + g.dphi + g.deta + g.dx]
 
+    g.capture()                          # before any eager step: the library creates nothing in a call
+    torch.cuda.synchronize()
+    g.replay_forward()
+    g.replay_backward()
+    torch.cuda.synchronize()
+    first = outputs()
     g.forward()
     g.backward()
     torch.cuda.synchronize()
     ref = outputs()
-    g.capture()
+    for a, b in zip(first, ref):
+        assert torch.equal(a, b)
     for _ in range(3):
         for t in [g.loss, g.logits, g.deps] + g.ddelta + g.dphi + g.deta + g.dx:
             t.zero_()                    # eager work between replays; the replay rewrites them
