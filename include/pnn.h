@@ -72,7 +72,8 @@ enum {
   PNN_ERR_UNSUPPORTED = -5, /* a valid network this library does not run (e.g. channels not a multiple of 16) */
   PNN_ERR_HIP = -6,         /* a HIP call failed */
   PNN_ERR_INDEX = -7,       /* sub-network / coarse block index out of range */
-  PNN_ERR_ALIGN = -8        /* a pointer violates the alignment rules above */
+  PNN_ERR_ALIGN = -8,       /* a pointer violates the alignment rules above */
+  PNN_ERR_TOO_LARGE = -9    /* the problem exceeds the fixed scratch of an allocation-free entry point */
 };
 
 typedef enum { PNN_F32 = 0, PNN_BF16 = 1 } pnn_dtype;
@@ -186,6 +187,18 @@ pnn_status coarse_fwd_all(pnn_plan* plan, void* const* rt, const void* const* et
 pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps,
                             const int32_t* labels, float* logits, float* loss, void* D_N,
                             float* deps, void* scratch, void* stream);
+
+/* For callers that cannot allocate device memory or hand over a workspace (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): pnn_head_fwd_bwd with the same
+ * arguments and results, minus the scratch workspace.  Its temporaries (B * (C + classes + 1)
+ * floats for a batch of B and C channels of ytilde) live in a fixed 4 MiB device array of the
+ * library, one per GPU, kept until the process ends; a larger problem returns PNN_ERR_TOO_LARGE.
+ * Calls nothing that allocates.  The first call on a device (with that device current) looks up
+ * the array's address (PNN_ERR_HIP if that fails).  Every call on one GPU shares that array:
+ * calls that overlap in time on one GPU race. */
+pnn_status pnn_head_fwd_bwd_noalloc(pnn_plan* plan, const void* ytilde, const float* eps,
+                                    const int32_t* labels, float* logits, float* loss, void* D_N,
+                                    float* deps, void* stream);
 
 /* ---- backward (Alg. para3) ---------------------------------------------------------------- */
 

@@ -18,7 +18,7 @@ PNN_WS_SAVED, PNN_WS_SCRATCH = 0, 1
 OPS = {"conv": 0, "bnact": 1, "maxpool3": 2}
 STATUS = {0: "PNN_OK", -1: "PNN_ERR_NULL", -2: "PNN_ERR_SHAPE", -3: "PNN_ERR_DTYPE",
           -4: "PNN_ERR_WORKSPACE", -5: "PNN_ERR_UNSUPPORTED", -6: "PNN_ERR_HIP", -7: "PNN_ERR_INDEX",
-          -8: "PNN_ERR_ALIGN"}
+          -8: "PNN_ERR_ALIGN", -9: "PNN_ERR_TOO_LARGE"}
 
 # every symbol include/pnn.h declares
 EXPORTS = ["pnn_plan_create", "pnn_plan_destroy", "pnn_workspace_size", "pnn_param_layout",
@@ -27,7 +27,7 @@ EXPORTS = ["pnn_plan_create", "pnn_plan_destroy", "pnn_workspace_size", "pnn_par
            "parareal_combine_bwd", "pnn_pre_bwd", "pnn_status_string", "pnn_inspect",
            "pnn_timing_enable", "pnn_timing_read", "pnn_sgd_step", "coarse_bwd_all", "coarse_fwd_all",
            "pnn_set_streams",
-           "parareal_bwd"]
+           "parareal_bwd", "pnn_head_fwd_bwd_noalloc"]
 
 
 class PnnError(RuntimeError):
@@ -80,6 +80,7 @@ def lib():
     L.parareal_combine_fwd.argtypes = [_vp, _PP, _PP, _PP, _vp, _vp, _vp]
     L.coarse_fwd.argtypes = [_vp, i, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
     L.pnn_head_fwd_bwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+    L.pnn_head_fwd_bwd_noalloc.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
     L.coarse_bwd.argtypes = [_vp, i, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
     L.parareal_fine_bwd.argtypes = [_vp, _PP, _PP, _PP, _vp, _PP, _PP, _vp, _vp]
     L.parareal_combine_bwd.argtypes = [_vp, _PP, _PP, _vp]
@@ -239,6 +240,12 @@ def pnn_head_fwd_bwd(plan, ytilde, eps, labels, logits, loss, D_N, deps, scratch
     _check(lib().pnn_head_fwd_bwd(plan.handle, _ptr(ytilde), _ptr(eps), _ptr(labels), _ptr(logits),
                                   _ptr(loss), _ptr(D_N), _ptr(deps), _ptr(scratch), stream),
            "pnn_head_fwd_bwd")
+
+
+def pnn_head_fwd_bwd_noalloc(plan, ytilde, eps, labels, logits, loss, D_N, deps, stream):
+    _check(lib().pnn_head_fwd_bwd_noalloc(plan.handle, _ptr(ytilde), _ptr(eps), _ptr(labels), _ptr(logits),
+                                          _ptr(loss), _ptr(D_N), _ptr(deps), stream),
+           "pnn_head_fwd_bwd_noalloc")
 
 
 def coarse_bwd(plan, j, D_next, rt_j, eta_j, saved, D_j, deta_j, scratch, stream):

@@ -1369,6 +1369,7 @@ const char* pnn_status_string(pnn_status s) {
     case PNN_ERR_HIP: return "a HIP call failed";
     case PNN_ERR_INDEX: return "index out of range";
     case PNN_ERR_ALIGN: return "a pointer is not aligned as the interface requires";
+    case PNN_ERR_TOO_LARGE: return "the problem exceeds the fixed scratch of an allocation-free entry point";
     default: return "unknown status";
   }
 }
@@ -1647,6 +1648,23 @@ pnn_status coarse_fwd_all(pnn_plan* plan, void* const* rt, const void* const* et
   }
   return PNN_OK;
 }
+
+}  // extern "C"
+
+// head shape of a plan, for the allocation-free head entry point (noalloc.hip)
+int pnn::head_geometry(const pnn_plan* p, int* B, int* HW, int* C, int* K, int* dtype) {
+  if (p == nullptr) return PNN_ERR_NULL;
+  const SegP& S = p->fine[p->N - 1];
+  const SlotP& yo = S.slots[S.out];
+  *B = p->B;
+  *HW = yo.H * yo.W;
+  *C = yo.C;
+  *K = p->classes;
+  *dtype = p->dtype;
+  return PNN_OK;
+}
+
+extern "C" {
 
 pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps, const int32_t* labels,
                             float* logits, float* loss, void* D_N, float* deps, void* scratch, void* stream) {

@@ -11,6 +11,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+struct pnn_plan;
+
 #define PNN_MAXG 20
 #define PNN_BN_EPS 1e-5f
 
@@ -258,6 +260,8 @@ int launch_maxpool3(const MaxPool3Launch& L, int tiles, int dtype, hipStream_t s
 int launch_transpose(const TransposeLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_sub(const AxpyLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_sumsq(const float* part, int n, float* out, hipStream_t s);
+// shape of the head of a plan (batch, pixels and channels of ytilde, classes, storage type)
+int head_geometry(const pnn_plan* p, int* B, int* HW, int* C, int* K, int* dtype);
 int launch_head(const void* yt, const float* eps, const int32_t* labels, float* logits,
                 float* loss, void* D_N, float* deps, float* scratch, int B, int HW, int C,
                 int K, int dtype, hipStream_t s);
