@@ -260,11 +260,18 @@ pnn_status pnn_pre_bwd(pnn_plan* plan, const void* image, const void* const* g,
  *                   buffer (float, pnn_param_layout(.., 1, ..)); momentum[j]: float buffer laid out
  *                   like the gradient buffer, updated in place (zero before the first step).
  *   part 3:         the head: params[0] = eps, grads[0] = deps, momentum[0]; K * C + K floats.
+ * master (nullable; used by PNN_BF16 plans, parts 0 - 2): master[j] is a float buffer laid out
+ * like the gradient buffer that holds an fp32 master copy of the segment's bf16 filters.  With it,
+ * each filter update reads w from the master (master_init != 0: from the stored bf16 filter, for
+ * the first step), writes the updated fp32 w back to the master and its nearest-even bf16 rounding
+ * to params, so updates smaller than half a bf16 ulp (weight decay, late-training steps)
+ * accumulate instead of being rounded away.  Without it the bf16 filter itself is the state.
+ * BN parameters and the head are float and need no master.
  * Buffers may not alias one another.  PNN_ERR_INDEX for another part; PNN_ERR_NULL for a missing
  * buffer of a segment that has parameters. */
 pnn_status pnn_sgd_step(pnn_plan* plan, int part, void* const* params, const float* const* grads,
-                        float* const* momentum, float lr, float mu, float weight_decay, int nesterov,
-                        void* stream);
+                        float* const* momentum, float* const* master, int master_init, float lr,
+                        float mu, float weight_decay, int nesterov, void* stream);
 
 /* ---- misc ----------------------------------------------------------------------------------- */
 

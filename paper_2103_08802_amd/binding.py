@@ -96,7 +96,7 @@ def lib():
     L.coarse_fwd_all.argtypes = [_vp, _PP, _PP, _PP, _vp, _vp, _vp]
     L.parareal_bwd.argtypes = [_vp, _PP, _PP, _PP, _PP, _PP, _PP, _PP, _PP, _vp, _vp, _vp]
     f = ctypes.c_float
-    L.pnn_sgd_step.argtypes = [_vp, i, _PP, _PP, _PP, f, f, f, i, _vp]
+    L.pnn_sgd_step.argtypes = [_vp, i, _PP, _PP, _PP, _PP, i, f, f, f, i, _vp]
     for name in EXPORTS:
         getattr(L, name)          # every declared entry point must be exported
     _lib = L
@@ -299,12 +299,14 @@ def parareal_bwd(plan, D, rt, eta, deta, x, phi, dx, dphi, saved, scratch, strea
            "parareal_bwd")
 
 
-def pnn_sgd_step(plan, part, params, grads, momentum, lr, mu, weight_decay, nesterov, stream):
+def pnn_sgd_step(plan, part, params, grads, momentum, lr, mu, weight_decay, nesterov, stream,
+                 master=None, master_init=False):
     a1, k1 = _arr(params)
     a2, k2 = _arr(grads)
     a3, k3 = _arr(momentum)
-    _check(lib().pnn_sgd_step(plan.handle, part, a1, a2, a3, lr, mu, weight_decay, int(bool(nesterov)),
-                              stream), "pnn_sgd_step")
+    a4, k4 = _arr(master) if master is not None else (None, None)
+    _check(lib().pnn_sgd_step(plan.handle, part, a1, a2, a3, a4, int(bool(master_init)), lr, mu,
+                              weight_decay, int(bool(nesterov)), stream), "pnn_sgd_step")
 
 
 def pnn_pre_bwd(plan, image, g, delta, saved, ddelta, scratch, stream):

@@ -443,6 +443,31 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
     }
   __syncthreads();
 
+  // Forward BN statistics are summed about a per-tile pivot, the tile's first stored row (pro_s is
+  // free once the K loop is done): (sum d, sum d^2) with d = value - pivot do not cancel when a
+  // channel's mean is large against its spread; the tile's mean and sum of squared deviations are
+  // formed from them below.
+  const bool fstats = MODE == MODE_FWD && (P.flags & EPI_STATS) != 0;
+  float* piv_s = (float*)pro_s;
+  float pv[VE];
+  if (fstats) {
+    if (tid < ncc) {
+      Chunk<T> r0, x0;
+      unpack_chunk<T>(pre[0], r0);
+      unpack_chunk<T>(pre2[0], x0);
+#pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        float v = acc_s[c0 + e];
+        if (P.res) v += r0.v[e];
+        if (P.ext) v += x0.v[e];
+        piv_s[c0 + e] = St<T>::rnd(v);
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int e = 0; e < VE; ++e) pv[e] = fstats ? piv_s[c0 + e] : 0.f;
+
   float s1[VE], s2[VE];
 #pragma unroll
   for (int e = 0; e < VE; ++e) s1[e] = s2[e] = 0.f;
@@ -471,9 +496,9 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
       store_chunk<T>(P.out, idx, v);
 #pragma unroll
       for (int e = 0; e < VE; ++e) {
-        const float vr = St<T>::rnd(v[e]);
-        s1[e] += vr;
-        s2[e] += vr * vr;
+        const float d = St<T>::rnd(v[e]) - pv[e];
+        s1[e] += d;
+        s2[e] += d * d;
       }
     } else {
       if (P.flags & EPI_ACC_IN) {
@@ -578,7 +603,14 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
         b += red3[256 + q * BNc + tid];
       }
       float2* pp = (float2*)P.part + (long)tm * P.ncol + n0 + tid;
-      *pp = make_float2(a, b);
+      if (MODE == MODE_FWD) {
+        // the tile's mean and sum of squared deviations from its pivoted sums
+        const float n = (float)min(BM, P.M - tm * BM);
+        const float am = a / n;
+        *pp = make_float2(piv_s[tid] + am, fmaxf(b - a * am, 0.f));
+      } else {
+        *pp = make_float2(a, b);
+      }
     }
   }
 }
@@ -1299,6 +1331,7 @@ __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
   __shared__ __attribute__((aligned(16))) T zs[MODE == MODE_BWD ? TR * SZ : 8];
   __shared__ float2 pro_s[MODE == MODE_FWD ? MAXK : 1];
   __shared__ float2 red[WR][NC];
+  __shared__ float piv[MODE == MODE_FWD ? NC : 1];
 
   const int gi = find_group(L);
   const ConvProb& P = L.p[gi];
@@ -1382,9 +1415,24 @@ __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
     }
   };
 
+  // Forward BN statistics are summed about a per-workgroup pivot, the first row's output (an fp32
+  // dot product here), so that they do not cancel when a channel's mean is large against its spread
+  if (MODE == MODE_FWD && stats && tid < ncl) {
+    float a = 0.f;
+    for (int k = 0; k < K; ++k) {
+      float x = St<T>::ld(xin, (long)m_begin * K + k);
+      if (pro) x = fmaxf(fmaf(x, P.pro[k], P.pro[P.Cg + k]), 0.0f);
+      a = fmaf(x, St<T>::ld(P.wmat, (long)(c0 + tid) * K + k), a);
+    }
+    piv[tid] = St<T>::rnd(a);
+  }
   float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
   fetch(m_begin);
-  __syncthreads();                                    // pro_s
+  __syncthreads();                                    // pro_s, piv
+  float pv[4] = {0.f, 0.f, 0.f, 0.f};
+  if (MODE == MODE_FWD && stats && active)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pv[i] = piv[cl + i];
   for (int mt = m_begin; mt < m_end; mt += TR) {
 #pragma unroll
     for (int i = 0; i < NLA; ++i) {
@@ -1435,10 +1483,10 @@ __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             o[i] = v[i];
-            const float vr = St<T>::rnd(v[i]);
+            const float d = St<T>::rnd(v[i]) - pv[i];
             if (stats && mv) {
-              s1[i] += vr;
-              s2[i] += vr * vr;
+              s1[i] += d;
+              s2[i] += d * d;
             }
           }
         } else {
@@ -1521,7 +1569,13 @@ __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
       a += red[w][tid].x;
       b += red[w][tid].y;
     }
-    ((float2*)P.part)[(long)tm * ncol + c0 + tid] = make_float2(a, b);
+    if (MODE == MODE_FWD) {
+      // the workgroup's mean and sum of squared deviations from its pivoted sums
+      const float am = a / (float)(m_end - m_begin);
+      ((float2*)P.part)[(long)tm * ncol + c0 + tid] = make_float2(piv[tid] + am, fmaxf(b - a * am, 0.f));
+    } else {
+      ((float2*)P.part)[(long)tm * ncol + c0 + tid] = make_float2(a, b);
+    }
   }
 }
 

@@ -61,6 +61,54 @@ __global__ __launch_bounds__(1024) void colred_kernel(const ColRedLaunch L) {
     }
     return;
   }
+  if (P.mode == RED_BN_FWD) {
+    // partial row r holds, per channel, the mean and the sum of squared deviations of its n_r rows
+    // (rows of rowh, the last one ragged); combined about the overall mean in fp64, fixed order:
+    // M2 = sum_r M2_r + n_r (mean_r - mean)^2
+    constexpr int CH = RED_COLS / 2, RLN = 1024 / CH;
+    double (*red1)[CH] = (double (*)[CH])&red[0][0];
+    const int C = P.ncols / 2;
+    const int cl = threadIdx.x % CH, rl = threadIdx.x / CH;
+    const int c = (blockIdx.x - P.tile_begin) * CH + cl;
+    const double M = (double)P.count;
+    const float2* pp = (const float2*)P.part + c;
+    auto rows_of = [&](int r) { return (double)min((long)P.rowh, P.count - (long)r * P.rowh); };
+    double a = 0.0;
+    if (c < C)
+      for (int r = rl; r < P.rows; r += RLN) a += rows_of(r) * (double)pp[(long)r * C].x;
+    red1[rl][cl] = a;
+    __syncthreads();
+#pragma unroll
+    for (int h = RLN / 2; h >= 1; h >>= 1) {
+      if (rl < h) red1[rl][cl] += red1[rl + h][cl];
+      __syncthreads();
+    }
+    const double mean = red1[0][cl] / M;
+    __syncthreads();
+    double b = 0.0;
+    if (c < C)
+      for (int r = rl; r < P.rows; r += RLN) {
+        const float2 v = pp[(long)r * C];
+        const double d = (double)v.x - mean;
+        b += (double)v.y + rows_of(r) * d * d;
+      }
+    red1[rl][cl] = b;
+    __syncthreads();
+#pragma unroll
+    for (int h = RLN / 2; h >= 1; h >>= 1) {
+      if (rl < h) red1[rl][cl] += red1[rl + h][cl];
+      __syncthreads();
+    }
+    if (rl != 0 || c >= C) return;
+    const double var = red1[0][cl] / M;
+    const float invstd = (float)(1.0 / sqrt(var + (double)PNN_BN_EPS));
+    const float scale = P.gamma[c] * invstd;
+    P.stats[c] = (float)mean;
+    P.stats[C + c] = invstd;
+    P.stats[2 * C + c] = scale;
+    P.stats[3 * C + c] = P.beta[c] - (float)mean * scale;
+    return;
+  }
   const int c0 = (blockIdx.x - P.tile_begin) * RED_COLS;
   const int cl = threadIdx.x % RED_COLS;
   const int rl = threadIdx.x / RED_COLS;
@@ -102,17 +150,7 @@ __global__ __launch_bounds__(1024) void colred_kernel(const ColRedLaunch L) {
   const int c = col / 2;
   const double s1 = sum[cl], s2 = sum[cl + 1];
   const double M = (double)P.count;
-  if (P.mode == RED_BN_FWD) {
-    const double mean = s1 / M;
-    double var = s2 / M - mean * mean;
-    if (var < 0.0) var = 0.0;
-    const float invstd = (float)(1.0 / sqrt(var + (double)PNN_BN_EPS));
-    const float scale = P.gamma[c] * invstd;
-    P.stats[c] = (float)mean;
-    P.stats[C + c] = invstd;
-    P.stats[2 * C + c] = scale;
-    P.stats[3 * C + c] = P.beta[c] - (float)mean * scale;
-  } else {
+  {
     // dL/dz = c1 (dbn - mb - xhat mbx), xhat = (z - mean) invstd, c1 = gamma invstd, mb = sum dbn / M,
     // mbx = sum dbn xhat / M; written as A dbn + B z + K per channel
     P.dbeta[c] = (float)s1;
@@ -141,9 +179,17 @@ __global__ __launch_bounds__(256) void colstat_kernel(const ColStatLaunch L) {
   const int ncc = P.C / VE;
   const int RL = 256 / ncc;
   const int cc = threadIdx.x % ncc, rl = threadIdx.x / ncc;
-  float s1[VE], s2[VE];
+  // sums about a pivot, the workgroup's first row, so that they do not cancel when a channel's mean
+  // is large against its spread
+  float s1[VE], s2[VE], pv[VE];
 #pragma unroll
   for (int e = 0; e < VE; ++e) s1[e] = s2[e] = 0.f;
+  {
+    Chunk<T> c;
+    load_chunk<T>(P.x, r0 * P.C + cc * VE, c);
+#pragma unroll
+    for (int e = 0; e < VE; ++e) pv[e] = c.v[e];
+  }
   if (rl < RL) {
     long r = r0 + rl;
     for (; r + 3 * RL < r1; r += 4 * RL) {
@@ -156,8 +202,9 @@ __global__ __launch_bounds__(256) void colstat_kernel(const ColStatLaunch L) {
         unpack_chunk<T>(u[k], c);
 #pragma unroll
         for (int e = 0; e < VE; ++e) {
-          s1[e] += c.v[e];
-          s2[e] += c.v[e] * c.v[e];
+          const float d = c.v[e] - pv[e];
+          s1[e] += d;
+          s2[e] += d * d;
         }
       }
     }
@@ -166,8 +213,9 @@ __global__ __launch_bounds__(256) void colstat_kernel(const ColStatLaunch L) {
       load_chunk<T>(P.x, r * P.C + cc * VE, c);
 #pragma unroll
       for (int e = 0; e < VE; ++e) {
-        s1[e] += c.v[e];
-        s2[e] += c.v[e] * c.v[e];
+        const float d = c.v[e] - pv[e];
+        s1[e] += d;
+        s2[e] += d * d;
       }
     }
 #pragma unroll
@@ -181,7 +229,9 @@ __global__ __launch_bounds__(256) void colstat_kernel(const ColStatLaunch L) {
       a += v.x;
       b += v.y;
     }
-    ((float2*)P.part)[(long)tile * P.C + c] = make_float2(a, b);
+    // the workgroup's mean and sum of squared deviations
+    const float am = a / (float)(r1 - r0);
+    ((float2*)P.part)[(long)tile * P.C + c] = make_float2(St<T>::ld(P.x, r0 * P.C + c) + am, fmaxf(b - a * am, 0.f));
   }
 }
 
@@ -242,14 +292,19 @@ __global__ __launch_bounds__(256) void sgd_kernel(const SgdLaunch L) {
   float* vb = (float*)((char*)L.v[E.seg] + E.g_off) + i0;
   const bool nest = L.nesterov != 0;
   const int n = (int)min((long)8, (long)E.count - i0);
+  // fp32 master copy of a storage-type (bf16) filter: the update runs on it and the stored filter
+  // is its rounding to nearest even, so updates below half a bf16 ulp accumulate
+  float* mb = (!E.f32 && sizeof(T) == 2 && L.m[E.seg] != nullptr)
+                  ? (float*)((char*)L.m[E.seg] + E.g_off) + i0 : nullptr;
+  const bool from_master = mb != nullptr && !L.init;
   float w[8], g[8], v[8];
   if (n == 8) {
     const float4 g0 = *(const float4*)gb, g1 = *(const float4*)(gb + 4);
     const float4 v0 = *(const float4*)vb, v1 = *(const float4*)(vb + 4);
     g[0] = g0.x; g[1] = g0.y; g[2] = g0.z; g[3] = g0.w; g[4] = g1.x; g[5] = g1.y; g[6] = g1.z; g[7] = g1.w;
     v[0] = v0.x; v[1] = v0.y; v[2] = v0.z; v[3] = v0.w; v[4] = v1.x; v[5] = v1.y; v[6] = v1.z; v[7] = v1.w;
-    if (E.f32 || sizeof(T) == 4) {
-      const float* wp = (const float*)pb + i0;
+    if (E.f32 || sizeof(T) == 4 || from_master) {
+      const float* wp = from_master ? mb : (const float*)pb + i0;
       const float4 w0 = *(const float4*)wp, w1 = *(const float4*)(wp + 4);
       w[0] = w0.x; w[1] = w0.y; w[2] = w0.z; w[3] = w0.w; w[4] = w1.x; w[5] = w1.y; w[6] = w1.z; w[7] = w1.w;
     } else {
@@ -268,16 +323,25 @@ __global__ __launch_bounds__(256) void sgd_kernel(const SgdLaunch L) {
       *(float4*)(wp + 4) = make_float4(w[4], w[5], w[6], w[7]);
     } else {
       store_chunk<uint16_t>(pb, i0, w);
+      if (mb != nullptr) {
+        *(float4*)mb = make_float4(w[0], w[1], w[2], w[3]);
+        *(float4*)(mb + 4) = make_float4(w[4], w[5], w[6], w[7]);
+      }
     }
     return;
   }
   for (int e = 0; e < n; ++e) {        // tail of the tensor
-    float we = (E.f32 || sizeof(T) == 4) ? ((const float*)pb)[i0 + e] : St<uint16_t>::ld(pb, i0 + e);
+    float we = (E.f32 || sizeof(T) == 4) ? ((const float*)pb)[i0 + e]
+               : from_master ? mb[e] : St<uint16_t>::ld(pb, i0 + e);
     float ve = vb[e];
     sgd_elem(we, gb[e], ve, L.lr, L.mu, L.wd, nest);
     vb[e] = ve;
-    if (E.f32 || sizeof(T) == 4) ((float*)pb)[i0 + e] = we;
-    else St<uint16_t>::st(pb, i0 + e, we);
+    if (E.f32 || sizeof(T) == 4) {
+      ((float*)pb)[i0 + e] = we;
+    } else {
+      St<uint16_t>::st(pb, i0 + e, we);
+      if (mb != nullptr) mb[e] = we;
+    }
   }
 }
 

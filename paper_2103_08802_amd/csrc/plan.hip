@@ -60,6 +60,8 @@ struct BnP {
   bool bnsum = false;        // its backward sums come from bnsum_kernel (no data-gradient tile)
   int fwd_tiles_in = 0;      // coarse input BN: forward sums from the previous block's last
                              // convolution (coarse_fwd_all), in its row tiles; 0 = not chained
+  int fwd_rows = 0;          // rows of the normalised tensor per forward partial row
+  int fwd_rows_in = 0;       // the same for the chained sums
 };
 
 struct SegP {
@@ -403,7 +405,8 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
       }
     const bool sh = S.short_tiles;
     const int pw_rows = 64 * pw_wm(M, b.C, sh);
-    b.fwd_tiles = (int)cdiv(M, b.slot == 0 ? COLSTAT_ROWS : pwf ? pw_rows : 64 * conv_rows_wm(kf, M, b.C, sh));
+    b.fwd_rows = b.slot == 0 ? COLSTAT_ROWS : pwf ? pw_rows : 64 * conv_rows_wm(kf, M, b.C, sh);
+    b.fwd_tiles = (int)cdiv(M, b.fwd_rows);
     b.bwd_tiles = (int)cdiv(M, b.bnsum ? BNSUM_TR * bnsum_wm(M, b.C, sh) : pwb ? pw_rows : 64 * conv_rows_wm(kb, M, b.C, sh));
     if (b.bnact_consumer) {
       const NodeP& c = S.nodes[sl.bn_consumers[0]];
@@ -583,11 +586,13 @@ int fire_colred(std::vector<ColRedProb>& probs, hipStream_t s) {
       [&](const ColRedLaunch& L, int tiles, size_t) { return launch_colred(L, tiles, s); });
 }
 
-ColRedProb bn_fwd_red(const float* part, int rows, const float* gamma, float* stats, int C, long count) {
+ColRedProb bn_fwd_red(const float* part, int rows, int rowh, const float* gamma, float* stats, int C,
+                      long count) {
   ColRedProb r;
   std::memset(&r, 0, sizeof(r));
   r.part = part;
   r.rows = rows;
+  r.rowh = rowh;
   r.ncols = 2 * C;
   r.mode = RED_BN_FWD;
   r.gamma = gamma;
@@ -764,6 +769,7 @@ int run_fwd_begin(const Ctx& c, const std::vector<const SegP*>& segs, const std:
       p.C = s0.C;
       if (!chained) cs.push_back(p);
       fw.push_back(bn_fwd_red(p.part, chained ? b.fwd_tiles_in : b.fwd_tiles,
+                              chained ? b.fwd_rows_in : b.fwd_rows,
                               (const float*)(cp(ptrs[i].params) + b.p_off), stats_ptr(c, S, s0.bn), b.C, p.M));
     }
     int e = grouped<ColStatLaunch>(
@@ -840,7 +846,7 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
         if (so.bn >= 0) {
           const BnP& b = S.bns[so.bn];
           const long cnt = (long)B * so.H * so.W;
-          fw.push_back(bn_fwd_red(part_ptr(c, S, so.bn), S.bns[so.bn].fwd_tiles,
+          fw.push_back(bn_fwd_red(part_ptr(c, S, so.bn), b.fwd_tiles, b.fwd_rows,
                                   (const float*)(cp(P.params) + b.p_off), stats_ptr(c, S, so.bn), b.C, cnt));
         }
       }
@@ -1436,7 +1442,10 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
     t.k = prod->k; t.Cg = prod->cin; t.P = prod->Ho; t.Q = prod->Wo; t.ncol = prod->cout;
     t.M = p->B * prod->Ho * prod->Wo;
     set_tiles(t, pv.short_tiles);
-    if (t.ncol == nx.bns[bn].C && t.tiles_m <= cdiv(t.M, 64)) nx.bns[bn].fwd_tiles_in = t.tiles_m;
+    if (t.ncol == nx.bns[bn].C && t.tiles_m <= cdiv(t.M, 64)) {
+      nx.bns[bn].fwd_tiles_in = t.tiles_m;
+      nx.bns[bn].fwd_rows_in = 64 * t.wm;
+    }
   }
   // workspace layout: saved = [pre | fine | coarse]; scratch = [shared | per segment]
   size_t sv = 0;
@@ -1683,8 +1692,8 @@ pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps
 }
 
 pnn_status pnn_sgd_step(pnn_plan* plan, int part, void* const* params, const float* const* grads,
-                        float* const* momentum, float lr, float mu, float weight_decay, int nesterov,
-                        void* stream) {
+                        float* const* momentum, float* const* master, int master_init, float lr,
+                        float mu, float weight_decay, int nesterov, void* stream) {
   if (plan == nullptr || params == nullptr || grads == nullptr || momentum == nullptr) return PNN_ERR_NULL;
   if (part < 0 || part > 3) return PNN_ERR_INDEX;
   const hipStream_t st = (hipStream_t)stream;
@@ -1706,8 +1715,13 @@ pnn_status pnn_sgd_step(pnn_plan* plan, int part, void* const* params, const flo
   }
   for (const T& t : ts)
     if (params[t.seg] == nullptr || grads[t.seg] == nullptr || momentum[t.seg] == nullptr) return PNN_ERR_NULL;
-  for (const T& t : ts)
-    if (!al16({params[t.seg], grads[t.seg], momentum[t.seg]})) return PNN_ERR_ALIGN;
+  // the master copies of storage-type filters (bf16 plans, parts 0 - 2)
+  const bool use_master = master != nullptr && plan->dtype == PNN_BF16 && part != 3;
+  for (const T& t : ts) {
+    if (use_master && !t.f32 && master[t.seg] == nullptr) return PNN_ERR_NULL;
+    if (!al16({params[t.seg], grads[t.seg], momentum[t.seg], use_master ? master[t.seg] : nullptr}))
+      return PNN_ERR_ALIGN;
+  }
   // launches of at most SGD_MAXT tensors from at most SGD_MAXS consecutive segments
   size_t i = 0;
   while (i < ts.size()) {
@@ -1717,6 +1731,7 @@ pnn_status pnn_sgd_step(pnn_plan* plan, int part, void* const* params, const flo
     L.mu = mu;
     L.wd = weight_decay;
     L.nesterov = nesterov != 0;
+    L.init = master_init != 0;
     const int seg0 = ts[i].seg;
     int chunks = 0;
     while (i < ts.size() && L.nt < SGD_MAXT && ts[i].seg - seg0 < SGD_MAXS) {
@@ -1727,6 +1742,7 @@ pnn_status pnn_sgd_step(pnn_plan* plan, int part, void* const* params, const flo
       L.p[ls] = params[t.seg];
       L.g[ls] = grads[t.seg];
       L.v[ls] = momentum[t.seg];
+      L.m[ls] = use_master ? master[t.seg] : nullptr;
       SgdEnt& e = L.e[L.nt++];
       e.p_off = (uint32_t)t.po;
       e.g_off = (uint32_t)t.go;

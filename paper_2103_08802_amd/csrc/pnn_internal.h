@@ -87,7 +87,8 @@ struct WgradLaunch {
 // the sums are for:
 //   RED_SUM     dst[c] = sum_r part[r][c]                               (split-K weight gradients;
 //               ncols even, two columns per thread, rows split over 2^rl_log2 lanes)
-//   RED_BN_FWD  ncols = 2C, part[r][c][2] = (sum z, sum z^2) -> mean, invstd, scale, shift [4][C]
+//   RED_BN_FWD  ncols = 2C, part[r][c][2] = (mean, sum of squared deviations from it) of the rowh
+//               rows of partial row r (the last one ragged) -> mean, invstd, scale, shift [4][C]
 //   RED_BN_BWD  ncols = 2C, part[r][c][2] = (sum dbn, sum dbn*xhat) -> dbeta, dgamma and the
 //               apply coefficients c1 = gamma * invstd, mb = dbeta / M, mbx = dgamma / M  [3][C]
 enum { RED_SUM = 0, RED_BN_FWD = 1, RED_BN_BWD = 2 };
@@ -103,6 +104,7 @@ struct ColRedProb {
   long count;            // BN: number of rows M of the normalised tensor
   int rows, ncols, mode;
   int rl_log2;           // RED_SUM: log2 of the row lanes per column pair (0..5)
+  int rowh;              // RED_BN_FWD: rows of the normalised tensor per partial row
   int tile_begin;
 };
 struct ColRedLaunch {
@@ -218,12 +220,15 @@ struct SgdEnt {
 constexpr int SGD_MAXT = 180;      // entries per launch
 constexpr int SGD_MAXS = 8;        // segments per launch
 constexpr int SGD_CHUNK = 2048;    // elements per workgroup
+// m[seg] (nullable): fp32 master copy of the segment's storage-type filters, laid out like the
+// gradient buffer; the update reads the master (or, with init, the stored filters) and writes both.
 struct SgdLaunch {
-  int nt, nesterov;
+  int nt, nesterov, init;
   float lr, mu, wd;
   void* p[SGD_MAXS];
   const float* g[SGD_MAXS];
   float* v[SGD_MAXS];
+  float* m[SGD_MAXS];
   SgdEnt e[SGD_MAXT];
 };
 int launch_sgd(const SgdLaunch& L, int tiles, int dtype, hipStream_t s);

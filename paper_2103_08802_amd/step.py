@@ -310,12 +310,19 @@ class ParaRealGPU:
         G["pre_bwd"].replay()
 
     # -- parameter update (SGD with momentum; include/pnn.h pnn_sgd_step) -------------------------
-    def sgd_init(self):
-        """Zeroed momentum buffers laid out like the gradient buffers."""
+    def sgd_init(self, master=True):
+        """Zeroed momentum buffers laid out like the gradient buffers; for bf16 networks (with
+        ``master``) also fp32 master copies of the filters, filled from the stored filters by the
+        first step."""
         torch = _torch()
         self.mom = [[torch.zeros_like(b, dtype=torch.uint8) for b in bufs]
                     for bufs in (self.ddelta, self.dphi, self.deta)]
         self.mom.append([torch.zeros_like(self.deps)])
+        self.master = None
+        if master and self.net.dtype == "bf16":
+            self.master = [[torch.zeros_like(b, dtype=torch.uint8) for b in bufs]
+                           for bufs in (self.ddelta, self.dphi, self.deta)]
+        self._master_fresh = True
 
     def sgd_step(self, lr, mu=0.9, weight_decay=1e-4, nesterov=True, s=None):
         s = self.stream() if s is None else s
@@ -325,4 +332,7 @@ class ParaRealGPU:
         for part, (pb, gb) in enumerate(parts):
             if not pb:
                 continue
-            B.pnn_sgd_step(self.plan, part, pb, gb, self.mom[part], lr, mu, weight_decay, nesterov, s)
+            m = self.master[part] if (self.master is not None and part < 3) else None
+            B.pnn_sgd_step(self.plan, part, pb, gb, self.mom[part], lr, mu, weight_decay, nesterov, s,
+                           master=m, master_init=self._master_fresh)
+        self._master_fresh = False

@@ -130,7 +130,9 @@ def test_alignment_rules():
     assert L.pnn_pre_bwd(p.handle, base + (1 << 29), A_ok, A_ok, ws, A_bad, ws2, None) == -8
     assert L.pnn_head_fwd_bwd(p.handle, ok[0], ok[1], ok[2], None, ok[3] + 2, ok[4], ok[5], ws2, None) == -8
     assert L.pnn_head_fwd_bwd(p.handle, ok[0] + 8, ok[1], ok[2], None, ok[3], ok[4], ok[5], ws2, None) == -8
-    assert L.pnn_sgd_step(p.handle, 1, A_bad, A_ok, A_ok, ctypes.c_float(0.1), ctypes.c_float(0.9),
+    assert L.pnn_sgd_step(p.handle, 1, A_bad, A_ok, A_ok, None, 0, ctypes.c_float(0.1), ctypes.c_float(0.9),
                           ctypes.c_float(5e-4), 1, None) == -8
+    assert L.pnn_sgd_step(p.handle, 1, A_ok, A_ok, A_ok, A_bad, 1, ctypes.c_float(0.1), ctypes.c_float(0.9),
+                          ctypes.c_float(5e-4), 1, None) == -8                  # master copies too
     assert B.pnn_status_string(-8) == "a pointer is not aligned as the interface requires"
     p.close()

@@ -21,6 +21,19 @@ def _say(*a):
     print(*a, flush=True)
 
 
+class _E2(float):
+    """e_2 of a check, carrying its e_inf (max |diff| / max |ref|) for the report."""
+
+    def __new__(cls, e2, einf):
+        v = super().__new__(cls, e2)
+        v.inf = einf
+        return v
+
+
+def _rel_2_with_inf(a, ref):
+    return _E2(rel_2(a, ref), rel_inf(a, ref))
+
+
 def gpu_step(net, params, x, labels):
     import torch
     from paper_2103_08802_amd.step import ParaRealGPU
@@ -46,14 +59,17 @@ def sample_nodes(seg, rng, n_mid=3):
     return sorted(pick)
 
 
-def check_net(net, sample=None, fine_subset=None, seed=0, node_subset=False):
+def check_net(net, sample=None, fine_subset=None, seed=0, node_subset=False, x_offset=0.0):
     from oracle import prim as P
     x, labels, params = S.make_all(net)
+    if x_offset:
+        from pnn_synth.gen import to_storage
+        x = to_storage(x + x_offset, net.dtype)
     _say(f"[nodes] {net.name} batch {net.batch} {net.dtype}: GPU step")
     g, dx_fine = gpu_step(net, params, x, labels)
     bf16 = net.dtype == "bf16"
     st = P.round_bf16 if bf16 else (lambda a: a)
-    metric = rel_2 if bf16 else rel_inf
+    metric = _rel_2_with_inf if bf16 else rel_inf
     rng = np.random.default_rng(seed)
     errs = {}
     for part, key in ((0, "pre"), (1, "fine"), (2, "coarse")):
@@ -70,6 +86,9 @@ def check_net(net, sample=None, fine_subset=None, seed=0, node_subset=False):
     worst = max(errs, key=errs.get)
     _say(f"[nodes] {net.name}: {len(errs)} checks, worst {worst} = {errs[worst]:.3e}, "
          f"median {np.median(list(errs.values())):.3e}")
+    if bf16:
+        wi = max(errs, key=lambda k: getattr(errs[k], "inf", 0.0))
+        _say(f"[nodes] {net.name}: worst e_inf {wi} = {getattr(errs[wi], 'inf', 0.0):.3e}")
     return net, errs
 
 
@@ -122,3 +141,26 @@ def test_vgg224_nodes(batch, sample, fine_subset):
     every node of every segment at batch 1, and at the full batch the last sub-network with every
     preprocessing and coarse segment (sampled outputs)."""
     _assert(*check_net(S.config(5, batch), sample=sample, fine_subset=fine_subset))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_bn_statistics_of_large_mean_tensors(dtype):
+    """Images offset by 1000: x_2 = C^2(image) and the residual streams it feeds have channel means
+    up to about 2500 times their spread.  The batch statistics of every BN of a small bottleneck
+    ResNet (segment inputs; residual-unit outputs through the convolution epilogue; narrow 1x1
+    outputs) against the oracle's two-pass statistics of the same stored tensors: 1 / std to 1e-4
+    relative (summing squares about zero would lose the variance entirely here), the mean to 5e-4
+    standard deviations (it is kept in fp32, whose rounding alone is 2^-24 |mean| ~ 1.5e-4 std at
+    that ratio).  The other node values are not held to the usual bar here: at these ratios the fp32
+    BN shift's rounding moves the ReLU kink by ~1e-4 std, which flips single mask elements."""
+    from pnn_synth.nets import resnet_parareal
+    net = resnet_parareal(f"mini-resnet-largemean-{dtype}", 3, 16, 2, 10, dtype, (7, 8, 9),
+                          units_per_stage=2, widths=(64, 128, 256), stem=16)
+    net, errs = check_net(net, x_offset=1000.0)
+    inv = {k: v for k, v in errs.items() if k.endswith(".invstd")}
+    mean = {k: v for k, v in errs.items() if k.endswith(".mean")}
+    _say(f"[nodes] large-mean BN statistics: worst {max(inv, key=inv.get)} = {max(inv.values()):.3e}, "
+         f"{max(mean, key=mean.get)} = {max(mean.values()):.3e}")
+    bad = {k: v for k, v in inv.items() if not v <= 1e-4}
+    bad.update({k: v for k, v in mean.items() if not v <= 5e-4})
+    assert not bad, sorted(bad.items(), key=lambda kv: -kv[1])[:10]

@@ -137,6 +137,18 @@ def test_p2_bn_forward_moments():
     np.testing.assert_allclose(ybn.reshape(-1, C).var(0), gamma ** 2 * var / (var + 1e-5), rtol=1e-12)
 
 
+def test_bn_statistics_of_a_large_mean_tensor():
+    """Batch statistics of a channel whose mean is 1e6 times its spread: values 1e6 + k / 8 for
+    k = 0..7 (exact in fp64) have mean 1e6 + 7/16 and biased variance (63/12) / 64 = 21/256 in closed
+    form; the two-pass statistics reproduce them to fp64 rounding (a one-pass E[z^2] - mean^2 in
+    fp64 would lose about 12 of its 16 digits here)."""
+    from oracle.net import bn_batch_stats
+    z = (1e6 + np.arange(8) / 8.0).reshape(2, 2, 2, 1)
+    mean, invstd = bn_batch_stats(z)
+    assert mean[0] == 1e6 + 7.0 / 16.0
+    np.testing.assert_allclose(1.0 / invstd[0] ** 2 - 1e-5, 21.0 / 256.0, rtol=1e-9)
+
+
 def test_p3_bn_backward_invariants():
     """For x -> BN(x) (ReLU not reached): sum dx = 0 and, with eps > 0,
     sum dx * xhat = gamma * invstd * dgamma * eps / (var + eps)  (0 in the eps -> 0 limit)."""
