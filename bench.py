@@ -95,6 +95,19 @@ def stored_traffic(kernel):
     return rec["bytes_per_launch"]
 
 
+def stored_mfma(kernel):
+    """MFMA utilisation of ``kernel`` from a rocprofv3 --pmc run of the derived counters MfmaUtil
+    and MfmaFlopsBF16 (profiles/mfma_<kernel>.json, hash-guarded like the traffic record)."""
+    path = os.path.join(ROOT, "profiles", f"mfma_{kernel}.json")
+    if not os.path.exists(path) or kernel not in KERNEL_SOURCES:
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("sources_sha256") != _sources_sha(kernel):
+        return None
+    return {"mfma_util_pct": rec["mfma_util_pct"], "mfma_flops_per_launch": rec["mfma_flops_per_launch"]}
+
+
 def _short(name):
     return name.split("(")[0].replace("void ", "").split("<")[0].replace("pnn::", "")
 
@@ -178,6 +191,64 @@ def summarize_families(fetch_csv, write_csv, trace_csv, out_md, cmd):
             f.write(f"| `{n}` | {c} | {fm:.1f} | {wm:.1f} | {us:.2f} | {gbs:.0f} |\n")
 
 
+def summarize_mfma(csv_path, out_md, algo_flops, cmd):
+    """Per kernel family, from one rocprofv3 --pmc run of the derived counters MfmaUtil (MFMA busy
+    cycles summed over SIMDs / (GPU active cycles x SIMDs), percent) and MfmaFlopsBF16 (bf16 MFMA
+    operations x 512): the launch-weighted MFMA utilisation and the MFMA FLOPs per launch.  For
+    conv_kernel the counted FLOPs are set against the algorithmic 2 M N K per launch
+    (``algo_flops``, from the bench line's roofline record of the same build): their ratio is the
+    work the MFMA tiles do on padding (K rounded up to the instruction's 32, ragged row tiles)."""
+    import csv
+    util, flops, durs = {}, {}, {}
+    for r in csv.DictReader(open(csv_path)):
+        n = _short(r["Kernel_Name"])
+        v = float(r["Counter_Value"])
+        key = (n, r["Dispatch_Id"])
+        if r["Counter_Name"] == "MfmaUtil":
+            util[key] = v
+        elif r["Counter_Name"] == "MfmaFlopsBF16":
+            flops[key] = v
+        durs[key] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    fams = {}
+    for (n, d), u in util.items():
+        f = fams.setdefault(n, [0, 0.0, 0.0, 0.0])
+        f[0] += 1
+        f[1] += u * durs[(n, d)]
+        f[2] += durs[(n, d)]
+        f[3] += flops.get((n, d), 0.0)
+    rows = sorted(fams.items(), key=lambda kv: -kv[1][2])
+    rec = None
+    with open(out_md, "w") as fh:
+        fh.write("# MFMA utilisation per kernel family: parareal ResNet-1001, N=16, batch 128, bf16 "
+                 "(one stream)\n\nCommand (from the repository root, on one MI355X):\n\n```\n"
+                 f"{cmd}\n```\n\nMfmaUtil = SQ_VALU_MFMA_BUSY_CYCLES summed over SIMDs / "
+                 "(GRBM_GUI_ACTIVE x SIMD count), per dispatch, averaged weighted by dispatch "
+                 "duration; MFMA GFLOP = MfmaFlopsBF16 (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) per "
+                 "dispatch; TFLOP/s = that over the dispatch's duration.\n\n")
+        fh.write("| family | dispatches | MfmaUtil % | MFMA GFLOP / dispatch | MFMA TFLOP/s |\n"
+                 "|---|---:|---:|---:|---:|\n")
+        for n, (c, uw, t, fl) in rows:
+            fh.write(f"| `{n}` | {c} | {uw / t:.2f} | {fl / c / 1e9:.3f} | {fl / (t * 1e-6) / 1e12:.1f} |\n")
+        if "conv_kernel" in fams:
+            c, uw, t, fl = fams["conv_kernel"]
+            rec = {"kernel": "conv_kernel", "mfma_util_pct": round(uw / t, 3),
+                   "mfma_flops_per_launch": round(fl / c), "dispatches": c}
+            if algo_flops:
+                rec["algorithmic_flops_per_launch"] = algo_flops
+                rec["mfma_over_algorithmic"] = round(fl / c / algo_flops, 4)
+                fh.write(f"\nconv_kernel: {fl / c / 1e9:.3f} GFLOP of bf16 MFMA work per launch against "
+                         f"{algo_flops / 1e9:.3f} GFLOP algorithmic (2 M N K of the launch's problems, "
+                         f"bench line): ratio {fl / c / algo_flops:.3f} (padding of K to the "
+                         "instruction's 32 and of ragged row tiles).\n")
+    if rec is not None:
+        rec.update({"command": cmd, "sources": KERNEL_SOURCES["conv_kernel"],
+                    "sources_sha256": _sources_sha("conv_kernel")})
+        with open(os.path.join(ROOT, "profiles", "mfma_conv_kernel.json"), "w") as f:
+            json.dump(rec, f, indent=1)
+            f.write("\n")
+        print(json.dumps(rec))
+
+
 def summarize_sq(csv_path, out_md, cmd):
     """Per kernel instantiation, ratios of one rocprofv3 --pmc run of SQ counters (SQ_WAVES,
     SQ_WAVE_CYCLES, SQ_BUSY_CYCLES, SQ_WAIT_ANY, SQ_WAIT_INST_LDS, SQ_ACTIVE_INST_LDS,
@@ -194,11 +265,11 @@ def summarize_sq(csv_path, out_md, cmd):
         f.write("# SQ counters per conv_kernel instantiation: parareal ResNet-1001, N=16, batch 128, "
                 "bf16 (one stream)\n\nCommand (from the repository root, on one MI355X):\n\n```\n"
                 f"{cmd}\n```\n\nwave cycles = SQ_WAVE_CYCLES / SQ_WAVES; the waits and LDS activity as "
-                "fractions of SQ_WAVE_CYCLES; MFMA busy per SQ busy cycle; LDS bank-conflict cycles per "
-                "LDS-active cycle.\n\n")
+                "fractions of SQ_WAVE_CYCLES; LDS bank-conflict cycles per LDS-active cycle (MFMA "
+                "utilisation: the MfmaUtil summary).\n\n")
         f.write("| kernel | dispatches | waves / dispatch | cycles / wave | wait any | wait LDS | "
-                "LDS active | MFMA busy / busy | bank conflicts / LDS active |\n"
-                "|---|---:|---:|---:|---:|---:|---:|---:|---:|\n")
+                "LDS active | bank conflicts / LDS active |\n"
+                "|---|---:|---:|---:|---:|---:|---:|---:|\n")
         for n, c in rows:
             w, wc = c.get("SQ_WAVES", 0.0), c.get("SQ_WAVE_CYCLES", 0.0)
             if w <= 0 or wc <= 0:
@@ -207,7 +278,6 @@ def summarize_sq(csv_path, out_md, cmd):
             f.write(f"| `{n}` | {len(disp[n])} | {w / len(disp[n]):.0f} | {wc / w:.0f} | "
                     f"{c.get('SQ_WAIT_ANY', 0.0) / wc:.2f} | {c.get('SQ_WAIT_INST_LDS', 0.0) / wc:.2f} | "
                     f"{c.get('SQ_ACTIVE_INST_LDS', 0.0) / wc:.2f} | "
-                    f"{c.get('SQ_VALU_MFMA_BUSY_CYCLES', 0.0) / max(c.get('SQ_BUSY_CYCLES', 0.0), 1.0):.2f} | "
                     f"{c.get('SQ_LDS_BANK_CONFLICT', 0.0) / lds:.2f} |\n")
 
 
@@ -238,6 +308,47 @@ def summarize_trace(stats_csv, trace_csv, out_md, title, cmd):
                     f"{float(r['Percentage']):.2f} |\n")
 
 
+def time_config(idx, streams, steps, warmup):
+    """ms per step (4 streams, overlapped backward), images/s, and the fine sub-networks' conv
+    TFLOP/s and share of the bf16 MFMA peak (from as many steps with the separate calls) of
+    workload ``idx``."""
+    import torch
+    import pnn_synth as S
+    from paper_2103_08802_amd import binding as B
+    from paper_2103_08802_amd.step import ParaRealGPU
+    net = S.config(idx)
+    x, labels, params = S.make_all(net)
+    g = ParaRealGPU(net, params)
+    B.pnn_set_streams(g.plan, streams)
+    g.load_input(x, labels)
+    g.overlap_bwd = True
+    for _ in range(warmup):
+        g.forward()
+        g.backward()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        g.forward()
+        g.backward()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    g.overlap_bwd = False
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for e in ev:
+        g.forward(fine_events=(e[0], e[1]))
+        g.backward(fine_events=(e[2], e[3]))
+    torch.cuda.synchronize()
+    fine_ms = sum(e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev) / steps
+    tf = fine_flops(net) / (fine_ms * 1e-3) / 1e12
+    del g
+    torch.cuda.empty_cache()
+    return {"workload": f"{net.name}: batch {net.batch}, {net.in_shape[0]}x{net.in_shape[1]}x"
+                        f"{net.in_shape[2]} input, N={net.n_sub}",
+            "steps": steps, "ms_per_step": round(ms, 3), "images_per_s": round(net.batch / (ms * 1e-3), 1),
+            "fine_ms_per_step": round(fine_ms, 3), "fine_tflops": round(tf, 2),
+            "pct_bf16_mfma_peak": round(100.0 * tf / PEAK_BF16_TFLOPS, 3)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -266,6 +377,12 @@ def main():
                     help="no GPU work: write a markdown summary of a kernel-trace run")
     ap.add_argument("--summarize-families", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "TRACE_CSV", "OUT_MD"),
                     help="no GPU work: HBM bytes, duration and bandwidth per kernel family")
+    ap.add_argument("--summarize-mfma", nargs=2, metavar=("PMC_CSV", "OUT_MD"),
+                    help="MfmaUtil / MfmaFlopsBF16 summary of a rocprofv3 --pmc run (and profiles/mfma_conv_kernel.json)")
+    ap.add_argument("--algo-flops", type=float, default=0.0,
+                    help="algorithmic FLOPs per conv_kernel launch of the same build (bench line)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the timing of the other workloads (the line's 'configs' record)")
     ap.add_argument("--summarize-sq", nargs=2, metavar=("PMC_CSV", "OUT_MD"),
                     help="no GPU work: SQ counter ratios per kernel instantiation")
     ap.add_argument("--kernel", default="conv_kernel")
@@ -283,6 +400,9 @@ def main():
         return
     if args.summarize_sq:
         summarize_sq(*args.summarize_sq, args.cmd)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(*args.summarize_mfma, args.algo_flops, args.cmd)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this library runs the whole parareal network on ONE GPU (all N "
@@ -366,6 +486,7 @@ def main():
         B.pnn_timing_enable(g.plan, 0)
         fam[name] = {"ms": ms, "launches": n, "flops": fl, "bytes": by}
     dom = max(fam, key=lambda k: fam[k]["ms"])
+    default_cfg = (args.config, args.coarse, args.partition) == (3, "config", "contiguous")
     d = fam[dom]
     # the family's bound: MFMA when its algorithmic intensity is above the ridge point
     # (peak FLOP/s / peak bytes/s), else HBM
@@ -377,12 +498,14 @@ def main():
             "achieved": round(tflops_dom if mfma else achieved, 2 if mfma else 1),
             "peak": peak_f if mfma else PEAK_HBM_GBS, "unit": "TFLOP/s" if mfma else "GB/s",
             "frac": round((tflops_dom / peak_f) if mfma else (achieved / PEAK_HBM_GBS), 4),
-            "traffic": (stored_traffic(dom) if (args.config, args.coarse, args.partition) == (3, "config", "contiguous")
-                        else None),
+            "traffic": (stored_traffic(dom) if default_cfg else None),
             "algorithmic_bytes_per_launch": round(d["bytes"] / max(d["launches"], 1)),
             "algorithmic_flops_per_launch": round(d["flops"] / max(d["launches"], 1)),
             "kernel": dom, "avg_launch_us": round(d["ms"] * 1e3 / max(d["launches"], 1), 2),
             "hbm_gbs": round(achieved, 1), "mfma_tflops": round(tflops_dom, 2)}
+    mf = stored_mfma(dom) if default_cfg else None
+    if mf is not None:
+        roof.update(mf)
 
     # the parameter update (SGD, Nesterov momentum; not part of the step the metric times)
     g.sgd_init()
@@ -398,6 +521,15 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args.config, coarse=args.coarse)
+
+    # the other workloads the throughput target names, timed the same way (fewer steps)
+    configs = None
+    if default_cfg and not args.no_configs:
+        del g
+        torch.cuda.empty_cache()
+        configs = {}
+        for idx, key in ((1, "vgg16-n4-b128"), (2, "resnet1001-n4-b64"), (4, "resnet1001-64px-n8-b128")):
+            configs[key] = time_config(idx, args.streams, max(3, args.steps // 2), 2)
 
     out = {
         "metric": "fine-subnet conv TFLOP/s (fwd+bwd, % bf16 MFMA peak) + images/s per step",
@@ -428,6 +560,7 @@ def main():
         "sgd_ms_per_step": round(sgd_ms, 3),
         "roofline": roof,
         "cpu_baseline": cpu,
+        "configs": configs,
     }
     print(json.dumps(out), flush=True)
 

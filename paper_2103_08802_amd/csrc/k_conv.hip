@@ -448,25 +448,20 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
   // channel's mean is large against its spread; the tile's mean and sum of squared deviations are
   // formed from them below.
   const bool fstats = MODE == MODE_FWD && (P.flags & EPI_STATS) != 0;
-  float* piv_s = (float*)pro_s;
   float pv[VE];
   if (fstats) {
-    if (tid < ncc) {
+    if (tid < ncc) {                   // the threads that hold the tile's first row
       Chunk<T> r0, x0;
       unpack_chunk<T>(pre[0], r0);
       unpack_chunk<T>(pre2[0], x0);
 #pragma unroll
-      for (int e = 0; e < VE; ++e) {
-        float v = acc_s[c0 + e];
-        if (P.res) v += r0.v[e];
-        if (P.ext) v += x0.v[e];
-        piv_s[c0 + e] = St<T>::rnd(v);
-      }
+      for (int e = 0; e < VE; ++e)
+        ((float*)pro_s)[c0 + e] = St<T>::rnd(acc_s[c0 + e] + (P.res ? r0.v[e] : 0.f) + (P.ext ? x0.v[e] : 0.f));
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int e = 0; e < VE; ++e) pv[e] = fstats ? piv_s[c0 + e] : 0.f;
+  for (int e = 0; e < VE; ++e) pv[e] = fstats ? ((const float*)pro_s)[c0 + e] : 0.f;
 
   float s1[VE], s2[VE];
 #pragma unroll
@@ -604,10 +599,11 @@ __global__ __launch_bounds__(256) void conv_kernel(const ConvLaunch L) {
       }
       float2* pp = (float2*)P.part + (long)tm * P.ncol + n0 + tid;
       if (MODE == MODE_FWD) {
-        // the tile's mean and sum of squared deviations from its pivoted sums
+        // the tile's mean and sum of squared deviations from its pivoted sums (the pivot of column
+        // tid as the threads that summed it formed it)
         const float n = (float)min(BM, P.M - tm * BM);
         const float am = a / n;
-        *pp = make_float2(piv_s[tid] + am, fmaxf(b - a * am, 0.f));
+        *pp = make_float2(((const float*)pro_s)[tid] + am, fmaxf(b - a * am, 0.f));
       } else {
         *pp = make_float2(a, b);
       }
@@ -1332,6 +1328,7 @@ __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
   __shared__ float2 pro_s[MODE == MODE_FWD ? MAXK : 1];
   __shared__ float2 red[WR][NC];
   __shared__ float piv[MODE == MODE_FWD ? NC : 1];
+  __shared__ float pivp[MODE == MODE_FWD ? 256 : 1];   // pivot dot-product partials [256 / NC][NC]
 
   const int gi = find_group(L);
   const ConvProb& P = L.p[gi];
@@ -1415,24 +1412,30 @@ __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
     }
   };
 
-  // Forward BN statistics are summed about a per-workgroup pivot, the first row's output (an fp32
-  // dot product here), so that they do not cancel when a channel's mean is large against its spread
-  if (MODE == MODE_FWD && stats && tid < ncl) {
-    float a = 0.f;
-    for (int k = 0; k < K; ++k) {
-      float x = St<T>::ld(xin, (long)m_begin * K + k);
-      if (pro) x = fmaxf(fmaf(x, P.pro[k], P.pro[P.Cg + k]), 0.0f);
-      a = fmaf(x, St<T>::ld(P.wmat, (long)(c0 + tid) * K + k), a);
-    }
-    piv[tid] = St<T>::rnd(a);
-  }
   float s1[4] = {0.f, 0.f, 0.f, 0.f}, s2[4] = {0.f, 0.f, 0.f, 0.f};
   fetch(m_begin);
-  __syncthreads();                                    // pro_s, piv
-  float pv[4] = {0.f, 0.f, 0.f, 0.f};
-  if (MODE == MODE_FWD && stats && active)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pv[i] = piv[cl + i];
+  // Forward BN statistics are summed about a per-workgroup pivot, the first row's output (an fp32
+  // dot product here, its K terms split over 256 / NC threads per column; its loads overlap the
+  // first tile's), so that they do not cancel when a channel's mean is large against its spread
+  if (MODE == MODE_FWD && stats && sizeof(pivp) == 256 * sizeof(float)) {
+    constexpr int NQ = 256 / NC;
+    const int pc = tid % NC, pq = tid / NC;
+    const int kq = (K + NQ - 1) / NQ;
+    float a = 0.f;
+    if (pc < ncl)
+      for (int k = pq * kq; k < min(K, (pq + 1) * kq); ++k) {
+        float x = St<T>::ld(xin, (long)m_begin * K + k);
+        if (pro) x = fmaxf(fmaf(x, P.pro[k], P.pro[P.Cg + k]), 0.0f);
+        a = fmaf(x, St<T>::ld(P.wmat, (long)(c0 + pc) * K + k), a);
+      }
+    pivp[tid] = a;
+  }
+  __syncthreads();                                    // pro_s, pivp
+  if (MODE == MODE_FWD && stats && tid < ncl && sizeof(piv) == NC * sizeof(float)) {   // read after the first tile's barrier
+    float v = 0.f;
+    for (int q = 0; q < 256 / NC; ++q) v += pivp[q * NC + tid];
+    piv[tid] = St<T>::rnd(v);
+  }
   for (int mt = m_begin; mt < m_end; mt += TR) {
 #pragma unroll
     for (int i = 0; i < NLA; ++i) {
@@ -1483,7 +1486,7 @@ __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             o[i] = v[i];
-            const float d = St<T>::rnd(v[i]) - pv[i];
+            const float d = St<T>::rnd(v[i]) - (stats ? piv[cl + i] : 0.f);
             if (stats && mv) {
               s1[i] += d;
               s2[i] += d * d;

@@ -63,44 +63,55 @@ __global__ __launch_bounds__(1024) void colred_kernel(const ColRedLaunch L) {
   }
   if (P.mode == RED_BN_FWD) {
     // partial row r holds, per channel, the mean and the sum of squared deviations of its n_r rows
-    // (rows of rowh, the last one ragged); combined about the overall mean in fp64, fixed order:
-    // M2 = sum_r M2_r + n_r (mean_r - mean)^2
+    // (rows of rowh, the last one ragged).  In fp64, fixed order: A = sum_r n_r mean_r,
+    // Q = sum_r (M2_r + n_r mean_r^2); mean = A / M, var = Q / M - mean^2 (exact up to fp64
+    // rounding: the partial means carry the large part, the fp32 sums only the deviations)
     constexpr int CH = RED_COLS / 2, RLN = 1024 / CH;
-    double (*red1)[CH] = (double (*)[CH])&red[0][0];
+    double (*ra)[CH] = (double (*)[CH])&red[0][0];
+    double (*rq)[CH] = (double (*)[CH])&red[RLN / 2][0];
     const int C = P.ncols / 2;
     const int cl = threadIdx.x % CH, rl = threadIdx.x / CH;
     const int c = (blockIdx.x - P.tile_begin) * CH + cl;
-    const double M = (double)P.count;
     const float2* pp = (const float2*)P.part + c;
-    auto rows_of = [&](int r) { return (double)min((long)P.rowh, P.count - (long)r * P.rowh); };
-    double a = 0.0;
-    if (c < C)
-      for (int r = rl; r < P.rows; r += RLN) a += rows_of(r) * (double)pp[(long)r * C].x;
-    red1[rl][cl] = a;
-    __syncthreads();
+    const long h = P.rowh;
+    double a = 0.0, q = 0.0;
+    if (c < C) {
+      int r = rl;
+      for (; r + 3 * RLN < P.rows; r += 4 * RLN) {
+        float2 v[4];
 #pragma unroll
-    for (int h = RLN / 2; h >= 1; h >>= 1) {
-      if (rl < h) red1[rl][cl] += red1[rl + h][cl];
-      __syncthreads();
-    }
-    const double mean = red1[0][cl] / M;
-    __syncthreads();
-    double b = 0.0;
-    if (c < C)
-      for (int r = rl; r < P.rows; r += RLN) {
-        const float2 v = pp[(long)r * C];
-        const double d = (double)v.x - mean;
-        b += (double)v.y + rows_of(r) * d * d;
+        for (int u = 0; u < 4; ++u) v[u] = pp[(long)(r + u * RLN) * C];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const double n = (double)min(h, P.count - (long)(r + u * RLN) * h), m = (double)v[u].x;
+          a += n * m;
+          q += (double)v[u].y + n * m * m;
+        }
       }
-    red1[rl][cl] = b;
+      for (; r < P.rows; r += RLN) {
+        const float2 v = pp[(long)r * C];
+        const double n = (double)min(h, P.count - (long)r * h), m = (double)v.x;
+        a += n * m;
+        q += (double)v.y + n * m * m;
+      }
+    }
+    // ra / rq: [RLN][CH] doubles each; red holds 2 * RED_LANES * RED_COLS = 2 * RLN * CH doubles
+    ra[rl][cl] = a;
+    rq[rl][cl] = q;
     __syncthreads();
 #pragma unroll
-    for (int h = RLN / 2; h >= 1; h >>= 1) {
-      if (rl < h) red1[rl][cl] += red1[rl + h][cl];
+    for (int k = RLN / 2; k >= 1; k >>= 1) {
+      if (rl < k) {
+        ra[rl][cl] += ra[rl + k][cl];
+        rq[rl][cl] += rq[rl + k][cl];
+      }
       __syncthreads();
     }
     if (rl != 0 || c >= C) return;
-    const double var = red1[0][cl] / M;
+    const double M = (double)P.count;
+    const double mean = ra[0][cl] / M;
+    double var = rq[0][cl] / M - mean * mean;
+    if (var < 0.0) var = 0.0;
     const float invstd = (float)(1.0 / sqrt(var + (double)PNN_BN_EPS));
     const float scale = P.gamma[c] * invstd;
     P.stats[c] = (float)mean;

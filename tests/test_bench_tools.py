@@ -64,7 +64,36 @@ def test_sq_ratios(tmp_path):
     b.summarize_sq(str(tmp_path / "sq.csv"), str(out), "cmd")
     row = [l for l in out.read_text().splitlines() if "conv_kernel<unsigned short, 1, 3, 2, 4>" in l][0]
     cells = [c.strip() for c in row.strip("|").split("|")]
-    assert cells[1:] == ["1", "10", "100", "0.50", "0.03", "0.04", "0.50", "2.00"]
+    assert cells[1:] == ["1", "10", "100", "0.50", "0.03", "0.04", "2.00"]
+
+
+def test_mfma_summary_and_record(tmp_path, monkeypatch):
+    """MfmaUtil weighted by dispatch duration, MFMA FLOPs per dispatch and their ratio to the
+    algorithmic FLOPs; the conv_kernel record carries the sources' hash and is read back by
+    stored_mfma (None once a source changes)."""
+    b = _bench()
+    k = "void pnn::conv_kernel<unsigned short, 0, 0, 2, 4>(pnn::ConvLaunch)"
+    rows = []
+    for d, (u, fl, t0, t1) in enumerate([(10.0, 3e9, 0, 1000), (40.0, 1e9, 2000, 5000)]):
+        rows.append([d, k, "MfmaUtil", u, t0, t1])
+        rows.append([d, k, "MfmaFlopsBF16", fl, t0, t1])
+    _write(tmp_path / "m.csv", ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value",
+                                "Start_Timestamp", "End_Timestamp"], rows)
+    monkeypatch.setattr(b, "ROOT", str(tmp_path))
+    os.makedirs(tmp_path / "profiles")
+    os.makedirs(tmp_path / "paper_2103_08802_amd" / "csrc")
+    for n in b.KERNEL_SOURCES["conv_kernel"]:
+        (tmp_path / "paper_2103_08802_amd" / "csrc" / n).write_text(n)
+    out = tmp_path / "m.md"
+    b.summarize_mfma(str(tmp_path / "m.csv"), str(out), 1e9, "cmd")
+    row = [l for l in out.read_text().splitlines() if l.startswith("| `conv_kernel`")][0]
+    cells = [c.strip() for c in row.strip("|").split("|")]
+    assert cells[1] == "2" and cells[2] == "32.50" and cells[3] == "2.000"   # (10*1 + 40*3) / 4 us
+    rec = json.loads((tmp_path / "profiles" / "mfma_conv_kernel.json").read_text())
+    assert rec["mfma_over_algorithmic"] == 2.0
+    assert b.stored_mfma("conv_kernel") == {"mfma_util_pct": 32.5, "mfma_flops_per_launch": 2000000000}
+    (tmp_path / "paper_2103_08802_amd" / "csrc" / "k_conv.hip").write_text("changed")
+    assert b.stored_mfma("conv_kernel") is None
 
 
 def test_pmc_record_and_source_hash(tmp_path, monkeypatch):
