@@ -281,6 +281,9 @@ pnn_status pnn_sgd_step(pnn_plan* plan, int part, void* const* params, const flo
  *   what = 1: gradient dL/d(slot idx) (in scratch, storage type)
  *   what = 2: dL/d(BN output) of BN instance idx as stored before the BN backward (scratch)
  *   what = 3: statistics of BN instance idx: mean, invstd, scale, shift, float [4][C] (saved)
+ *   what = 4: (part, j, idx ignored) the resident kernel's barrier words in scratch: uint32 [0] an
+ *             error flag, non-zero when a barrier wait gave up, [1] barriers completed by the last
+ *             resident launch (one per batch-normalisation point per unit and sub-network)
  * *offset receives the byte offset into that workspace.  PNN_ERR_INDEX when the tensor is not held
  * by the library (slot 0 and the segment output are the caller's tensors) or does not exist. */
 pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx, size_t* offset);
@@ -297,6 +300,16 @@ const char* pnn_status_string(pnn_status s);
  * set-up call: needs a HIP device, allocates no device memory); PNN_ERR_HIP if that fails.
  * PNN_ERR_INDEX outside 1 .. 4. */
 pnn_status pnn_set_streams(pnn_plan* plan, int streams);
+
+/* Resident forward of bottleneck-unit runs (PNN_BF16 plans; default off, 1 turns it on):
+ * parareal_fine_fwd then runs each fine sub-network's run of identity pre-activation bottleneck units
+ * at 32x32 with 64 channels (ResNet-1001's first stage, Table resnet) in one kernel per wave of
+ * sub-networks, the residual stream kept on chip across the units and every BN point a barrier
+ * over the sub-network's workgroups (one workgroup per image; sub-networks in waves of as many
+ * images as the device holds at once).  Same results as the unit-by-unit kernels up to the
+ * summation order of the BN statistics.  Off by default: on gfx950 its barriers and the
+ * one-workgroup-per-CU schedule make it slower than the unit-by-unit kernels at these shapes. */
+pnn_status pnn_set_resident(pnn_plan* plan, int on);
 
 /* Per-kernel-family GPU time accounting with HIP events recorded on the call's stream around
  * every launch of one family (0 = off).  Families: 1 = grouped conv forward / data-gradient

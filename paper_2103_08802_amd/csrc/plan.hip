@@ -33,6 +33,7 @@ struct NodeP {
   size_t w_off = NONE, gw_off = NONE, wt_off = NONE;
   bool dgrad = false;      // data gradient needed in the backward
   bool first_of_two = false;
+  bool resident = false;   // part of the segment's run of resident units (unit_fwd_kernel)
 };
 
 struct SlotP {
@@ -77,6 +78,11 @@ struct SegP {
   size_t param_bytes = 0, grad_bytes = 0;
   size_t saved_base = 0, saved_bytes = 0;
   size_t scr_base = 0, scr_bytes = 0;
+  // run of bottleneck units the resident kernel can take (find_unit_run): its first node, unit
+  // count, the levels it covers, its input slot and the first unit's offsets / per-unit strides
+  int ru_node = -1, ru_n = 0, ru_lo = 0, ru_hi = 0, ru_xslot = 0;
+  UnitJob ru_job{};
+  unsigned ru_dw = 0, ru_dg = 0, ru_dz = 0, ru_ds = 0;
 };
 
 struct WgradGeom {
@@ -95,6 +101,11 @@ struct pnn_plan {
   size_t wpart_off = 0, wpart_bytes = 0;
   size_t head_off = 0, head_bytes = 0;
   size_t sq_off = 0, sq_bytes = 0;
+  // resident units: on / off (pnn_set_resident), workgroups that fit the device at once (queried
+  // once, -1: not yet), scratch region: barrier words, then per fine segment its partial sums
+  int resident_on = 0;
+  int unit_cap = -1;
+  size_t unit_off = 0, unit_part_stride = 0;
   // independent chains of the fine sub-networks: up to `streams` streams, the call's stream and
   // internal ones created by pnn_set_streams (default priority, non-blocking); compute calls never
   // create streams or events
@@ -446,6 +457,89 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
   return PNN_OK;
 }
 
+// A pre-activation bottleneck unit at node i in the resident kernel's form: 1x1 squeeze C -> MID,
+// 3x3 MID -> MID, 1x1 expand MID -> C with the unit input as residual, every convolution behind a
+// BN of its input, stride 1, UNIT_H x UNIT_W maps; z1 and z2 feed only the next convolution, the
+// unit input only the squeeze's BN and the residual; the output is the segment output or feeds a BN.
+bool unit_at(const SegP& S, int i) {
+  if (i < 0 || i + 2 >= (int)S.nodes.size()) return false;
+  const NodeP &a = S.nodes[i], &b = S.nodes[i + 1], &c = S.nodes[i + 2];
+  auto conv = [](const NodeP& n, int k, int cin, int cout) {
+    return n.op == PNN_OP_CONV && n.k == k && n.stride == 1 && n.pad == (k - 1) / 2 && n.cin == cin &&
+           n.cout == cout && n.bn >= 0;
+  };
+  if (!conv(a, 1, UNIT_C, UNIT_MID) || !conv(b, 3, UNIT_MID, UNIT_MID) || !conv(c, 1, UNIT_MID, UNIT_C)) return false;
+  if (a.H != UNIT_H || a.W != UNIT_W || b.src != a.dst || c.src != b.dst || c.res != a.src || a.res >= 0 ||
+      b.res >= 0)
+    return false;
+  const SlotP &x = S.slots[a.src], &z1 = S.slots[a.dst], &z2 = S.slots[b.dst], &o = S.slots[c.dst];
+  if (x.bn_consumers.size() != 1 || x.res_consumer != i + 2 || x.direct_consumer != -1) return false;
+  if (z1.bn_consumers.size() != 1 || z1.res_consumer != -1 || z1.direct_consumer != -1) return false;
+  if (z2.bn_consumers.size() != 1 || z2.res_consumer != -1 || z2.direct_consumer != -1) return false;
+  return c.dst == S.out || o.bn >= 0;
+}
+
+// The segment's first run of at least two consecutive resident-form units whose tensors sit at
+// constant per-unit strides (so the kernel addresses unit u as the first unit plus u strides).
+void find_unit_run(SegP& S) {
+  const int nn = (int)S.nodes.size();
+  for (int i0 = 0; i0 + 2 < nn; ++i0) {
+    if (!unit_at(S, i0)) continue;
+    auto offs = [&](int k, unsigned* o) {   // w1 w2 w3 g1 g2 g3 z1 z2 s1 s2 s3 xo
+      const int i = i0 + 3 * k;
+      const NodeP &a = S.nodes[i], &b = S.nodes[i + 1], &c = S.nodes[i + 2];
+      const size_t v[12] = {a.w_off, b.w_off, c.w_off, S.bns[a.bn].p_off, S.bns[b.bn].p_off, S.bns[c.bn].p_off,
+                            S.slots[a.dst].saved_off, S.slots[b.dst].saved_off, S.bns[a.bn].stats_off,
+                            S.bns[b.bn].stats_off, S.bns[c.bn].stats_off, S.slots[c.dst].saved_off};
+      for (int t = 0; t < 12; ++t) o[t] = v[t] == NONE ? 0xffffffffu : (unsigned)v[t];
+      for (int t = 0; t < 12; ++t)
+        if (v[t] != NONE && v[t] > 0xfffffff0u) return false;
+      return true;
+    };
+    unsigned o0[12], ok_[12];
+    if (!offs(0, o0)) return;
+    int n = 1;
+    unsigned st[12] = {0};
+    while (unit_at(S, i0 + 3 * n) && S.nodes[i0 + 3 * n].src == S.nodes[i0 + 3 * n - 1].dst) {
+      if (!offs(n, ok_)) break;
+      if (n == 1) {
+        for (int t = 0; t < 12; ++t) st[t] = ok_[t] - o0[t];
+        if (st[0] != st[1] || st[1] != st[2] || st[3] != st[4] || st[4] != st[5] || st[6] != st[7] ||
+            st[8] != st[9] || st[9] != st[10])
+          break;
+      } else {
+        bool same = true;
+        for (int t = 0; t < 11; ++t) same = same && ok_[t] == o0[t] + n * st[t];
+        if (!same) break;
+      }
+      // the previous unit's output slot is this unit's input: saved at the slot stride
+      if (S.slots[S.nodes[i0 + 3 * n - 1].dst].saved_off != (size_t)o0[6] + (size_t)(n - 1) * st[6] +
+                                                              (size_t)(o0[11] - o0[6]))
+        break;
+      ++n;
+    }
+    if (n < 2) return;
+    const NodeP& last = S.nodes[i0 + 3 * n - 1];
+    UnitJob& J = S.ru_job;
+    J.nu = n;
+    J.w1 = o0[0]; J.w2 = o0[1]; J.w3 = o0[2];
+    J.g1 = o0[3]; J.g2 = o0[4]; J.g3 = o0[5];
+    J.z1 = o0[6]; J.z2 = o0[7]; J.xo = o0[11];
+    J.s1 = o0[8]; J.s2 = o0[9]; J.s3 = o0[10];
+    const SlotP& lo = S.slots[last.dst];
+    J.gN = (last.dst != S.out && lo.bn >= 0) ? (unsigned)S.bns[lo.bn].p_off : 0xffffffffu;
+    J.sN = (last.dst != S.out && lo.bn >= 0) ? (unsigned)S.bns[lo.bn].stats_off : 0xffffffffu;
+    S.ru_dw = st[0]; S.ru_dg = st[3]; S.ru_dz = st[6]; S.ru_ds = st[8];
+    S.ru_node = i0;
+    S.ru_n = n;
+    S.ru_lo = S.nodes[i0].level;
+    S.ru_hi = last.level;
+    S.ru_xslot = S.nodes[i0].src;
+    for (int i = i0; i < i0 + 3 * n; ++i) S.nodes[i].resident = true;
+    return;
+  }
+}
+
 // wgrad partial bytes needed by every level of a set of segments at once (deferred weight gradients)
 size_t wgrad_all_bytes(const std::vector<SegP>& segs, int B, int es) {
   size_t tot = 0;
@@ -497,6 +591,7 @@ struct Ptrs {
   bool in_sums = false;               // forward: the input BN's sums are already in its partial rows
   const SegP* out_sums = nullptr;     // forward: the output's convolution also forms the sums of
                                       // this segment's input BN (the next coarse block)
+  bool resident = false;              // forward: the segment's unit run goes to the resident kernel
 };
 
 struct Ctx {
@@ -793,7 +888,7 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
       const SegP& S = *segs[i];
       const Ptrs& P = ptrs[i];
       for (const NodeP& n : S.nodes) {
-        if (n.level != L) continue;
+        if (n.level != L || (P.resident && n.resident)) continue;
         const SlotP& so = S.slots[n.dst];
         const void* ext = (n.dst == S.out) ? P.ext : nullptr;
         if (n.op == PNN_OP_CONV) {
@@ -1258,12 +1353,15 @@ int chains_group(const Ctx& c, const std::vector<const SegP*>& segs, const std::
   auto work = [&](size_t g) {
     size_t w = 0;
     for (auto* sp : ch.segs[g]) w += sp->saved_bytes;
+    for (auto& pp : ch.ptrs[g])
+      if (pp.resident) return (size_t)0;   // resident runs stay in one chain (one launch at a time)
     return w;
   };
   while ((int)ch.segs.size() < maxg) {
     size_t big = 0;
     for (size_t g = 1; g < ch.segs.size(); ++g)
       if (work(g) > work(big)) big = g;
+    if (work(big) == 0) break;
     const size_t n = ch.segs[big].size();
     if (n < 2) break;
     ch.segs.emplace_back(ch.segs[big].begin() + n / 2, ch.segs[big].end());
@@ -1310,14 +1408,71 @@ int chains_join(const Ctx& c, const Chains& ch) {
   return st;
 }
 
+// The resident kernel's launches for the unit runs of the segments flagged in ptrs: one workgroup
+// per image, the segments packed in waves of at most plan->unit_cap workgroups (all of a launch's
+// workgroups must be resident together; the launches follow each other on the one stream).
+int fire_units(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
+  pnn_plan* plan = c.plan;
+  const int B = plan->B;
+  unsigned* sync = (unsigned*)(c.scratch + plan->unit_off);
+  UnitLaunch L;
+  std::memset(&L, 0, sizeof(L));
+  auto fire = [&]() -> int {
+    if (L.n == 0) return PNN_OK;
+    if (launch_unit_reset(sync, c.stream) || launch_unit_fwd(L, c.stream)) return (int)PNN_ERR_HIP;
+    L.n = 0;
+    L.nwg = 0;
+    L.nu_max = 0;
+    return (int)PNN_OK;
+  };
+  for (size_t i = 0; i < segs.size(); ++i) {
+    const SegP& S = *segs[i];
+    const Ptrs& P = ptrs[i];
+    if (!P.resident) continue;
+    if (L.n == UNIT_MAXJ || L.nwg + B > plan->unit_cap) {
+      const int e = fire();
+      if (e) return e;
+    }
+    L.B = B;
+    L.dw = S.ru_dw; L.dg = S.ru_dg; L.dz = S.ru_dz; L.ds = S.ru_ds;
+    L.sync = sync;
+    UnitJob J = S.ru_job;
+    J.x_in = slot_ptr(c, S, P, S.ru_xslot);
+    J.params = cp(P.params);
+    J.saved = c.saved + S.saved_base;
+    J.y_out = P.out;
+    J.part = (float*)(c.scratch + plan->unit_off + UNIT_SYNC_BYTES + (size_t)S.index * plan->unit_part_stride);
+    J.wg_begin = L.nwg;
+    L.j[L.n++] = J;
+    L.nwg += B;
+    L.nu_max = std::max(L.nu_max, J.nu);
+  }
+  return fire();
+}
+
+// Resident unit runs of one chain: the level from which they all can start (each run's own first
+// level, the latest of them), after dropping the runs that would end before it.
+int resident_level(const std::vector<const SegP*>& segs, std::vector<Ptrs>& ptrs) {
+  int lf = 0;
+  for (size_t i = 0; i < segs.size(); ++i)
+    if (ptrs[i].resident) lf = std::max(lf, segs[i]->ru_lo);
+  for (size_t i = 0; i < segs.size(); ++i)
+    if (ptrs[i].resident && segs[i]->ru_hi < lf) ptrs[i].resident = false;
+  return lf;
+}
+
 int run_fwd_chains(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
   Chains ch;
   int e = chains_fork(c, segs, ptrs, ch);
   const int G = (int)ch.segs.size();
+  std::vector<int> lf(G, 0);
+  for (int g = 0; g < G; ++g) lf[g] = resident_level(ch.segs[g], ch.ptrs[g]);
   for (int g = 0; e == PNN_OK && g < G; ++g) e = run_fwd_begin(ch.ctx[g], ch.segs[g], ch.ptrs[g]);
   for (int L = 1, maxL = seg_max_level(segs); e == PNN_OK && L <= maxL; ++L)
-    for (int g = 0; e == PNN_OK && g < G; ++g)
-      if (L <= seg_max_level(ch.segs[g])) e = run_fwd_level(ch.ctx[g], ch.segs[g], ch.ptrs[g], L);
+    for (int g = 0; e == PNN_OK && g < G; ++g) {
+      if (L == lf[g]) e = fire_units(ch.ctx[g], ch.segs[g], ch.ptrs[g]);
+      if (e == PNN_OK && L <= seg_max_level(ch.segs[g])) e = run_fwd_level(ch.ctx[g], ch.segs[g], ch.ptrs[g], L);
+    }
   const int ej = chains_join(c, ch);
   return e != PNN_OK ? e : ej;
 }
@@ -1334,6 +1489,13 @@ int run_bwd_chains(const Ctx& c, const std::vector<const SegP*>& segs, const std
   for (int g = 0; e == PNN_OK && g < G; ++g) e = run_bwd_end(ch.ctx[g], ch.segs[g], ch.ptrs[g], pending[g]);
   const int ej = chains_join(c, ch);
   return e != PNN_OK ? e : ej;
+}
+
+// The resident kernel runs when enabled and one sub-network's batch fits the device at once (the
+// occupancy, queried when it is turned on).
+bool resident_ok(pnn_plan* plan) {
+  if (!plan->resident_on || plan->dtype != PNN_BF16) return false;
+  return plan->unit_cap >= plan->B;
 }
 
 bool ok_ctx(pnn_plan* plan, void* saved, void* scratch) {
@@ -1474,6 +1636,12 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
   p->sq_off = sc;
   p->sq_bytes = (size_t)sqt * 4;
   sc = align256(sc + p->sq_bytes);
+  // resident units (bf16 storage): runs in the fine segments, their barrier words and partials
+  if (p->dtype == PNN_BF16)
+    for (auto& f : p->fine) find_unit_run(f);
+  p->unit_off = sc;
+  p->unit_part_stride = align256((size_t)p->B * (2 * UNIT_MID + UNIT_C) * 2 * 4);
+  sc = align256(sc + UNIT_SYNC_BYTES + (size_t)N * p->unit_part_stride);
   for (auto* v : {&p->pre, &p->fine, &p->coarse})
     for (auto& s : *v) {
       s.scr_base = sc;
@@ -1565,6 +1733,7 @@ pnn_status parareal_fine_fwd(pnn_plan* plan, const void* const* x, const void* c
     p.in = x[j];
     p.out = y[j];
     p.params = phi[j];
+    p.resident = resident_ok(plan) && plan->fine[j].ru_n >= 2;
     segs.push_back(&plan->fine[j]);
     ptrs.push_back(p);
   }
@@ -2011,6 +2180,10 @@ pnn_status pnn_pre_bwd(pnn_plan* plan, const void* image, const void* const* g, 
 
 pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx, size_t* offset) {
   if (plan == nullptr || offset == nullptr) return PNN_ERR_NULL;
+  if (what == 4) {                 // the resident kernel's barrier words (scratch)
+    *offset = plan->unit_off;
+    return PNN_OK;
+  }
   const std::vector<SegP>* v = part == 0 ? &plan->pre : part == 1 ? &plan->fine : part == 2 ? &plan->coarse : nullptr;
   if (v == nullptr || j < 0 || j >= (int)v->size()) return PNN_ERR_INDEX;
   const SegP& S = (*v)[j];
@@ -2057,6 +2230,13 @@ pnn_status pnn_set_streams(pnn_plan* plan, int streams) {
     plan->fj.push_back(e);
   }
   plan->streams = streams;
+  return PNN_OK;
+}
+
+pnn_status pnn_set_resident(pnn_plan* plan, int on) {
+  if (plan == nullptr) return PNN_ERR_NULL;
+  plan->resident_on = on != 0;
+  if (plan->resident_on && plan->unit_cap < 0) plan->unit_cap = unit_fwd_occupancy();
   return PNN_OK;
 }
 

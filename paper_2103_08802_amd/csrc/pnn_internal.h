@@ -233,11 +233,48 @@ struct SgdLaunch {
 };
 int launch_sgd(const SgdLaunch& L, int tiles, int dtype, hipStream_t s);
 
+// Resident forward of a run of pre-activation bottleneck units (k_unit.hip): identity skip, stride
+// 1, UNIT_H x UNIT_W maps, UNIT_C channels squeezed to UNIT_MID.  One workgroup per image of a
+// sub-network ("job"); unit u's tensors sit at the first unit's byte offsets plus u times the
+// launch's strides.
+constexpr int UNIT_H = 32, UNIT_W = 32, UNIT_C = 64, UNIT_MID = 16;
+constexpr int UNIT_WAVES = 8;       // waves per workgroup (one image)
+constexpr int UNIT_MAXJ = 8;
+// Barrier words at the start of the unit scratch (uint32): [0] error flag (a wait gave up), [1]
+// barriers completed; job j's arrival counter and generation each on a 128-byte line of its own.
+constexpr int UNIT_SYNC_BYTES = 4096;
+__host__ __device__ constexpr int unit_sync_word(int job, int which) { return 64 * (job + 1) + 32 * which; }
+static_assert(unit_sync_word(UNIT_MAXJ - 1, 1) * 4 + 4 <= UNIT_SYNC_BYTES, "unit barrier words");
+struct UnitJob {
+  const void* x_in;          // input of the first unit [B][H][W][C]
+  const char* params;        // the segment's parameter buffer
+  char* saved;               // the segment's saved workspace
+  void* y_out;               // the segment output (the last unit's output when it has no BN)
+  float* part;               // per-image statistics: z1 [B][MID][2], z2 [B][MID][2], x [B][C][2]
+  int nu;                    // units
+  int wg_begin;              // first workgroup of the job (one per image)
+  unsigned w1, w2, w3;       // filters of the first unit's three convolutions (params)
+  unsigned g1, g2, g3;       // gamma | beta of BN(x), BN(z1), BN(z2) (params)
+  unsigned z1, z2, xo;       // z1, z2 and output slots of the first unit (saved)
+  unsigned s1, s2, s3;       // BN statistics of BN(x), BN(z1), BN(z2) (saved)
+  unsigned gN, sN;           // BN of the last unit's output (params, saved); 0xffffffff: none
+};
+struct UnitLaunch {
+  int n, B, nu_max, nwg;
+  unsigned dw, dg, dz, ds;   // per-unit strides: filters, BN parameters, slots, statistics
+  unsigned* sync;            // barrier words (UNIT_SYNC_BYTES)
+  UnitJob j[UNIT_MAXJ];
+};
+int launch_unit_reset(unsigned* sync, hipStream_t s);
+int launch_unit_fwd(const UnitLaunch& L, hipStream_t s);
+int unit_fwd_occupancy();    // workgroups of the resident kernel that fit the device at once
+
 // gk: 0 = pointwise (1x1, stride 1, pad 0), 1 = vector gather, 2 = element-wise gather,
 //     3 = 3x3 / stride 1 / pad 1 through an LDS halo tile;
 // wn: 16-column sub-tiles per wave (1, 2, 4) shared by every problem of the launch
 // every launch record fits the 4 KB of kernel arguments
 static_assert(sizeof(ConvLaunch) <= 4096 && sizeof(WgradLaunch) <= 4096 && sizeof(ColRedLaunch) <= 4096 &&
+              sizeof(UnitLaunch) <= 4096 &&
               sizeof(BnApplyLaunch) <= 4096 && sizeof(TransposeLaunch) <= 4096 && sizeof(SgdLaunch) <= 4096,
               "kernel argument size");
 int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, int wm, hipStream_t s);

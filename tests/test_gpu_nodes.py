@@ -34,12 +34,22 @@ def _rel_2_with_inf(a, ref):
     return _E2(rel_2(a, ref), rel_inf(a, ref))
 
 
-def gpu_step(net, params, x, labels):
+def gpu_step(net, params, x, labels, resident=False):
     import torch
+    from paper_2103_08802_amd import binding as B
     from paper_2103_08802_amd.step import ParaRealGPU
     g = ParaRealGPU(net, params)
+    if resident:
+        B.pnn_set_resident(g.plan, 1)
     g.load_input(x, labels)
     g.forward()
+    if resident:
+        torch.cuda.synchronize()
+        off = g.plan.inspect(0, 0, 4, 0)
+        words = g.scratch[off:off + 8].view(torch.int32).cpu().tolist()
+        _say(f"[nodes] resident barrier words {words}")
+        assert words[0] == 0, "a resident barrier wait gave up"
+        assert words[1] > 0 and words[1] % 3 == 0, "resident kernel did not run"
     g.backward_coarse_fine()
     torch.cuda.synchronize()
     dx_fine = [t.clone() for t in g.dx]
@@ -59,14 +69,14 @@ def sample_nodes(seg, rng, n_mid=3):
     return sorted(pick)
 
 
-def check_net(net, sample=None, fine_subset=None, seed=0, node_subset=False, x_offset=0.0):
+def check_net(net, sample=None, fine_subset=None, seed=0, node_subset=False, x_offset=0.0, resident=False):
     from oracle import prim as P
     x, labels, params = S.make_all(net)
     if x_offset:
         from pnn_synth.gen import to_storage
         x = to_storage(x + x_offset, net.dtype)
     _say(f"[nodes] {net.name} batch {net.batch} {net.dtype}: GPU step")
-    g, dx_fine = gpu_step(net, params, x, labels)
+    g, dx_fine = gpu_step(net, params, x, labels, resident)
     bf16 = net.dtype == "bf16"
     st = P.round_bf16 if bf16 else (lambda a: a)
     metric = _rel_2_with_inf if bf16 else rel_inf
@@ -119,6 +129,15 @@ def test_random_bn_nodes(idx, batch, dtype):
     net.dtype = dtype
     net.bn_init = "random"
     _assert(*check_net(net, node_subset=idx != 1))
+
+
+@pytest.mark.parametrize("batch,sample,fine_subset", [(3, None, [0, 4, 5]), (None, 256, [0, 5])])
+def test_resident_unit_nodes(batch, sample, fine_subset):
+    """The resident forward of the first-stage unit runs (ResNet-1001, N = 16): sub-networks 0-4 run
+    their whole fine forward in it, sub-network 5 its first units; whole tensors at batch 3 and
+    sampled at the full batch of 128 (two sub-networks per launch, three launches)."""
+    net = S.config(3, batch)
+    _assert(*check_net(net, sample=sample, fine_subset=fine_subset, node_subset=sample is None, resident=True))
 
 
 @pytest.mark.parametrize("idx,fine_subset", [(1, None), (2, [0, 1, 3]), (3, [0, 5, 10, 15]), (4, [0, 2, 5, 7])])
