@@ -159,7 +159,9 @@ pnn_status parareal_fine_fwd(pnn_plan* plan, const void* const* x, const void* c
                              void* const* y, void* saved, void* scratch, void* stream);
 
 /* r_j = y_j - x_{j+1}, j = 0..N-2 (eq. (rk)), r[j] shaped like y_j.  rnorm2 (nullable, float[N-1])
- * receives ||r_j||^2 (the interface mismatch the coarse network corrects, Sec. 3.1). */
+ * receives ||r_j||^2 (the interface mismatch the coarse network corrects, Sec. 3.1).  With a
+ * scratch (nullable when rnorm2 is NULL) a non-finite element of some r_j sets non-finite flag 0
+ * (pnn_inspect what = 5). */
 pnn_status parareal_combine_fwd(pnn_plan* plan, const void* const* y, const void* const* x,
                                 void* const* r, float* rnorm2, void* scratch, void* stream);
 
@@ -183,7 +185,8 @@ pnn_status coarse_fwd_all(pnn_plan* plan, void* const* rt, const void* const* et
  * mean_{h,w}(ytilde) W^T + b (eps = [W (classes x C) | b (classes)] float), loss = mean softmax
  * cross-entropy over the batch.  Writes logits[B][classes] (float, nullable), *loss (float,
  * device), D_N = dL/dytilde (X_N shaped) and deps = [dW | db] (float). labels: int32[B]; a label
- * outside [0, classes) makes that sample's loss term, and so *loss, NaN. */
+ * outside [0, classes) makes that sample's loss term, and so *loss, NaN.  A non-finite loss or
+ * element of deps sets non-finite flag 1 (pnn_inspect what = 5). */
 pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps,
                             const int32_t* labels, float* logits, float* loss, void* D_N,
                             float* deps, void* scratch, void* stream);
@@ -195,7 +198,8 @@ pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps
  * library, one per GPU, kept until the process ends; a larger problem returns PNN_ERR_TOO_LARGE.
  * Calls nothing that allocates.  The first call on a device (with that device current) looks up
  * the array's address (PNN_ERR_HIP if that fails).  Every call on one GPU shares that array:
- * calls that overlap in time on one GPU race. */
+ * calls that overlap in time on one GPU race.  It raises no non-finite flag (they live in the
+ * scratch workspace). */
 pnn_status pnn_head_fwd_bwd_noalloc(pnn_plan* plan, const void* ytilde, const float* eps,
                                     const int32_t* labels, float* logits, float* loss, void* D_N,
                                     float* deps, void* stream);
@@ -284,6 +288,10 @@ pnn_status pnn_sgd_step(pnn_plan* plan, int part, void* const* params, const flo
  *   what = 4: (part, j, idx ignored) the resident kernel's barrier words in scratch: uint32 [0] an
  *             error flag, non-zero when a barrier wait gave up, [1] barriers completed by the last
  *             resident launch (one per batch-normalisation point per unit and sub-network)
+ *   what = 5: (part, j, idx ignored) the non-finite flags in scratch, uint32 [2]: [0] set to 1 by
+ *             parareal_combine_fwd (given a scratch) when an element of some r_j is not finite,
+ *             [1] by pnn_head_fwd_bwd when the loss or an element of deps is not finite; sticky
+ *             until pnn_flags_clear
  * *offset receives the byte offset into that workspace.  PNN_ERR_INDEX when the tensor is not held
  * by the library (slot 0 and the segment output are the caller's tensors) or does not exist. */
 pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx, size_t* offset);
@@ -300,6 +308,12 @@ const char* pnn_status_string(pnn_status s);
  * set-up call: needs a HIP device, allocates no device memory); PNN_ERR_HIP if that fails.
  * PNN_ERR_INDEX outside 1 .. 4. */
 pnn_status pnn_set_streams(pnn_plan* plan, int streams);
+
+/* Clears the non-finite flags (pnn_inspect what = 5) with a one-workgroup kernel on stream (no
+ * memset node, so the call can be captured in a graph).  Scratch content is undefined after
+ * allocation: clear before the first step whose flags are read.  PNN_ERR_NULL, PNN_ERR_ALIGN
+ * (scratch not 256-byte aligned), PNN_ERR_HIP. */
+pnn_status pnn_flags_clear(pnn_plan* plan, void* scratch, void* stream);
 
 /* Resident forward of bottleneck-unit runs (PNN_BF16 plans; default off, 1 turns it on):
  * parareal_fine_fwd then runs each fine sub-network's run of identity pre-activation bottleneck units

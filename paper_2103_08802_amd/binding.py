@@ -27,7 +27,7 @@ EXPORTS = ["pnn_plan_create", "pnn_plan_destroy", "pnn_workspace_size", "pnn_par
            "parareal_combine_bwd", "pnn_pre_bwd", "pnn_status_string", "pnn_inspect",
            "pnn_timing_enable", "pnn_timing_read", "pnn_sgd_step", "coarse_bwd_all", "coarse_fwd_all",
            "pnn_set_streams",
-           "parareal_bwd", "pnn_head_fwd_bwd_noalloc", "pnn_set_resident"]
+           "parareal_bwd", "pnn_head_fwd_bwd_noalloc", "pnn_set_resident", "pnn_flags_clear"]
 
 
 class PnnError(RuntimeError):
@@ -91,6 +91,7 @@ def lib():
     L.pnn_timing_enable.argtypes = [_vp, i]
     L.pnn_set_streams.argtypes = [_vp, i]
     L.pnn_set_resident.argtypes = [_vp, i]
+    L.pnn_flags_clear.argtypes = [_vp, _vp, _vp]
     L.pnn_timing_read.argtypes = [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_longlong),
                                   ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     L.coarse_bwd_all.argtypes = [_vp, _PP, _PP, _PP, _vp, _PP, _vp, _vp]
@@ -324,6 +325,10 @@ def pnn_set_streams(plan, streams):
 
 def pnn_set_resident(plan, on):
     _check(lib().pnn_set_resident(plan.handle, int(bool(on))), "pnn_set_resident")
+
+
+def pnn_flags_clear(plan, scratch, stream):
+    _check(lib().pnn_flags_clear(plan.handle, _ptr(scratch), stream), "pnn_flags_clear")
 
 
 def pnn_timing_enable(plan, family):

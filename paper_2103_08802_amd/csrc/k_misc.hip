@@ -507,9 +507,9 @@ __global__ __launch_bounds__(256) void transpose_kernel(const TransposeLaunch L)
   }
 }
 
-// out = a - b (rounded to storage); optional per-tile partial of sum(out^2).  SUB_TILE elements per
-// workgroup; a whole tile goes as 16-byte chunks with every load issued before the first store, a
-// ragged last tile element by element.
+// out = a - b (rounded to storage); optional per-tile partial of sum(out^2) and non-finite flag.
+// SUB_TILE elements per workgroup; a whole tile goes as 16-byte chunks with every load issued before
+// the first store, a ragged last tile element by element.
 template <typename T>
 __global__ __launch_bounds__(256) void sub_kernel(const AxpyLaunch L) {
   constexpr int VE = St<T>::VE;
@@ -520,6 +520,7 @@ __global__ __launch_bounds__(256) void sub_kernel(const AxpyLaunch L) {
   const int tile = blockIdx.x - P.tile_begin;
   const long base = (long)tile * SUB_TILE;
   float sq = 0.f;
+  bool bad = false;
   if (base + SUB_TILE <= P.n) {
     uint4 ua[NCH], ub[NCH];
 #pragma unroll
@@ -540,6 +541,7 @@ __global__ __launch_bounds__(256) void sub_kernel(const AxpyLaunch L) {
         v[e] = ca.v[e] - cb.v[e];
         const float vr = St<T>::rnd(v[e]);
         sq += vr * vr;
+        bad |= !isfinite(vr);
       }
       store_chunk<T>(P.out, i, v);
     }
@@ -551,8 +553,11 @@ __global__ __launch_bounds__(256) void sub_kernel(const AxpyLaunch L) {
       St<T>::st(P.out, i, v);
       const float vr = St<T>::rnd(v);
       sq += vr * vr;
+      bad |= !isfinite(vr);
     }
   }
+  if (L.flag != nullptr && __syncthreads_or(bad) && threadIdx.x == 0)
+    __hip_atomic_store(L.flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if (P.sq_part != nullptr) {
     sq = wave_sum(sq);
     if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sq;
@@ -703,7 +708,7 @@ __global__ __launch_bounds__(256) void head_sample_kernel(const void* yt, const 
 // 64 outputs of [dW | db | loss] per workgroup; wave w sums the samples of its quarter of the
 // batch, the four partial sums are added in wave order.
 __global__ __launch_bounds__(256) void head_reduce_kernel(const float* scratch, float* deps,
-                                                          float* loss, int B, int C, int K) {
+                                                          float* loss, int B, int C, int K, unsigned* flag) {
   __shared__ float rs[4][64];
   __shared__ double rl[4];
   const float* pooled = scratch;
@@ -729,12 +734,24 @@ __global__ __launch_bounds__(256) void head_reduce_kernel(const float* scratch, 
   }
   rs[wave][lane] = acc;
   __syncthreads();
+  bool bad = false;
   if (wave == 0) {
-    if (i < nW + K)
-      deps[i] = ((rs[0][lane] + rs[1][lane]) + rs[2][lane]) + rs[3][lane];
-    else if (i == nW + K)
-      *loss = (float)((((rl[0] + rl[1]) + rl[2]) + rl[3]) / (double)B);
+    if (i < nW + K) {
+      const float v = ((rs[0][lane] + rs[1][lane]) + rs[2][lane]) + rs[3][lane];
+      deps[i] = v;
+      bad = !isfinite(v);
+    } else if (i == nW + K) {
+      const float v = (float)((((rl[0] + rl[1]) + rl[2]) + rl[3]) / (double)B);
+      *loss = v;
+      bad = !isfinite(v);
+    }
   }
+  if (flag != nullptr && __syncthreads_or(bad) && threadIdx.x == 0)
+    __hip_atomic_store(flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ void flags_clear_kernel(unsigned* flags) {
+  if (threadIdx.x < PNN_NFLAGS) flags[threadIdx.x] = 0u;
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -777,6 +794,10 @@ int launch_transpose(const TransposeLaunch& L, int tiles, int dtype, hipStream_t
 int launch_sub(const AxpyLaunch& L, int tiles, int dtype, hipStream_t s) {
   PNN_LAUNCH_T(sub_kernel, L, tiles, dtype, s);
 }
+int launch_flags_clear(unsigned* flags, hipStream_t s) {
+  hipLaunchKernelGGL(flags_clear_kernel, dim3(1), dim3(64), 0, s, flags);
+  return (int)hipGetLastError();
+}
 int launch_sumsq(const float* part, int n, float* out, hipStream_t s) {
   hipLaunchKernelGGL(sumsq_kernel, dim3(1), dim3(64), 0, s, part, n, out);
   return (int)hipGetLastError();
@@ -784,7 +805,7 @@ int launch_sumsq(const float* part, int n, float* out, hipStream_t s) {
 
 int launch_head(const void* yt, const float* eps, const int32_t* labels, float* logits, float* loss,
                 void* D_N, float* deps, float* scratch, int B, int HW, int C, int K, int dtype,
-                hipStream_t s) {
+                unsigned* flag, hipStream_t s) {
   const int es = dtype == 1 ? 2 : 4, ve = 16 / es;
   const bool vec = C % ve == 0 && ((uintptr_t)yt % 16) == 0 && ((uintptr_t)D_N % 16) == 0;
   int G = 0;
@@ -803,7 +824,7 @@ int launch_head(const void* yt, const float* eps, const int32_t* labels, float* 
   if (e) return e;
   const long n = (long)K * C + K + 1;
   hipLaunchKernelGGL(head_reduce_kernel, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, s,
-                     scratch, deps, loss, B, C, K);
+                     scratch, deps, loss, B, C, K, flag);
   return (int)hipGetLastError();
 }
 

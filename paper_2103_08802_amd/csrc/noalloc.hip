@@ -65,6 +65,6 @@ extern "C" pnn_status pnn_head_fwd_bwd_noalloc(pnn_plan* plan, const void* ytild
   float* s = device_scratch();
   if (s == nullptr) return PNN_ERR_HIP;
   const int e = pnn::launch_head(ytilde, eps, labels, logits, loss, D_N, deps, s, B, HW, C, K, dtype,
-                                 (hipStream_t)stream);
+                                 nullptr, (hipStream_t)stream);
   return e ? PNN_ERR_HIP : PNN_OK;
 }

@@ -106,6 +106,7 @@ struct pnn_plan {
   int resident_on = 0;
   int unit_cap = -1;
   size_t unit_off = 0, unit_part_stride = 0;
+  size_t flags_off = 0;             // non-finite flags (PNN_NFLAGS uint32, scratch)
   // independent chains of the fine sub-networks: up to `streams` streams, the call's stream and
   // internal ones created by pnn_set_streams (default priority, non-blocking); compute calls never
   // create streams or events
@@ -1636,6 +1637,8 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
   p->sq_off = sc;
   p->sq_bytes = (size_t)sqt * 4;
   sc = align256(sc + p->sq_bytes);
+  p->flags_off = sc;
+  sc = align256(sc + PNN_NFLAGS * 4);
   // resident units (bf16 storage): runs in the fine segments, their barrier words and partials
   if (p->dtype == PNN_BF16)
     for (auto& f : p->fine) find_unit_run(f);
@@ -1750,6 +1753,7 @@ pnn_status parareal_combine_fwd(pnn_plan* plan, const void* const* y, const void
   hipStream_t s = (hipStream_t)stream;
   std::vector<AxpyProb> pr;
   float* sq = rnorm2 ? (float*)((char*)scratch + plan->sq_off) : nullptr;
+  unsigned* flag = scratch ? (unsigned*)((char*)scratch + plan->flags_off) : nullptr;
   long off = 0;
   for (int j = 0; j + 1 < plan->N; ++j) {
     if (y[j] == nullptr || x[j + 1] == nullptr || r[j] == nullptr) return PNN_ERR_NULL;
@@ -1765,7 +1769,11 @@ pnn_status parareal_combine_fwd(pnn_plan* plan, const void* const* y, const void
   }
   int e = grouped<AxpyLaunch>(
       pr, [](const AxpyProb& p) { return (int)cdiv(p.n, SUB_TILE); },
-      [&](const AxpyLaunch& L, int tiles, size_t) { return launch_sub(L, tiles, plan->dtype, s); });
+      [&](const AxpyLaunch& L, int tiles, size_t) {
+        AxpyLaunch M = L;
+        M.flag = flag;
+        return launch_sub(M, tiles, plan->dtype, s);
+      });
   if (e) return e;
   if (sq) {
     off = 0;
@@ -1856,7 +1864,8 @@ pnn_status pnn_head_fwd_bwd(pnn_plan* plan, const void* ytilde, const float* eps
   if (plan->classes > 4096 || yo.C > 8192) return PNN_ERR_UNSUPPORTED;
   int e = launch_head(ytilde, eps, labels, logits, loss, D_N, deps,
                       (float*)((char*)scratch + plan->head_off), plan->B, yo.H * yo.W, yo.C,
-                      plan->classes, plan->dtype, (hipStream_t)stream);
+                      plan->classes, plan->dtype, (unsigned*)((char*)scratch + plan->flags_off) + 1,
+                      (hipStream_t)stream);
   return e ? PNN_ERR_HIP : PNN_OK;
 }
 
@@ -2184,6 +2193,10 @@ pnn_status pnn_inspect(const pnn_plan* plan, int part, int j, int what, int idx,
     *offset = plan->unit_off;
     return PNN_OK;
   }
+  if (what == 5) {                 // the non-finite flags (scratch)
+    *offset = plan->flags_off;
+    return PNN_OK;
+  }
   const std::vector<SegP>* v = part == 0 ? &plan->pre : part == 1 ? &plan->fine : part == 2 ? &plan->coarse : nullptr;
   if (v == nullptr || j < 0 || j >= (int)v->size()) return PNN_ERR_INDEX;
   const SegP& S = (*v)[j];
@@ -2231,6 +2244,13 @@ pnn_status pnn_set_streams(pnn_plan* plan, int streams) {
   }
   plan->streams = streams;
   return PNN_OK;
+}
+
+pnn_status pnn_flags_clear(pnn_plan* plan, void* scratch, void* stream) {
+  if (plan == nullptr || scratch == nullptr) return PNN_ERR_NULL;
+  if (!al(scratch, 256)) return PNN_ERR_ALIGN;
+  return launch_flags_clear((unsigned*)((char*)scratch + plan->flags_off), (hipStream_t)stream) ? PNN_ERR_HIP
+                                                                                               : PNN_OK;
 }
 
 pnn_status pnn_set_resident(pnn_plan* plan, int on) {

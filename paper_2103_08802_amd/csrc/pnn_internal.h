@@ -207,8 +207,12 @@ struct AxpyProb {        // out = a - b (rounded to storage); partial sum of squ
 };
 struct AxpyLaunch {
   int n;
+  unsigned* flag = nullptr;   // set to 1 when an output is not finite (nullable)
   AxpyProb p[PNN_MAXG];
 };
+// non-finite flags (uint32 words in scratch): [0] combine output r_j, [1] head loss / dW / db
+constexpr int PNN_NFLAGS = 2;
+int launch_flags_clear(unsigned* flags, hipStream_t s);
 
 // SGD with momentum over a list of parameter tensors.  Entry e covers count elements at byte
 // offset p_off of params[seg] and g_off of grads[seg] / momentum[seg]; workgroups
@@ -306,7 +310,7 @@ int launch_sumsq(const float* part, int n, float* out, hipStream_t s);
 int head_geometry(const pnn_plan* p, int* B, int* HW, int* C, int* K, int* dtype);
 int launch_head(const void* yt, const float* eps, const int32_t* labels, float* logits,
                 float* loss, void* D_N, float* deps, float* scratch, int B, int HW, int C,
-                int K, int dtype, hipStream_t s);
+                int K, int dtype, unsigned* flag, hipStream_t s);
 
 // tile sizes shared by host and device code
 // conv workgroup tile: 16 x 16 sub-tiles per wave (row sub-tiles x column sub-tiles); a problem with

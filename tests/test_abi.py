@@ -57,6 +57,43 @@ def test_plans_and_layouts(idx, coarse):
     p.close()
 
 
+@pytest.mark.parametrize("idx,coarse,dtype", [(i, "config", None) for i in range(6)] +
+                         [(2, "paper", None), (3, "config", "f32"), (1, "config", "f32")])
+def test_inspect_walk(idx, coarse, dtype):
+    """Every tensor pnn_inspect can name lies inside its workspace: slot values (saved) and slot
+    gradients (scratch) with their whole NHWC extent, BN output gradients and statistics by their
+    offset; indices past the last answer PNN_ERR_INDEX."""
+    _lib_or_skip()
+    net = S.config(idx, 2, coarse=coarse)
+    if dtype is not None:
+        net.dtype = dtype
+    p = B.Plan(net)
+    saved, scratch = p.workspace_size(B.PNN_WS_SAVED), p.workspace_size(B.PNN_WS_SCRATCH)
+    es = 2 if net.dtype == "bf16" else 4
+    for part, segs in ((0, net.pre), (1, net.fine), (2, net.coarse)):
+        for j, seg in enumerate(segs):
+            sh = S.segment_shapes(seg)
+            for what, ws in ((0, saved), (1, scratch)):
+                for k in range(len(sh) + 2):
+                    off = p.inspect(part, j, what, k)
+                    if k == 0 or k == seg.out or k >= len(sh):
+                        assert off is None, (part, j, what, k)
+                        continue
+                    if off is None:
+                        continue
+                    h, w, c = sh[k]
+                    assert off + net.batch * h * w * c * es <= ws, (part, j, what, k)
+            for what, ws in ((2, scratch), (3, saved)):
+                n_ok = 0
+                for k in range(len(seg.bns) + 2):
+                    off = p.inspect(part, j, what, k)
+                    if off is not None:
+                        assert 0 <= off < ws
+                        n_ok += 1
+                assert n_ok <= len(seg.bns)
+    p.close()
+
+
 def test_error_codes():
     L = _lib_or_skip()
     h = ctypes.c_void_p()
@@ -134,5 +171,20 @@ def test_alignment_rules():
                           ctypes.c_float(5e-4), 1, None) == -8
     assert L.pnn_sgd_step(p.handle, 1, A_ok, A_ok, A_ok, A_bad, 1, ctypes.c_float(0.1), ctypes.c_float(0.9),
                           ctypes.c_float(5e-4), 1, None) == -8                  # master copies too
+    assert L.pnn_flags_clear(p.handle, ws + 64, None) == -8
     assert B.pnn_status_string(-8) == "a pointer is not aligned as the interface requires"
+    p.close()
+
+
+def test_nonfinite_flag_words():
+    """The non-finite flags: PNN_NFLAGS uint32 words inside scratch, on a 256-byte boundary, apart
+    from the resident kernel's barrier words; pnn_flags_clear rejects NULL before enqueuing."""
+    L = _lib_or_skip()
+    p = B.Plan(S.config(3, 2))
+    scr = p.workspace_size(B.PNN_WS_SCRATCH)
+    off = p.inspect(0, 0, 5, 0)
+    assert off % 256 == 0 and off + 8 <= scr
+    assert off != p.inspect(0, 0, 4, 0)
+    assert L.pnn_flags_clear(p.handle, None, None) == -1
+    assert L.pnn_flags_clear(None, 1 << 30, None) == -1
     p.close()

@@ -364,6 +364,45 @@ def test_head_repeatable_and_label_range(idx, batch):
     assert torch.equal(g.logits, first[1])
 
 
+@pytest.mark.gpu
+@pytest.mark.parametrize("idx,batch", [(0, 4), (3, 2)])
+def test_nonfinite_flags(idx, batch):
+    """The non-finite flags: clear after a clean step; the combine raises flag 0 when an r_j element
+    is not finite (only when given a scratch), the head raises flag 1 when the loss is not finite;
+    pnn_flags_clear resets both."""
+    import torch
+    from paper_2103_08802_amd import binding as B
+    from paper_2103_08802_amd.step import ParaRealGPU
+    net = S.config(idx, batch)
+    x, labels, params = S.make_all(net)
+    g = ParaRealGPU(net, params)
+    g.load_input(x, labels)
+    off = g.plan.inspect(0, 0, 5, 0)
+
+    def flags():
+        torch.cuda.synchronize()
+        return g.scratch[off:off + 8].view(torch.int32).cpu().tolist()
+
+    B.pnn_flags_clear(g.plan, g.scratch, None)
+    g.forward()
+    assert flags() == [0, 0]
+    N = net.n_sub
+    y = g.y[N - 2].clone()
+    g.y[N - 2].view(-1)[7] = float("nan")
+    B.parareal_combine_fwd(g.plan, g.y, g.x, g.r, None, None, None)            # no scratch: no flag
+    assert flags() == [0, 0]
+    B.parareal_combine_fwd(g.plan, g.y, g.x, g.r, None, g.scratch, None)
+    assert flags() == [1, 0]
+    B.pnn_flags_clear(g.plan, g.scratch, None)
+    assert flags() == [0, 0]
+    g.y[N - 2].copy_(y)
+    g.ytilde.view(-1)[3] = float("inf")
+    B.pnn_head_fwd_bwd(g.plan, g.ytilde, g.eps, g.labels, g.logits, g.loss, g.D[N - 1], g.deps,
+                       g.scratch, None)
+    assert flags() == [0, 1]
+    assert not torch.isfinite(g.loss).all()
+
+
 def pooled_16ch_net(dtype, batch):
     """Two sub-networks on a 16-channel 32x32 input, g^1 ending at 16x16: C^2 max-pools the
     16-channel input (whole 16-byte channel chunks per thread) before its 1x1 convolution."""
