@@ -1,0 +1,250 @@
+// Implicit-GEMM kernel for the wide 3x3 convolutions (forward and data gradient) of the parareal
+// VGG sub-networks (Table vgg: 128-512 channels, K = 9 C_in = 1152-4608 per output) for gfx950,
+// where the contraction, not HBM, bounds the layer: bf16 v_mfma_f32_32x32x16_bf16 with fp32
+// accumulation, operands staged through LDS.
+//
+// A workgroup of four waves owns a 128 x 128 output tile (rows = output pixels, columns = output
+// channels); each wave a 64 x 64 quarter as 2 x 2 MFMA tiles of 32 x 32.  K runs in steps of GEMM_BK
+// (one filter tap and GEMM_BK channels per step, C_in being a multiple of it): the step's A rows (the
+// 128 output pixels' input pixels at the tap, BN prologue applied on the way into LDS, zeros for
+// padding) and B rows (128 filter rows) are loaded with 16-byte vector loads two steps ahead of
+// their use, written to one of two LDS stages, and read back as MFMA fragments from rows padded by
+// 16 bytes (conflict-free 16-byte fragment reads).  The fp32 tile is then staged in LDS and the
+// convolution epilogue shared with the other conv kernels does residual, BN-mask / BN-apply forms,
+// stores and per-tile BN partials (128-row tiles, the same partial rows as the other kernels).
+#include "device_common.h"
+#include "pnn_internal.h"
+#include "conv_epilogue.h"
+
+namespace pnn {
+
+namespace {
+
+constexpr int GM = GEMM_BM, GN = GEMM_BN, GKS = GEMM_BK;   // tile rows, columns; K per step
+constexpr int GAS = GKS + 8;                          // LDS row stride of an operand tile (bf16)
+constexpr int GLDA = GN + 4;                          // row stride of the staged fp32 tile
+constexpr int GOPS = GM * GAS + GN * GAS;             // bf16 elements of one stage (A then B)
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int GSMEM = 2 * GOPS * 2 > GM * GLDA * 4 ? 2 * GOPS * 2 : GM * GLDA * 4;   // bytes: stages | staging
+constexpr int GCH = GKS / 8;                          // 16-byte chunks per operand row and step
+constexpr int GLR = 256 / GCH;                        // rows per loader pass
+constexpr int GLP = GM / GLR;                         // loader passes (chunks per thread and operand)
+static_assert(GM == 128 && GN == 128 && GM % GLR == 0, "gemm tile: four waves of 64 x 64");
+
+}  // namespace
+
+// Problems: 3x3, stride 1, pad 1, output grid = input grid, Cg % GKS == 0, ncol % 128 == 0, bf16.
+template <int MODE>
+__global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
+  using T = uint16_t;
+  constexpr int VE = 8;
+  __shared__ __attribute__((aligned(16))) float smem[GSMEM / 4];
+  __shared__ __attribute__((aligned(16))) float2 pro_s[CONV_PRO_MAXC];
+  __shared__ __attribute__((aligned(16))) float bn_s[MODE == MODE_BWD ? 7 * GN : 1];
+  uint16_t* ops = (uint16_t*)smem;
+
+  const int gi = find_group(L);
+  const ConvProb& P = L.p[gi];
+  const int local = blockIdx.x - P.tile_begin;
+  const int tm = local / P.tiles_n;
+  const int tn = local - tm * P.tiles_n;
+  const int n0 = tn * GN;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int r32 = lane & 31, kh = lane >> 5;
+  const int wr = wave >> 1, wc = wave & 1;
+  const bool prologue = MODE == MODE_FWD && P.pro != nullptr;
+  const bool bnmask = MODE == MODE_BWD && (P.flags & (EPI_BN_MASK | EPI_BN_APPLY));
+
+  // loader geometry: thread tid moves 16-byte chunk ch of rows (and filter rows) lr + GLR h.  Per
+  // row: the element offset of its own pixel (the tap offset is uniform: ((r - 1) W + s - 1) Cg in
+  // the forward, mirrored in the data gradient) and a mask of the taps whose pixel is inside the image.
+  const int ch = tid % GCH, lr = tid / GCH;
+  const int PQ = P.P * P.Q;
+  long abase[GLP];
+  unsigned amask[GLP];
+#pragma unroll
+  for (int h = 0; h < GLP; ++h) {
+    const int m = tm * GM + lr + GLR * h;
+    const bool v = m < P.M;
+    const int mm = v ? m : 0;
+    const int n = div_l2(mm, PQ, P.pq_log2);
+    const int rem = mm - n * PQ;
+    const int p = div_l2(rem, P.Q, P.q_log2);
+    const int q = rem - p * P.Q;
+    abase[h] = (((long)n * P.H + p) * P.W + q) * P.Cg + 8 * ch;
+    unsigned mk = 0;
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int dr = MODE == MODE_FWD ? t / 3 - 1 : 1 - t / 3;
+      const int dq = MODE == MODE_FWD ? t % 3 - 1 : 1 - t % 3;
+      mk |= (v && (unsigned)(p + dr) < (unsigned)P.H && (unsigned)(q + dq) < (unsigned)P.W) ? 1u << t : 0u;
+    }
+    amask[h] = mk;
+  }
+  const T* wrow = (const T*)P.wmat + (long)(n0 + lr) * P.K + 8 * ch;   // ncol % GN == 0: all valid
+
+  if (prologue)
+    for (int c = tid; c < P.Cg; c += 256) pro_s[c] = make_float2(P.pro[c], P.pro[P.Cg + c]);
+  if (bnmask && tid < GN) {
+    const int col = n0 + tid;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) bn_s[k * GN + tid] = P.bnst[k * P.ncol + col];
+    if (P.flags & EPI_BN_APPLY) {
+#pragma unroll
+      for (int k = 0; k < 3; ++k) bn_s[(4 + k) * GN + tid] = P.coef[k * P.ncol + col];
+    }
+  }
+
+  // K step s covers tap s / (Cg / GKS), channels (s % (Cg / GKS)) GKS .. + GKS - 1.  Loads are
+  // issued for every step unconditionally (padding and rows past M from a clamped, valid address,
+  // zeroed when stored), so that no branch separates a load from the MFMAs it overlaps.
+  const T* const in = (const T*)P.in;
+  const int W = P.W, Cg = P.Cg, Kt = P.K;
+  const int spt = Cg / GKS;                        // steps per tap
+  const int spt_l2 = (spt & (spt - 1)) == 0 ? __builtin_ctz(spt) : -1;
+  const int nsteps = Kt / GKS;
+  struct Set {
+    uint4 a[GLP], b[GLP];
+    unsigned ok;                                   // bit h: row h of A is inside the image
+    int c;                                         // channel of the thread's chunk
+  };
+  auto gload = [&](int s, Set& R) {
+    s = s < nsteps ? s : nsteps - 1;               // past the end: a repeat of the last step
+    const int tap = spt_l2 >= 0 ? s >> spt_l2 : s / spt;
+    const int k0 = s * GKS;
+    const int cs = (s - tap * spt) * GKS;
+    R.c = cs + 8 * ch;
+    const int dr = MODE == MODE_FWD ? tap / 3 - 1 : 1 - tap / 3;
+    const int dq = MODE == MODE_FWD ? tap % 3 - 1 : 1 - tap % 3;
+    const long toff = ((long)dr * W + dq) * Cg + cs;
+    R.ok = 0;
+#pragma unroll
+    for (int h = 0; h < GLP; ++h) {
+      const bool ok = (amask[h] >> tap) & 1u;
+      R.ok |= ok ? 1u << h : 0u;
+      R.a[h] = *(const uint4*)(in + (ok ? abase[h] + toff : 0));
+    }
+#pragma unroll
+    for (int h = 0; h < GLP; ++h) R.b[h] = *(const uint4*)(wrow + (long)GLR * h * Kt + k0);
+  };
+  // a step's chunks into LDS stage st (prologue: ReLU(x scale + shift) of the stored values;
+  // padding and rows past M are zeros of the activated operand)
+  auto lstore = [&](int st, const Set& R) {
+    uint16_t* A = ops + st * GOPS;
+    uint16_t* Bt = A + GM * GAS;
+    float2 ps[VE];                                 // the chunk's (scale, shift): one channel set per step
+    if (prologue) {
+#pragma unroll
+      for (int e = 0; e < VE; e += 2) {
+        const float4 u = *(const float4*)&pro_s[R.c + e];
+        ps[e] = make_float2(u.x, u.y);
+        ps[e + 1] = make_float2(u.z, u.w);
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < GLP; ++h) {
+      const unsigned keep = 0u - ((R.ok >> h) & 1u);   // all ones for a row inside the image
+      uint4 w = make_uint4(R.a[h].x & keep, R.a[h].y & keep, R.a[h].z & keep, R.a[h].w & keep);
+      if (prologue) {
+        Chunk<T> v;
+        unpack_chunk<T>(w, v);
+        float f[VE];
+#pragma unroll
+        for (int e = 0; e < VE; ++e) f[e] = fmaxf(fmaf(v.v[e], ps[e].x, ps[e].y), 0.0f);
+        store_chunk<T>(&w, 0, f);
+        w = make_uint4(w.x & keep, w.y & keep, w.z & keep, w.w & keep);
+      }
+      *(uint4*)(A + (lr + GLR * h) * GAS + 8 * ch) = w;
+      *(uint4*)(Bt + (lr + GLR * h) * GAS + 8 * ch) = R.b[h];
+    }
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  auto compute = [&](int st) {
+    const uint16_t* A = ops + st * GOPS;
+    const uint16_t* Bt = A + GM * GAS;
+#pragma unroll
+    for (int kk = 0; kk < GKS / 16; ++kk) {
+      bf16x8 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        a[i] = *(const bf16x8*)(A + (wr * 64 + 32 * i + r32) * GAS + 16 * kk + 8 * kh);
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        b[j] = *(const bf16x8*)(Bt + (wc * 64 + 32 * j + r32) * GAS + 16 * kk + 8 * kh);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  // Step s computes from stage s & 1.  Two register sets: while step s computes, step s + 1's
+  // loads (issued a step earlier) are written to the other stage after the MFMAs and step s + 2's
+  // are in flight.  Each half of the loop body is straight-line code.
+  Set R0, R1;
+  gload(0, R0);
+  gload(1, R1);
+  __syncthreads();                                 // prologue constants in LDS
+  lstore(0, R0);
+  __syncthreads();
+  auto half = [&](int s, int st, Set& far, const Set& next) {
+    gload(s + 2, far);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(st);
+    __builtin_amdgcn_sched_barrier(0);
+    lstore(st ^ 1, next);
+    __syncthreads();
+  };
+  int s = 0;
+  for (; s + 1 < nsteps; s += 2) {
+    half(s, 0, R0, R1);
+    half(s + 1, 1, R1, R0);
+  }
+  if (s < nsteps) compute(0);                      // an odd step count: the last step
+  __syncthreads();
+
+  // stage the fp32 tile: D lane layout of the 32 x 32 MFMA (column r32, rows 8 (e / 4) + 4 kh + e % 4)
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        smem[(wr * 64 + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3)) * GLDA + wc * 64 + 32 * j + r32] = acc[i][j][e];
+
+  // streamed epilogue operands of the thread's chunks (as the other conv kernels)
+  constexpr int ncc = GN / VE, rpp = 256 / ncc, NCH = GM / rpp;
+  const int cc0 = (tid % ncc) * VE;
+  const void* pf = (MODE == MODE_FWD) ? P.res
+                   : ((P.flags & EPI_STORE_F32) ? nullptr : (bnmask ? P.zsrc : P.res));
+  const void* pf2 = (MODE == MODE_FWD) ? P.ext : ((P.flags & EPI_BN_APPLY) ? P.res : nullptr);
+  uint4 pre[NCH], pre2[NCH];
+#pragma unroll
+  for (int k = 0; k < NCH; ++k) {
+    const int m = tm * GM + tid / ncc + k * rpp;
+    const long o = (long)m * P.ncol + n0 + cc0;
+    pre[k] = (pf != nullptr && m < P.M) ? *(const uint4*)((const T*)pf + o) : make_uint4(0, 0, 0, 0);
+    pre2[k] = (pf2 != nullptr && m < P.M) ? *(const uint4*)((const T*)pf2 + o) : make_uint4(0, 0, 0, 0);
+  }
+  __syncthreads();
+  conv_epilogue<T, MODE, GM, GN, GLDA, GN>(P, smem, (float*)pro_s, bn_s, tm, n0, pre, pre2);
+}
+
+int launch_gemm(const ConvLaunch& L, int tiles, int mode, hipStream_t s) {
+  if (mode == MODE_FWD)
+    hipLaunchKernelGGL(gemm_conv_kernel<MODE_FWD>, dim3(tiles), dim3(256), 0, s, L);
+  else
+    hipLaunchKernelGGL(gemm_conv_kernel<MODE_BWD>, dim3(tiles), dim3(256), 0, s, L);
+  return (int)hipGetLastError();
+}
+
+}  // namespace pnn

@@ -727,7 +727,8 @@ int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk, i
           by += conv_bytes(L.p[i], plan->es, mode);
         }
         Timer t(plan, 1, c.stream);
-        int e = launch_conv(L, tiles, plan->dtype, mode, gk, wn, wm, c.stream);
+        int e = gk == 4 ? launch_gemm(L, tiles, mode, c.stream)
+                        : launch_conv(L, tiles, plan->dtype, mode, gk, wn, wm, c.stream);
         t.done(c.stream, fl, by);
         return e;
       });
@@ -748,23 +749,38 @@ bool halo_ok(const ConvProb& p, int es) {
   return nimg * (rows + 2) * (p.Q + 2) * ps * es <= CONV_HALO_BYTES;
 }
 
+// A wide 3x3 / stride 1 / pad 1 bf16 problem for the GEMM kernel: K steps of GEMM_BK channels
+// within one tap, 128-column tiles, 128-row tiles (the tall tiles it would otherwise take).
+bool gemm_ok(const ConvProb& p, int es) {
+  return es == 2 && p.k == 3 && p.stride == 1 && p.pad == 1 && p.H == p.P && p.W == p.Q &&
+         p.Cg % GEMM_BK == 0 && p.Cg <= CONV_PRO_MAXC && p.ncol % GEMM_BN == 0 && 64 * p.wm == GEMM_BM;
+}
+
 // Gather kind of a convolution problem: 0 pointwise, 1 vector gather, 2 element-wise gather,
-// 3 halo tile.
+// 3 halo tile, 4 the GEMM kernel.
 int gather_kind(const ConvProb& p, int es) {
   if (p.Cg % (16 / es) != 0) return 2;
   if (p.k == 1 && p.stride == 1 && p.pad == 0) return 0;
+  if (gemm_ok(p, es)) return 4;
   if (halo_ok(p, es)) return 3;
   return 1;
 }
 
 // one grouped launch per (gather kind, column sub-tiles, tall / short tiles)
 int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode) {
-  std::vector<ConvProb> by[4][3][2];
+  std::vector<ConvProb> by[5][3][2];
   for (auto& p : probs) {
     const int w = p.wn == 1 ? 0 : p.wn == 2 ? 1 : 2;
-    by[gather_kind(p, c.plan->es)][w][p.wm == conv_wm(p.wn, false) ? 0 : 1].push_back(p);
+    const int gk = gather_kind(p, c.plan->es);
+    ConvProb q = p;
+    if (gk == 4) q.tiles_n = q.ncol / GEMM_BN;
+    by[gk][w][p.wm == conv_wm(p.wn, false) ? 0 : 1].push_back(q);
   }
-  for (int gk = 0; gk < 4; ++gk)
+  // GEMM launches: the longest K first, so that the longest tiles start first
+  for (auto& v : by[4])
+    for (auto& t : v)
+      std::stable_sort(t.begin(), t.end(), [](const ConvProb& a, const ConvProb& b) { return a.K > b.K; });
+  for (int gk = 0; gk < 5; ++gk)
     for (int w = 0; w < 3; ++w)
       for (int t = 0; t < 2; ++t) {
         if (by[gk][w][t].empty()) continue;

@@ -282,6 +282,11 @@ static_assert(sizeof(ConvLaunch) <= 4096 && sizeof(WgradLaunch) <= 4096 && sizeo
               sizeof(BnApplyLaunch) <= 4096 && sizeof(TransposeLaunch) <= 4096 && sizeof(SgdLaunch) <= 4096,
               "kernel argument size");
 int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, int wm, hipStream_t s);
+// wide 3x3 problems (k_gemm.hip): GEMM_BM x GEMM_BN tiles, bf16; the tile rows equal the tall conv
+// tiles of 64-column problems, so BN partial rows do not depend on which kernel runs a problem
+constexpr int GEMM_BM = 128, GEMM_BN = 128, GEMM_BK = 64;
+constexpr int CONV_PRO_MAXC = 512;     // largest Cg of a forward BN prologue held in LDS
+int launch_gemm(const ConvLaunch& L, int tiles, int mode, hipStream_t s);
 // activation gather of wgrad_kernel: element-wise (any channel count), 16-byte chunks through the
 // filter taps (Cg a multiple of the chunk), or pointwise (1x1 / stride 1 / pad 0: input row m)
 enum { WG_GEN = 0, WG_VEC = 1, WG_PW = 2 };

@@ -16,7 +16,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2103_08802_amd", "csrc")
 OUT = os.path.join(ROOT, "_build", "asan")
-KERNEL_SOURCES = ["k_conv.hip", "k_misc.hip", "k_unit.hip", "noalloc.hip"]
+KERNEL_SOURCES = ["k_conv.hip", "k_gemm.hip", "k_misc.hip", "k_unit.hip", "noalloc.hip"]
 HOST_SAN = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
             "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer"]
 
