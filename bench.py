@@ -66,7 +66,7 @@ def cpu_baseline(idx, batch=24, coarse="config"):
 # sources a kernel family's code and launch shapes come from; a stored traffic figure is void
 # once any of them changes
 KERNEL_SOURCES = {
-    "conv_kernel": ["k_conv.hip", "device_common.h", "pnn_internal.h", "plan.hip"],
+    "conv_kernel": ["k_conv.hip", "conv_epilogue.h", "device_common.h", "pnn_internal.h", "plan.hip"],
     "wgrad_kernel": ["k_conv.hip", "device_common.h", "pnn_internal.h", "plan.hip"],
 }
 COPY_BYTES = 256 << 20          # the --copy-calibration copy
@@ -191,7 +191,7 @@ def summarize_families(fetch_csv, write_csv, trace_csv, out_md, cmd):
             f.write(f"| `{n}` | {c} | {fm:.1f} | {wm:.1f} | {us:.2f} | {gbs:.0f} |\n")
 
 
-def summarize_mfma(csv_path, out_md, algo_flops, cmd):
+def summarize_mfma(csv_path, out_md, algo_flops, cmd, title="parareal ResNet-1001, N=16, batch 128, bf16 (one stream)"):
     """Per kernel family, from one rocprofv3 --pmc run of the derived counters MfmaUtil (MFMA busy
     cycles summed over SIMDs / (GPU active cycles x SIMDs), percent) and MfmaFlopsBF16 (bf16 MFMA
     operations x 512): the launch-weighted MFMA utilisation and the MFMA FLOPs per launch.  For
@@ -219,8 +219,8 @@ def summarize_mfma(csv_path, out_md, algo_flops, cmd):
     rows = sorted(fams.items(), key=lambda kv: -kv[1][2])
     rec = None
     with open(out_md, "w") as fh:
-        fh.write("# MFMA utilisation per kernel family: parareal ResNet-1001, N=16, batch 128, bf16 "
-                 "(one stream)\n\nCommand (from the repository root, on one MI355X):\n\n```\n"
+        fh.write(f"# MFMA utilisation per kernel family: {title}\n\nCommand (from the repository root, "
+                 "on one MI355X):\n\n```\n"
                  f"{cmd}\n```\n\nMfmaUtil = SQ_VALU_MFMA_BUSY_CYCLES summed over SIMDs / "
                  "(GRBM_GUI_ACTIVE x SIMD count), per dispatch, averaged weighted by dispatch "
                  "duration; MFMA GFLOP = MfmaFlopsBF16 (SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512) per "
@@ -293,12 +293,21 @@ def summarize_trace(stats_csv, trace_csv, out_md, title, cmd):
         t = fam.setdefault(n, [0, 0.0])
         t[0] += 1
         t[1] += d
+    # every step runs the head once: its dispatch count is the number of steps in the run
+    steps = fam.get("head_sample_kernel", [0, 0.0])[0]
     with open(out_md, "w") as f:
         f.write(f"# {title}\n\nCommand (from the repository root, on one MI355X):\n\n```\n{cmd}\n```\n\n")
         f.write("Per kernel family, all dispatches of the run (warm-up, timed and instrumented steps):\n\n")
-        f.write("| family | dispatches | avg us | total ms |\n|---|---:|---:|---:|\n")
+        f.write("| family | dispatches | per step | avg us | total ms |\n|---|---:|---:|---:|---:|\n")
+        lib = 0
         for n, (c, t) in sorted(fam.items(), key=lambda kv: -kv[1][1]):
-            f.write(f"| `{n}` | {c} | {t / c:.2f} | {t / 1e3:.1f} |\n")
+            per = f"{c / steps:.1f}" if steps else "-"
+            f.write(f"| `{n}` | {c} | {per} | {t / c:.2f} | {t / 1e3:.1f} |\n")
+            if not n.startswith(("at::", "__amd")):
+                lib += c
+        if steps:
+            f.write(f"\n{steps} steps in the run (one head launch each): {lib / steps:.0f} library kernel "
+                    "launches per step (torch fills and copies excluded).\n")
         f.write("\nPer instantiation (rocprofv3 --stats):\n\n")
         f.write("| kernel | calls | avg us | min us | max us | total % |\n|---|---:|---:|---:|---:|---:|\n")
         for r in rows[:24]:
@@ -402,7 +411,8 @@ def main():
         summarize_sq(*args.summarize_sq, args.cmd)
         return
     if args.summarize_mfma:
-        summarize_mfma(*args.summarize_mfma, args.algo_flops, args.cmd)
+        summarize_mfma(*args.summarize_mfma, args.algo_flops, args.cmd,
+                       args.title or "parareal ResNet-1001, N=16, batch 128, bf16 (one stream)")
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this library runs the whole parareal network on ONE GPU (all N "
