@@ -142,8 +142,8 @@ __device__ __forceinline__ void load_b(const ConvProb& P, int col, int k0, Frag<
 // GK_HALO main loop.  The tile's BM output rows are whole image rows (BM a multiple of Q): either
 // R = BM / Q rows of one image or BM / PQ whole images.  LDS holds those rows plus a one-pixel halo
 // of the (activated, for the forward prologue) input; padding pixels are zeros.  A pixel's Cg
-// channels are followed by 0, 1 or 2 unused 16-byte chunks (conv_halo_pad) so that each half-wave's
-// A reads (16 pixels x an aligned chunk pair) fall on distinct LDS banks.  Wave w
+// channels are followed by 0 or 2 unused 16-byte chunks (conv_halo_pad), a pixel stride that keeps
+// each half-wave's A reads (16 pixels x an aligned chunk pair) on few shared LDS banks.  Wave w
 // owns column sub-tile w % WN and WM * WN row sub-tiles; its filter fragments for all K steps (at most
 // conv_halo_nkb(WN)) are loaded into registers before the LDS fill completes.  Steps past K read a
 // valid A position; the filter fragment there is zero.
