@@ -101,8 +101,6 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
   // zeroed when stored), so that no branch separates a load from the MFMAs it overlaps.
   const T* const in = (const T*)P.in;
   const int W = P.W, Cg = P.Cg, Kt = P.K;
-  const int spt = Cg / GKS;                        // steps per tap
-  const int spt_l2 = (spt & (spt - 1)) == 0 ? __builtin_ctz(spt) : -1;
   const int nsteps = Kt / GKS;
   struct Set {
     uint4 a[GLP], b[GLP];
@@ -111,9 +109,11 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
   };
   auto gload = [&](int s, Set& R) {
     s = s < nsteps ? s : nsteps - 1;               // past the end: a repeat of the last step
-    const int tap = spt_l2 >= 0 ? s >> spt_l2 : s / spt;
-    const int k0 = s * GKS;
-    const int cs = (s - tap * spt) * GKS;
+    // channel chunk outer, tap inner: consecutive steps read the same channels of rows shifted by
+    // one pixel or one image row, which the vector L1 of the CU serves again
+    const int cb = s / 9, tap = s - 9 * cb;
+    const int cs = cb * GKS;
+    const int k0 = tap * Cg + cs;
     R.c = cs + 8 * ch;
     const int dr = MODE == MODE_FWD ? tap / 3 - 1 : 1 - tap / 3;
     const int dq = MODE == MODE_FWD ? tap % 3 - 1 : 1 - tap % 3;
