@@ -17,6 +17,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import statistics
 import os
 import sys
 import time
@@ -347,7 +348,7 @@ def time_config(idx, streams, steps, warmup):
         g.forward(fine_events=(e[0], e[1]))
         g.backward(fine_events=(e[2], e[3]))
     torch.cuda.synchronize()
-    fine_ms = sum(e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev) / steps
+    fine_ms = statistics.median(e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev)
     tf = fine_flops(net) / (fine_ms * 1e-3) / 1e12
     del g
     torch.cuda.empty_cache()
@@ -362,7 +363,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=3, help="workload index 0..4")
     ap.add_argument("--partition", default="contiguous",
                     choices=("contiguous", "per_stage", "balanced", "balanced_flops"),
@@ -476,8 +477,9 @@ def main():
             step(k)
         torch.cuda.synchronize()
         g.overlap_bwd = True
-    fine_ms = sum(e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev) / args.steps
-    coarse_ms = (sum(e[4].elapsed_time(e[5]) + e[6].elapsed_time(e[7]) for e in ev) / args.steps
+    # per-step GPU times of the fine calls and of the coarse chain: the median over the timed steps
+    fine_ms = statistics.median(e[0].elapsed_time(e[1]) + e[2].elapsed_time(e[3]) for e in ev)
+    coarse_ms = (statistics.median(e[4].elapsed_time(e[5]) + e[6].elapsed_time(e[7]) for e in ev)
                  if net.n_sub > 1 else 0.0)
     ff = fine_flops(net)
     tflops = ff / (fine_ms * 1e-3) / 1e12
