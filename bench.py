@@ -152,32 +152,43 @@ def summarize_families(fetch_csv, write_csv, trace_csv, out_md, cmd):
     build and workload, and the HBM bandwidth they give."""
     import csv
 
-    def load(p):
+    def inst(name):
+        return name.split("(")[0].replace("void ", "").replace("pnn::", "")
+
+    def load(p, key):
         per, copy = {}, None
         for r in csv.DictReader(open(p)):
             v = float(r["Counter_Value"]) * 1024.0
-            n = _short(r["Kernel_Name"])
-            if n == "__amd_rocclr_copyBuffer":
+            if _short(r["Kernel_Name"]) == "__amd_rocclr_copyBuffer":
                 copy = max(copy or 0.0, v)
-            per.setdefault(n, []).append(v)
+            per.setdefault(key(r["Kernel_Name"]), []).append(v)
         return per, copy
 
-    fe, fcopy = load(fetch_csv)
-    wr, wcopy = load(write_csv)
-    ffac, wfac = COPY_BYTES / fcopy, COPY_BYTES / wcopy
-    dur = {}
-    for r in csv.DictReader(open(trace_csv)):
-        dur.setdefault(_short(r["Kernel_Name"]), []).append(
-            (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
-    rows = []
-    for n in fe:
-        if n not in wr or n not in dur or n.startswith("__amd") or n.startswith("at::"):
-            continue
-        fb = sum(fe[n]) / len(fe[n]) * ffac
-        wb = sum(wr[n]) / len(wr[n]) * wfac
-        us = sum(dur[n]) / len(dur[n])
-        rows.append((n, len(dur[n]), fb / 1e6, wb / 1e6, us, (fb + wb) / (us * 1e3)))
-    rows.sort(key=lambda r: -r[1] * r[4])
+    def durations(key):
+        dur = {}
+        for r in csv.DictReader(open(trace_csv)):
+            dur.setdefault(key(r["Kernel_Name"]), []).append(
+                (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+        return dur
+
+    def table(key):
+        fe, fcopy = load(fetch_csv, key)
+        wr, wcopy = load(write_csv, key)
+        ffac, wfac = COPY_BYTES / fcopy, COPY_BYTES / wcopy
+        dur = durations(key)
+        rows = []
+        for n in fe:
+            if n not in wr or n not in dur or "__amd" in n or n.startswith("at::"):
+                continue
+            fb = sum(fe[n]) / len(fe[n]) * ffac
+            wb = sum(wr[n]) / len(wr[n]) * wfac
+            us = sum(dur[n]) / len(dur[n])
+            rows.append((n, len(dur[n]), fb / 1e6, wb / 1e6, us, (fb + wb) / (us * 1e3)))
+        rows.sort(key=lambda r: -r[1] * r[4])
+        return rows, ffac, wfac
+
+    rows, ffac, wfac = table(_short)
+    irows = [r for r in table(inst)[0] if r[0].startswith("conv_kernel<")]
     with open(out_md, "w") as f:
         f.write("# HBM traffic per kernel family: parareal ResNet-1001, N=16, batch 128, bf16 (one "
                 "stream)\n\nCommands (from the repository root, on one MI355X):\n\n```\n"
@@ -189,6 +200,13 @@ def summarize_families(fetch_csv, write_csv, trace_csv, out_md, cmd):
         f.write("| family | launches (trace) | fetched MB | written MB | avg us | HBM GB/s |\n"
                 "|---|---:|---:|---:|---:|---:|\n")
         for n, c, fm, wm, us, gbs in rows:
+            f.write(f"| `{n}` | {c} | {fm:.1f} | {wm:.1f} | {us:.2f} | {gbs:.0f} |\n")
+        f.write("\nPer `conv_kernel` instantiation (template arguments: storage type, mode 0 forward / 1 "
+                "data gradient, gather kind 0 pointwise / 1 vector / 2 element-wise / 3 3x3 halo tile, "
+                "row and column sub-tiles per wave):\n\n")
+        f.write("| instantiation | launches (trace) | fetched MB | written MB | avg us | HBM GB/s |\n"
+                "|---|---:|---:|---:|---:|---:|\n")
+        for n, c, fm, wm, us, gbs in irows:
             f.write(f"| `{n}` | {c} | {fm:.1f} | {wm:.1f} | {us:.2f} | {gbs:.0f} |\n")
 
 
