@@ -12,6 +12,8 @@
 // 16 bytes (conflict-free 16-byte fragment reads).  The fp32 tile is then staged in LDS and the
 // convolution epilogue shared with the other conv kernels does residual, BN-mask / BN-apply forms,
 // stores and per-tile BN partials (128-row tiles, the same partial rows as the other kernels).
+// Problems with few tiles split K over several workgroups per tile (fp32 partial tiles, summed in
+// split order by a second pass that then runs the epilogue).
 #include "device_common.h"
 #include "pnn_internal.h"
 #include "conv_epilogue.h"
@@ -47,8 +49,12 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
   const int gi = find_group(L);
   const ConvProb& P = L.p[gi];
   const int local = blockIdx.x - P.tile_begin;
-  const int tm = local / P.tiles_n;
-  const int tn = local - tm * P.tiles_n;
+  const int ntile = P.tiles_m * P.tiles_n;
+  const int ks = P.ksplit > 1 ? P.ksplit : 1;      // workgroups per tile along K
+  const int split = local / ntile;
+  const int tl = local - split * ntile;
+  const int tm = tl / P.tiles_n;
+  const int tn = tl - tm * P.tiles_n;
   const int n0 = tn * GN;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int r32 = lane & 31, kh = lane >> 5;
@@ -101,14 +107,17 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
   // zeroed when stored), so that no branch separates a load from the MFMAs it overlaps.
   const T* const in = (const T*)P.in;
   const int W = P.W, Cg = P.Cg, Kt = P.K;
-  const int nsteps = Kt / GKS;
+  // this workgroup's K steps: [s_begin, s_begin + nsteps) of the problem's Kt / GKS
+  const int ktot = Kt / GKS;
+  const int s_begin = split * ktot / ks;
+  const int nsteps = (split + 1) * ktot / ks - s_begin;
   struct Set {
     uint4 a[GLP], b[GLP];
     unsigned ok;                                   // bit h: row h of A is inside the image
     int c;                                         // channel of the thread's chunk
   };
   auto gload = [&](int s, Set& R) {
-    s = s < nsteps ? s : nsteps - 1;               // past the end: a repeat of the last step
+    s = s_begin + (s < nsteps ? s : nsteps - 1);   // past the end: a repeat of the last step
     // channel chunk outer, tap inner: consecutive steps read the same channels of rows shifted by
     // one pixel or one image row, which the vector L1 of the CU serves again
     const int cb = s / 9, tap = s - 9 * cb;
@@ -212,6 +221,25 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
   if (s < nsteps) compute(0);                      // an odd step count: the last step
   __syncthreads();
 
+  if (ks > 1) {
+    // a split of K: the raw fp32 tile to the partial buffer in the accumulators' own order, one
+    // 32 x 32 block after the other (blocks by wave row, wave column, i, j); within a block the
+    // float4 of lane l and row group g (rows 8 g + 4 (l / 32) .. + 3 of column l % 32) at g * 64 + l,
+    // so each store writes 1 KB contiguously.  The epilogue runs once every split is done.
+    float4* dst = (float4*)(P.kpart + ((long)split * ntile + tl) * (GM * GN));
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int blk = ((wr * 2 + wc) * 2 + i) * 2 + j;
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          dst[blk * 256 + g * 64 + lane] =
+              make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+      }
+    return;
+  }
+
   // stage the fp32 tile: D lane layout of the 32 x 32 MFMA (column r32, rows 8 (e / 4) + 4 kh + e % 4)
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -237,6 +265,107 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
   }
   __syncthreads();
   conv_epilogue<T, MODE, GM, GN, GLDA, GN>(P, smem, (float*)pro_s, bn_s, tm, n0, pre, pre2);
+}
+
+// Second pass of the split problems: one workgroup per slab of GEMM_RBN = 16 columns of a 128 x 128
+// tile (half of one 32-column block column of the first pass's order).  Thread t sums, in split
+// order, the float4s f = t and t + 256 of the slab (f: lane within the half, its row-group half, row
+// group, i, wave row), eight splits' loads in flight per round (repeats of the last split past
+// the end); the sums go to the staged row-major slab, then the slab's epilogue.
+template <int MODE>
+__global__ __launch_bounds__(256) void gemm_reduce_kernel(const ConvLaunch L) {
+  using T = uint16_t;
+  constexpr int VE = 8, RB = GEMM_RBN, LDA = RB + 4, CPT = GN / RB;
+  constexpr int ACCW = 2 * 256 * VE + 512;       // the epilogue's stats scratch exceeds the staged slab
+  static_assert(GM * 2 == 256 && RB == 16 && CPT == 8, "slab layout");
+  __shared__ __attribute__((aligned(16))) float smem[ACCW > GM * LDA ? ACCW : GM * LDA];
+  __shared__ __attribute__((aligned(16))) float piv_s[RB];
+  __shared__ __attribute__((aligned(16))) float bn_s[MODE == MODE_BWD ? 7 * RB : 1];
+
+  const int gi = find_group(L);
+  const ConvProb& P = L.p[gi];
+  const int local = blockIdx.x - P.tile_begin;
+  const int tl = local / CPT;
+  const int cs = local - tl * CPT;
+  const int ntile = P.tiles_m * P.tiles_n;
+  const int tm = tl / P.tiles_n;
+  const int cn = (tl - tm * P.tiles_n) * GN + cs * RB;   // the slab's first column
+  const int tid = threadIdx.x;
+  const bool bnmask = MODE == MODE_BWD && (P.flags & (EPI_BN_MASK | EPI_BN_APPLY));
+  // every global load is issued before the first LDS write: the BN constants of the slab's
+  // columns, the epilogue operands, then the partials
+  const bool bnload = bnmask && tid < RB;
+  float bnv[7];
+  if (bnload) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) bnv[k] = P.bnst[k * P.ncol + cn + tid];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) bnv[4 + k] = (P.flags & EPI_BN_APPLY) ? P.coef[k * P.ncol + cn + tid] : 0.f;
+  }
+  const void* pf = (MODE == MODE_FWD) ? P.res
+                   : ((P.flags & EPI_STORE_F32) ? nullptr : (bnmask ? P.zsrc : P.res));
+  const void* pf2 = (MODE == MODE_FWD) ? P.ext : ((P.flags & EPI_BN_APPLY) ? P.res : nullptr);
+  uint4 pre[1], pre2[1];
+  {
+    const int m = tm * GM + (tid >> 1);            // the epilogue's chunk: row tid / 2, 8 columns
+    const long o = (long)m * P.ncol + cn + (tid & 1) * VE;
+    pre[0] = (pf != nullptr && m < P.M) ? *(const uint4*)((const T*)pf + o) : make_uint4(0, 0, 0, 0);
+    pre2[0] = (pf2 != nullptr && m < P.M) ? *(const uint4*)((const T*)pf2 + o) : make_uint4(0, 0, 0, 0);
+  }
+  // the slab in the first pass's order: wave column wc, block column j, half h of the 32 columns
+  const int wc = cs >> 2, j = (cs >> 1) & 1, h = cs & 1;
+  int off[2], row[2];
+  const int l16 = tid & 15;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int f = tid + 256 * u;
+    const int kh = (f >> 4) & 1, g = (f >> 5) & 3, i = (f >> 7) & 1, wr = f >> 8;
+    off[u] = (((wr * 2 + wc) * 2 + i) * 2 + j) * 256 + g * 64 + kh * 32 + h * 16 + l16;
+    row[u] = wr * 64 + 32 * i + 8 * g + 4 * kh;
+  }
+  const float4* src = (const float4*)(P.kpart + (long)tl * (GM * GN));
+  const long ss = (long)ntile * (GM * GN / 4);
+  const int S = P.ksplit;
+  float4 a[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
+  for (int k0 = 0; k0 < S; k0 += 8) {
+    float4 v[8][2];
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      const long k = min(k0 + w, S - 1);
+      v[w][0] = src[k * ss + off[0]];
+      v[w][1] = src[k * ss + off[1]];
+    }
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      if (k0 + w < S) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          a[u].x += v[w][u].x; a[u].y += v[w][u].y; a[u].z += v[w][u].z; a[u].w += v[w][u].w;
+        }
+      }
+    }
+  }
+  if (bnload) {
+#pragma unroll
+    for (int k = 0; k < 7; ++k) bn_s[k * RB + tid] = bnv[k];
+  }
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    smem[(row[u] + 0) * LDA + l16] = a[u].x;
+    smem[(row[u] + 1) * LDA + l16] = a[u].y;
+    smem[(row[u] + 2) * LDA + l16] = a[u].z;
+    smem[(row[u] + 3) * LDA + l16] = a[u].w;
+  }
+  __syncthreads();
+  conv_epilogue<T, MODE, GM, RB, LDA, RB>(P, smem, piv_s, bn_s, tm, cn, pre, pre2);
+}
+
+int launch_gemm_reduce(const ConvLaunch& L, int tiles, int mode, hipStream_t s) {   // tiles: slabs
+  if (mode == MODE_FWD)
+    hipLaunchKernelGGL(gemm_reduce_kernel<MODE_FWD>, dim3(tiles), dim3(256), 0, s, L);
+  else
+    hipLaunchKernelGGL(gemm_reduce_kernel<MODE_BWD>, dim3(tiles), dim3(256), 0, s, L);
+  return (int)hipGetLastError();
 }
 
 int launch_gemm(const ConvLaunch& L, int tiles, int mode, hipStream_t s) {

@@ -115,6 +115,9 @@ struct pnn_plan {
   std::vector<hipEvent_t> fj;          // fork / join events (no timing), used round robin
   size_t fj_next = 0;
   size_t wpart_stride = 0;             // one split-K partial region per chain
+  // GEMM-kernel K-split partial tiles: one region per chain like the weight-gradient partials
+  // (stride 0: no problem of the plan is split)
+  size_t kpart_off = 0, kpart_stride = 0;
   // timing of one kernel family
   int timing_family = 0;
   std::vector<hipEvent_t> ev;
@@ -601,6 +604,7 @@ struct Ctx {
   char* scratch;
   hipStream_t stream;
   char* wpart = nullptr;   // split-K weight-gradient partials (nullptr: the plan's first region)
+  char* kpart = nullptr;   // K-split GEMM partial tiles (nullptr: the plan's first region)
 };
 
 inline char* cp(const void* p) { return (char*)const_cast<void*>(p); }
@@ -719,7 +723,7 @@ double conv_bytes(const ConvProb& p, int es, int mode) {
 int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk, int wn, int wm) {
   pnn_plan* plan = c.plan;
   return grouped<ConvLaunch>(
-      probs, [](const ConvProb& p) { return p.tiles_m * p.tiles_n; },
+      probs, [](const ConvProb& p) { return p.tiles_m * p.tiles_n * std::max(p.ksplit, 1); },
       [&](const ConvLaunch& L, int tiles, size_t) {
         double fl = 0, by = 0;
         for (int i = 0; i < L.n; ++i) {
@@ -756,6 +760,15 @@ bool gemm_ok(const ConvProb& p, int es) {
          p.Cg % GEMM_BK == 0 && p.Cg <= CONV_PRO_MAXC && p.ncol % GEMM_BN == 0 && 64 * p.wm == GEMM_BM;
 }
 
+// K splits of the GEMM problems with fewer than GEMM_SPLIT_BELOW tiles (`small`: their tiles in
+// one call): about GEMM_SPLIT_WG workgroups over all of them, GEMM_MIN_SPLIT_STEPS K steps each at
+// least (1: no split)
+int gemm_split(const ConvProb& q, long small) {
+  if (small <= 0 || q.tiles_m * q.tiles_n >= GEMM_SPLIT_BELOW) return 1;
+  const long s = std::min<long>({GEMM_MAX_SPLIT, GEMM_SPLIT_WG / small, (q.K / GEMM_BK) / GEMM_MIN_SPLIT_STEPS});
+  return s >= 2 ? (int)s : 1;
+}
+
 // Gather kind of a convolution problem: 0 pointwise, 1 vector gather, 2 element-wise gather,
 // 3 halo tile, 4 the GEMM kernel.
 int gather_kind(const ConvProb& p, int es) {
@@ -776,10 +789,33 @@ int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode) {
     if (gk == 4) q.tiles_n = q.ncol / GEMM_BN;
     by[gk][w][p.wm == conv_wm(p.wn, false) ? 0 : 1].push_back(q);
   }
-  // GEMM launches: the longest K first, so that the longest tiles start first
+  // GEMM launches: the longest K first, so that the longest tiles start first; the problems with
+  // few tiles split K (their partial tiles in the context's region, summed by a second pass)
+  long small = 0;
+  for (auto& v : by[4])
+    for (auto& t : v) {
+      std::stable_sort(t.begin(), t.end(), [](const ConvProb& a, const ConvProb& b) { return a.K > b.K; });
+      for (auto& q : t)
+        if (q.tiles_m * q.tiles_n < GEMM_SPLIT_BELOW) small += q.tiles_m * q.tiles_n;
+    }
+  pnn_plan* plan = c.plan;
+  char* region = c.kpart != nullptr ? c.kpart
+                 : plan->kpart_stride != 0 ? c.scratch + plan->kpart_off : nullptr;
+  std::vector<ConvProb> split;
+  size_t koff = 0;
   for (auto& v : by[4])
     for (auto& t : v)
-      std::stable_sort(t.begin(), t.end(), [](const ConvProb& a, const ConvProb& b) { return a.K > b.K; });
+      for (auto& q : t) {
+        q.ksplit = region != nullptr ? gemm_split(q, small) : 1;
+        const size_t need = (size_t)q.ksplit * q.tiles_m * q.tiles_n * GEMM_BM * GEMM_BN * 4;
+        if (q.ksplit < 2 || koff + need > plan->kpart_stride) {   // (the region holds them all)
+          q.ksplit = 1;
+          continue;
+        }
+        q.kpart = (float*)(region + koff);
+        koff += need;
+        split.push_back(q);
+      }
   for (int gk = 0; gk < 5; ++gk)
     for (int w = 0; w < 3; ++w)
       for (int t = 0; t < 2; ++t) {
@@ -787,7 +823,17 @@ int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode) {
         int e = fire_conv_gk(c, by[gk][w][t], mode, gk, 1 << w, conv_wm(1 << w, t == 1));
         if (e) return e;
       }
-  return PNN_OK;
+  return grouped<ConvLaunch>(
+      split, [](const ConvProb& p) { return p.tiles_m * p.tiles_n * (GEMM_BN / GEMM_RBN); },
+      [&](const ConvLaunch& L, int tiles, size_t) {
+        double by2 = 0;
+        for (int i = 0; i < L.n; ++i)
+          by2 += (double)L.p[i].ksplit * L.p[i].tiles_m * L.p[i].tiles_n * GEMM_BM * GEMM_BN * 4;
+        Timer tm(plan, 1, c.stream);
+        int e = launch_gemm_reduce(L, tiles, mode, c.stream);
+        tm.done(c.stream, 0.0, by2);
+        return e;
+      });
 }
 
 // streaming pointwise problems: one grouped launch
@@ -839,6 +885,28 @@ void set_tiles(ConvProb& p, bool short_tiles) {
   p.wm = conv_rows_wm(p.k, p.M, p.ncol, short_tiles);
   p.tiles_m = (int)cdiv(p.M, 64 * p.wm);
   p.tiles_n = p.ncol / (16 * p.wn);
+}
+
+// Whether some convolution of the plan, forward or data gradient, is a GEMM-kernel problem with
+// fewer than GEMM_SPLIT_BELOW tiles (the problems fire_conv splits along K).
+bool plan_splits_k(const pnn_plan* plan) {
+  for (auto* v : {&plan->pre, &plan->fine, &plan->coarse})
+    for (const SegP& S : *v)
+      for (const NodeP& n : S.nodes) {
+        if (n.op != PNN_OP_CONV) continue;
+        for (int dir = 0; dir < 2; ++dir) {
+          ConvProb p = conv_common(plan, n);
+          p.B = plan->B;
+          p.H = dir ? n.Ho : n.H; p.W = dir ? n.Wo : n.W; p.Cg = dir ? n.cout : n.cin;
+          p.P = dir ? n.H : n.Ho; p.Q = dir ? n.W : n.Wo; p.ncol = dir ? n.cin : n.cout;
+          p.M = plan->B * p.P * p.Q;
+          p.K = n.k * n.k * p.Cg;
+          set_tiles(p, S.short_tiles);
+          if (gather_kind(p, plan->es) == 4 && cdiv(p.M, GEMM_BM) * (p.ncol / GEMM_BN) < GEMM_SPLIT_BELOW)
+            return true;
+        }
+      }
+  return false;
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -1390,6 +1458,7 @@ int chains_group(const Ctx& c, const std::vector<const SegP*>& segs, const std::
   for (int g = 0; g < G; ++g) {
     Ctx d = c;
     d.wpart = c.scratch + p->wpart_off + (size_t)(g + 1) * p->wpart_stride;
+    if (p->kpart_stride != 0) d.kpart = c.scratch + p->kpart_off + (size_t)(g + 1) * p->kpart_stride;
     ch.ctx.push_back(d);
   }
   if (G <= 1) return PNN_OK;
@@ -1644,6 +1713,9 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
   p->wpart_bytes = wp;
   p->wpart_stride = align256(wp);
   sc = align256(sc + p->wpart_stride * (PNN_MAX_CHAINS + 1));
+  p->kpart_off = sc;
+  p->kpart_stride = plan_splits_k(p) ? GEMM_KPART_BYTES : 0;
+  sc = align256(sc + p->kpart_stride * (PNN_MAX_CHAINS + 1));
   const SlotP& yo = p->fine[N - 1].slots[p->fine[N - 1].out];
   p->head_off = sc;
   p->head_bytes = (size_t)p->B * (yo.C + p->classes + 1) * 4;

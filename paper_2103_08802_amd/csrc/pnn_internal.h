@@ -50,6 +50,7 @@ struct ConvProb {
   const float* acc_in;  // EPI_ACC_IN: [M][ncol] float
   const float* coef;    // EPI_BN_APPLY: A, B, K [3][ncol]
   float* out32;         // EPI_STORE_F32: [M][ncol] float
+  float* kpart;         // GEMM kernel, ksplit > 1: fp32 partial tiles [ksplit][tiles][GEMM_BM][GEMM_BN]
   int B, H, W, Cg;      // gathered tensor
   int P, Q;             // output pixel grid (M = B * P * Q)
   int ncol;
@@ -57,6 +58,7 @@ struct ConvProb {
   int M, K;
   int tiles_m, tiles_n, wn, wm;   // tiles; column and row sub-tiles per wave
   int flags;
+  int ksplit;           // GEMM kernel: K split over this many workgroups per tile (<= 1: none)
   int cg_log2;          // log2(Cg) when Cg is a power of two, else -1
   int q_log2, pq_log2;  // log2(Q), log2(P*Q) when powers of two, else -1
   int tile_begin;
@@ -287,6 +289,16 @@ int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int
 constexpr int GEMM_BM = 128, GEMM_BN = 128, GEMM_BK = 64;
 constexpr int CONV_PRO_MAXC = 512;     // largest Cg of a forward BN prologue held in LDS
 int launch_gemm(const ConvLaunch& L, int tiles, int mode, hipStream_t s);
+// the split problems' second pass: partial tiles summed in split order, then the epilogue, one
+// workgroup per GEMM_RBN-column slab of a tile
+int launch_gemm_reduce(const ConvLaunch& L, int tiles, int mode, hipStream_t s);
+constexpr int GEMM_RBN = 16;
+constexpr int GEMM_SPLIT_BELOW = 128;          // tiles of a problem below which its K is split
+constexpr int GEMM_SPLIT_WG = 256;             // workgroups a split problem aims at (one per CU)
+constexpr int GEMM_MAX_SPLIT = 16;
+constexpr int GEMM_MIN_SPLIT_STEPS = 4;        // K steps of GEMM_BK per split, at least
+// partial region of one chain: at most GEMM_SPLIT_WG partial tiles are live at once
+constexpr size_t GEMM_KPART_BYTES = (size_t)GEMM_SPLIT_WG * GEMM_BM * GEMM_BN * 4;
 // activation gather of wgrad_kernel: element-wise (any channel count), 16-byte chunks through the
 // filter taps (Cg a multiple of the chunk), or pointwise (1x1 / stride 1 / pad 0: input row m)
 enum { WG_GEN = 0, WG_VEC = 1, WG_PW = 2 };
