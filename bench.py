@@ -67,7 +67,7 @@ def cpu_baseline(idx, batch=24, coarse="config"):
 # sources a kernel family's code and launch shapes come from; a stored traffic figure is void
 # once any of them changes
 KERNEL_SOURCES = {
-    "conv_kernel": ["k_conv.hip", "conv_epilogue.h", "device_common.h", "pnn_internal.h", "plan.hip"],
+    "conv_kernel": ["k_conv.hip", "conv_epilogue.h", "bn_fuse.h", "device_common.h", "pnn_internal.h", "plan.hip"],
     "wgrad_kernel": ["k_conv.hip", "device_common.h", "pnn_internal.h", "plan.hip"],
 }
 COPY_BYTES = 256 << 20          # the --copy-calibration copy

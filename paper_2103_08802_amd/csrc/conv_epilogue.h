@@ -1,6 +1,7 @@
 // Epilogue of the grouped convolution kernels (forward and data gradient), shared by the
 // implicit-GEMM kernels of k_conv.hip and k_gemm.hip.
 #pragma once
+#include "bn_fuse.h"
 #include "device_common.h"
 #include "pnn_internal.h"
 
@@ -8,7 +9,8 @@ namespace pnn {
 
 // The epilogue shared by the convolution kernels, once the workgroup's fp32 tile (BM rows x BNc
 // columns from n0, row stride LDA) is staged in acc_s: residual / addend, BN-mask and BN-apply
-// forms, 16-byte stores, and the per-tile BN partials of the stored result.  Each thread owns
+// forms, 16-byte stores, and the per-tile BN partials of the stored result (EPI_BN_FUSE: and the
+// statistics finalised from them by the last workgroup, bn_fwd_fuse).  Each thread owns
 // 16-byte column chunks of rows tid / ncc + k * rpp; pre / pre2 hold the streamed epilogue operands
 // of those chunks (loaded by the caller); piv_s is BNc floats of LDS for the forward pivot; bn is
 // [7][BNS] floats of LDS (mean, invstd, scale, shift; A, B, K) for the data-gradient BN forms.
@@ -185,11 +187,14 @@ __device__ __forceinline__ void conv_epilogue(const ConvProb& P, float* acc_s, f
         // tid as the threads that summed it formed it)
         const float n = (float)min(BM, P.M - tm * BM);
         const float am = a / n;
-        *pp = make_float2(piv_s[tid] + am, fmaxf(b - a * am, 0.f));
+        bnf_store(pp, make_float2(piv_s[tid] + am, fmaxf(b - a * am, 0.f)));   // (read across XCDs)
       } else {
         *pp = make_float2(a, b);
       }
     }
+    if (MODE == MODE_FWD && (P.flags & EPI_BN_FUSE))
+      bn_fwd_fuse((float2*)P.part, P.tiles_m, BM, (long)P.M, P.ncol, P.bn_gamma, P.bn_stats, P.bn_cnt, tm, n0 / BNc,
+                  n0, BNc, (double*)acc_s);
   }
 }
 

@@ -1410,11 +1410,14 @@ __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
     if (MODE == MODE_FWD) {
       // the workgroup's mean and sum of squared deviations from its pivoted sums
       const float am = a / (float)(m_end - m_begin);
-      ((float2*)P.part)[(long)tm * ncol + c0 + tid] = make_float2(piv[tid] + am, fmaxf(b - a * am, 0.f));
+      bnf_store((float2*)P.part + (long)tm * ncol + c0 + tid, make_float2(piv[tid] + am, fmaxf(b - a * am, 0.f)));
     } else {
       ((float2*)P.part)[(long)tm * ncol + c0 + tid] = make_float2(a, b);
     }
   }
+  if (MODE == MODE_FWD && (P.flags & EPI_BN_FUSE))
+    bn_fwd_fuse((float2*)P.part, P.tiles_m, P.wm * TR, (long)P.M, ncol, P.bn_gamma, P.bn_stats, P.bn_cnt, tm, tn, c0,
+                ncl, (double*)xs);
 }
 
 // ------------------------------------------------------------------------------------------------

@@ -4,6 +4,7 @@
 // normalisation and ReLU) is split around the convolutions: its statistics are reduced from
 // per-tile partial sums written by the producing kernel, and its affine map + ReLU is applied in
 // the consuming kernel's operand load.  All reductions run in a fixed order (deterministic).
+#include "bn_fuse.h"
 #include "device_common.h"
 #include "pnn_internal.h"
 
@@ -242,8 +243,11 @@ __global__ __launch_bounds__(256) void colstat_kernel(const ColStatLaunch L) {
     }
     // the workgroup's mean and sum of squared deviations
     const float am = a / (float)(r1 - r0);
-    ((float2*)P.part)[(long)tile * P.C + c] = make_float2(St<T>::ld(P.x, r0 * P.C + c) + am, fmaxf(b - a * am, 0.f));
+    bnf_store((float2*)P.part + (long)tile * P.C + c, make_float2(St<T>::ld(P.x, r0 * P.C + c) + am, fmaxf(b - a * am, 0.f)));
   }
+  if (P.fuse)
+    bn_fwd_fuse((float2*)P.part, (int)((P.M + COLSTAT_ROWS - 1) / COLSTAT_ROWS), COLSTAT_ROWS, P.M, P.C, P.gamma,
+                P.stats, P.cnt, tile, 0, 0, P.C, (double*)red);
 }
 
 // out = A dbn + B z + K [+ skip] per channel (the BN backward, coefficients from the column
@@ -754,6 +758,15 @@ __global__ void flags_clear_kernel(unsigned* flags) {
   if (threadIdx.x < PNN_NFLAGS) flags[threadIdx.x] = 0u;
 }
 
+// word ranges set to zero (arrival counters), ZERO_WORDS words per workgroup
+__global__ __launch_bounds__(256) void zero_kernel(const ZeroLaunch L) {
+  const int gi = find_group(L);
+  const ZeroProb& P = L.p[gi];
+  const int w0 = (blockIdx.x - P.tile_begin) * ZERO_WORDS;
+  const int w1 = min(P.words, w0 + ZERO_WORDS);
+  for (int w = w0 + (int)threadIdx.x; w < w1; w += 256) P.p[w] = 0u;
+}
+
 // ------------------------------------------------------------------------------------------------
 // launchers
 // ------------------------------------------------------------------------------------------------
@@ -793,6 +806,10 @@ int launch_transpose(const TransposeLaunch& L, int tiles, int dtype, hipStream_t
 }
 int launch_sub(const AxpyLaunch& L, int tiles, int dtype, hipStream_t s) {
   PNN_LAUNCH_T(sub_kernel, L, tiles, dtype, s);
+}
+int launch_zero(const ZeroLaunch& L, int tiles, hipStream_t s) {
+  hipLaunchKernelGGL(zero_kernel, dim3(tiles), dim3(256), 0, s, L);
+  return (int)hipGetLastError();
 }
 int launch_flags_clear(unsigned* flags, hipStream_t s) {
   hipLaunchKernelGGL(flags_clear_kernel, dim3(1), dim3(64), 0, s, flags);

@@ -63,6 +63,7 @@ struct BnP {
                              // convolution (coarse_fwd_all), in its row tiles; 0 = not chained
   int fwd_rows = 0;          // rows of the normalised tensor per forward partial row
   int fwd_rows_in = 0;       // the same for the chained sums
+  size_t cnt_word = 0;       // its arrival counters (bn_fwd_fuse): word offset in the segment's block
 };
 
 struct SegP {
@@ -78,6 +79,8 @@ struct SegP {
   size_t param_bytes = 0, grad_bytes = 0;
   size_t saved_base = 0, saved_bytes = 0;
   size_t scr_base = 0, scr_bytes = 0;
+  size_t cnt_off = 0;          // the BN arrival counters of the segment (scratch, relative), words
+  long cnt_words = 0;
   // run of bottleneck units the resident kernel can take (find_unit_run): its first node, unit
   // count, the levels it covers, its input slot and the first unit's offsets / per-unit strides
   int ru_node = -1, ru_n = 0, ru_lo = 0, ru_hi = 0, ru_xslot = 0;
@@ -433,6 +436,8 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
     if (part == 2 && b.slot == 0) tiles = std::max(tiles, (int)cdiv(M, 64));
     b.part_off = sc;
     sc = align256(sc + (size_t)tiles * 2 * b.C * 4);
+    b.cnt_word = (size_t)S.cnt_words;
+    S.cnt_words += bnf_words(b.C, tiles);
     b.coef_off = sc;
     sc = align256(sc + (size_t)b.C * 12);
     if (!sl.bn_consumers.empty() && !b.defer_apply) {
@@ -457,6 +462,8 @@ pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, 
     n.wt_off = sc;
     sc = align256(sc + (size_t)n.cout * n.k * n.k * n.cin * es);
   }
+  S.cnt_off = sc;
+  sc = align256(sc + (size_t)S.cnt_words * 4);
   S.scr_bytes = sc;
   return PNN_OK;
 }
@@ -595,6 +602,7 @@ struct Ptrs {
   bool in_sums = false;               // forward: the input BN's sums are already in its partial rows
   const SegP* out_sums = nullptr;     // forward: the output's convolution also forms the sums of
                                       // this segment's input BN (the next coarse block)
+  const void* out_params = nullptr;   // forward: that segment's parameters (its BN's gamma, beta)
   bool resident = false;              // forward: the segment's unit run goes to the resident kernel
 };
 
@@ -619,6 +627,16 @@ float* stats_ptr(const Ctx& c, const SegP& S, int b) {
 }
 float* part_ptr(const Ctx& c, const SegP& S, int b) {
   return (float*)(c.scratch + S.scr_base + S.bns[b].part_off);
+}
+unsigned* cnt_ptr(const Ctx& c, const SegP& S, int b) {
+  return (unsigned*)(c.scratch + S.scr_base + S.cnt_off) + S.bns[b].cnt_word;
+}
+// a forward producer of BN b's partial rows (EPI_STATS) also finalises its statistics
+void set_bn_fuse(ConvProb& p, const Ctx& c, const SegP& S, int b, const void* params) {
+  p.flags |= EPI_BN_FUSE;
+  p.bn_cnt = cnt_ptr(c, S, b);
+  p.bn_gamma = (const float*)(cp(params) + S.bns[b].p_off);
+  p.bn_stats = stats_ptr(c, S, b);
 }
 void* grad_ptr(const Ctx& c, const SegP& S, const Ptrs& p, int s) {
   if (s == S.out) return const_cast<void*>(p.gout);
@@ -942,15 +960,26 @@ int run_fwd_begin(const Ctx& c, const std::vector<const SegP*>& segs, const std:
       if (s0.bn < 0) continue;
       const BnP& b = S.bns[s0.bn];
       const bool chained = ptrs[i].in_sums && b.fwd_tiles_in > 0;
-      ColStatProb p;
-      p.x = ptrs[i].in;
-      p.part = part_ptr(c, S, s0.bn);
-      p.M = (long)B * s0.H * s0.W;
-      p.C = s0.C;
-      if (!chained) cs.push_back(p);
-      fw.push_back(bn_fwd_red(p.part, chained ? b.fwd_tiles_in : b.fwd_tiles,
-                              chained ? b.fwd_rows_in : b.fwd_rows,
-                              (const float*)(cp(ptrs[i].params) + b.p_off), stats_ptr(c, S, s0.bn), b.C, p.M));
+      const long M = (long)B * s0.H * s0.W;
+      const long rows = chained ? b.fwd_tiles_in : cdiv(M, COLSTAT_ROWS);
+      // few partial rows: the column statistics (or, chained, the previous block's last
+      // convolution) finalise the statistics themselves (bn_fwd_fuse)
+      const bool fuse = rows <= BNF_MAX_ROWS;
+      if (!chained) {
+        ColStatProb p;
+        p.x = ptrs[i].in;
+        p.part = part_ptr(c, S, s0.bn);
+        p.gamma = (const float*)(cp(ptrs[i].params) + b.p_off);
+        p.stats = stats_ptr(c, S, s0.bn);
+        p.cnt = cnt_ptr(c, S, s0.bn);
+        p.M = M;
+        p.C = s0.C;
+        p.fuse = fuse ? 1 : 0;
+        cs.push_back(p);
+      }
+      if (!fuse)
+        fw.push_back(bn_fwd_red(part_ptr(c, S, s0.bn), (int)rows, chained ? b.fwd_rows_in : b.fwd_rows,
+                                (const float*)(cp(ptrs[i].params) + b.p_off), stats_ptr(c, S, s0.bn), b.C, M));
     }
     int e = grouped<ColStatLaunch>(
         cs, [](const ColStatProb& p) { return (int)cdiv(p.M, COLSTAT_ROWS); },
@@ -976,6 +1005,7 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
         if (n.level != L || (P.resident && n.resident)) continue;
         const SlotP& so = S.slots[n.dst];
         const void* ext = (n.dst == S.out) ? P.ext : nullptr;
+        bool fused = false;             // its output BN finalised by the producer
         if (n.op == PNN_OP_CONV) {
           ConvProb p = conv_common(plan, n);
           p.in = slot_ptr(c, S, P, n.src);
@@ -984,25 +1014,33 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
           p.res = n.res >= 0 ? slot_ptr(c, S, P, n.res) : nullptr;
           p.ext = ext;
           p.pro = n.bn >= 0 ? stats_ptr(c, S, n.bn) + 2 * S.bns[n.bn].C : nullptr;
+          const SegP* fs = nullptr;       // the BN whose partial rows this convolution writes
+          int fb = -1;
+          const void* fparams = nullptr;
           if (so.bn >= 0) {
             p.part = part_ptr(c, S, so.bn);
             p.flags = EPI_STATS;
+            fs = &S; fb = so.bn; fparams = P.params;
           } else if (n.dst == S.out && P.out_sums != nullptr) {
             const SegP& nx = *P.out_sums;
             p.part = part_ptr(c, nx, nx.slots[0].bn);
             p.flags = EPI_STATS;
+            fs = &nx; fb = nx.slots[0].bn; fparams = P.out_params;
           }
           p.B = B; p.H = n.H; p.W = n.W; p.Cg = n.cin;
           p.P = n.Ho; p.Q = n.Wo; p.ncol = n.cout;
           p.M = B * n.Ho * n.Wo;
           p.K = n.k * n.k * n.cin;
-          if (pw_fwd_node(S, n, es)) {
-            set_pw_tiles(p, S.short_tiles);
-            cv_pw.push_back(p);
-          } else {
-            set_tiles(p, S.short_tiles);
-            (n.cin % (16 / es) == 0 ? cv_vec : cv_gen).push_back(p);
+          const bool pwn = pw_fwd_node(S, n, es);
+          if (pwn) set_pw_tiles(p, S.short_tiles);
+          else set_tiles(p, S.short_tiles);
+          // few partial rows: the producer finalises the statistics itself (bn_fwd_fuse)
+          if (fs != nullptr && p.tiles_m <= BNF_MAX_ROWS) {
+            set_bn_fuse(p, c, *fs, fb, fparams);
+            fused = so.bn >= 0;
           }
+          if (pwn) cv_pw.push_back(p);
+          else (n.cin % (16 / es) == 0 ? cv_vec : cv_gen).push_back(p);
         } else if (n.op == PNN_OP_BNACT) {
           BnActProb p;
           std::memset(&p, 0, sizeof(p));
@@ -1023,7 +1061,7 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
           p.ve = (p.C % ve == 0 && (((uintptr_t)p.x | (uintptr_t)p.y) & 15) == 0) ? ve : 1;
           mp.push_back(p);
         }
-        if (so.bn >= 0) {
+        if (so.bn >= 0 && !fused) {
           const BnP& b = S.bns[so.bn];
           const long cnt = (long)B * so.H * so.W;
           fw.push_back(bn_fwd_red(part_ptr(c, S, so.bn), b.fwd_tiles, b.fwd_rows,
@@ -1046,6 +1084,23 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
     if (fire_colred(fw, c.stream)) return PNN_ERR_HIP;
   }
   return PNN_OK;
+}
+
+// The BN arrival counters of the segments a forward call uses set to zero, ahead of its launches
+// (one grouped launch; the counters are left zero by the kernels that use them, so this only
+// covers a scratch not yet used by this plan or one left by a failed call).
+int clear_counters(const Ctx& c, const std::vector<const SegP*>& segs) {
+  std::vector<ZeroProb> z;
+  for (const SegP* S : segs)
+    if (S->cnt_words > 0) {
+      ZeroProb q;
+      q.p = (unsigned*)(c.scratch + S->scr_base + S->cnt_off);
+      q.words = (int)S->cnt_words;
+      z.push_back(q);
+    }
+  return grouped<ZeroLaunch>(
+      z, [](const ZeroProb& q) { return (int)cdiv(q.words, ZERO_WORDS); },
+      [&](const ZeroLaunch& L, int tiles, size_t) { return launch_zero(L, tiles, c.stream); });
 }
 
 int run_fwd(const Ctx& c, const std::vector<const SegP*>& segs, const std::vector<Ptrs>& ptrs) {
@@ -1807,6 +1862,7 @@ pnn_status pnn_pre_fwd(pnn_plan* plan, const void* image, void* const* x, const 
     segs.push_back(&S);
     ptrs.push_back(p);
   }
+  if (clear_counters(c, segs)) return PNN_ERR_HIP;
   return run_fwd(c, segs, ptrs);
 }
 
@@ -1828,6 +1884,7 @@ pnn_status parareal_fine_fwd(pnn_plan* plan, const void* const* x, const void* c
     segs.push_back(&plan->fine[j]);
     ptrs.push_back(p);
   }
+  if (clear_counters(c, segs)) return PNN_ERR_HIP;
   return run_fwd_chains(c, segs, ptrs);
 }
 
@@ -1887,6 +1944,7 @@ pnn_status coarse_fwd(pnn_plan* plan, int j, const void* rt_j, const void* eta_j
   p.out = rt_next;
   p.params = eta_j;
   p.ext = add;
+  if (clear_counters(c, {&plan->coarse[j]})) return PNN_ERR_HIP;
   return run_fwd(c, {&plan->coarse[j]}, {p});
 }
 
@@ -1909,6 +1967,9 @@ pnn_status coarse_fwd_all(pnn_plan* plan, void* const* rt, const void* const* et
     const SegP& S = plan->coarse[j];
     return j > 0 && S.slots[0].bn >= 0 && S.bns[S.slots[0].bn].fwd_tiles_in > 0;
   };
+  std::vector<const SegP*> all;
+  for (int j = 0; j + 1 < N; ++j) all.push_back(&plan->coarse[j]);
+  if (clear_counters(c, all)) return PNN_ERR_HIP;
   for (int j = 0; j + 1 < N; ++j) {
     Ptrs p;
     p.in = rt[j];
@@ -1917,6 +1978,7 @@ pnn_status coarse_fwd_all(pnn_plan* plan, void* const* rt, const void* const* et
     p.ext = add[j];
     p.in_sums = chained(j);
     p.out_sums = (j + 2 < N && chained(j + 1)) ? &plan->coarse[j + 1] : nullptr;
+    p.out_params = p.out_sums != nullptr ? eta[j + 1] : nullptr;
     const int e = run_fwd(c, {&plan->coarse[j]}, {p});
     if (e) return e;
   }

@@ -32,6 +32,9 @@ enum {
   EPI_PW_WGRAD = 64,  // pw_kernel BWD / bnsum_kernel: also the convolution's weight gradient from
                       // the same tiles, split-K partial row tm of out32 [tiles_m][K][ncol]
                       // (g^T . ReLU(BN(z)))
+  EPI_BN_FUSE = 128,  // FWD + EPI_STATS: the producer also finalises the BN statistics from the
+                      // partial rows (bn_fwd_fuse: the last workgroup of a row group folds the
+                      // group, the last group the whole column) into bn_stats; no column-reduce pass
 };
 
 // Implicit-GEMM convolution problem.  FWD: out[m][n] = sum_k A[m][k] wmat[n][k] with
@@ -45,11 +48,20 @@ struct ConvProb {
   const void* ext;      // second addend [M][ncol] (nullable)
   const float* pro;     // FWD prologue scale[Cg], shift[Cg]: A = ReLU(x * scale + shift) (nullable)
   float* part;          // per-tile column partial sums [tiles_m][ncol][2]
-  const void* zsrc;     // BWD + EPI_BN_MASK: BN input z [M][ncol]
-  const float* bnst;    // BWD + EPI_BN_MASK: mean, invstd, scale, shift [4][ncol]
+  union {
+    const void* zsrc;   // BWD + EPI_BN_MASK: BN input z [M][ncol]
+    unsigned* bn_cnt;   // FWD + EPI_BN_FUSE: arrival counters (bn_fwd_fuse), zero at launch
+  };
+  union {
+    const float* bnst;      // BWD + EPI_BN_MASK: mean, invstd, scale, shift [4][ncol]
+    const float* bn_gamma;  // FWD + EPI_BN_FUSE: gamma [ncol], then beta [ncol]
+  };
   const float* acc_in;  // EPI_ACC_IN: [M][ncol] float
   const float* coef;    // EPI_BN_APPLY: A, B, K [3][ncol]
-  float* out32;         // EPI_STORE_F32: [M][ncol] float
+  union {
+    float* out32;       // EPI_STORE_F32: [M][ncol] float
+    float* bn_stats;    // FWD + EPI_BN_FUSE: mean, invstd, scale, shift [4][ncol] (written)
+  };
   float* kpart;         // GEMM kernel, ksplit > 1: fp32 partial tiles [ksplit][tiles][GEMM_BM][GEMM_BN]
   int B, H, W, Cg;      // gathered tensor
   int P, Q;             // output pixel grid (M = B * P * Q)
@@ -130,8 +142,12 @@ inline int colred_tiles(int ncols, int mode, int rl_log2) {
 struct ColStatProb {
   const void* x;
   float* part;          // [tiles][C][2]
+  const float* gamma;   // fuse: gamma [C], then beta [C]
+  float* stats;         // fuse: mean, invstd, scale, shift [4][C] (written)
+  unsigned* cnt;        // fuse: arrival counters (bn_fwd_fuse), zero at launch
   long M;
   int C;
+  int fuse;             // finalise the statistics as EPI_BN_FUSE does
   int tile_begin;
 };
 struct ColStatLaunch {
@@ -316,6 +332,28 @@ int launch_bnsum(const ConvLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_wgrad3(const WgradLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_colred(const ColRedLaunch& L, int tiles, hipStream_t s);
 int launch_colstat(const ColStatLaunch& L, int tiles, int dtype, hipStream_t s);
+// fused BN forward finalisation (bn_fwd_fuse): partial rows folded per group by its last workgroup
+constexpr int BNF_GROUP = 32;
+constexpr int BNF_STRIDE = 32;     // words between two counters (one 128-byte line each)
+constexpr int BNF_MAX_ROWS = 128;  // producers with more partial rows keep the column-reduce pass
+// counter words of a BN with C channels and at most `rows` partial rows: per column tile of >= 16
+// columns, one counter per row group and one for the groups
+__host__ __device__ inline long bnf_groups(long rows) { return rows / BNF_GROUP > 1 ? rows / BNF_GROUP : 1; }
+inline long bnf_words(int C, long rows) {
+  return (long)((C + 15) / 16) * (bnf_groups(rows < BNF_MAX_ROWS ? rows : BNF_MAX_ROWS) + 1) * BNF_STRIDE;
+}
+// zero-fill of word ranges (counters), one grouped launch
+struct ZeroProb {
+  unsigned* p;
+  int words;
+  int tile_begin;
+};
+struct ZeroLaunch {
+  int n;
+  ZeroProb p[64];
+};
+constexpr int ZERO_WORDS = 4096;   // words per workgroup
+int launch_zero(const ZeroLaunch& L, int tiles, hipStream_t s);
 int launch_bn_apply(const BnApplyLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_bnact_fwd(const BnActLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_bnact_bwd(const BnActLaunch& L, int tiles, int dtype, hipStream_t s);
