@@ -6,31 +6,7 @@
 
 namespace pnn {
 
-// Device-coherent 8-byte accesses for the partial rows and the group results: agent-scope relaxed
-// atomics, i.e. plain loads / stores with the coherence bit (every XCD sees them without an L2
-// writeback or invalidate, which a device-scope fence would cost on each call).
-__device__ __forceinline__ void bnf_store(float2* p, float2 v) {
-  __hip_atomic_store((unsigned long long*)p, __builtin_bit_cast(unsigned long long, v), __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float2 bnf_load(const float2* p) {
-  return __builtin_bit_cast(float2, __hip_atomic_load((unsigned long long*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-}
-__device__ __forceinline__ void bnf_store(double* p, double v) {
-  __hip_atomic_store((unsigned long long*)p, __builtin_bit_cast(unsigned long long, v), __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ double bnf_load(const double* p) {
-  return __builtin_bit_cast(double, __hip_atomic_load((unsigned long long*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-}
-// the wave's memory operations complete (its coherent stores have reached the device-wide level)
-__device__ __forceinline__ void bnf_wait() {
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_waitcnt(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
-
-// part[r][c] (r < rows, c < C, stored with bnf_store) holds the mean and the sum of squared deviations of partial row r's
+// part[r][c] (r < rows, c < C, stored with st_coherent) holds the mean and the sum of squared deviations of partial row r's
 // n_r = min(rowh, count - r * rowh) rows of channel c.  Rows form groups of BNF_GROUP (the last
 // group takes the remainder; a single group when rows < 2 BNF_GROUP).  Called by all 256 threads of
 // a workgroup right after it wrote row tm, columns [c0, c0 + ncl) (column tile ct): the workgroup
@@ -41,7 +17,7 @@ __device__ __forceinline__ void bnf_wait() {
 // the column-reduce kernel's finalisation).  Arrival counters cnt[ct][group], cnt[ct][groups] (each
 // BNF_STRIDE words apart) are
 // zero when the launch starts and are left zero.  Ordering: coherent stores, then each wave waits
-// for its own (bnf_wait) before the barrier that precedes the counter update; the reads follow the
+// for its own (wait_mem) before the barrier that precedes the counter update; the reads follow the
 // counter's result.  red: 512 doubles of LDS, free at the call.
 __device__ __forceinline__ void bn_fwd_fuse(float2* part, int rows, int rowh, long count, int C, const float* gamma,
                                             float* stats, unsigned* cnt, int tm, int ct, int c0, int ncl,
@@ -52,7 +28,7 @@ __device__ __forceinline__ void bn_fwd_fuse(float2* part, int rows, int rowh, lo
   const int g = min(tm / BNF_GROUP, NG - 1);
   const int r0 = g * BNF_GROUP, r1 = g == NG - 1 ? rows : r0 + BNF_GROUP;
   unsigned* gc = cnt + (long)ct * (NG + 1) * BNF_STRIDE;
-  bnf_wait();                         // this workgroup's partial row, device-wide
+  wait_mem();                         // this workgroup's partial row, device-wide
   __syncthreads();
   if (tid == 0)
     bnf_last = __hip_atomic_fetch_add(&gc[g * BNF_STRIDE], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (unsigned)(r1 - r0 - 1);
@@ -84,7 +60,7 @@ __device__ __forceinline__ void bn_fwd_fuse(float2* part, int rows, int rowh, lo
       for (; r + 3 * LN < r1; r += 4 * LN) {
         float2 v[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = bnf_load(part + (long)(r + u * LN) * C + c);
+        for (int u = 0; u < 4; ++u) v[u] = ld_coherent(part + (long)(r + u * LN) * C + c);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const double n = (double)min((long)rowh, count - (long)(r + u * LN) * rowh), m = (double)v[u].x;
@@ -93,7 +69,7 @@ __device__ __forceinline__ void bn_fwd_fuse(float2* part, int rows, int rowh, lo
         }
       }
       for (; r < r1; r += LN) {
-        const float2 v = bnf_load(part + (long)r * C + c);
+        const float2 v = ld_coherent(part + (long)r * C + c);
         const double n = (double)min((long)rowh, count - (long)r * rowh), m = (double)v.x;
         A += n * m;
         Q += (double)v.y + n * m * m;
@@ -112,14 +88,14 @@ __device__ __forceinline__ void bn_fwd_fuse(float2* part, int rows, int rowh, lo
       if (NG == 1) {
         finish(c, A, Q);
       } else {
-        bnf_store(dpart + (long)r0 * C + c, A);
-        bnf_store(dpart + (long)(r0 + 1) * C + c, Q);
+        st_coherent(dpart + (long)r0 * C + c, A);
+        st_coherent(dpart + (long)(r0 + 1) * C + c, Q);
       }
     }
     __syncthreads();
   }
   if (NG == 1) return;
-  bnf_wait();                        // the group's (A, Q), device-wide
+  wait_mem();                        // the group's (A, Q), device-wide
   __syncthreads();
   if (tid == 0)
     bnf_last = __hip_atomic_fetch_add(&gc[NG * BNF_STRIDE], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == (unsigned)(NG - 1);
@@ -131,8 +107,8 @@ __device__ __forceinline__ void bn_fwd_fuse(float2* part, int rows, int rowh, lo
     double A = 0.0, Q = 0.0;
     if (lane < LN && cb + j < ncl)
       for (int h = lane; h < NG; h += LN) {
-        A += bnf_load(dpart + (long)h * BNF_GROUP * C + c);
-        Q += bnf_load(dpart + ((long)h * BNF_GROUP + 1) * C + c);
+        A += ld_coherent(dpart + (long)h * BNF_GROUP * C + c);
+        Q += ld_coherent(dpart + ((long)h * BNF_GROUP + 1) * C + c);
       }
     if (lane < LN) {
       red[lane * CW + j] = A;

@@ -187,7 +187,7 @@ __device__ __forceinline__ void conv_epilogue(const ConvProb& P, float* acc_s, f
         // tid as the threads that summed it formed it)
         const float n = (float)min(BM, P.M - tm * BM);
         const float am = a / n;
-        bnf_store(pp, make_float2(piv_s[tid] + am, fmaxf(b - a * am, 0.f)));   // (read across XCDs)
+        st_coherent(pp, make_float2(piv_s[tid] + am, fmaxf(b - a * am, 0.f)));   // (read across XCDs)
       } else {
         *pp = make_float2(a, b);
       }

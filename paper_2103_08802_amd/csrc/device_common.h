@@ -156,4 +156,31 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Device-coherent 8-byte accesses for data that workgroups of one launch exchange (BN partial rows,
+// their folds): agent-scope relaxed atomics, i.e. plain loads / stores with the coherence bit, so
+// every XCD sees them without the writeback and invalidate of its whole L2 that a device-scope
+// fence costs.  Ordering: the writer's waves wait for their own stores (wait_mem) before the
+// barrier and counter update that publish them; the readers load after observing the counter.
+__device__ __forceinline__ void st_coherent(float2* p, float2 v) {
+  __hip_atomic_store((unsigned long long*)p, __builtin_bit_cast(unsigned long long, v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 ld_coherent(const float2* p) {
+  return __builtin_bit_cast(float2, __hip_atomic_load((unsigned long long*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+__device__ __forceinline__ void st_coherent(double* p, double v) {
+  __hip_atomic_store((unsigned long long*)p, __builtin_bit_cast(unsigned long long, v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double ld_coherent(const double* p) {
+  return __builtin_bit_cast(double, __hip_atomic_load((unsigned long long*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+// the wave's memory operations complete (its coherent stores have reached the device-wide level)
+__device__ __forceinline__ void wait_mem() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+
 }  // namespace pnn

@@ -1410,7 +1410,7 @@ __global__ __launch_bounds__(256) void pw_kernel(const ConvLaunch L) {
     if (MODE == MODE_FWD) {
       // the workgroup's mean and sum of squared deviations from its pivoted sums
       const float am = a / (float)(m_end - m_begin);
-      bnf_store((float2*)P.part + (long)tm * ncol + c0 + tid, make_float2(piv[tid] + am, fmaxf(b - a * am, 0.f)));
+      st_coherent((float2*)P.part + (long)tm * ncol + c0 + tid, make_float2(piv[tid] + am, fmaxf(b - a * am, 0.f)));
     } else {
       ((float2*)P.part)[(long)tm * ncol + c0 + tid] = make_float2(a, b);
     }

@@ -243,7 +243,7 @@ __global__ __launch_bounds__(256) void colstat_kernel(const ColStatLaunch L) {
     }
     // the workgroup's mean and sum of squared deviations
     const float am = a / (float)(r1 - r0);
-    bnf_store((float2*)P.part + (long)tile * P.C + c, make_float2(St<T>::ld(P.x, r0 * P.C + c) + am, fmaxf(b - a * am, 0.f)));
+    st_coherent((float2*)P.part + (long)tile * P.C + c, make_float2(St<T>::ld(P.x, r0 * P.C + c) + am, fmaxf(b - a * am, 0.f)));
   }
   if (P.fuse)
     bn_fwd_fuse((float2*)P.part, (int)((P.M + COLSTAT_ROWS - 1) / COLSTAT_ROWS), COLSTAT_ROWS, P.M, P.C, P.gamma,

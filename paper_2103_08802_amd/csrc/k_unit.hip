@@ -59,18 +59,21 @@ __device__ __forceinline__ constexpr int blk_off(int p, int c) { return (p / 2) 
 
 // Barrier of the nwg workgroups of one job: job words arrive (arrivals) and gen (generation), on
 // cache lines of their own; glob[0] is the launch's error flag, glob[1] counts completed barriers.
-// The workgroup's writes are complete at workgroup scope after its barrier; one thread then
-// releases them at agent scope, arrives, waits, and acquires for the whole workgroup.
+// What workgroups exchange across it (the BN partials) is written and read with device-coherent
+// accesses, so no cache-wide fence is needed (a device-scope fence writes back and invalidates the
+// whole L2 of the XCD): every wave waits for its own stores, then one thread arrives and waits.
 __device__ void job_sync(unsigned* arrive, unsigned* gen, unsigned* glob, unsigned nwg) {
+  wait_mem();
   __syncthreads();
   if (threadIdx.x == 0) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     if (__hip_atomic_load(glob, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0) {
       const unsigned g = __hip_atomic_load(gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      wait_mem();                      // the generation read before the arrival
       const unsigned old = __hip_atomic_fetch_add(arrive, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (old == nwg - 1) {
         __hip_atomic_store(arrive, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_fetch_add(gen, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        wait_mem();                    // the reset lands before the next generation opens
+        __hip_atomic_fetch_add(gen, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_fetch_add(glob + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       } else {
         unsigned spins = 0;
@@ -83,7 +86,6 @@ __device__ void job_sync(unsigned* arrive, unsigned* gen, unsigned* glob, unsign
         }
       }
     }
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
   __syncthreads();
 }
@@ -127,7 +129,7 @@ __device__ void image_stats16(const uint16_t* zs, float* red, float* part) {
   if (t < 16) {
     float a = 0.f;
     for (int k = 0; k < NG; ++k) a += red[k * 16 + t];
-    ((float2*)part)[t] = make_float2(red[UNT + t], a);
+    st_coherent((float2*)part + t, make_float2(red[UNT + t], a));
   }
   __syncthreads();
 }
@@ -146,7 +148,7 @@ __device__ void batch_stats(const float* part, int B, const float* gamma_beta, f
     float2 v[U];
 #pragma unroll
     for (int k = 0; k < U; ++k)
-      v[k] = n0 + k * NQ < B ? ((const float2*)part)[(long)(n0 + k * NQ) * C + c] : make_float2(0.f, 0.f);
+      v[k] = n0 + k * NQ < B ? ld_coherent((const float2*)part + (long)(n0 + k * NQ) * C + c) : make_float2(0.f, 0.f);
 #pragma unroll
     for (int k = 0; k < U; ++k) {
       const double m = (double)v[k].x;
@@ -455,7 +457,7 @@ __global__ __launch_bounds__(UNT) void unit_fwd_kernel(const UnitLaunch L) {
       if (tid < UC) {
         float a = 0.f;
         for (int w = 0; w < UWV; ++w) a += red[w * UC + tid];
-        ((float2*)part_x)[(long)n * UC + tid] = make_float2(red[UNT + tid], a);
+        st_coherent((float2*)part_x + (long)n * UC + tid, make_float2(red[UNT + tid], a));
       }
     }
     job_sync(arrive, gen, L.sync, L.B);
