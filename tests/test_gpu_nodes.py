@@ -140,6 +140,16 @@ def test_resident_unit_nodes(batch, sample, fine_subset):
     _assert(*check_net(net, sample=sample, fine_subset=fine_subset, node_subset=sample is None, resident=True))
 
 
+def test_bn_fused_statistics_ragged_groups():
+    """BN forward statistics finalised by the kernels that write their partial rows (the last
+    workgroup of each group of 32 rows folds it, the last group finalises) next to the
+    column-reduce pass: at batch 150 the ResNet-1001 N = 4 workload's 8x8 producers have 75
+    partial rows (two groups, the second of 43), its 16x16 ones 300 (nine, the last of 44), both
+    fused; its 32x32 ones 1200, above the fused limit of 512.  Sampled outputs and every BN's
+    mean / invstd / scale / shift against the oracle."""
+    _assert(*check_net(S.config(2, 150), sample=256, fine_subset=[1, 2, 3]))
+
+
 @pytest.mark.parametrize("idx,fine_subset", [(1, None), (2, [0, 1, 3]), (3, [0, 5, 10, 15]), (4, [0, 2, 5, 7])])
 def test_sampled_nodes_full_size(idx, fine_subset):
     _assert(*check_net(S.config(idx), sample=256, fine_subset=fine_subset))
