@@ -998,6 +998,18 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
     std::vector<BnActProb> ba;
     std::vector<MaxPool3Prob> mp;
     std::vector<ColRedProb> fw;
+    // producers of BN partial rows that may finalise the statistics themselves (bn_fwd_fuse): the
+    // problem (list, index), the BN and its parameters, and the column reduce it would need
+    struct Cand {
+      std::vector<ConvProb>* v;
+      size_t i;
+      const SegP* fs;
+      int fb;
+      const void* fparams;
+      bool own;                       // the BN of the node's own output (else the next block's)
+      ColRedProb red;
+    };
+    std::vector<Cand> cands;
     for (size_t i = 0; i < segs.size(); ++i) {
       const SegP& S = *segs[i];
       const Ptrs& P = ptrs[i];
@@ -1005,7 +1017,6 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
         if (n.level != L || (P.resident && n.resident)) continue;
         const SlotP& so = S.slots[n.dst];
         const void* ext = (n.dst == S.out) ? P.ext : nullptr;
-        bool fused = false;             // its output BN finalised by the producer
         if (n.op == PNN_OP_CONV) {
           ConvProb p = conv_common(plan, n);
           p.in = slot_ptr(c, S, P, n.src);
@@ -1034,13 +1045,18 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
           const bool pwn = pw_fwd_node(S, n, es);
           if (pwn) set_pw_tiles(p, S.short_tiles);
           else set_tiles(p, S.short_tiles);
-          // few partial rows: the producer finalises the statistics itself (bn_fwd_fuse)
-          if (fs != nullptr && p.tiles_m <= BNF_MAX_ROWS) {
-            set_bn_fuse(p, c, *fs, fb, fparams);
-            fused = so.bn >= 0;
+          std::vector<ConvProb>& dst = pwn ? cv_pw : (n.cin % (16 / es) == 0 ? cv_vec : cv_gen);
+          dst.push_back(p);
+          if (fs != nullptr) {
+            Cand cd{&dst, dst.size() - 1, fs, fb, fparams, so.bn >= 0, {}};
+            if (cd.own) {
+              const BnP& b = S.bns[so.bn];
+              cd.red = bn_fwd_red(part_ptr(c, S, so.bn), b.fwd_tiles, b.fwd_rows,
+                                  (const float*)(cp(P.params) + b.p_off), stats_ptr(c, S, so.bn), b.C,
+                                  (long)B * so.H * so.W);
+            }
+            cands.push_back(cd);
           }
-          if (pwn) cv_pw.push_back(p);
-          else (n.cin % (16 / es) == 0 ? cv_vec : cv_gen).push_back(p);
         } else if (n.op == PNN_OP_BNACT) {
           BnActProb p;
           std::memset(&p, 0, sizeof(p));
@@ -1061,13 +1077,26 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
           p.ve = (p.C % ve == 0 && (((uintptr_t)p.x | (uintptr_t)p.y) & 15) == 0) ? ve : 1;
           mp.push_back(p);
         }
-        if (so.bn >= 0 && !fused) {
+        if (so.bn >= 0 && n.op != PNN_OP_CONV) {
           const BnP& b = S.bns[so.bn];
           const long cnt = (long)B * so.H * so.W;
           fw.push_back(bn_fwd_red(part_ptr(c, S, so.bn), b.fwd_tiles, b.fwd_rows,
                                   (const float*)(cp(P.params) + b.p_off), stats_ptr(c, S, so.bn), b.C, cnt));
         }
       }
+    }
+    // the level's producers finalise their BN statistics themselves when each has few partial rows
+    // and the level's convolutions fit the device in one wave (there the finalisation replaces a
+    // launch gap; in larger levels every workgroup's arrival would cost more than the launch); the
+    // next block's input BN (chained) by its rows alone, as that block's call decides it
+    long level_wg = 0;
+    for (auto* v : {&cv_vec, &cv_gen, &cv_pw})
+      for (const ConvProb& q : *v) level_wg += (long)q.tiles_m * q.tiles_n;
+    for (Cand& cd : cands) {
+      ConvProb& q = (*cd.v)[cd.i];
+      const bool fuse = q.tiles_m <= BNF_MAX_ROWS && (!cd.own || level_wg <= BNF_MAX_WG);
+      if (fuse) set_bn_fuse(q, c, *cd.fs, cd.fb, cd.fparams);
+      else if (cd.own) fw.push_back(cd.red);
     }
     int e;
     if ((e = fire_conv(c, cv_vec, MODE_FWD))) return e;

@@ -336,6 +336,7 @@ int launch_colstat(const ColStatLaunch& L, int tiles, int dtype, hipStream_t s);
 constexpr int BNF_GROUP = 32;
 constexpr int BNF_STRIDE = 32;     // words between two counters (one 128-byte line each)
 constexpr int BNF_MAX_ROWS = 512;  // producers with more partial rows keep the column-reduce pass
+constexpr int BNF_MAX_WG = 512;    // ... and so do those of a level with more convolution workgroups
 // counter words of a BN with C channels and at most `rows` partial rows: per column tile of >= 16
 // columns, one counter per row group and one for the groups
 __host__ __device__ inline long bnf_groups(long rows) { return rows / BNF_GROUP > 1 ? rows / BNF_GROUP : 1; }
