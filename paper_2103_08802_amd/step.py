@@ -262,13 +262,19 @@ class ParaRealGPU:
                 del parts[k]
         return parts
 
-    def capture(self):
+    def capture(self, whole=False):
         """Capture one training step (forward and backward, as ``forward`` + ``backward`` run it)
-        into HIP graphs, one per part (no eager step is needed first: the library's calls create
-        nothing).  A replay repeats the step on what the buffers hold then."""
+        into HIP graphs (no eager step is needed first: the library's calls create nothing).  A
+        replay repeats the step on what the buffers hold then.  ``whole=False``: one graph per part
+        (the fine and coarse parts can be timed between replays; the backward's calls separate);
+        ``whole=True``: the forward as one graph and the backward as another, the backward as
+        ``overlap_bwd`` makes it (the coarse chain overlapped with the fine backward, its fork and
+        join across the plan's side streams captured with it)."""
         torch = _torch()
         self.graphs = {}
-        for name, fn in self._parts().items():
+        self.whole = whole
+        parts = {"fwd": self.forward, "bwd": self.backward} if whole else self._parts()
+        for name, fn in parts.items():
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
                 fn()
@@ -276,8 +282,12 @@ class ParaRealGPU:
         torch.cuda.synchronize()
 
     def replay_forward(self, fine_events=None, coarse_events=None):
-        """``forward`` from the captured graphs; the events as in ``forward``."""
+        """``forward`` from the captured graphs; the events as in ``forward`` (whole-step graphs:
+        none)."""
         G = self.graphs
+        if getattr(self, "whole", False):
+            G["fwd"].replay()
+            return
         G["pre_fwd"].replay()
         if fine_events:
             fine_events[0].record()
@@ -294,8 +304,12 @@ class ParaRealGPU:
         G["head"].replay()
 
     def replay_backward(self, fine_events=None, coarse_events=None):
-        """``backward`` from the captured graphs; the events as in ``backward``."""
+        """``backward`` from the captured graphs; the events as in ``backward`` (whole-step graphs:
+        none)."""
         G = self.graphs
+        if getattr(self, "whole", False):
+            G["bwd"].replay()
+            return
         if coarse_events:
             coarse_events[0].record()
         if "coarse_bwd" in G:

@@ -213,11 +213,14 @@ def test_streams_do_not_change_results(idx, batch):
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("idx,batch,streams", [(2, 2, 4), (3, 4, 4), (3, 4, 1)])
-def test_graph_replay_matches_eager(idx, batch, streams):
-    """The step captured into HIP graphs (one per part, captured before any eager call) and replayed
-    gives bit-identical loss, logits, parameter gradients and input gradients to the eager step, on
-    every replay, with eager steps, output clearing and synchronisations in between."""
+@pytest.mark.parametrize("idx,batch,streams,whole", [(2, 2, 4, False), (3, 4, 4, False), (3, 4, 1, False),
+                                                     (2, 2, 4, True), (3, 4, 4, True)])
+def test_graph_replay_matches_eager(idx, batch, streams, whole):
+    """The step captured into HIP graphs (one per part, or with ``whole`` the forward and the
+    overlapped backward as one graph each, its fork and join across the side streams captured
+    with it; captured before any eager call) and replayed gives bit-identical loss, logits,
+    parameter gradients and input gradients to the eager step, on every replay, with eager steps,
+    output clearing and synchronisations in between."""
     import torch
     from paper_2103_08802_amd import binding as B
     from paper_2103_08802_amd.step import ParaRealGPU
@@ -226,11 +229,12 @@ def test_graph_replay_matches_eager(idx, batch, streams):
     g = ParaRealGPU(net, params)
     B.pnn_set_streams(g.plan, streams)
     g.load_input(x, labels)
+    g.overlap_bwd = whole                # the eager reference runs the backward the graphs hold
 
     def outputs():
         return [t.clone() for t in [g.loss, g.logits, g.deps] + g.ddelta + g.dphi + g.deta + g.dx]
 
-    g.capture()                          # before any eager step: the library creates nothing in a call
+    g.capture(whole=whole)               # before any eager step: the library creates nothing in a call
     torch.cuda.synchronize()
     g.replay_forward()
     g.replay_backward()
