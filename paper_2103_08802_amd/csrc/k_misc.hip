@@ -363,80 +363,225 @@ __global__ __launch_bounds__(256) void sgd_kernel(const SgdLaunch L) {
 // ------------------------------------------------------------------------------------------------
 // bnact: out = pool(ReLU(BN(z))) [+ res] [+ ext]; backward routes the output gradient to the first
 // maximum of each 2x2 window, masks it by ReLU' and reduces dbn, dbn * xhat per channel.
-// One workgroup = BNACT_PIX output pixels x all channels; a thread owns channels.
+// One workgroup = P.pix output pixels x all channels.  With C a multiple of the 16-byte chunk (VE
+// elements) and at most BNACT_MAXC, a thread owns 16-byte chunks of channels (per-channel constants
+// in LDS): forward work items are (pixel, chunk) pairs, several in flight per thread; backward, the
+// 256 threads are (pixel lane, chunk) pairs, each lane summing its pixels' dbn, dbn * xhat, the
+// lanes added in lane order.  Otherwise a thread owns channels, element by element.
 // ------------------------------------------------------------------------------------------------
 template <typename T>
+__device__ __forceinline__ long bnact_zi(const BnActProb& P, long px, int Ho, int Wo, int pool, int w, int ch) {
+  const int n = (int)(px / ((long)Ho * Wo));
+  const int rem = (int)(px - (long)n * Ho * Wo);
+  const int p = rem / Wo, q = rem - (rem / Wo) * Wo;
+  return (((long)n * P.H + p * pool + w / pool) * P.W + q * pool + w % pool) * P.C + ch;
+}
+
+template <typename T>
 __global__ __launch_bounds__(256) void bnact_fwd_kernel(const BnActLaunch L) {
+  constexpr int VE = St<T>::VE;
+  constexpr int U = 4;                                  // work items in flight per thread
+  __shared__ float2 ss[BNACT_MAXC];                     // scale, shift per channel
   const int gi = find_group(L);
   const BnActProb& P = L.p[gi];
   const int pool = P.pool ? 2 : 1;
   const int Ho = P.H / pool, Wo = P.W / pool;
-  const long px0 = (long)(blockIdx.x - P.tile_begin) * BNACT_PIX;
-  for (int c = threadIdx.x; c < P.C; c += 256) {
-    const float sc = P.stats[2 * P.C + c], sh = P.stats[3 * P.C + c];
-    for (int k = 0; k < BNACT_PIX; ++k) {
-      const long px = px0 + k;
-      if (px >= P.n_out) break;
-      const int n = (int)(px / ((long)Ho * Wo));
-      const int rem = (int)(px - (long)n * Ho * Wo);
-      const int p = rem / Wo, q = rem - (rem / Wo) * Wo;
-      float m = -INFINITY;
-      for (int a = 0; a < pool; ++a)
-        for (int b = 0; b < pool; ++b) {
-          const long zi = (((long)n * P.H + p * pool + a) * P.W + q * pool + b) * P.C + c;
-          const float y = fmaxf(fmaf(St<T>::ld(P.z, zi), sc, sh), 0.0f);
-          m = fmaxf(m, y);
+  const long px0 = (long)(blockIdx.x - P.tile_begin) * P.pix;
+  const int tid = threadIdx.x;
+  if (P.C % VE != 0 || P.C > BNACT_MAXC) {
+    for (int c = tid; c < P.C; c += 256) {
+      const float sc = P.stats[2 * P.C + c], sh = P.stats[3 * P.C + c];
+      for (int k = 0; k < P.pix; ++k) {
+        const long px = px0 + k;
+        if (px >= P.n_out) break;
+        float m = -INFINITY;
+        for (int w = 0; w < pool * pool; ++w)
+          m = fmaxf(m, fmaxf(fmaf(St<T>::ld(P.z, bnact_zi<T>(P, px, Ho, Wo, pool, w, c)), sc, sh), 0.0f));
+        const long oi = px * P.C + c;
+        if (P.res) m += St<T>::ld(P.res, oi);
+        if (P.ext) m += St<T>::ld(P.ext, oi);
+        St<T>::st(P.out, oi, m);
+      }
+    }
+    return;
+  }
+  for (int c = tid; c < P.C; c += 256) ss[c] = make_float2(P.stats[2 * P.C + c], P.stats[3 * P.C + c]);
+  __syncthreads();
+  const int CC = P.C / VE;
+  const int items = P.pix * CC;
+  const int npool = pool * pool;
+  for (int i0 = tid; i0 < items; i0 += 256 * U) {
+    uint4 zv[U][4], rv[U], xv[U];
+    long pxs[U];
+    int chs[U];
+    bool on[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int it = i0 + u * 256;
+      pxs[u] = px0 + it / CC;
+      chs[u] = (it % CC) * VE;
+      on[u] = it < items && pxs[u] < P.n_out;
+      const long px = on[u] ? pxs[u] : px0;
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        zv[u][w] = w < npool ? *(const uint4*)((const T*)P.z + bnact_zi<T>(P, px, Ho, Wo, pool, w, chs[u]))
+                             : make_uint4(0, 0, 0, 0);
+      const long oi = px * P.C + chs[u];
+      rv[u] = P.res ? *(const uint4*)((const T*)P.res + oi) : make_uint4(0, 0, 0, 0);
+      xv[u] = P.ext ? *(const uint4*)((const T*)P.ext + oi) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (!on[u]) continue;
+      float m[VE];
+#pragma unroll
+      for (int e = 0; e < VE; ++e) m[e] = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        if (w >= npool) break;
+        Chunk<T> z;
+        unpack_chunk<T>(zv[u][w], z);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          const float2 q = ss[chs[u] + e];
+          m[e] = fmaxf(m[e], fmaxf(fmaf(z.v[e], q.x, q.y), 0.0f));
         }
-      const long oi = px * P.C + c;
-      if (P.res) m += St<T>::ld(P.res, oi);
-      if (P.ext) m += St<T>::ld(P.ext, oi);
-      St<T>::st(P.out, oi, m);
+      }
+      if (P.res) {
+        Chunk<T> r;
+        unpack_chunk<T>(rv[u], r);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) m[e] += r.v[e];
+      }
+      if (P.ext) {
+        Chunk<T> x;
+        unpack_chunk<T>(xv[u], x);
+#pragma unroll
+        for (int e = 0; e < VE; ++e) m[e] += x.v[e];
+      }
+      store_chunk<T>(P.out, pxs[u] * P.C + chs[u], m);
     }
   }
 }
 
 template <typename T>
 __global__ __launch_bounds__(256) void bnact_bwd_kernel(const BnActLaunch L) {
+  constexpr int VE = St<T>::VE;
+  __shared__ float4 cs[BNACT_MAXC];                     // mean, invstd, scale, shift per channel
+  __shared__ float2 red[256 * VE];                      // per-lane sums [lanes][C]
   const int gi = find_group(L);
   const BnActProb& P = L.p[gi];
   const int pool = P.pool ? 2 : 1;
   const int Ho = P.H / pool, Wo = P.W / pool;
+  const int npool = pool * pool;
   const int tile = blockIdx.x - P.tile_begin;
-  const long px0 = (long)tile * BNACT_PIX;
-  for (int c = threadIdx.x; c < P.C; c += 256) {
-    const float mean = P.stats[c], invstd = P.stats[P.C + c];
-    const float sc = P.stats[2 * P.C + c], sh = P.stats[3 * P.C + c];
-    float s1 = 0.f, s2 = 0.f;
-    for (int k = 0; k < BNACT_PIX; ++k) {
-      const long px = px0 + k;
-      if (px >= P.n_out) break;
-      const int n = (int)(px / ((long)Ho * Wo));
-      const int rem = (int)(px - (long)n * Ho * Wo);
-      const int p = rem / Wo, q = rem - (rem / Wo) * Wo;
-      // first maximum of the window (row-major), on the unrounded activation
-      int arg = 0;
-      float best = 0.f;
-      for (int w = 0; w < pool * pool; ++w) {
-        const long zi = (((long)n * P.H + p * pool + w / pool) * P.W + q * pool + w % pool) * P.C + c;
-        const float y = fmaxf(fmaf(St<T>::ld(P.z, zi), sc, sh), 0.0f);
-        if (w == 0 || y > best) {
-          best = y;
-          arg = w;
+  const long px0 = (long)tile * P.pix;
+  const int tid = threadIdx.x;
+  if (P.C % VE != 0 || P.C > BNACT_MAXC) {
+    for (int c = tid; c < P.C; c += 256) {
+      const float mean = P.stats[c], invstd = P.stats[P.C + c];
+      const float sc = P.stats[2 * P.C + c], sh = P.stats[3 * P.C + c];
+      float s1 = 0.f, s2 = 0.f;
+      for (int k = 0; k < P.pix; ++k) {
+        const long px = px0 + k;
+        if (px >= P.n_out) break;
+        // first maximum of the window (row-major), on the unrounded activation
+        int arg = 0;
+        float best = 0.f;
+        for (int w = 0; w < npool; ++w) {
+          const float y = fmaxf(fmaf(St<T>::ld(P.z, bnact_zi<T>(P, px, Ho, Wo, pool, w, c)), sc, sh), 0.0f);
+          if (w == 0 || y > best) {
+            best = y;
+            arg = w;
+          }
+        }
+        const float gv = St<T>::ld(P.g, px * P.C + c);
+        for (int w = 0; w < npool; ++w) {
+          const long zi = bnact_zi<T>(P, px, Ho, Wo, pool, w, c);
+          const float z = St<T>::ld(P.z, zi);
+          const float y = fmaf(z, sc, sh);
+          const float d = (w == arg && y > 0.f) ? gv : 0.f;
+          St<T>::st(P.out, zi, d);
+          const float dr = St<T>::rnd(d);
+          s1 += dr;
+          s2 += dr * ((z - mean) * invstd);
         }
       }
-      const float gv = St<T>::ld(P.g, px * P.C + c);
-      for (int w = 0; w < pool * pool; ++w) {
-        const long zi = (((long)n * P.H + p * pool + w / pool) * P.W + q * pool + w % pool) * P.C + c;
-        const float z = St<T>::ld(P.z, zi);
-        const float y = fmaf(z, sc, sh);
-        const float d = (w == arg && y > 0.f) ? gv : 0.f;
-        St<T>::st(P.out, zi, d);
-        const float dr = St<T>::rnd(d);
-        s1 += dr;
-        s2 += dr * ((z - mean) * invstd);
+      ((float2*)P.part)[(long)tile * P.C + c] = make_float2(s1, s2);
+    }
+    return;
+  }
+  for (int c = tid; c < P.C; c += 256)
+    cs[c] = make_float4(P.stats[c], P.stats[P.C + c], P.stats[2 * P.C + c], P.stats[3 * P.C + c]);
+  __syncthreads();
+  const int CC = P.C / VE;                              // chunks per pixel (<= 256 / 1 for C <= BNACT_MAXC)
+  const int PL = 256 / CC;                              // pixel lanes
+  const int cc = tid % CC, pl = tid / CC;
+  const int ch = cc * VE;
+  float s1[VE], s2[VE];
+#pragma unroll
+  for (int e = 0; e < VE; ++e) s1[e] = s2[e] = 0.f;
+  if (pl < PL) {
+#pragma unroll 2
+    for (int k = pl; k < P.pix; k += PL) {
+      const long px = px0 + k;
+      if (px >= P.n_out) break;
+      uint4 zv[4];
+      long zi[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        zi[w] = bnact_zi<T>(P, px, Ho, Wo, pool, w < npool ? w : 0, ch);
+        zv[w] = w < npool ? *(const uint4*)((const T*)P.z + zi[w]) : make_uint4(0, 0, 0, 0);
+      }
+      Chunk<T> g;
+      unpack_chunk<T>(*(const uint4*)((const T*)P.g + px * P.C + ch), g);
+      Chunk<T> z[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) unpack_chunk<T>(zv[w], z[w]);
+      // first maximum of each channel's window (row-major), on the unrounded activation
+      int arg[VE];
+#pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        const float4 q = cs[ch + e];
+        float best = 0.f;
+        arg[e] = 0;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          if (w >= npool) break;
+          const float y = fmaxf(fmaf(z[w].v[e], q.z, q.w), 0.0f);
+          if (w == 0 || y > best) {
+            best = y;
+            arg[e] = w;
+          }
+        }
+      }
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        if (w >= npool) break;
+        float d[VE];
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          const float4 q = cs[ch + e];
+          const float y = fmaf(z[w].v[e], q.z, q.w);
+          d[e] = (w == arg[e] && y > 0.f) ? g.v[e] : 0.f;
+          const float dr = St<T>::rnd(d[e]);
+          s1[e] += dr;
+          s2[e] += dr * ((z[w].v[e] - q.x) * q.y);
+        }
+        store_chunk<T>(P.out, zi[w], d);
       }
     }
-    ((float2*)P.part)[(long)tile * P.C + c] = make_float2(s1, s2);
+#pragma unroll
+    for (int e = 0; e < VE; ++e) red[pl * P.C + ch + e] = make_float2(s1[e], s2[e]);
+  }
+  __syncthreads();
+  for (int c = tid; c < P.C; c += 256) {
+    float a = 0.f, b = 0.f;
+    for (int l = 0; l < PL; ++l) {
+      a += red[l * P.C + c].x;
+      b += red[l * P.C + c].y;
+    }
+    ((float2*)P.part)[(long)tile * P.C + c] = make_float2(a, b);
   }
 }
 

@@ -1067,6 +1067,7 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
           p.stats = stats_ptr(c, S, n.bn);
           p.B = B; p.H = n.H; p.W = n.W; p.C = n.cin; p.pool = n.pool;
           p.n_out = (long)B * n.Ho * n.Wo;
+          p.pix = bnact_fwd_pix(n.cin, es);
           ba.push_back(p);
         } else {
           MaxPool3Prob p;
@@ -1103,7 +1104,7 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
     if ((e = fire_conv(c, cv_gen, MODE_FWD))) return e;
     if ((e = fire_pw(c, cv_pw, MODE_FWD))) return e;
     e = grouped<BnActLaunch>(
-        ba, [](const BnActProb& p) { return (int)cdiv(p.n_out, BNACT_PIX); },
+        ba, [](const BnActProb& p) { return (int)cdiv(p.n_out, p.pix); },
         [&](const BnActLaunch& Lx, int tiles, size_t) { return launch_bnact_fwd(Lx, tiles, plan->dtype, c.stream); });
     if (e) return e;
     e = grouped<MaxPool3Launch>(
@@ -1366,6 +1367,7 @@ int run_bwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
             p.part = part_ptr(c, S, n.bn);
             p.B = B; p.H = n.H; p.W = n.W; p.C = n.cin; p.pool = n.pool;
             p.n_out = (long)B * n.Ho * n.Wo;
+            p.pix = BNACT_PIX;
             ba.push_back(p);
             continue;
           }
@@ -1442,7 +1444,7 @@ int run_bwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
       e = fire_pw(c, pw, MODE_BWD);
       if (e) return e;
       e = grouped<BnActLaunch>(
-          ba, [](const BnActProb& p) { return (int)cdiv(p.n_out, BNACT_PIX); },
+          ba, [](const BnActProb& p) { return (int)cdiv(p.n_out, p.pix); },
           [&](const BnActLaunch& Lx, int tiles, size_t) { return launch_bnact_bwd(Lx, tiles, plan->dtype, c.stream); });
       if (e) return e;
     }

@@ -184,6 +184,7 @@ struct BnActProb {
   float* part;          // BWD: [tiles][C][2]
   int B, H, W, C, pool;
   long n_out;           // output pixels (B * Ho * Wo)
+  int pix;              // output pixels per workgroup (BWD: BNACT_PIX, the partial rows' pixels)
   int tile_begin;
 };
 struct BnActLaunch {
@@ -396,7 +397,16 @@ constexpr int BNSUM_ROWS = 512;    // rows per BN-sum workgroup (short-tile segm
 constexpr int BNSUM_MAXK = 64;     // gradient channels of a BN-sum problem
 constexpr int BNSUM_TR = 64;       // rows per LDS tile of bnsum_kernel
 constexpr int COLSTAT_ROWS = 128;  // rows per column-statistics workgroup
-constexpr int BNACT_PIX = 32;      // output pixels per bnact workgroup
+constexpr int BNACT_PIX = 32;      // output pixels per bnact_bwd workgroup (one BN partial row)
+constexpr int BNACT_MAXC = 512;    // channels of the chunked bnact path (per-channel constants in LDS)
+// output pixels per bnact_fwd workgroup: about 1024 16-byte chunks of C channels, 1 to 64 pixels
+// (channel counts off the chunk or above BNACT_MAXC: BNACT_PIX, the element-wise path)
+inline int bnact_fwd_pix(int C, int es) {
+  const int ve = 16 / es;
+  if (C % ve != 0 || C > BNACT_MAXC) return BNACT_PIX;
+  const int cc = C / ve;
+  return 1024 / cc < 1 ? 1 : 1024 / cc > 64 ? 64 : 1024 / cc;
+}
 constexpr int CONV_HALO_BYTES = 40960;  // LDS of a 3x3 halo tile (input rows + halo, padded pixels)
 // K steps whose filter fragments a wave keeps in registers, by column sub-tiles per wave (the
 // register budget of narrow tiles, which carry more row sub-tiles, is smaller)
