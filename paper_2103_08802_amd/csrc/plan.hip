@@ -138,7 +138,8 @@ namespace {
 // Weight-gradient tiling.  3x3 / stride 1 / pad 1 convolutions whose stages of W3 rows are whole
 // image rows go to the halo kernel: 16 output channels x one 16-channel input block x 9 taps per
 // workgroup, split-K in multiples of the stage.  Everything else: (16 wr) x 64 dW tiles, split-K
-// over m in multiples of 128 rows.
+// over m in multiples of 128 rows into about 1024 workgroups (four per CU: a wide layer's few tiles
+// would otherwise each walk hundreds of thousands of rows).
 WgradGeom wgrad_geom(int Co, int K, long M);
 
 WgradGeom wgrad_geom_node(const NodeP& n, int B, int es) {
@@ -174,7 +175,7 @@ WgradGeom wgrad_geom(int Co, int K, long M) {
   g.tiles_co = Co / (16 * g.wr);
   g.tiles_k = (int)cdiv(K, 64);
   const long base = (long)g.tiles_co * g.tiles_k;
-  long splits = std::max(1L, std::min(cdiv(M, 512), cdiv(256, base)));
+  long splits = std::max(1L, std::min(cdiv(M, 512), cdiv(1024, base)));
   long mchunk = cdiv(cdiv(M, splits), 128) * 128;
   g.mchunk = (int)mchunk;
   g.splits = (int)cdiv(M, mchunk);
