@@ -376,4 +376,170 @@ int launch_gemm(const ConvLaunch& L, int tiles, int mode, hipStream_t s) {
   return (int)hipGetLastError();
 }
 
+// ------------------------------------------------------------------------------------------------
+// Weight gradient of a wide 3x3 / stride 1 / pad 1 bf16 convolution as a GEMM over the output
+// pixels: dW[co][(tap, c)] = sum_m g[m][co] * act(in)[pixel(m) + tap][c] (the weight gradient of the
+// layers of Table vgg), 128 output channels x 128 filter columns (one tap's 128 input channels) per
+// workgroup, split over m.  Stages of 64 pixels: the output-gradient rows and the gathered input
+// rows (BN prologue applied on the way, zeros outside the image) are staged m-major in LDS (rows
+// padded to 144 elements: the four rows of a transposed read fall on distinct banks), read as MFMA
+// fragments with the gfx950 transposed LDS read; four waves of 64 x 64 (4 x 4 16x16x32 MFMAs).
+// Loads run two stages ahead in two register sets; two LDS stages.  The fp32 partial tile goes to
+// part[split][co][K] for the split-K column reduce.
+// ------------------------------------------------------------------------------------------------
+namespace {
+constexpr int WGM_T = 128;                  // output channels and filter columns per tile
+constexpr int WGM_KC = 64;                  // pixels per stage
+constexpr int WGM_RS = WGM_T + 16;          // LDS row stride (elements)
+constexpr int WGM_STG = 2 * WGM_KC * WGM_RS;   // elements per LDS stage (gradient, then input)
+
+typedef short wv4s16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) wv4s16 lds_wv4s16;
+
+// the 16x16x32 MFMA fragment of 16 columns (cbase ..) over 8 rows (row0 .. row0 + 7) of an m-major
+// tile: lane group rows 4 (r16 / 4) apart by the transposed read
+__device__ __forceinline__ void tr_frag(const uint16_t* base, int row0, int cbase, int r16, Frag<uint16_t>& f) {
+  const uint16_t* p0 = base + (row0 + (r16 >> 2)) * WGM_RS + cbase + 4 * (r16 & 3);
+  const wv4s16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_wv4s16*)p0);
+  const wv4s16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_wv4s16*)(p0 + 4 * WGM_RS));
+  const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
+  f.from_raw(make_uint4(l2.x, l2.y, h2.x, h2.y));
+}
+}  // namespace
+
+__global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L) {
+  using T = uint16_t;
+  constexpr int VE = 8;
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * WGM_STG];
+  __shared__ float2 pro_s[WGM_T];
+  const int gi = find_group(L);
+  const WgradProb& P = L.p[gi];
+  const int local = blockIdx.x - P.tile_begin;
+  const int tk = local % P.tiles_k;
+  const int rest = local / P.tiles_k;
+  const int tco = rest % P.tiles_co;
+  const int split = rest / P.tiles_co;
+  const int co0 = tco * WGM_T, k0 = tk * WGM_T;
+  const int tap = k0 / P.Cg, c0 = k0 - tap * P.Cg;      // (Cg a multiple of 128)
+  const int dr = tap / 3 - 1, dc = tap - 3 * (tap / 3) - 1;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int wr = wave >> 1, wc = wave & 1;
+  const int m_begin = split * P.mchunk;
+  const int m_end = min(P.M, m_begin + P.mchunk);
+  const int nst = (m_end - m_begin + WGM_KC - 1) / WGM_KC;
+  const bool prologue = P.pro != nullptr;
+  if (tid < WGM_T) pro_s[tid] = prologue ? make_float2(P.pro[c0 + tid], P.pro[P.Cg + c0 + tid]) : make_float2(1.f, 0.f);
+
+  // loader: chunk h (< 4) of a stage is row lrow + 16 h, 16-byte column lcol
+  const int lcol = (tid & 15) * VE, lrow = tid >> 4;
+  const int PQ = P.P * P.Q;
+  const float rPQ = 1.0f / (float)PQ, rQ = 1.0f / (float)P.Q;
+  const T* gbase = (const T*)P.g + co0 + lcol;
+  const T* ibase = (const T*)P.in + c0 + lcol;
+  struct Set {
+    uint4 g[4], a[4];
+    unsigned ok;       // bit h: row h's gradient exists; bit 4 + h: its input pixel exists
+  };
+  auto load = [&](int s, Set& R) {
+    const int mc = m_begin + (s < nst ? s : nst - 1) * WGM_KC;   // past the end: a repeat, masked
+    R.ok = 0;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const int m = mc + lrow + 16 * h;
+      const bool vm = s < nst && m < m_end;
+      int n, pix, p, q;
+      divmod_small(vm ? m : 0, PQ, rPQ, n, pix);
+      divmod_small(pix, P.Q, rQ, p, q);
+      const int ih = p + dr, iw = q + dc;
+      const bool vi = vm && (unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W;
+      R.g[h] = *(const uint4*)(gbase + (vm ? (long)m * P.Co : 0));
+      R.a[h] = *(const uint4*)(ibase + (vi ? (((long)n * P.H + ih) * P.W + iw) * P.Cg : 0));
+      R.ok |= (vm ? 1u : 0u) << h | (vi ? 1u : 0u) << (4 + h);
+    }
+  };
+  auto store = [&](int st, const Set& R) {
+    uint16_t* G = smem + st * WGM_STG;
+    uint16_t* A = G + WGM_KC * WGM_RS;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const unsigned kg = 0u - ((R.ok >> h) & 1u), ka = 0u - ((R.ok >> (4 + h)) & 1u);
+      uint4 w = R.a[h];
+      if (prologue) {
+        Chunk<T> v;
+        unpack_chunk<T>(w, v);
+        float f[VE];
+#pragma unroll
+        for (int e = 0; e < VE; ++e) f[e] = fmaxf(fmaf(v.v[e], pro_s[lcol + e].x, pro_s[lcol + e].y), 0.0f);
+        store_chunk<T>(&w, 0, f);
+      }
+      const int o = (lrow + 16 * h) * WGM_RS + lcol;
+      *(uint2*)(G + o) = make_uint2(R.g[h].x & kg, R.g[h].y & kg);
+      *(uint2*)(G + o + 4) = make_uint2(R.g[h].z & kg, R.g[h].w & kg);
+      *(uint2*)(A + o) = make_uint2(w.x & ka, w.y & ka);
+      *(uint2*)(A + o + 4) = make_uint2(w.z & ka, w.w & ka);
+    }
+  };
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int st) {
+    const uint16_t* G = smem + st * WGM_STG;
+    const uint16_t* A = G + WGM_KC * WGM_RS;
+#pragma unroll
+    for (int sub = 0; sub < WGM_KC / 32; ++sub) {
+      const int row0 = sub * 32 + VE * grp;
+      Frag<T> a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) tr_frag(G, row0, wr * 64 + 16 * i, r16, a[i]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) tr_frag(A, row0, wc * 64 + 16 * j, r16, b[j]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mma(a[i], b[j], acc[i][j]);
+    }
+  };
+
+  Set R0, R1;
+  load(0, R0);
+  load(1, R1);
+  __syncthreads();                                   // pro_s
+  store(0, R0);
+  __syncthreads();
+  auto half = [&](int s, int st, Set& far, const Set& next) {
+    load(s + 2, far);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(st);
+    __builtin_amdgcn_sched_barrier(0);
+    store(st ^ 1, next);
+    __syncthreads();
+  };
+  int s = 0;
+  for (; s + 1 < nst; s += 2) {
+    half(s, 0, R0, R1);
+    half(s + 1, 1, R1, R0);
+  }
+  if (s < nst) compute(0);
+
+  // the partial tile: lane (r16, grp) holds rows 4 grp + e of each 16 x 16 block
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int co = co0 + wr * 64 + 16 * i + 4 * grp + e;
+        const int k = k0 + wc * 64 + 16 * j + r16;
+        P.part[((long)split * P.Co + co) * P.K + k] = acc[i][j][e];
+      }
+}
+
+int launch_wgrad_gemm(const WgradLaunch& L, int tiles, hipStream_t s) {
+  hipLaunchKernelGGL(wgrad_gemm_kernel, dim3(tiles), dim3(256), 0, s, L);
+  return (int)hipGetLastError();
+}
+
 }  // namespace pnn

@@ -91,6 +91,7 @@ struct SegP {
 struct WgradGeom {
   int wr, tiles_co, tiles_k, splits, mchunk;
   bool halo3 = false;      // 3x3 / stride 1 / pad 1 through the halo kernel (tiles_k = Cg / 16)
+  bool gemm = false;       // wide 3x3 / stride 1 / pad 1 bf16 through the GEMM kernel (128 x 128 tiles)
 };
 
 }  // namespace
@@ -166,6 +167,22 @@ WgradGeom wgrad_geom_node(const NodeP& n, int B, int es) {
       return g;
     }
   }
+  // wide 3x3 bf16 problems the halo kernel does not take: 128 x 128 GEMM tiles (a tile's 128 filter
+  // columns one tap's channels), split over m in 64-pixel stages into about 512 workgroups (two per
+  // CU), at least 16 stages each
+  if (es == 2 && n.k == 3 && n.stride == 1 && n.pad == 1 && n.H == n.Ho && n.W == n.Wo && n.cin % 128 == 0 &&
+      n.cout % 128 == 0 && M < (1L << 22)) {
+    WgradGeom g;
+    g.gemm = true;
+    g.wr = 0;
+    g.tiles_co = n.cout / 128;
+    g.tiles_k = K / 128;
+    const long base = (long)g.tiles_co * g.tiles_k;
+    const long splits = std::max(1L, std::min(cdiv(M, 16L * 64), cdiv(512, base)));
+    g.mchunk = (int)(cdiv(cdiv(M, splits), 64) * 64);
+    g.splits = (int)cdiv(M, g.mchunk);
+    return g;
+  }
   return wgrad_geom(n.cout, K, M);
 }
 
@@ -228,7 +245,7 @@ long wgrad_fused_rows(const SegP& S, const NodeP& n, int B, int es) {
   else
     return 0;
   const WgradGeom g = wgrad_geom_node(n, B, es);
-  return !g.halo3 && tiles_m <= g.splits ? tiles_m : 0;
+  return !g.halo3 && !g.gemm && tiles_m <= g.splits ? tiles_m : 0;
 }
 
 pnn_status build_segment(const pnn_segment_desc& d, int part, int index, int B, int es, SegP& S) {
@@ -1219,7 +1236,7 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
   pnn_plan* plan = c.plan;
   const int B = plan->B, es = plan->es;
   char* wpart = c.wpart != nullptr ? c.wpart : c.scratch + plan->wpart_off;
-  std::vector<WgradProb> wg_vec, wg_gen, wg_h3, wg_pw;
+  std::vector<WgradProb> wg_vec, wg_gen, wg_h3, wg_pw, wg_gemm;
   size_t woff = 0;
   for (size_t i = 0; i < segs.size(); ++i) {
     const SegP& S = *segs[i];
@@ -1250,7 +1267,7 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
       } else {
         const bool vec = n.cin % (16 / es) == 0;
         const bool pw = vec && n.k == 1 && n.stride == 1 && n.pad == 0;
-        (g.halo3 ? wg_h3 : pw ? wg_pw : vec ? wg_vec : wg_gen).push_back(p);
+        (g.gemm ? wg_gemm : g.halo3 ? wg_h3 : pw ? wg_pw : vec ? wg_vec : wg_gen).push_back(p);
       }
       ColRedProb r;
       std::memset(&r, 0, sizeof(r));
@@ -1263,8 +1280,8 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
       red.push_back(r);
     }
   }
-  for (int v = 0; v < 4; ++v) {
-    auto& list = v == 0 ? wg_vec : v == 1 ? wg_gen : v == 2 ? wg_h3 : wg_pw;
+  for (int v = 0; v < 5; ++v) {
+    auto& list = v == 0 ? wg_vec : v == 1 ? wg_gen : v == 2 ? wg_h3 : v == 3 ? wg_pw : wg_gemm;
     int e = grouped<WgradLaunch>(
         list, [](const WgradProb& p) { return p.tiles_co * p.tiles_k * p.splits; },
         [&](const WgradLaunch& Lx, int tiles, size_t) {
@@ -1275,9 +1292,10 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
             by += (double)p.M * p.Co * es + (double)p.B * p.H * p.W * p.Cg * es + (double)p.Co * p.K * 4;
           }
           Timer t(plan, 2, c.stream);
-          int e2 = v == 2 ? launch_wgrad3(Lx, tiles, plan->dtype, c.stream)
-                          : launch_wgrad(Lx, tiles, plan->dtype, v == 0 ? WG_VEC : v == 1 ? WG_GEN : WG_PW,
-                                         c.stream);
+          int e2 = v == 2   ? launch_wgrad3(Lx, tiles, plan->dtype, c.stream)
+                   : v == 4 ? launch_wgrad_gemm(Lx, tiles, c.stream)
+                            : launch_wgrad(Lx, tiles, plan->dtype, v == 0 ? WG_VEC : v == 1 ? WG_GEN : WG_PW,
+                                           c.stream);
           t.done(c.stream, fl, by);
           return e2;
         });

@@ -320,6 +320,9 @@ constexpr size_t GEMM_KPART_BYTES = (size_t)GEMM_SPLIT_WG * GEMM_BM * GEMM_BN * 
 // filter taps (Cg a multiple of the chunk), or pointwise (1x1 / stride 1 / pad 0: input row m)
 enum { WG_GEN = 0, WG_VEC = 1, WG_PW = 2 };
 int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, int gather, hipStream_t s);
+// wide 3x3 / stride 1 / pad 1 bf16 weight gradients (C_in, C_out multiples of 128) as 128 x 128 GEMM
+// tiles over the pixels (k_gemm.hip); tiles_co = C_out / 128, tiles_k = 9 C_in / 128
+int launch_wgrad_gemm(const WgradLaunch& L, int tiles, hipStream_t s);
 // Streaming pointwise convolution of narrow problems (1x1 / stride 1 / pad 0, ncol % 32 != 0,
 // K <= PW_MAXK): FWD with an optional BN prologue and EPI_STATS (no residual or addend); BWD with
 // EPI_BN_MASK.  16-column workgroup tiles; wm = tiles of PW_TR rows per workgroup;
