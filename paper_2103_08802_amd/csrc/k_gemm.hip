@@ -431,30 +431,50 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
   const bool prologue = P.pro != nullptr;
   if (tid < WGM_T) pro_s[tid] = prologue ? make_float2(P.pro[c0 + tid], P.pro[P.Cg + c0 + tid]) : make_float2(1.f, 0.f);
 
-  // loader: chunk h (< 4) of a stage is row lrow + 16 h, 16-byte column lcol
+  // loader: chunk h (< 4) of a stage is row lrow + 16 h, 16-byte column lcol.  Stride 1 and equal
+  // maps: the input pixel of output pixel m at the tap is m + dr W + dc; the row's (p, q) in its
+  // image, needed only for the in-image test, advance by WGM_KC pixels a stage as a mixed-radix count
   const int lcol = (tid & 15) * VE, lrow = tid >> 4;
   const int PQ = P.P * P.Q;
-  const float rPQ = 1.0f / (float)PQ, rQ = 1.0f / (float)P.Q;
   const T* gbase = (const T*)P.g + co0 + lcol;
   const T* ibase = (const T*)P.in + c0 + lcol;
+  const int toff = dr * P.W + dc;
+  const int sq = WGM_KC % P.Q, sp = (WGM_KC / P.Q) % P.P;    // a stage's step in (p, q)
+  int rp[4], rqq[4];
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
+    int n, pix;
+    divmod_small(m_begin + lrow + 16 * h, PQ, 1.0f / (float)PQ, n, pix);
+    divmod_small(pix, P.Q, 1.0f / (float)P.Q, rp[h], rqq[h]);
+  }
+  int lstage = 0;                                            // the stage (rp, rqq) describe
   struct Set {
     uint4 g[4], a[4];
     unsigned ok;       // bit h: row h's gradient exists; bit 4 + h: its input pixel exists
   };
   auto load = [&](int s, Set& R) {
-    const int mc = m_begin + (s < nst ? s : nst - 1) * WGM_KC;   // past the end: a repeat, masked
+    const int sc = s < nst ? s : nst - 1;                    // past the end: a repeat, masked
+    if (sc != lstage) {                                      // (stages are loaded in order)
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        int q = rqq[h] + sq, p = rp[h] + sp;
+        if (q >= P.Q) { q -= P.Q; ++p; }
+        if (p >= P.P) p -= P.P;
+        rqq[h] = q;
+        rp[h] = p;
+      }
+      lstage = sc;
+    }
+    const int mc = m_begin + sc * WGM_KC;
     R.ok = 0;
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
       const int m = mc + lrow + 16 * h;
       const bool vm = s < nst && m < m_end;
-      int n, pix, p, q;
-      divmod_small(vm ? m : 0, PQ, rPQ, n, pix);
-      divmod_small(pix, P.Q, rQ, p, q);
-      const int ih = p + dr, iw = q + dc;
+      const int ih = rp[h] + dr, iw = rqq[h] + dc;
       const bool vi = vm && (unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W;
       R.g[h] = *(const uint4*)(gbase + (vm ? (long)m * P.Co : 0));
-      R.a[h] = *(const uint4*)(ibase + (vi ? (((long)n * P.H + ih) * P.W + iw) * P.Cg : 0));
+      R.a[h] = *(const uint4*)(ibase + (vi ? (long)(m + toff) * P.Cg : 0));
       R.ok |= (vm ? 1u : 0u) << h | (vi ? 1u : 0u) << (4 + h);
     }
   };
