@@ -25,40 +25,53 @@ namespace {
 constexpr int GM = GEMM_BM, GN = GEMM_BN, GKS = GEMM_BK;   // tile rows, columns; K per step
 constexpr int GAS = GKS + 8;                          // LDS row stride of an operand tile (bf16)
 constexpr int GLDA = GN + 4;                          // row stride of the staged fp32 tile
-constexpr int GOPS = GM * GAS + GN * GAS;             // bf16 elements of one stage (A then B)
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int GSMEM = 2 * GOPS * 2 > GM * GLDA * 4 ? 2 * GOPS * 2 : GM * GLDA * 4;   // bytes: stages | staging
 constexpr int GCH = GKS / 8;                          // 16-byte chunks per operand row and step
 constexpr int GLR = 256 / GCH;                        // rows per loader pass
 constexpr int GLP = GM / GLR;                         // loader passes (chunks per thread and operand)
 static_assert(GM == 128 && GN == 128 && GM % GLR == 0, "gemm tile: four waves of 64 x 64");
 
+// the tile geometry of a column-tile width TN (128: four waves of 64 x 64; 64: four waves of 32 x 64)
+template <int TN>
+struct GemmTile {
+  static constexpr int OPS = GM * GAS + TN * GAS;     // bf16 elements of one stage (A then B)
+  static constexpr int LDA = TN + 4;                  // row stride of the staged fp32 tile
+  static constexpr int SMEM = 2 * OPS * 2 > GM * LDA * 4 ? 2 * OPS * 2 : GM * LDA * 4;   // bytes
+  static constexpr int LPB = TN / GLR;                // loader passes of the filter rows
+  static constexpr int WROWS = TN == 128 ? 64 : 32;   // rows per wave
+  static constexpr int MI = WROWS / 32;               // 32-row MFMA blocks per wave
+  static_assert(TN == 128 || TN == 64, "column tile");
+};
+
 }  // namespace
 
-// Problems: 3x3, stride 1, pad 1, output grid = input grid, Cg % GKS == 0, ncol % 128 == 0, bf16.
-template <int MODE>
+// Problems: 3x3, stride 1, pad 1, output grid = input grid, Cg % GKS == 0, ncol % TN == 0, bf16
+// (TN = 64: ncol of 64 columns, never split along K).
+template <int MODE, int TN>
 __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
   using T = uint16_t;
+  using G = GemmTile<TN>;
   constexpr int VE = 8;
-  __shared__ __attribute__((aligned(16))) float smem[GSMEM / 4];
+  constexpr int GOPS = G::OPS;
+  __shared__ __attribute__((aligned(16))) float smem[G::SMEM / 4];
   __shared__ __attribute__((aligned(16))) float2 pro_s[CONV_PRO_MAXC];
-  __shared__ __attribute__((aligned(16))) float bn_s[MODE == MODE_BWD ? 7 * GN : 1];
+  __shared__ __attribute__((aligned(16))) float bn_s[MODE == MODE_BWD ? 7 * TN : 1];
   uint16_t* ops = (uint16_t*)smem;
 
   const int gi = find_group(L);
   const ConvProb& P = L.p[gi];
   const int local = blockIdx.x - P.tile_begin;
   const int ntile = P.tiles_m * P.tiles_n;
-  const int ks = P.ksplit > 1 ? P.ksplit : 1;      // workgroups per tile along K
+  const int ks = TN == 128 && P.ksplit > 1 ? P.ksplit : 1;   // workgroups per tile along K
   const int split = local / ntile;
   const int tl = local - split * ntile;
   const int tm = tl / P.tiles_n;
   const int tn = tl - tm * P.tiles_n;
-  const int n0 = tn * GN;
+  const int n0 = tn * TN;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int r32 = lane & 31, kh = lane >> 5;
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = TN == 128 ? wave >> 1 : wave, wc = TN == 128 ? wave & 1 : 0;
   const bool prologue = MODE == MODE_FWD && P.pro != nullptr;
   const bool bnmask = MODE == MODE_BWD && (P.flags & (EPI_BN_MASK | EPI_BN_APPLY));
 
@@ -88,17 +101,17 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
     }
     amask[h] = mk;
   }
-  const T* wrow = (const T*)P.wmat + (long)(n0 + lr) * P.K + 8 * ch;   // ncol % GN == 0: all valid
+  const T* wrow = (const T*)P.wmat + (long)(n0 + lr) * P.K + 8 * ch;   // ncol % TN == 0: all valid
 
   if (prologue)
     for (int c = tid; c < P.Cg; c += 256) pro_s[c] = make_float2(P.pro[c], P.pro[P.Cg + c]);
-  if (bnmask && tid < GN) {
+  if (bnmask && tid < TN) {
     const int col = n0 + tid;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) bn_s[k * GN + tid] = P.bnst[k * P.ncol + col];
+    for (int k = 0; k < 4; ++k) bn_s[k * TN + tid] = P.bnst[k * P.ncol + col];
     if (P.flags & EPI_BN_APPLY) {
 #pragma unroll
-      for (int k = 0; k < 3; ++k) bn_s[(4 + k) * GN + tid] = P.coef[k * P.ncol + col];
+      for (int k = 0; k < 3; ++k) bn_s[(4 + k) * TN + tid] = P.coef[k * P.ncol + col];
     }
   }
 
@@ -112,7 +125,7 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
   const int s_begin = split * ktot / ks;
   const int nsteps = (split + 1) * ktot / ks - s_begin;
   struct Set {
-    uint4 a[GLP], b[GLP];
+    uint4 a[GLP], b[G::LPB];
     unsigned ok;                                   // bit h: row h of A is inside the image
     int c;                                         // channel of the thread's chunk
   };
@@ -135,7 +148,7 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
       R.a[h] = *(const uint4*)(in + (ok ? abase[h] + toff : 0));
     }
 #pragma unroll
-    for (int h = 0; h < GLP; ++h) R.b[h] = *(const uint4*)(wrow + (long)GLR * h * Kt + k0);
+    for (int h = 0; h < G::LPB; ++h) R.b[h] = *(const uint4*)(wrow + (long)GLR * h * Kt + k0);
   };
   // a step's chunks into LDS stage st (prologue: ReLU(x scale + shift) of the stored values;
   // padding and rows past M are zeros of the activated operand)
@@ -165,13 +178,15 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
         w = make_uint4(w.x & keep, w.y & keep, w.z & keep, w.w & keep);
       }
       *(uint4*)(A + (lr + GLR * h) * GAS + 8 * ch) = w;
-      *(uint4*)(Bt + (lr + GLR * h) * GAS + 8 * ch) = R.b[h];
     }
+#pragma unroll
+    for (int h = 0; h < G::LPB; ++h) *(uint4*)(Bt + (lr + GLR * h) * GAS + 8 * ch) = R.b[h];
   };
 
-  f32x16 acc[2][2];
+  constexpr int MI = G::MI;
+  f32x16 acc[MI][2];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -182,15 +197,15 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
     const uint16_t* Bt = A + GM * GAS;
 #pragma unroll
     for (int kk = 0; kk < GKS / 16; ++kk) {
-      bf16x8 a[2], b[2];
+      bf16x8 a[MI], b[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        a[i] = *(const bf16x8*)(A + (wr * 64 + 32 * i + r32) * GAS + 16 * kk + 8 * kh);
+      for (int i = 0; i < MI; ++i)
+        a[i] = *(const bf16x8*)(A + (wr * G::WROWS + 32 * i + r32) * GAS + 16 * kk + 8 * kh);
 #pragma unroll
       for (int j = 0; j < 2; ++j)
         b[j] = *(const bf16x8*)(Bt + (wc * 64 + 32 * j + r32) * GAS + 16 * kk + 8 * kh);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
@@ -221,7 +236,7 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
   if (s < nsteps) compute(0);                      // an odd step count: the last step
   __syncthreads();
 
-  if (ks > 1) {
+  if (TN == 128 && ks > 1) {
     // a split of K: the raw fp32 tile to the partial buffer in the accumulators' own order, one
     // 32 x 32 block after the other (blocks by wave row, wave column, i, j); within a block the
     // float4 of lane l and row group g (rows 8 g + 4 (l / 32) .. + 3 of column l % 32) at g * 64 + l,
@@ -235,22 +250,24 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
 #pragma unroll
         for (int g = 0; g < 4; ++g)
           dst[blk * 256 + g * 64 + lane] =
-              make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+              make_float4(acc[i % MI][j][4 * g], acc[i % MI][j][4 * g + 1], acc[i % MI][j][4 * g + 2],
+                          acc[i % MI][j][4 * g + 3]);
       }
     return;
   }
 
   // stage the fp32 tile: D lane layout of the 32 x 32 MFMA (column r32, rows 8 (e / 4) + 4 kh + e % 4)
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e)
-        smem[(wr * 64 + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3)) * GLDA + wc * 64 + 32 * j + r32] = acc[i][j][e];
+        smem[(wr * G::WROWS + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3)) * G::LDA + wc * 64 + 32 * j + r32] =
+            acc[i][j][e];
 
   // streamed epilogue operands of the thread's chunks (as the other conv kernels)
-  constexpr int ncc = GN / VE, rpp = 256 / ncc, NCH = GM / rpp;
+  constexpr int ncc = TN / VE, rpp = 256 / ncc, NCH = GM / rpp;
   const int cc0 = (tid % ncc) * VE;
   const void* pf = (MODE == MODE_FWD) ? P.res
                    : ((P.flags & EPI_STORE_F32) ? nullptr : (bnmask ? P.zsrc : P.res));
@@ -264,7 +281,7 @@ __global__ __launch_bounds__(256, 2) void gemm_conv_kernel(const ConvLaunch L) {
     pre2[k] = (pf2 != nullptr && m < P.M) ? *(const uint4*)((const T*)pf2 + o) : make_uint4(0, 0, 0, 0);
   }
   __syncthreads();
-  conv_epilogue<T, MODE, GM, GN, GLDA, GN>(P, smem, (float*)pro_s, bn_s, tm, n0, pre, pre2);
+  conv_epilogue<T, MODE, GM, TN, G::LDA, TN>(P, smem, (float*)pro_s, bn_s, tm, n0, pre, pre2);
 }
 
 // Second pass of the split problems: one workgroup per slab of GEMM_RBN = 16 columns of a 128 x 128
@@ -368,11 +385,18 @@ int launch_gemm_reduce(const ConvLaunch& L, int tiles, int mode, hipStream_t s) 
   return (int)hipGetLastError();
 }
 
-int launch_gemm(const ConvLaunch& L, int tiles, int mode, hipStream_t s) {
-  if (mode == MODE_FWD)
-    hipLaunchKernelGGL(gemm_conv_kernel<MODE_FWD>, dim3(tiles), dim3(256), 0, s, L);
-  else
-    hipLaunchKernelGGL(gemm_conv_kernel<MODE_BWD>, dim3(tiles), dim3(256), 0, s, L);
+int launch_gemm(const ConvLaunch& L, int tiles, int mode, int tn, hipStream_t s) {
+  if (tn == 64) {
+    if (mode == MODE_FWD)
+      hipLaunchKernelGGL((gemm_conv_kernel<MODE_FWD, 64>), dim3(tiles), dim3(256), 0, s, L);
+    else
+      hipLaunchKernelGGL((gemm_conv_kernel<MODE_BWD, 64>), dim3(tiles), dim3(256), 0, s, L);
+  } else {
+    if (mode == MODE_FWD)
+      hipLaunchKernelGGL((gemm_conv_kernel<MODE_FWD, 128>), dim3(tiles), dim3(256), 0, s, L);
+    else
+      hipLaunchKernelGGL((gemm_conv_kernel<MODE_BWD, 128>), dim3(tiles), dim3(256), 0, s, L);
+  }
   return (int)hipGetLastError();
 }
 

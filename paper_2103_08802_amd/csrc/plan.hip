@@ -767,7 +767,7 @@ int fire_conv_gk(const Ctx& c, std::vector<ConvProb>& probs, int mode, int gk, i
           by += conv_bytes(L.p[i], plan->es, mode);
         }
         Timer t(plan, 1, c.stream);
-        int e = gk == 4 ? launch_gemm(L, tiles, mode, c.stream)
+        int e = gk >= 4 ? launch_gemm(L, tiles, mode, gk == 5 ? 64 : GEMM_BN, c.stream)
                         : launch_conv(L, tiles, plan->dtype, mode, gk, wn, wm, c.stream);
         t.done(c.stream, fl, by);
         return e;
@@ -789,11 +789,14 @@ bool halo_ok(const ConvProb& p, int es) {
   return nimg * (rows + 2) * (p.Q + 2) * ps * es <= CONV_HALO_BYTES;
 }
 
-// A wide 3x3 / stride 1 / pad 1 bf16 problem for the GEMM kernel: K steps of GEMM_BK channels
-// within one tap, 128-column tiles, 128-row tiles (the tall tiles it would otherwise take).
-bool gemm_ok(const ConvProb& p, int es) {
-  return es == 2 && p.k == 3 && p.stride == 1 && p.pad == 1 && p.H == p.P && p.W == p.Q &&
-         p.Cg % GEMM_BK == 0 && p.Cg <= CONV_PRO_MAXC && p.ncol % GEMM_BN == 0 && 64 * p.wm == GEMM_BM;
+// A 3x3 / stride 1 / pad 1 bf16 problem for the GEMM kernel: K steps of GEMM_BK channels within
+// one tap, 128-row tiles (the tall tiles it would otherwise take), 128-column tiles where ncol
+// allows them, else 64-column ones.  Returns the column tile width, 0 for another kernel.
+int gemm_tn(const ConvProb& p, int es) {
+  if (!(es == 2 && p.k == 3 && p.stride == 1 && p.pad == 1 && p.H == p.P && p.W == p.Q &&
+        p.Cg % GEMM_BK == 0 && p.Cg <= CONV_PRO_MAXC && 64 * p.wm == GEMM_BM))
+    return 0;
+  return p.ncol % GEMM_BN == 0 ? GEMM_BN : p.ncol % 64 == 0 ? 64 : 0;
 }
 
 // K splits of the GEMM problems with fewer than GEMM_SPLIT_BELOW tiles (`small`: their tiles in
@@ -806,27 +809,46 @@ int gemm_split(const ConvProb& q, long small) {
 }
 
 // Gather kind of a convolution problem: 0 pointwise, 1 vector gather, 2 element-wise gather,
-// 3 halo tile, 4 the GEMM kernel.
+// 3 halo tile, 4 the GEMM kernel with 128-column tiles, 5 with 64-column tiles.
 int gather_kind(const ConvProb& p, int es) {
   if (p.Cg % (16 / es) != 0) return 2;
   if (p.k == 1 && p.stride == 1 && p.pad == 0) return 0;
-  if (gemm_ok(p, es)) return 4;
+  const int tn = gemm_tn(p, es);
+  if (tn != 0) return tn == GEMM_BN ? 4 : 5;
   if (halo_ok(p, es)) return 3;
   return 1;
 }
 
 // one grouped launch per (gather kind, column sub-tiles, tall / short tiles)
 int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode) {
-  std::vector<ConvProb> by[5][3][2];
+  std::vector<ConvProb> by[6][3][2];
   for (auto& p : probs) {
     const int w = p.wn == 1 ? 0 : p.wn == 2 ? 1 : 2;
     const int gk = gather_kind(p, c.plan->es);
     ConvProb q = p;
-    if (gk == 4) q.tiles_n = q.ncol / GEMM_BN;
+    if (gk >= 4) q.tiles_n = q.ncol / (gk == 4 ? GEMM_BN : 64);
     by[gk][w][p.wm == conv_wm(p.wn, false) ? 0 : 1].push_back(q);
   }
   // GEMM launches: the longest K first, so that the longest tiles start first; the problems with
   // few tiles split K (their partial tiles in the context's region, summed by a second pass)
+  // 64-column GEMM launches with fewer tiles than compute units run at one tile's latency, where
+  // the halo kernel's tile (its input read once into LDS) is the shorter: those go back to it
+  for (int w = 0; w < 3; ++w)
+    for (int t = 0; t < 2; ++t) {
+      auto& v = by[5][w][t];
+      long tiles = 0;
+      bool halo = true;
+      for (auto& q : v) {
+        tiles += (long)q.tiles_m * q.tiles_n;
+        halo = halo && halo_ok(q, c.plan->es);
+      }
+      if (tiles < GEMM_NARROW_MIN_TILES && halo) {
+        by[3][w][t].insert(by[3][w][t].end(), v.begin(), v.end());
+        v.clear();
+      }
+      std::stable_sort(v.begin(), v.end(), [](const ConvProb& a, const ConvProb& b) { return a.K > b.K; });
+      for (auto& q : v) q.ksplit = 1;
+    }
   long small = 0;
   for (auto& v : by[4])
     for (auto& t : v) {
@@ -852,7 +874,7 @@ int fire_conv(const Ctx& c, std::vector<ConvProb>& probs, int mode) {
         koff += need;
         split.push_back(q);
       }
-  for (int gk = 0; gk < 5; ++gk)
+  for (int gk = 0; gk < 6; ++gk)
     for (int w = 0; w < 3; ++w)
       for (int t = 0; t < 2; ++t) {
         if (by[gk][w][t].empty()) continue;

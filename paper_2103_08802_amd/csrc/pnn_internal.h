@@ -305,11 +305,12 @@ int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int
 // tiles of 64-column problems, so BN partial rows do not depend on which kernel runs a problem
 constexpr int GEMM_BM = 128, GEMM_BN = 128, GEMM_BK = 64;
 constexpr int CONV_PRO_MAXC = 512;     // largest Cg of a forward BN prologue held in LDS
-int launch_gemm(const ConvLaunch& L, int tiles, int mode, hipStream_t s);
+int launch_gemm(const ConvLaunch& L, int tiles, int mode, int tn, hipStream_t s);   // tn: 128 or 64
 // the split problems' second pass: partial tiles summed in split order, then the epilogue, one
 // workgroup per GEMM_RBN-column slab of a tile
 int launch_gemm_reduce(const ConvLaunch& L, int tiles, int mode, hipStream_t s);
 constexpr int GEMM_RBN = 16;
+constexpr int GEMM_NARROW_MIN_TILES = 256;   // fewest tiles of a 64-column GEMM launch (else: halo kernel)
 constexpr int GEMM_SPLIT_BELOW = 128;          // tiles of a problem below which its K is split
 constexpr int GEMM_SPLIT_WG = 256;             // workgroups a split problem aims at (one per CU)
 constexpr int GEMM_MAX_SPLIT = 16;
