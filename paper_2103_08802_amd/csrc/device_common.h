@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "pnn_internal.h"
+
 namespace pnn {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -118,18 +120,29 @@ __device__ __forceinline__ void mma(const Frag<float>& a, const Frag<float>& b, 
   for (int e = 0; e < 4; ++e) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[e], b.v[e], acc, 0, 0, 0);
 }
 
-// Problem of this workgroup in a grouped launch: the last p with p.tile_begin <= blockIdx.x
-// (tile_begin is non-decreasing; problems without tiles share the next one's begin).
+// Problem of this workgroup in a grouped launch: the last p whose first workgroup is <= blockIdx.x,
+// by binary search.  With the table, the search reads one line of it (16 problems per 64 bytes)
+// where a search over the problem records misses the scalar cache at every step.
 template <typename Launch>
 __device__ __forceinline__ int find_group(const Launch& L) {
   const int t = blockIdx.x;
-  int lo = 0, hi = L.n - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (L.p[mid].tile_begin <= t) lo = mid;
-    else hi = mid - 1;
+  if constexpr (HasTb<Launch>::value) {
+    int lo = 0, hi = L.tb[0] - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (L.tb[mid] <= t) lo = mid;
+      else hi = mid - 1;
+    }
+    return lo;
+  } else {
+    int lo = 0, hi = L.n - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (L.p[mid].tile_begin <= t) lo = mid;
+      else hi = mid - 1;
+    }
+    return lo;
   }
-  return lo;
 }
 
 // x / d and x % d for a divisor given with log2(d) (>= 0) or as a plain value (lg < 0)

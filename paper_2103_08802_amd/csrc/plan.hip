@@ -705,8 +705,13 @@ int grouped(std::vector<Prob>& probs, TilesOf tiles_of, Fire fire) {
       Prob pr = probs[i];
       pr.tile_begin = tiles;
       tiles += tiles_of(pr);
+      if constexpr (HasTb<Launch>::value) L.tb[L.n] = pr.tile_begin;
       L.p[L.n++] = pr;
       ++i;
+    }
+    if constexpr (HasTb<Launch>::value) {
+      static_assert(sizeof(L.tb) / sizeof(L.tb[0]) == sizeof(L.p) / sizeof(L.p[0]), "lookup table per problem");
+      L.tb[0] = L.n;   // (the first problem begins at 0: the entry holds the count)
     }
     if (tiles > 0) {
       int e = fire(L, tiles, first);

@@ -11,6 +11,9 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 struct pnn_plan;
 
 #define PNN_MAXG 20
@@ -75,7 +78,13 @@ struct ConvProb {
   int q_log2, pq_log2;  // log2(Q), log2(P*Q) when powers of two, else -1
   int tile_begin;
 };
+// Launch records that open with a lookup table tb (tb[0]: problem count; tb[p], p >= 1: first
+// workgroup of problem p, non-decreasing, problems without tiles sharing the next one's begin)
+template <typename L, typename = void> struct HasTb : std::false_type {};
+template <typename L> struct HasTb<L, std::void_t<decltype(std::declval<L>().tb)>> : std::true_type {};
+
 struct ConvLaunch {
+  int tb[PNN_MAXG];   // [0]: problem count; [p >= 1]: first workgroup of problem p (the lookup table)
   int n;
   ConvProb p[PNN_MAXG];
 };
@@ -93,6 +102,7 @@ struct WgradProb {
   int tile_begin;
 };
 struct WgradLaunch {
+  int tb[PNN_MAXG];   // [0]: problem count; [p >= 1]: first workgroup of problem p (the lookup table)
   int n;
   WgradProb p[PNN_MAXG];
 };
@@ -122,6 +132,7 @@ struct ColRedProb {
   int tile_begin;
 };
 struct ColRedLaunch {
+  int tb[40];   // [0]: problem count; [p >= 1]: first workgroup of problem p (the lookup table)
   int n;
   ColRedProb p[40];
 };
@@ -151,6 +162,7 @@ struct ColStatProb {
   int tile_begin;
 };
 struct ColStatLaunch {
+  int tb[PNN_MAXG];   // [0]: problem count; [p >= 1]: first workgroup of problem p (the lookup table)
   int n;
   ColStatProb p[PNN_MAXG];
 };
@@ -168,6 +180,7 @@ struct BnApplyProb {
   int tile_begin;
 };
 struct BnApplyLaunch {
+  int tb[60];   // [0]: problem count; [p >= 1]: first workgroup of problem p (the lookup table)
   int n;
   BnApplyProb p[60];
 };
@@ -188,6 +201,7 @@ struct BnActProb {
   int tile_begin;
 };
 struct BnActLaunch {
+  int tb[PNN_MAXG];   // [0]: problem count; [p >= 1]: first workgroup of problem p (the lookup table)
   int n;
   BnActProb p[PNN_MAXG];
 };
@@ -201,6 +215,7 @@ struct MaxPool3Prob {     // 256 * ve outputs per workgroup, ve per thread (1, o
   int tile_begin;
 };
 struct MaxPool3Launch {
+  int tb[PNN_MAXG];   // [0]: problem count; [p >= 1]: first workgroup of problem p (the lookup table)
   int n;
   MaxPool3Prob p[PNN_MAXG];
 };
@@ -211,7 +226,7 @@ struct TransposeProb {   // wt[c][r][s][o] = w[o][r][s][c]; T * ceil(O / 64) * c
   int O, T, C;           // T = k * k taps
   int tile_begin;
 };
-struct TransposeLaunch {
+struct TransposeLaunch {   // (no lookup table: 120 problems fill the argument space)
   int n;
   TransposeProb p[120];
 };
@@ -225,6 +240,7 @@ struct AxpyProb {        // out = a - b (rounded to storage); partial sum of squ
   int tile_begin;
 };
 struct AxpyLaunch {
+  int tb[PNN_MAXG];   // [0]: problem count; [p >= 1]: first workgroup of problem p (the lookup table)
   int n;
   unsigned* flag = nullptr;   // set to 1 when an output is not finite (nullable)
   AxpyProb p[PNN_MAXG];
@@ -297,7 +313,8 @@ int unit_fwd_occupancy();    // workgroups of the resident kernel that fit the d
 // wn: 16-column sub-tiles per wave (1, 2, 4) shared by every problem of the launch
 // every launch record fits the 4 KB of kernel arguments
 static_assert(sizeof(ConvLaunch) <= 4096 && sizeof(WgradLaunch) <= 4096 && sizeof(ColRedLaunch) <= 4096 &&
-              sizeof(UnitLaunch) <= 4096 &&
+              sizeof(UnitLaunch) <= 4096 && sizeof(AxpyLaunch) <= 4096 &&
+              sizeof(ColStatLaunch) <= 4096 && sizeof(BnActLaunch) <= 4096 && sizeof(MaxPool3Launch) <= 4096 &&
               sizeof(BnApplyLaunch) <= 4096 && sizeof(TransposeLaunch) <= 4096 && sizeof(SgdLaunch) <= 4096,
               "kernel argument size");
 int launch_conv(const ConvLaunch& L, int tiles, int dtype, int mode, int gk, int wn, int wm, hipStream_t s);
@@ -355,10 +372,12 @@ struct ZeroProb {
   int tile_begin;
 };
 struct ZeroLaunch {
+  int tb[64];   // [0]: problem count; [p >= 1]: first workgroup of problem p (the lookup table)
   int n;
   ZeroProb p[64];
 };
 constexpr int ZERO_WORDS = 4096;   // words per workgroup
+static_assert(sizeof(ZeroLaunch) <= 4096, "kernel argument size");
 int launch_zero(const ZeroLaunch& L, int tiles, hipStream_t s);
 int launch_bn_apply(const BnApplyLaunch& L, int tiles, int dtype, hipStream_t s);
 int launch_bnact_fwd(const BnActLaunch& L, int tiles, int dtype, hipStream_t s);
