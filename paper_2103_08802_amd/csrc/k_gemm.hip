@@ -403,39 +403,53 @@ int launch_gemm(const ConvLaunch& L, int tiles, int mode, int tn, hipStream_t s)
 // ------------------------------------------------------------------------------------------------
 // Weight gradient of a wide 3x3 / stride 1 / pad 1 bf16 convolution as a GEMM over the output
 // pixels: dW[co][(tap, c)] = sum_m g[m][co] * act(in)[pixel(m) + tap][c] (the weight gradient of the
-// layers of Table vgg), 128 output channels x 128 filter columns (one tap's 128 input channels) per
-// workgroup, split over m.  Stages of 64 pixels: the output-gradient rows and the gathered input
-// rows (BN prologue applied on the way, zeros outside the image) are staged m-major in LDS (rows
-// padded to 144 elements: the four rows of a transposed read fall on distinct banks), read as MFMA
-// fragments with the gfx950 transposed LDS read; four waves of 64 x 64 (4 x 4 16x16x32 MFMAs).
-// Loads run two stages ahead in two register sets; two LDS stages.  The fp32 partial tile goes to
-// part[split][co][K] for the split-K column reduce.
+// layers of Table vgg), TC output channels x TK filter columns (one tap's TK input channels) per
+// workgroup, TC and TK 128 or 64, split over m.  Stages of 64 pixels: the output-gradient rows and
+// the gathered input rows (BN prologue applied on the way, zeros outside the image) are staged
+// m-major in LDS (rows padded by 16 elements: the four rows of a transposed read fall on distinct
+// banks), read as MFMA fragments with the gfx950 transposed LDS read; four waves of
+// (TC / 2) x (TK / 2) (16x16x32 MFMAs).  Loads run two stages ahead in two register sets; two LDS
+// stages.  The fp32 partial tile goes to part[split][co][K] for the split-K column reduce.
 // ------------------------------------------------------------------------------------------------
 namespace {
-constexpr int WGM_T = 128;                  // output channels and filter columns per tile
 constexpr int WGM_KC = 64;                  // pixels per stage
-constexpr int WGM_RS = WGM_T + 16;          // LDS row stride (elements)
-constexpr int WGM_STG = 2 * WGM_KC * WGM_RS;   // elements per LDS stage (gradient, then input)
 
 typedef short wv4s16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) wv4s16 lds_wv4s16;
 
 // the 16x16x32 MFMA fragment of 16 columns (cbase ..) over 8 rows (row0 .. row0 + 7) of an m-major
-// tile: lane group rows 4 (r16 / 4) apart by the transposed read
+// tile of row stride RS: lane group rows 4 (r16 / 4) apart by the transposed read
+template <int RS>
 __device__ __forceinline__ void tr_frag(const uint16_t* base, int row0, int cbase, int r16, Frag<uint16_t>& f) {
-  const uint16_t* p0 = base + (row0 + (r16 >> 2)) * WGM_RS + cbase + 4 * (r16 & 3);
+  const uint16_t* p0 = base + (row0 + (r16 >> 2)) * RS + cbase + 4 * (r16 & 3);
   const wv4s16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_wv4s16*)p0);
-  const wv4s16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_wv4s16*)(p0 + 4 * WGM_RS));
+  const wv4s16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_wv4s16*)(p0 + 4 * RS));
   const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
   f.from_raw(make_uint4(l2.x, l2.y, h2.x, h2.y));
 }
+
+// loader geometry of a W-column m-major operand: 16-byte chunks, 256 threads
+template <int W>
+struct WgmOp {
+  static constexpr int CPR = W / 8;              // chunks per row
+  static constexpr int RPP = 256 / CPR;          // rows per pass
+  static constexpr int NP = WGM_KC / RPP;        // passes per stage
+  static constexpr int RS = W + 16;              // LDS row stride (elements)
+};
 }  // namespace
 
+template <int TC, int TK>
 __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L) {
   using T = uint16_t;
+  using OG = WgmOp<TC>;
+  using OA = WgmOp<TK>;
   constexpr int VE = 8;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * WGM_STG];
-  __shared__ float2 pro_s[WGM_T];
+  constexpr int STG = WGM_KC * (OG::RS + OA::RS);   // elements per LDS stage (gradient, then input)
+  constexpr int NI = TC / 32, NJ = TK / 32;         // 16-row MFMA blocks per wave
+  static_assert(OG::NP <= 4 && OA::NP <= 4 && OG::NP * OG::RPP == WGM_KC && OA::NP * OA::RPP == WGM_KC,
+                "loader");
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * STG];
+  __shared__ float2 pro_s[TK];
   const int gi = find_group(L);
   const WgradProb& P = L.p[gi];
   const int local = blockIdx.x - P.tile_begin;
@@ -443,8 +457,8 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
   const int rest = local / P.tiles_k;
   const int tco = rest % P.tiles_co;
   const int split = rest / P.tiles_co;
-  const int co0 = tco * WGM_T, k0 = tk * WGM_T;
-  const int tap = k0 / P.Cg, c0 = k0 - tap * P.Cg;      // (Cg a multiple of 128)
+  const int co0 = tco * TC, k0 = tk * TK;
+  const int tap = k0 / P.Cg, c0 = k0 - tap * P.Cg;      // (Cg a multiple of TK)
   const int dr = tap / 3 - 1, dc = tap - 3 * (tap / 3) - 1;
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int r16 = lane & 15, grp = lane >> 4;
@@ -453,34 +467,36 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
   const int m_end = min(P.M, m_begin + P.mchunk);
   const int nst = (m_end - m_begin + WGM_KC - 1) / WGM_KC;
   const bool prologue = P.pro != nullptr;
-  if (tid < WGM_T) pro_s[tid] = prologue ? make_float2(P.pro[c0 + tid], P.pro[P.Cg + c0 + tid]) : make_float2(1.f, 0.f);
+  if (tid < TK) pro_s[tid] = prologue ? make_float2(P.pro[c0 + tid], P.pro[P.Cg + c0 + tid]) : make_float2(1.f, 0.f);
 
-  // loader: chunk h (< 4) of a stage is row lrow + 16 h, 16-byte column lcol.  Stride 1 and equal
-  // maps: the input pixel of output pixel m at the tap is m + dr W + dc; the row's (p, q) in its
-  // image, needed only for the in-image test, advance by WGM_KC pixels a stage as a mixed-radix count
-  const int lcol = (tid & 15) * VE, lrow = tid >> 4;
+  // loaders: gradient chunk h of a stage is row lrg + RPP h, 16-byte column lcg; input chunk h row
+  // lra + RPP h, column lca.  Stride 1 and equal maps: the input pixel of output pixel m at the tap is
+  // m + dr W + dc; the input row's (p, q) in its image, needed only for the in-image test, advance by
+  // WGM_KC pixels a stage as a mixed-radix count
+  const int lcg = (tid % OG::CPR) * VE, lrg = tid / OG::CPR;
+  const int lca = (tid % OA::CPR) * VE, lra = tid / OA::CPR;
   const int PQ = P.P * P.Q;
-  const T* gbase = (const T*)P.g + co0 + lcol;
-  const T* ibase = (const T*)P.in + c0 + lcol;
+  const T* gbase = (const T*)P.g + co0 + lcg;
+  const T* ibase = (const T*)P.in + c0 + lca;
   const int toff = dr * P.W + dc;
   const int sq = WGM_KC % P.Q, sp = (WGM_KC / P.Q) % P.P;    // a stage's step in (p, q)
-  int rp[4], rqq[4];
+  int rp[OA::NP], rqq[OA::NP];
 #pragma unroll
-  for (int h = 0; h < 4; ++h) {
-    int n, pix;
-    divmod_small(m_begin + lrow + 16 * h, PQ, 1.0f / (float)PQ, n, pix);
-    divmod_small(pix, P.Q, 1.0f / (float)P.Q, rp[h], rqq[h]);
+  for (int h = 0; h < OA::NP; ++h) {
+    const int pix = (m_begin + lra + OA::RPP * h) % PQ;     // (once per workgroup)
+    rp[h] = pix / P.Q;
+    rqq[h] = pix - rp[h] * P.Q;
   }
   int lstage = 0;                                            // the stage (rp, rqq) describe
   struct Set {
-    uint4 g[4], a[4];
-    unsigned ok;       // bit h: row h's gradient exists; bit 4 + h: its input pixel exists
+    uint4 g[OG::NP], a[OA::NP];
+    unsigned ok;       // bit h: gradient row h exists; bit 4 + h: input row h's pixel exists
   };
   auto load = [&](int s, Set& R) {
     const int sc = s < nst ? s : nst - 1;                    // past the end: a repeat, masked
     if (sc != lstage) {                                      // (stages are loaded in order)
 #pragma unroll
-      for (int h = 0; h < 4; ++h) {
+      for (int h = 0; h < OA::NP; ++h) {
         int q = rqq[h] + sq, p = rp[h] + sp;
         if (q >= P.Q) { q -= P.Q; ++p; }
         if (p >= P.P) p -= P.P;
@@ -492,58 +508,69 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
     const int mc = m_begin + sc * WGM_KC;
     R.ok = 0;
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
-      const int m = mc + lrow + 16 * h;
+    for (int h = 0; h < OG::NP; ++h) {
+      const int m = mc + lrg + OG::RPP * h;
+      const bool vm = s < nst && m < m_end;
+      R.g[h] = *(const uint4*)(gbase + (vm ? (long)m * P.Co : 0));
+      R.ok |= (vm ? 1u : 0u) << h;
+    }
+#pragma unroll
+    for (int h = 0; h < OA::NP; ++h) {
+      const int m = mc + lra + OA::RPP * h;
       const bool vm = s < nst && m < m_end;
       const int ih = rp[h] + dr, iw = rqq[h] + dc;
       const bool vi = vm && (unsigned)ih < (unsigned)P.H && (unsigned)iw < (unsigned)P.W;
-      R.g[h] = *(const uint4*)(gbase + (vm ? (long)m * P.Co : 0));
       R.a[h] = *(const uint4*)(ibase + (vi ? (long)(m + toff) * P.Cg : 0));
-      R.ok |= (vm ? 1u : 0u) << h | (vi ? 1u : 0u) << (4 + h);
+      R.ok |= (vi ? 1u : 0u) << (4 + h);
     }
   };
   auto store = [&](int st, const Set& R) {
-    uint16_t* G = smem + st * WGM_STG;
-    uint16_t* A = G + WGM_KC * WGM_RS;
+    uint16_t* G = smem + st * STG;
+    uint16_t* A = G + WGM_KC * OG::RS;
 #pragma unroll
-    for (int h = 0; h < 4; ++h) {
-      const unsigned kg = 0u - ((R.ok >> h) & 1u), ka = 0u - ((R.ok >> (4 + h)) & 1u);
+    for (int h = 0; h < OG::NP; ++h) {
+      const unsigned kg = 0u - ((R.ok >> h) & 1u);
+      const int o = (lrg + OG::RPP * h) * OG::RS + lcg;
+      *(uint2*)(G + o) = make_uint2(R.g[h].x & kg, R.g[h].y & kg);
+      *(uint2*)(G + o + 4) = make_uint2(R.g[h].z & kg, R.g[h].w & kg);
+    }
+#pragma unroll
+    for (int h = 0; h < OA::NP; ++h) {
+      const unsigned ka = 0u - ((R.ok >> (4 + h)) & 1u);
       uint4 w = R.a[h];
       if (prologue) {
         Chunk<T> v;
         unpack_chunk<T>(w, v);
         float f[VE];
 #pragma unroll
-        for (int e = 0; e < VE; ++e) f[e] = fmaxf(fmaf(v.v[e], pro_s[lcol + e].x, pro_s[lcol + e].y), 0.0f);
+        for (int e = 0; e < VE; ++e) f[e] = fmaxf(fmaf(v.v[e], pro_s[lca + e].x, pro_s[lca + e].y), 0.0f);
         store_chunk<T>(&w, 0, f);
       }
-      const int o = (lrow + 16 * h) * WGM_RS + lcol;
-      *(uint2*)(G + o) = make_uint2(R.g[h].x & kg, R.g[h].y & kg);
-      *(uint2*)(G + o + 4) = make_uint2(R.g[h].z & kg, R.g[h].w & kg);
+      const int o = (lra + OA::RPP * h) * OA::RS + lca;
       *(uint2*)(A + o) = make_uint2(w.x & ka, w.y & ka);
       *(uint2*)(A + o + 4) = make_uint2(w.z & ka, w.w & ka);
     }
   };
-  f32x4 acc[4][4];
+  f32x4 acc[NI][NJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto compute = [&](int st) {
-    const uint16_t* G = smem + st * WGM_STG;
-    const uint16_t* A = G + WGM_KC * WGM_RS;
+    const uint16_t* G = smem + st * STG;
+    const uint16_t* A = G + WGM_KC * OG::RS;
 #pragma unroll
     for (int sub = 0; sub < WGM_KC / 32; ++sub) {
       const int row0 = sub * 32 + VE * grp;
-      Frag<T> a[4], b[4];
+      Frag<T> a[NI], b[NJ];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) tr_frag(G, row0, wr * 64 + 16 * i, r16, a[i]);
+      for (int i = 0; i < NI; ++i) tr_frag<OG::RS>(G, row0, wr * (TC / 2) + 16 * i, r16, a[i]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) tr_frag(A, row0, wc * 64 + 16 * j, r16, b[j]);
+      for (int j = 0; j < NJ; ++j) tr_frag<OA::RS>(A, row0, wc * (TK / 2) + 16 * j, r16, b[j]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < NI; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) mma(a[i], b[j], acc[i][j]);
+        for (int j = 0; j < NJ; ++j) mma(a[i], b[j], acc[i][j]);
     }
   };
 
@@ -570,19 +597,28 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
 
   // the partial tile: lane (r16, grp) holds rows 4 grp + e of each 16 x 16 block
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int co = co0 + wr * 64 + 16 * i + 4 * grp + e;
-        const int k = k0 + wc * 64 + 16 * j + r16;
+        const int co = co0 + wr * (TC / 2) + 16 * i + 4 * grp + e;
+        const int k = k0 + wc * (TK / 2) + 16 * j + r16;
         P.part[((long)split * P.Co + co) * P.K + k] = acc[i][j][e];
       }
 }
 
-int launch_wgrad_gemm(const WgradLaunch& L, int tiles, hipStream_t s) {
-  hipLaunchKernelGGL(wgrad_gemm_kernel, dim3(tiles), dim3(256), 0, s, L);
+int launch_wgrad_gemm(const WgradLaunch& L, int tiles, int tc, int tk, hipStream_t s) {
+  if (tc == 128 && tk == 128)
+    hipLaunchKernelGGL((wgrad_gemm_kernel<128, 128>), dim3(tiles), dim3(256), 0, s, L);
+  else if (tc == 128 && tk == 64)
+    hipLaunchKernelGGL((wgrad_gemm_kernel<128, 64>), dim3(tiles), dim3(256), 0, s, L);
+  else if (tc == 64 && tk == 128)
+    hipLaunchKernelGGL((wgrad_gemm_kernel<64, 128>), dim3(tiles), dim3(256), 0, s, L);
+  else if (tc == 64 && tk == 64)
+    hipLaunchKernelGGL((wgrad_gemm_kernel<64, 64>), dim3(tiles), dim3(256), 0, s, L);
+  else
+    return (int)hipErrorInvalidValue;
   return (int)hipGetLastError();
 }
 

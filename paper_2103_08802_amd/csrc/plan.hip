@@ -91,7 +91,8 @@ struct SegP {
 struct WgradGeom {
   int wr, tiles_co, tiles_k, splits, mchunk;
   bool halo3 = false;      // 3x3 / stride 1 / pad 1 through the halo kernel (tiles_k = Cg / 16)
-  bool gemm = false;       // wide 3x3 / stride 1 / pad 1 bf16 through the GEMM kernel (128 x 128 tiles)
+  bool gemm = false;       // wide 3x3 / stride 1 / pad 1 bf16 through the GEMM kernel
+  int gtc = 0, gtk = 0;    // its tile: output channels, filter columns (128 or 64)
 };
 
 }  // namespace
@@ -167,16 +168,18 @@ WgradGeom wgrad_geom_node(const NodeP& n, int B, int es) {
       return g;
     }
   }
-  // wide 3x3 bf16 problems the halo kernel does not take: 128 x 128 GEMM tiles (a tile's 128 filter
-  // columns one tap's channels), split over m in 64-pixel stages into about 512 workgroups (two per
-  // CU), at least 16 stages each
-  if (es == 2 && n.k == 3 && n.stride == 1 && n.pad == 1 && n.H == n.Ho && n.W == n.Wo && n.cin % 128 == 0 &&
-      n.cout % 128 == 0 && M < (1L << 22)) {
+  // wide 3x3 bf16 problems the halo kernel does not take: GEMM tiles of 128 (else 64) output
+  // channels x 128 (else 64) filter columns (one tap's channels), split over m in 64-pixel stages
+  // into about 512 workgroups (two per CU), at least 16 stages each
+  if (es == 2 && n.k == 3 && n.stride == 1 && n.pad == 1 && n.H == n.Ho && n.W == n.Wo && n.cin % 64 == 0 &&
+      n.cout % 64 == 0 && M < (1L << 30)) {
     WgradGeom g;
     g.gemm = true;
     g.wr = 0;
-    g.tiles_co = n.cout / 128;
-    g.tiles_k = K / 128;
+    g.gtc = n.cout % 128 == 0 ? 128 : 64;
+    g.gtk = n.cin % 128 == 0 ? 128 : 64;
+    g.tiles_co = n.cout / g.gtc;
+    g.tiles_k = K / g.gtk;
     const long base = (long)g.tiles_co * g.tiles_k;
     const long splits = std::max(1L, std::min(cdiv(M, 16L * 64), cdiv(512, base)));
     g.mchunk = (int)(cdiv(cdiv(M, splits), 64) * 64);
@@ -1281,6 +1284,7 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
       p.K = n.k * n.k * n.cin;
       WgradGeom g = wgrad_geom_node(n, B, es);
       p.wr = g.wr; p.tiles_co = g.tiles_co; p.tiles_k = g.tiles_k; p.splits = g.splits; p.mchunk = g.mchunk;
+      p.gtc = g.gtc; p.gtk = g.gtk;
       p.cg_log2 = log2_or(p.Cg);
       p.q_log2 = log2_or(p.Q);
       p.pq_log2 = log2_or(p.P * p.Q);
@@ -1307,8 +1311,11 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
       red.push_back(r);
     }
   }
-  for (int v = 0; v < 5; ++v) {
-    auto& list = v == 0 ? wg_vec : v == 1 ? wg_gen : v == 2 ? wg_h3 : v == 3 ? wg_pw : wg_gemm;
+  // the GEMM problems by tile shape (one launch per shape)
+  std::vector<WgradProb> wg_gemm_by[4];
+  for (const WgradProb& p : wg_gemm) wg_gemm_by[(p.gtc == 128 ? 0 : 2) + (p.gtk == 128 ? 0 : 1)].push_back(p);
+  for (int v = 0; v < 8; ++v) {
+    auto& list = v == 0 ? wg_vec : v == 1 ? wg_gen : v == 2 ? wg_h3 : v == 3 ? wg_pw : wg_gemm_by[v - 4];
     int e = grouped<WgradLaunch>(
         list, [](const WgradProb& p) { return p.tiles_co * p.tiles_k * p.splits; },
         [&](const WgradLaunch& Lx, int tiles, size_t) {
@@ -1320,7 +1327,7 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
           }
           Timer t(plan, 2, c.stream);
           int e2 = v == 2   ? launch_wgrad3(Lx, tiles, plan->dtype, c.stream)
-                   : v == 4 ? launch_wgrad_gemm(Lx, tiles, c.stream)
+                   : v >= 4 ? launch_wgrad_gemm(Lx, tiles, Lx.p[0].gtc, Lx.p[0].gtk, c.stream)
                             : launch_wgrad(Lx, tiles, plan->dtype, v == 0 ? WG_VEC : v == 1 ? WG_GEN : WG_PW,
                                            c.stream);
           t.done(c.stream, fl, by);

@@ -97,6 +97,7 @@ struct WgradProb {
   float* part;          // [splits][Co][K] float
   int B, H, W, Cg, P, Q, Co, k, stride, pad, M, K;
   int wr;               // tile = (16 wr) output channels x 64 filter columns
+  int gtc, gtk;         // GEMM kernel tile: output channels, filter columns (128 or 64 each)
   int tiles_co, tiles_k, splits, mchunk;
   int cg_log2, q_log2, pq_log2;   // as in ConvProb
   int tile_begin;
@@ -340,7 +341,7 @@ enum { WG_GEN = 0, WG_VEC = 1, WG_PW = 2 };
 int launch_wgrad(const WgradLaunch& L, int tiles, int dtype, int gather, hipStream_t s);
 // wide 3x3 / stride 1 / pad 1 bf16 weight gradients (C_in, C_out multiples of 128) as 128 x 128 GEMM
 // tiles over the pixels (k_gemm.hip); tiles_co = C_out / 128, tiles_k = 9 C_in / 128
-int launch_wgrad_gemm(const WgradLaunch& L, int tiles, hipStream_t s);
+int launch_wgrad_gemm(const WgradLaunch& L, int tiles, int tc, int tk, hipStream_t s);   // tc, tk: 128 or 64
 // Streaming pointwise convolution of narrow problems (1x1 / stride 1 / pad 0, ncol % 32 != 0,
 // K <= PW_MAXK): FWD with an optional BN prologue and EPI_STATS (no residual or addend); BWD with
 // EPI_BN_MASK.  16-column workgroup tiles; wm = tiles of PW_TR rows per workgroup;
