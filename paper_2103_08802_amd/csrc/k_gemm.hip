@@ -435,6 +435,7 @@ struct WgmOp {
   static constexpr int RPP = 256 / CPR;          // rows per pass
   static constexpr int NP = WGM_KC / RPP;        // passes per stage
   static constexpr int RS = W + 16;              // LDS row stride (elements)
+  static_assert(RS * 2 % 16 == 0, "16-byte aligned rows");
 };
 }  // namespace
 
@@ -530,9 +531,8 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
 #pragma unroll
     for (int h = 0; h < OG::NP; ++h) {
       const unsigned kg = 0u - ((R.ok >> h) & 1u);
-      const int o = (lrg + OG::RPP * h) * OG::RS + lcg;
-      *(uint2*)(G + o) = make_uint2(R.g[h].x & kg, R.g[h].y & kg);
-      *(uint2*)(G + o + 4) = make_uint2(R.g[h].z & kg, R.g[h].w & kg);
+      const int o = (lrg + OG::RPP * h) * OG::RS + lcg;     // (rows 16-byte aligned: 16-byte writes)
+      *(uint4*)(G + o) = make_uint4(R.g[h].x & kg, R.g[h].y & kg, R.g[h].z & kg, R.g[h].w & kg);
     }
 #pragma unroll
     for (int h = 0; h < OA::NP; ++h) {
@@ -547,8 +547,7 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
         store_chunk<T>(&w, 0, f);
       }
       const int o = (lra + OA::RPP * h) * OA::RS + lca;
-      *(uint2*)(A + o) = make_uint2(w.x & ka, w.y & ka);
-      *(uint2*)(A + o + 4) = make_uint2(w.z & ka, w.w & ka);
+      *(uint4*)(A + o) = make_uint4(w.x & ka, w.y & ka, w.z & ka, w.w & ka);
     }
   };
   f32x4 acc[NI][NJ];
