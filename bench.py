@@ -67,10 +67,14 @@ def cpu_baseline(idx, batch=24, coarse="config"):
 # sources a kernel family's code and launch shapes come from; a stored traffic figure is void
 # once any of them changes
 KERNEL_SOURCES = {
-    "conv_kernel": ["k_conv.hip", "conv_epilogue.h", "bn_fuse.h", "device_common.h", "pnn_internal.h", "plan.hip"],
+    "conv_kernel": ["k_conv.hip", "k_gemm.hip", "conv_epilogue.h", "bn_fuse.h", "device_common.h", "pnn_internal.h",
+                    "plan.hip"],
     "wgrad_kernel": ["k_conv.hip", "device_common.h", "pnn_internal.h", "plan.hip"],
 }
 COPY_BYTES = 256 << 20          # the --copy-calibration copy
+# the kernels of a family: the launches the library's timing family covers (conv: every forward
+# and data-gradient convolution launch, the GEMM kernel's and its split-K reduce's included)
+FAMILY_KERNELS = {"conv_kernel": ("conv_kernel", "gemm_conv_kernel", "gemm_reduce_kernel")}
 
 
 def _sources_sha(kernel):
@@ -131,10 +135,13 @@ def summarize_pmc(fetch_csv, write_csv, kernel, cmd):
     fe, fcopy = load(fetch_csv)
     wr, wcopy = load(write_csv)
     ffac, wfac = COPY_BYTES / fcopy, COPY_BYTES / wcopy
+    names = FAMILY_KERNELS.get(kernel, (kernel,))
+    fe = {kernel: [v for n in names for v in fe.get(n, [])]}
+    wr = {kernel: [v for n in names for v in wr.get(n, [])]}
     fb = sum(fe[kernel]) / len(fe[kernel]) * ffac
     wb = sum(wr[kernel]) / len(wr[kernel]) * wfac
     rec = {"kernel": kernel, "bytes_per_launch": round(fb + wb), "fetch_bytes_per_launch": round(fb),
-           "write_bytes_per_launch": round(wb), "dispatches": len(fe[kernel]),
+           "write_bytes_per_launch": round(wb), "dispatches": len(fe[kernel]), "family_kernels": list(names),
            "fetch_scale": round(ffac, 4), "write_scale": round(wfac, 4),
            "calibration": f"one {COPY_BYTES >> 20} MiB device-to-device copy reads and writes "
                           f"{COPY_BYTES} bytes; FETCH_SIZE read {fcopy:.0f}, WRITE_SIZE {wcopy:.0f}",
@@ -248,14 +255,17 @@ def summarize_mfma(csv_path, out_md, algo_flops, cmd, title="parareal ResNet-100
                  "|---|---:|---:|---:|---:|\n")
         for n, (c, uw, t, fl) in rows:
             fh.write(f"| `{n}` | {c} | {uw / t:.2f} | {fl / c / 1e9:.3f} | {fl / (t * 1e-6) / 1e12:.1f} |\n")
-        if "conv_kernel" in fams:
-            c, uw, t, fl = fams["conv_kernel"]
+        members = [fams[n] for n in FAMILY_KERNELS["conv_kernel"] if n in fams]
+        if members and algo_flops:      # the record: the workload whose algorithmic FLOPs are given
+            c, uw, t, fl = (sum(m[i] for m in members) for i in range(4))
+            fh.write(f"| conv family ({' + '.join(FAMILY_KERNELS['conv_kernel'])}) | {c} | {uw / t:.2f} | "
+                     f"{fl / c / 1e9:.3f} | {fl / (t * 1e-6) / 1e12:.1f} |\n")
             rec = {"kernel": "conv_kernel", "mfma_util_pct": round(uw / t, 3),
                    "mfma_flops_per_launch": round(fl / c), "dispatches": c}
             if algo_flops:
                 rec["algorithmic_flops_per_launch"] = algo_flops
                 rec["mfma_over_algorithmic"] = round(fl / c / algo_flops, 4)
-                fh.write(f"\nconv_kernel: {fl / c / 1e9:.3f} GFLOP of bf16 MFMA work per launch against "
+                fh.write(f"\nconv family: {fl / c / 1e9:.3f} GFLOP of bf16 MFMA work per launch against "
                          f"{algo_flops / 1e9:.3f} GFLOP algorithmic (2 M N K of the launch's problems, "
                          f"bench line): ratio {fl / c / algo_flops:.3f} (padding of K to the "
                          "instruction's 32 and of ragged row tiles).\n")
@@ -327,6 +337,11 @@ def summarize_trace(stats_csv, trace_csv, out_md, title, cmd):
         if steps:
             f.write(f"\n{steps} steps in the run (one head launch each): {lib / steps:.0f} library kernel "
                     "launches per step (torch fills and copies excluded).\n")
+        cf = [fam[n] for n in FAMILY_KERNELS["conv_kernel"] if n in fam]
+        if cf:
+            c, t = sum(x[0] for x in cf), sum(x[1] for x in cf)
+            f.write(f"\nconv family ({' + '.join(FAMILY_KERNELS['conv_kernel'])}: the launches the bench's "
+                    f"conv timing covers): {c} dispatches, {t / c:.2f} us on average.\n")
         f.write("\nPer instantiation (rocprofv3 --stats):\n\n")
         f.write("| kernel | calls | avg us | min us | max us | total % |\n|---|---:|---:|---:|---:|---:|\n")
         for r in rows[:24]:
@@ -531,7 +546,8 @@ def main():
             "traffic": (stored_traffic(dom) if default_cfg else None),
             "algorithmic_bytes_per_launch": round(d["bytes"] / max(d["launches"], 1)),
             "algorithmic_flops_per_launch": round(d["flops"] / max(d["launches"], 1)),
-            "kernel": dom, "avg_launch_us": round(d["ms"] * 1e3 / max(d["launches"], 1), 2),
+            "kernel": dom, "kernels": list(FAMILY_KERNELS.get(dom, (dom,))),
+            "avg_launch_us": round(d["ms"] * 1e3 / max(d["launches"], 1), 2),
             "hbm_gbs": round(achieved, 1), "mfma_tflops": round(tflops_dom, 2)}
     mf = stored_mfma(dom) if default_cfg else None
     if mf is not None:
