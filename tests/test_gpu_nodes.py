@@ -164,11 +164,12 @@ def test_paper_coarse_nodes(idx, batch, sample, fine_subset):
     _assert(*check_net(S.config(idx, batch, coarse="paper"), sample=sample, fine_subset=fine_subset))
 
 
-@pytest.mark.parametrize("batch,sample,fine_subset", [(1, 256, None), (None, 256, [3])])
+@pytest.mark.parametrize("batch,sample,fine_subset", [(1, 256, None), (None, 256, [3]), (None, 256, [0])])
 def test_vgg224_nodes(batch, sample, fine_subset):
     """The ImageNet-shaped Parareal VGG-16-4 (224x224, 1000 classes, the paper's coarse blocks):
-    every node of every segment at batch 1, and at the full batch the last sub-network with every
-    preprocessing and coarse segment (sampled outputs)."""
+    every node of every segment at batch 1; at the full batch the first sub-network (its 224x224
+    layers: 6.4 M output rows, the weight-gradient GEMM's integer set-up past 2^22 rows) and the
+    last one, each with every preprocessing and coarse segment (sampled outputs)."""
     _assert(*check_net(S.config(5, batch), sample=sample, fine_subset=fine_subset))
 
 
