@@ -34,11 +34,13 @@ def _rel_2_with_inf(a, ref):
     return _E2(rel_2(a, ref), rel_inf(a, ref))
 
 
-def gpu_step(net, params, x, labels, resident=False):
+def gpu_step(net, params, x, labels, resident=False, streams=None):
     import torch
     from paper_2103_08802_amd import binding as B
     from paper_2103_08802_amd.step import ParaRealGPU
     g = ParaRealGPU(net, params)
+    if streams is not None:
+        B.pnn_set_streams(g.plan, streams)
     if resident:
         B.pnn_set_resident(g.plan, 1)
     g.load_input(x, labels)
@@ -69,14 +71,15 @@ def sample_nodes(seg, rng, n_mid=3):
     return sorted(pick)
 
 
-def check_net(net, sample=None, fine_subset=None, seed=0, node_subset=False, x_offset=0.0, resident=False):
+def check_net(net, sample=None, fine_subset=None, seed=0, node_subset=False, x_offset=0.0, resident=False,
+              streams=None):
     from oracle import prim as P
     x, labels, params = S.make_all(net)
     if x_offset:
         from pnn_synth.gen import to_storage
         x = to_storage(x + x_offset, net.dtype)
     _say(f"[nodes] {net.name} batch {net.batch} {net.dtype}: GPU step")
-    g, dx_fine = gpu_step(net, params, x, labels, resident)
+    g, dx_fine = gpu_step(net, params, x, labels, resident, streams)
     bf16 = net.dtype == "bf16"
     st = P.round_bf16 if bf16 else (lambda a: a)
     metric = _rel_2_with_inf if bf16 else rel_inf
@@ -153,6 +156,15 @@ def test_bn_fused_statistics_ragged_groups():
 @pytest.mark.parametrize("idx,fine_subset", [(1, None), (2, [0, 1, 3]), (3, [0, 5, 10, 15]), (4, [0, 2, 5, 7])])
 def test_sampled_nodes_full_size(idx, fine_subset):
     _assert(*check_net(S.config(idx), sample=256, fine_subset=fine_subset))
+
+
+def test_single_chain_full_size_nodes():
+    """All sixteen sub-networks in one chain (one stream, as the per-kernel timing passes run them):
+    every launch groups all sub-networks' problems of a level, so the stage-3 3x3 problems (8x8
+    images) take the 64-column GEMM tiles and launch records exceed one line of their problem
+    table.  Two stage-3 sub-networks and every preprocessing and coarse segment, sampled at the
+    full batch."""
+    _assert(*check_net(S.config(3), sample=256, fine_subset=[12, 15], streams=1))
 
 
 @pytest.mark.parametrize("idx,batch,sample,fine_subset",
