@@ -123,6 +123,7 @@ struct pnn_plan {
   // GEMM-kernel K-split partial tiles: one region per chain like the weight-gradient partials
   // (stride 0: no problem of the plan is split)
   size_t kpart_off = 0, kpart_stride = 0;
+  size_t act_off = 0, act_stride = 0;   // activated GEMM inputs (act_materialize), per chain
   // timing of one kernel family
   int timing_family = 0;
   std::vector<hipEvent_t> ev;
@@ -634,6 +635,7 @@ struct Ctx {
   hipStream_t stream;
   char* wpart = nullptr;   // split-K weight-gradient partials (nullptr: the plan's first region)
   char* kpart = nullptr;   // K-split GEMM partial tiles (nullptr: the plan's first region)
+  char* act = nullptr;     // activated GEMM inputs (nullptr: the plan's first region)
 };
 
 inline char* cp(const void* p) { return (char*)const_cast<void*>(p); }
@@ -975,6 +977,50 @@ bool plan_splits_k(const pnn_plan* plan) {
   return false;
 }
 
+// A forward GEMM problem with a BN prologue whose input holds at least ACT_MIN_BYTES: its input is
+// activated once, ReLU(BN(z)) by the BN-ReLU pass into a per-chain region, and the GEMM reads that
+// without a prologue.  The prologue would activate every input element once per tap and column
+// tile (9 x ncol / 128 times), which costs the forward GEMM a quarter of its MFMA rate on such
+// layers; the pass costs two tensor passes at the HBM rate.  Results are bit-identical (the same
+// fused multiply-add, ReLU and rounding).
+constexpr long ACT_MIN_BYTES = 32L << 20;
+bool act_materialize(const ConvProb& p, int es) {
+  return p.pro != nullptr && gemm_tn(p, es) != 0 && (long)p.B * p.H * p.W * p.Cg * es >= ACT_MIN_BYTES;
+}
+
+// the forward geometry of conv node n (its prologue pointer only marked)
+ConvProb fwd_geom(const pnn_plan* plan, const SegP& S, const NodeP& n) {
+  ConvProb p = conv_common(plan, n);
+  p.B = plan->B; p.H = n.H; p.W = n.W; p.Cg = n.cin;
+  p.P = n.Ho; p.Q = n.Wo; p.ncol = n.cout;
+  p.M = plan->B * n.Ho * n.Wo;
+  p.K = n.k * n.k * n.cin;
+  p.pro = n.bn >= 0 ? (const float*)&S : nullptr;
+  if (pw_fwd_node(S, n, plan->es)) set_pw_tiles(p, S.short_tiles);
+  else set_tiles(p, S.short_tiles);
+  return p;
+}
+
+// bytes of the activated GEMM inputs a forward level of these segments needs at once (the largest
+// over the levels; a chain runs a subset of the segments)
+size_t act_level_bytes(const pnn_plan* plan, const std::vector<SegP>& segs) {
+  size_t best = 0;
+  int maxL = 0;
+  for (const SegP& S : segs)
+    for (const NodeP& n : S.nodes) maxL = std::max(maxL, n.level);
+  for (int L = 1; L <= maxL; ++L) {
+    size_t b = 0;
+    for (const SegP& S : segs)
+      for (const NodeP& n : S.nodes) {
+        if (n.level != L || n.op != PNN_OP_CONV) continue;
+        const ConvProb p = fwd_geom(plan, S, n);
+        if (act_materialize(p, plan->es)) b = align256(b + (size_t)p.B * p.H * p.W * p.Cg * plan->es);
+      }
+    best = std::max(best, b);
+  }
+  return best;
+}
+
 // ------------------------------------------------------------------------------------------------
 // forward of a set of segments
 // ------------------------------------------------------------------------------------------------
@@ -1043,9 +1089,11 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
   const int B = plan->B, es = plan->es;
   {
     std::vector<ConvProb> cv_vec, cv_gen, cv_pw;
-    std::vector<BnActProb> ba;
+    std::vector<BnActProb> ba, act;     // act: activated GEMM inputs, ahead of the convolutions
     std::vector<MaxPool3Prob> mp;
     std::vector<ColRedProb> fw;
+    char* act_region = c.act != nullptr ? c.act : plan->act_stride != 0 ? c.scratch + plan->act_off : nullptr;
+    size_t act_used = 0;
     // producers of BN partial rows that may finalise the statistics themselves (bn_fwd_fuse): the
     // problem (list, index), the BN and its parameters, and the column reduce it would need
     struct Cand {
@@ -1093,6 +1141,21 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
           const bool pwn = pw_fwd_node(S, n, es);
           if (pwn) set_pw_tiles(p, S.short_tiles);
           else set_tiles(p, S.short_tiles);
+          const size_t abytes = (size_t)p.B * p.H * p.W * p.Cg * es;
+          if (act_region != nullptr && act_materialize(p, es) && act_used + abytes <= plan->act_stride) {
+            BnActProb a;
+            std::memset(&a, 0, sizeof(a));
+            a.z = p.in;
+            a.out = act_region + act_used;
+            a.stats = stats_ptr(c, S, n.bn);
+            a.B = B; a.H = n.H; a.W = n.W; a.C = n.cin; a.pool = 0;
+            a.n_out = (long)B * n.H * n.W;
+            a.pix = bnact_fwd_pix(n.cin, es);
+            act.push_back(a);
+            act_used = align256(act_used + abytes);
+            p.in = a.out;
+            p.pro = nullptr;
+          }
           std::vector<ConvProb>& dst = pwn ? cv_pw : (n.cin % (16 / es) == 0 ? cv_vec : cv_gen);
           dst.push_back(p);
           if (fs != nullptr) {
@@ -1147,7 +1210,10 @@ int run_fwd_level(const Ctx& c, const std::vector<const SegP*>& segs, const std:
       if (fuse) set_bn_fuse(q, c, *cd.fs, cd.fb, cd.fparams);
       else if (cd.own) fw.push_back(cd.red);
     }
-    int e;
+    int e = grouped<BnActLaunch>(
+        act, [](const BnActProb& p) { return (int)cdiv(p.n_out, p.pix); },
+        [&](const BnActLaunch& Lx, int tiles, size_t) { return launch_bnact_fwd(Lx, tiles, plan->dtype, c.stream); });
+    if (e) return e;
     if ((e = fire_conv(c, cv_vec, MODE_FWD))) return e;
     if ((e = fire_conv(c, cv_gen, MODE_FWD))) return e;
     if ((e = fire_pw(c, cv_pw, MODE_FWD))) return e;
@@ -1598,6 +1664,7 @@ int chains_group(const Ctx& c, const std::vector<const SegP*>& segs, const std::
     Ctx d = c;
     d.wpart = c.scratch + p->wpart_off + (size_t)(g + 1) * p->wpart_stride;
     if (p->kpart_stride != 0) d.kpart = c.scratch + p->kpart_off + (size_t)(g + 1) * p->kpart_stride;
+    if (p->act_stride != 0) d.act = c.scratch + p->act_off + (size_t)(g + 1) * p->act_stride;
     ch.ctx.push_back(d);
   }
   if (G <= 1) return PNN_OK;
@@ -1855,6 +1922,12 @@ pnn_status pnn_plan_create(const pnn_net_desc* d, pnn_plan** out) {
   p->kpart_off = sc;
   p->kpart_stride = plan_splits_k(p) ? GEMM_KPART_BYTES : 0;
   sc = align256(sc + p->kpart_stride * (PNN_MAX_CHAINS + 1));
+  size_t ab = act_level_bytes(p, p->fine);
+  ab = std::max(ab, act_level_bytes(p, p->pre));
+  for (auto& cs : p->coarse) ab = std::max(ab, act_level_bytes(p, std::vector<SegP>{cs}));
+  p->act_off = sc;
+  p->act_stride = ab;
+  sc = align256(sc + p->act_stride * (PNN_MAX_CHAINS + 1));
   const SlotP& yo = p->fine[N - 1].slots[p->fine[N - 1].out];
   p->head_off = sc;
   p->head_bytes = (size_t)p->B * (yo.C + p->classes + 1) * 4;
