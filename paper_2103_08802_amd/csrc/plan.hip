@@ -988,6 +988,12 @@ bool act_materialize(const ConvProb& p, int es) {
   return p.pro != nullptr && gemm_tn(p, es) != 0 && (long)p.B * p.H * p.W * p.Cg * es >= ACT_MIN_BYTES;
 }
 
+// Likewise the input of a GEMM weight gradient with a BN prologue (the prologue there activates
+// each input element once per tap and output-channel tile).
+bool wgrad_act(const NodeP& n, int B, int es) {
+  return n.bn >= 0 && wgrad_geom_node(n, B, es).gemm && (long)B * n.H * n.W * n.cin * es >= ACT_MIN_BYTES;
+}
+
 // the forward geometry of conv node n (its prologue pointer only marked)
 ConvProb fwd_geom(const pnn_plan* plan, const SegP& S, const NodeP& n) {
   ConvProb p = conv_common(plan, n);
@@ -1009,14 +1015,16 @@ size_t act_level_bytes(const pnn_plan* plan, const std::vector<SegP>& segs) {
   for (const SegP& S : segs)
     for (const NodeP& n : S.nodes) maxL = std::max(maxL, n.level);
   for (int L = 1; L <= maxL; ++L) {
-    size_t b = 0;
+    size_t b = 0, bw = 0;   // forward convolutions, weight gradients (wgrad_act) of the level
     for (const SegP& S : segs)
       for (const NodeP& n : S.nodes) {
         if (n.level != L || n.op != PNN_OP_CONV) continue;
         const ConvProb p = fwd_geom(plan, S, n);
-        if (act_materialize(p, plan->es)) b = align256(b + (size_t)p.B * p.H * p.W * p.Cg * plan->es);
+        const size_t bytes = (size_t)p.B * p.H * p.W * p.Cg * plan->es;
+        if (act_materialize(p, plan->es)) b = align256(b + bytes);
+        if (wgrad_act(n, plan->B, plan->es)) bw = align256(bw + bytes);
       }
-    best = std::max(best, b);
+    best = std::max({best, b, bw});
   }
   return best;
 }
@@ -1333,6 +1341,9 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
   const int B = plan->B, es = plan->es;
   char* wpart = c.wpart != nullptr ? c.wpart : c.scratch + plan->wpart_off;
   std::vector<WgradProb> wg_vec, wg_gen, wg_h3, wg_pw, wg_gemm;
+  std::vector<BnActProb> act;          // activated inputs of the GEMM weight gradients (wgrad_act)
+  char* act_region = c.act != nullptr ? c.act : plan->act_stride != 0 ? c.scratch + plan->act_off : nullptr;
+  size_t act_used = 0;
   size_t woff = 0;
   for (size_t i = 0; i < segs.size(); ++i) {
     const SegP& S = *segs[i];
@@ -1351,6 +1362,21 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
       WgradGeom g = wgrad_geom_node(n, B, es);
       p.wr = g.wr; p.tiles_co = g.tiles_co; p.tiles_k = g.tiles_k; p.splits = g.splits; p.mchunk = g.mchunk;
       p.gtc = g.gtc; p.gtk = g.gtk;
+      const size_t abytes = (size_t)B * n.H * n.W * n.cin * es;
+      if (act_region != nullptr && wgrad_act(n, B, es) && act_used + abytes <= plan->act_stride) {
+        BnActProb a;
+        std::memset(&a, 0, sizeof(a));
+        a.z = p.in;
+        a.out = act_region + act_used;
+        a.stats = stats_ptr(c, S, n.bn);
+        a.B = B; a.H = n.H; a.W = n.W; a.C = n.cin; a.pool = 0;
+        a.n_out = (long)B * n.H * n.W;
+        a.pix = bnact_fwd_pix(n.cin, es);
+        act.push_back(a);
+        act_used = align256(act_used + abytes);
+        p.in = a.out;
+        p.pro = nullptr;
+      }
       p.cg_log2 = log2_or(p.Cg);
       p.q_log2 = log2_or(p.Q);
       p.pq_log2 = log2_or(p.P * p.Q);
@@ -1376,6 +1402,12 @@ int fire_wgrads(const Ctx& c, const std::vector<const SegP*>& segs, const std::v
       r.rl_log2 = red_sum_rl_log2(r.rows);
       red.push_back(r);
     }
+  }
+  {
+    const int e = grouped<BnActLaunch>(
+        act, [](const BnActProb& q) { return (int)cdiv(q.n_out, q.pix); },
+        [&](const BnActLaunch& Lx, int tiles, size_t) { return launch_bnact_fwd(Lx, tiles, plan->dtype, c.stream); });
+    if (e) return e;
   }
   // the GEMM problems by tile shape (one launch per shape)
   std::vector<WgradProb> wg_gemm_by[4];
