@@ -454,10 +454,27 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
   const int gi = find_group(L);
   const WgradProb& P = L.p[gi];
   const int local = blockIdx.x - P.tile_begin;
-  const int tk = local % P.tiles_k;
-  const int rest = local / P.tiles_k;
-  const int tco = rest % P.tiles_co;
-  const int split = rest / P.tiles_co;
+  // Workgroups go to the eight XCDs round-robin by blockIdx, and each XCD has its own L2.  The
+  // tiles of one split (every tap and output-channel tile over the same pixels) read the same
+  // gradient rows and the same input rows shifted by a pixel.  For 64-channel output tiles (L2 hit
+  // rate 6 % in plain order) the first 8 floor(splits / 8) splits are grouped by XCD: local index
+  // 8 q + x takes split x + 8 (q / W), tile q % W (W tiles per split), so all of a split's tiles
+  // share one XCD (19 % faster there; the 128-channel tiles, 60 % hits already, ran 3 % slower so).
+  // The remaining splits, and every split of 128-channel tiles, in plain order.
+  const int W = P.tiles_co * P.tiles_k;
+  const int S8 = TC == 64 ? P.splits & ~7 : 0;
+  int t, split;
+  if (local < S8 * W) {
+    const int q = local >> 3;
+    split = (local & 7) + 8 * (q / W);
+    t = q % W;
+  } else {
+    const int l2 = local - S8 * W;
+    split = S8 + l2 / W;
+    t = l2 % W;
+  }
+  const int tk = t % P.tiles_k;
+  const int tco = t / P.tiles_k;
   const int co0 = tco * TC, k0 = tk * TK;
   const int tap = k0 / P.Cg, c0 = k0 - tap * P.Cg;      // (Cg a multiple of TK)
   const int dr = tap / 3 - 1, dc = tap - 3 * (tap / 3) - 1;
