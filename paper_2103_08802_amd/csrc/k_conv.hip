@@ -803,10 +803,24 @@ __global__ __launch_bounds__(256) void wgrad3_kernel(const WgradLaunch L) {
   const int gi = find_group(L);
   const WgradProb& P = L.p[gi];
   const int local = blockIdx.x - P.tile_begin;
-  const int tcb = local % P.tiles_k;                // 16-channel input block
-  const int rest = local / P.tiles_k;
-  const int tco = rest % P.tiles_co;
-  const int split = rest / P.tiles_co;
+  // a split's tiles (every input block and output-channel tile over the same pixels) read the same
+  // gradient and input rows: the first 8 floor(splits / 8) splits grouped by XCD (the XCDs take
+  // workgroups round-robin by blockIdx, each with its own L2): local index 8 q + x takes split
+  // x + 8 (q / W), tile q % W (W tiles per split); the remaining splits in plain order
+  const int W = P.tiles_co * P.tiles_k;
+  const int S8 = P.splits & ~7;
+  int t, split;
+  if (local < S8 * W) {
+    const int q = local >> 3;
+    split = (local & 7) + 8 * (q / W);
+    t = q % W;
+  } else {
+    const int l2 = local - S8 * W;
+    split = S8 + l2 / W;
+    t = l2 % W;
+  }
+  const int tcb = t % P.tiles_k;                    // 16-channel input block
+  const int tco = t / P.tiles_k;
   const int co0 = tco * 16, c0 = tcb * 16;
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
