@@ -407,7 +407,8 @@ int launch_gemm(const ConvLaunch& L, int tiles, int mode, int tn, hipStream_t s)
 // workgroup, TC and TK 128 or 64, split over m.  Stages of 64 pixels: the output-gradient rows and
 // the gathered input rows (BN prologue applied on the way, zeros outside the image) are staged
 // m-major in LDS (rows padded by 16 elements: the four rows of a transposed read fall on distinct
-// banks), read as MFMA fragments with the gfx950 transposed LDS read; four waves of
+// banks; in 128-column operands rows 8 .. 15 of every 16 are rotated by 64 columns, so that the two
+// lane groups of a half-wave, 8 rows apart, read disjoint banks), read as MFMA fragments with the gfx950 transposed LDS read; four waves of
 // (TC / 2) x (TK / 2) (16x16x32 MFMAs).  Loads run two stages ahead in two register sets; two LDS
 // stages.  The fp32 partial tile goes to part[split][co][K] for the split-K column reduce.
 // ------------------------------------------------------------------------------------------------
@@ -417,11 +418,18 @@ constexpr int WGM_KC = 64;                  // pixels per stage
 typedef short wv4s16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) wv4s16 lds_wv4s16;
 
-// the 16x16x32 MFMA fragment of 16 columns (cbase ..) over 8 rows (row0 .. row0 + 7) of an m-major
-// tile of row stride RS: lane group rows 4 (r16 / 4) apart by the transposed read
-template <int RS>
+// LDS column of element column c of row r of a W-column operand (W = 128: rows with bit 3 set
+// rotated by 64 columns; measured: 128 x 128 tiles 2010 -> 1956 us per VGG-224 launch, while the
+// 64-column operands, given 144-element rows for the same rotation, ran 1732 -> 2721 us)
+template <int W>
+__device__ __forceinline__ int wgm_col(int r, int c) { return W == 128 ? (c + ((r & 8) << 3)) & 127 : c; }
+
+// the 16x16x32 MFMA fragment of 16 columns (cbase ..) over 8 rows (row0 .. row0 + 7, row0 a multiple
+// of 8) of an m-major W-column tile of row stride RS: lane group rows 4 (r16 / 4) apart by the
+// transposed read
+template <int W, int RS>
 __device__ __forceinline__ void tr_frag(const uint16_t* base, int row0, int cbase, int r16, Frag<uint16_t>& f) {
-  const uint16_t* p0 = base + (row0 + (r16 >> 2)) * RS + cbase + 4 * (r16 & 3);
+  const uint16_t* p0 = base + (row0 + (r16 >> 2)) * RS + wgm_col<W>(row0, cbase + 4 * (r16 & 3));
   const wv4s16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_wv4s16*)p0);
   const wv4s16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_wv4s16*)(p0 + 4 * RS));
   const uint2 l2 = __builtin_bit_cast(uint2, lo), h2 = __builtin_bit_cast(uint2, hi);
@@ -435,7 +443,7 @@ struct WgmOp {
   static constexpr int RPP = 256 / CPR;          // rows per pass
   static constexpr int NP = WGM_KC / RPP;        // passes per stage
   static constexpr int RS = W + 16;              // LDS row stride (elements)
-  static_assert(RS * 2 % 16 == 0, "16-byte aligned rows");
+  static_assert((W == 64 || W == 128) && RS * 2 % 16 == 0, "16-byte aligned rows");
 };
 }  // namespace
 
@@ -548,7 +556,8 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
 #pragma unroll
     for (int h = 0; h < OG::NP; ++h) {
       const unsigned kg = 0u - ((R.ok >> h) & 1u);
-      const int o = (lrg + OG::RPP * h) * OG::RS + lcg;     // (rows 16-byte aligned: 16-byte writes)
+      const int r = lrg + OG::RPP * h;                      // (rows 16-byte aligned: 16-byte writes)
+      const int o = r * OG::RS + wgm_col<TC>(r, lcg);
       *(uint4*)(G + o) = make_uint4(R.g[h].x & kg, R.g[h].y & kg, R.g[h].z & kg, R.g[h].w & kg);
     }
 #pragma unroll
@@ -563,7 +572,8 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
         for (int e = 0; e < VE; ++e) f[e] = fmaxf(fmaf(v.v[e], pro_s[lca + e].x, pro_s[lca + e].y), 0.0f);
         store_chunk<T>(&w, 0, f);
       }
-      const int o = (lra + OA::RPP * h) * OA::RS + lca;
+      const int r = lra + OA::RPP * h;
+      const int o = r * OA::RS + wgm_col<TK>(r, lca);
       *(uint4*)(A + o) = make_uint4(w.x & ka, w.y & ka, w.z & ka, w.w & ka);
     }
   };
@@ -580,9 +590,9 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
       const int row0 = sub * 32 + VE * grp;
       Frag<T> a[NI], b[NJ];
 #pragma unroll
-      for (int i = 0; i < NI; ++i) tr_frag<OG::RS>(G, row0, wr * (TC / 2) + 16 * i, r16, a[i]);
+      for (int i = 0; i < NI; ++i) tr_frag<TC, OG::RS>(G, row0, wr * (TC / 2) + 16 * i, r16, a[i]);
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) tr_frag<OA::RS>(A, row0, wc * (TK / 2) + 16 * j, r16, b[j]);
+      for (int j = 0; j < NJ; ++j) tr_frag<TK, OA::RS>(A, row0, wc * (TK / 2) + 16 * j, r16, b[j]);
 #pragma unroll
       for (int i = 0; i < NI; ++i)
 #pragma unroll
