@@ -582,21 +582,30 @@ __global__ __launch_bounds__(256, 2) void wgrad_gemm_kernel(const WgradLaunch L)
   for (int i = 0; i < NI; ++i)
 #pragma unroll
     for (int j = 0; j < NJ; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // The next sub-step's fragments are read into the registers of the current one as soon as their
+  // last MFMA has issued (A fragment i after row i, B fragment j after the last row's MFMA j), so
+  // that the reads overlap the remaining MFMAs.
   auto compute = [&](int st) {
     const uint16_t* G = smem + st * STG;
     const uint16_t* A = G + WGM_KC * OG::RS;
+    Frag<T> a[NI], b[NJ];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) tr_frag<TC, OG::RS>(G, VE * grp, wr * (TC / 2) + 16 * i, r16, a[i]);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) tr_frag<TK, OA::RS>(A, VE * grp, wc * (TK / 2) + 16 * j, r16, b[j]);
 #pragma unroll
     for (int sub = 0; sub < WGM_KC / 32; ++sub) {
-      const int row0 = sub * 32 + VE * grp;
-      Frag<T> a[NI], b[NJ];
+      const bool more = sub + 1 < WGM_KC / 32;
+      const int row1 = (sub + 1) * 32 + VE * grp;
 #pragma unroll
-      for (int i = 0; i < NI; ++i) tr_frag<TC, OG::RS>(G, row0, wr * (TC / 2) + 16 * i, r16, a[i]);
+      for (int i = 0; i < NI; ++i) {
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) tr_frag<TK, OA::RS>(A, row0, wc * (TK / 2) + 16 * j, r16, b[j]);
-#pragma unroll
-      for (int i = 0; i < NI; ++i)
-#pragma unroll
-        for (int j = 0; j < NJ; ++j) mma(a[i], b[j], acc[i][j]);
+        for (int j = 0; j < NJ; ++j) {
+          mma(a[i], b[j], acc[i][j]);
+          if (more && i == NI - 1) tr_frag<TK, OA::RS>(A, row1, wc * (TK / 2) + 16 * j, r16, b[j]);
+        }
+        if (more) tr_frag<TC, OG::RS>(G, row1, wr * (TC / 2) + 16 * i, r16, a[i]);
+      }
     }
   };
 
